@@ -1,0 +1,179 @@
+/*
+ * precache.h -- C ABI of the PreLRShared hot path on MI355X (gfx950).
+ *
+ * PReCache's PreLRShared design (Sec. 3.1) lets N LoRA agents share one base
+ * KV cache.  Each agent i keeps a compact low-rank (LR) cache X A_i of r
+ * numbers per token (Sec. 2.2).  The LR caches of all agents are built once,
+ * when a context segment is first processed (the precompute).  Any agent can
+ * then attend over the shared base cache plus its own LR cache without
+ * re-processing the trajectory.  By Eq. 1 the keys and values an agent sees are
+ *     K = K_base + RoPE(L_k B_k),      V = V_base + L_v B_v,
+ * where RoPE is applied after the rank-r expansion (App. D.2).
+ *
+ * General conventions (every entry point):
+ *   - Tensor arguments are DEVICE pointers owned by the caller.  The library
+ *     never frees, retains or reallocates them.  bf16 data is passed as
+ *     uint16_t storage (IEEE bfloat16 bit patterns).
+ *   - Every call is asynchronous on `stream` (a hipStream_t; NULL = the
+ *     device's default stream).  No call synchronises, and no call allocates
+ *     device memory.
+ *   - Every call first validates its arguments on the host, before any HIP
+ *     call is made.  A failed check returns a non-zero prc_status and launches
+ *     nothing; prc_last_error() then gives a thread-local message naming the
+ *     argument.  HIP launch failures return PRC_ELAUNCH.
+ *   - Row-major layouts throughout; "[a, b, c]" lists dimensions from
+ *     outermost to innermost; the innermost dimension is contiguous.
+ *   - All bf16 pointers must be 16-byte aligned, and every row stride given
+ *     in elements must keep rows 16-byte aligned.  int32 and fp32 pointers
+ *     must be 4-byte aligned.
+ *   - Values that live in device memory (positions, kv_len) cannot be checked
+ *     by the host.  Kernels clamp kv_len[b] into [0, s_cap], so no access ever
+ *     leaves the caller's buffers.
+ *
+ * Orientation of the LoRA weights.  The paper writes Y = X (W0 + A B) with
+ * A in R^{d_in x r} and B in R^{r x d_out}.  This ABI stores both factors
+ * transposed, as PEFT stores them: down-projections as rows (A^T) and
+ * up-projections as [d_out, r] (B^T).  Both MFMA operands are then contiguous
+ * along the contracted dimension.
+ */
+#ifndef PRECACHE_H
+#define PRECACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum prc_status {
+  PRC_OK = 0,
+  PRC_EINVAL = 1,       /* null pointer, negative size, non-finite scalar     */
+  PRC_ESHAPE = 2,       /* inconsistent sizes or strides                      */
+  PRC_EALIGN = 3,       /* pointer or stride breaks the alignment rules       */
+  PRC_EUNSUPPORTED = 4, /* head_dim, rank or GQA group outside the set built  */
+  PRC_EWORKSPACE = 5,   /* workspace null or smaller than the size query      */
+  PRC_ELAUNCH = 6,      /* a HIP launch reported an error                     */
+  PRC_EDEVICE = 7       /* no usable gfx950 device is current                 */
+} prc_status;
+
+/* Thread-local message describing the last non-OK status on this thread. */
+const char* prc_last_error(void);
+/* Static name of a status code. */
+const char* prc_status_string(prc_status s);
+/* Library version string, e.g. "0.1.0". */
+const char* prc_version(void);
+
+/*
+ * precompute_lr_cache -- the LR-cache precompute of Sec. 3.1 (Fig. 1 A1-A3).
+ *
+ * For a newly processed segment of T hidden states, apply EVERY agent's LoRA
+ * down-projection, for every adapted projection, in one batched GEMM:
+ *     L[p][a][tok_offset + t][j] = sum_k X[t][k] * A_rows[(p*N + a)*r + j][k]
+ * This is X A_k of Sec. 2.2 for all agents k at once.
+ *
+ *   X        [T, d_in] bf16, row stride ld_x (elements, >= d_in).  These are
+ *            the hidden states that feed k_proj/v_proj.
+ *   A_rows   [n_proj*N*r, d_in] bf16, contiguous.  Row (p*N + a)*r + j is
+ *            column j of agent a's down-projection A for projection p
+ *            (p = 0: k_proj, p = 1: v_proj when n_proj = 2).
+ *   L_out    [n_proj, N, s_cap, r] bf16, contiguous.  Rows
+ *            [tok_offset, tok_offset + T) of every plane are overwritten;
+ *            nothing else is touched.
+ * Arithmetic: bf16 inputs, fp32 accumulation, round-to-nearest-even to bf16.
+ * Requires d_in % 8 == 0, ld_x % 8 == 0, r in {8, 16, 32, 64},
+ * 0 <= tok_offset and tok_offset + T <= s_cap.  T == 0 is a no-op.
+ */
+prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
+                               const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                               int32_t rank, uint16_t* L_out, int64_t s_cap,
+                               int64_t tok_offset, void* stream);
+
+/* Dimensions of one LR-shared attention call (a batch of B requests). */
+typedef struct lrsa_dims {
+  int32_t batch;        /* B >= 0 requests                                     */
+  int32_t n_tok;        /* query tokens per request (1 = decode)               */
+  int32_t n_q_heads;    /* query heads                                         */
+  int32_t n_kv_heads;   /* KV heads; n_q_heads / n_kv_heads in 1..8            */
+  int32_t head_dim;     /* d in {64, 128}                                      */
+  int32_t rank;         /* r in {8, 16, 32, 64}; ignored when no LR is given   */
+  int64_t s_cap;        /* token capacity of each request's caches             */
+  int64_t kv_req_stride;/* elements between requests in K_base/V_base
+                           (>= s_cap*n_kv*d, or 0: all requests share one)     */
+  int64_t l_req_stride; /* elements between requests' LR planes (0: shared)    */
+  int64_t b_req_stride; /* elements between requests' up-projections (0: shared) */
+  float softmax_scale;  /* <= 0 selects 1/sqrt(head_dim)                       */
+  float reserved0;      /* must be 0                                           */
+  double rope_theta;    /* RoPE base, > 0                                      */
+} lrsa_dims;
+
+/*
+ * lr_shared_attention -- attention of an agent over the shared base cache plus
+ * its own LR cache (Sec. 3.1, reuse step; value-side reordering of App. D.2).
+ *
+ * For request b, query token i and query head h (KV head g = h / (n_q/n_kv)):
+ *     K[t] = K_base[t][g] + RoPE(L_k[t] . B_k[g*d:(g+1)*d], t)
+ *     V[t] = V_base[t][g] + L_v[t] . B_v[g*d:(g+1)*d]
+ *     O[b][i][h] = softmax_t( scale * Q[b][i][h] . K[t] ) . V[t]
+ * over the keys t with t < kv_len[b] and t <= positions[b][i].  KV token t sits
+ * at absolute position t.  RoPE is rotate-half: element j pairs with j + d/2,
+ * at angle t * theta^(-2j/d).  The full per-agent K/V is never written to
+ * memory: each KV tile is rebuilt on chip.
+ *
+ *   Q          [B, n_tok, n_q, d] bf16, already rotated at positions[b][i].
+ *   K_base     [B, s_cap, n_kv, d] bf16 (request stride kv_req_stride), already
+ *              rotated at each token's position.
+ *   V_base     same layout as K_base.
+ *   L_k, L_v   [B, s_cap, r] bf16 (request stride l_req_stride): each request's
+ *              agent plane of the LR cache.  NULL = that projection is not
+ *              adapted.  The QV setting of the paper passes L_k = NULL.
+ *   B_k, B_v   [B, n_kv*d, r] bf16 (request stride b_req_stride): each request's
+ *              agent up-projection, stored transposed (B^T).  Must be NULL
+ *              exactly when the matching L is NULL.
+ *   positions  [B, n_tok] int32, absolute query positions.
+ *   kv_len     [B] int32, number of valid cache rows per request (device memory).
+ *   O          [B, n_tok, n_q, d] bf16 output.
+ *   lse        [B, n_tok, n_q] fp32 natural-log log-sum-exp of the scaled scores,
+ *              or NULL.  A row that sees no key gets O = 0 and lse = -inf.
+ *   workspace  device scratch of at least lr_shared_attention_workspace_size(dims)
+ *              bytes (only decode, n_tok == 1, uses it; NULL allowed when the size
+ *              is 0).  Contents need no initialisation; calls that share a
+ *              workspace must be ordered on one stream.
+ * Arithmetic: bf16 inputs; fp32 accumulation and softmax; rebuilt K tiles are
+ * rounded to bf16 before the QK^T contraction; output rounded to bf16.
+ */
+prc_status lr_shared_attention(const lrsa_dims* dims, const uint16_t* Q,
+                               const uint16_t* K_base, const uint16_t* V_base,
+                               const uint16_t* L_k, const uint16_t* L_v,
+                               const uint16_t* B_k, const uint16_t* B_v,
+                               const int32_t* positions, const int32_t* kv_len,
+                               uint16_t* O, float* lse, void* workspace,
+                               size_t workspace_bytes, void* stream);
+
+/* Workspace bytes lr_shared_attention needs for `dims` (0 when none, or when
+ * dims is invalid; validation errors are reported by the call itself). */
+size_t lr_shared_attention_workspace_size(const lrsa_dims* dims);
+
+/*
+ * materialize_agent_kv -- the reference point: write out each request's full
+ * per-agent K/V (the keys and values NonShared/BaseShared agents would hold,
+ * Sec. 3.1) so that a plain attention call (L_k = L_v = NULL) can consume them.
+ *     K_full[b][t][g] = K_base[b][t][g] + RoPE(L_k[b][t] . B_k[g], t)
+ *     V_full[b][t][g] = V_base[b][t][g] + L_v[b][t] . B_v[g]
+ * for t < kv_len[b].  Rows t >= kv_len[b] of K_full/V_full are not written.
+ *   K_full, V_full  [B, s_cap, n_kv, d] bf16, contiguous (request stride
+ *                   s_cap*n_kv*d), and must not alias the inputs.
+ * Other arguments as in lr_shared_attention (n_tok, softmax_scale ignored).
+ * A NULL L_k (or L_v) copies K_base (or V_base) unchanged.
+ */
+prc_status materialize_agent_kv(const lrsa_dims* dims, const uint16_t* K_base,
+                                const uint16_t* V_base, const uint16_t* L_k,
+                                const uint16_t* L_v, const uint16_t* B_k,
+                                const uint16_t* B_v, const int32_t* kv_len,
+                                uint16_t* K_full, uint16_t* V_full, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PRECACHE_H */

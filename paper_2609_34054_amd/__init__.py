@@ -1,0 +1,19 @@
+"""PreLRShared hot path (PReCache, Sec. 3.1) for MI355X / gfx950.
+
+The compute lives in ``libprecache.so`` (hand-written HIP kernels behind the C
+ABI declared in ``include/precache.h``); this package is its thin Python
+binding.  Torch provides device memory and streams only.
+"""
+from .binding import (  # noqa: F401
+    EXPORTS,
+    LrsaDims,
+    PrecacheError,
+    lib,
+    lr_shared_attention,
+    make_dims,
+    materialize_agent_kv,
+    precompute_lr_cache,
+    workspace_size,
+)
+
+__version__ = "0.1.0"

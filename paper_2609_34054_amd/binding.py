@@ -1,0 +1,224 @@
+"""ctypes binding of libprecache.so (argument marshalling only).
+
+Every step of the hot path runs in the library's HIP kernels.  These wrappers
+take torch tensors for device memory and torch's current stream, derive the
+sizes and strides the C ABI wants, and raise :class:`PrecacheError` on any
+non-OK status.  There is no fallback: if the library is missing, the call
+fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from .build import LIB_PATH
+
+_LIB = None
+
+STATUS_NAMES = {0: "PRC_OK", 1: "PRC_EINVAL", 2: "PRC_ESHAPE", 3: "PRC_EALIGN",
+                4: "PRC_EUNSUPPORTED", 5: "PRC_EWORKSPACE", 6: "PRC_ELAUNCH", 7: "PRC_EDEVICE"}
+
+EXPORTS = ("precompute_lr_cache", "lr_shared_attention", "lr_shared_attention_workspace_size",
+           "materialize_agent_kv", "prc_last_error", "prc_status_string", "prc_version")
+
+
+class PrecacheError(RuntimeError):
+    def __init__(self, func: str, status: int, message: str):
+        self.status = status
+        self.status_name = STATUS_NAMES.get(status, f"status {status}")
+        super().__init__(f"{func}: {self.status_name}: {message}")
+
+
+class LrsaDims(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int32),
+        ("n_tok", ctypes.c_int32),
+        ("n_q_heads", ctypes.c_int32),
+        ("n_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("rank", ctypes.c_int32),
+        ("s_cap", ctypes.c_int64),
+        ("kv_req_stride", ctypes.c_int64),
+        ("l_req_stride", ctypes.c_int64),
+        ("b_req_stride", ctypes.c_int64),
+        ("softmax_scale", ctypes.c_float),
+        ("reserved0", ctypes.c_float),
+        ("rope_theta", ctypes.c_double),
+    ]
+
+
+def lib() -> ctypes.CDLL:
+    """Load libprecache.so (built in-tree by ``build()``); raise if absent."""
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
+                               "(python -m paper_2609_34054_amd.build)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        L.precompute_lr_cache.argtypes = [vp, i64, i64, i64, vp, i32, i32, i32, vp, i64, i64, vp]
+        L.precompute_lr_cache.restype = ctypes.c_int
+        L.lr_shared_attention.argtypes = [ctypes.POINTER(LrsaDims), vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                          vp, vp, vp, ctypes.c_size_t, vp]
+        L.lr_shared_attention.restype = ctypes.c_int
+        L.lr_shared_attention_workspace_size.argtypes = [ctypes.POINTER(LrsaDims)]
+        L.lr_shared_attention_workspace_size.restype = ctypes.c_size_t
+        L.materialize_agent_kv.argtypes = [ctypes.POINTER(LrsaDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+        L.materialize_agent_kv.restype = ctypes.c_int
+        L.prc_last_error.restype = ctypes.c_char_p
+        L.prc_status_string.argtypes = [ctypes.c_int]
+        L.prc_status_string.restype = ctypes.c_char_p
+        L.prc_version.restype = ctypes.c_char_p
+        _LIB = L
+    return _LIB
+
+
+def _check(func: str, status: int) -> None:
+    if status != 0:
+        raise PrecacheError(func, status, lib().prc_last_error().decode())
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _bf16(name, t, ndim):
+    if t is None:
+        return
+    if t.dtype != torch.bfloat16:
+        raise TypeError(f"{name} must be bfloat16, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
+    if t.stride(-1) != 1:
+        raise ValueError(f"{name} must be contiguous in its last dimension")
+
+
+def _req_stride(t, batch):
+    """Elements between requests: 0 when one buffer serves every request."""
+    if t is None or t.shape[0] == 1:
+        return 0
+    if t.shape[0] != batch:
+        raise ValueError(f"leading dim {t.shape[0]} is neither 1 nor the batch {batch}")
+    return t.stride(0)
+
+
+def precompute_lr_cache(X, A_rows, n_proj: int, n_agents: int, rank: int, L_out, tok_offset: int = 0,
+                        stream=None):
+    """``L_out[p][a][tok_offset + t] = X[t] @ A_rows[(p*N+a)*r:(p*N+a+1)*r].T`` (Sec. 3.1).
+
+    ``X [T, d_in]`` bf16 (row stride may exceed d_in), ``A_rows [n_proj*N*r, d_in]``,
+    ``L_out [n_proj, N, s_cap, r]`` bf16 contiguous.
+    """
+    _bf16("X", X, 2)
+    _bf16("A_rows", A_rows, 2)
+    _bf16("L_out", L_out, 4)
+    if not A_rows.is_contiguous() or not L_out.is_contiguous():
+        raise ValueError("A_rows and L_out must be contiguous")
+    if tuple(L_out.shape[:2]) != (n_proj, n_agents) or L_out.shape[3] != rank:
+        raise ValueError(f"L_out shape {tuple(L_out.shape)} does not match ({n_proj}, {n_agents}, s_cap, {rank})")
+    T, d_in = X.shape
+    st = lib().precompute_lr_cache(_ptr(X), T, d_in, X.stride(0), _ptr(A_rows), n_proj, n_agents, rank,
+                                   _ptr(L_out), L_out.shape[2], tok_offset, _stream(stream))
+    _check("precompute_lr_cache", st)
+    return L_out
+
+
+def make_dims(Q, K_base, L_k, L_v, B_k, B_v, rope_theta: float, softmax_scale: float = 0.0,
+              batch=None, n_q=None):
+    """The lrsa_dims of a call, from tensor shapes (Q may be None for materialise)."""
+    lr = L_k if L_k is not None else L_v
+    bt = B_k if B_k is not None else B_v
+    if Q is not None:
+        batch, n_tok, n_q, d = Q.shape
+    else:
+        n_tok, d = 0, K_base.shape[3]
+    s_cap, n_kv = K_base.shape[1], K_base.shape[2]
+    if K_base.shape[3] != d:
+        raise ValueError("head dims of Q and K_base differ")
+    rank = lr.shape[-1] if lr is not None else 0
+    if lr is not None and lr.shape[-2] != s_cap:
+        raise ValueError(f"LR cache holds {lr.shape[-2]} rows, the base cache {s_cap}")
+    if bt is not None and (bt.shape[-2] != n_kv * d or bt.shape[-1] != rank):
+        raise ValueError(f"up-projection shape {tuple(bt.shape)} is not (.., {n_kv * d}, {rank})")
+    return LrsaDims(batch=batch, n_tok=n_tok, n_q_heads=n_q, n_kv_heads=n_kv, head_dim=d, rank=rank,
+                    s_cap=s_cap, kv_req_stride=_req_stride(K_base, batch),
+                    l_req_stride=_req_stride(lr, batch), b_req_stride=_req_stride(bt, batch),
+                    softmax_scale=softmax_scale, reserved0=0.0, rope_theta=rope_theta)
+
+
+def workspace_size(dims: LrsaDims) -> int:
+    return int(lib().lr_shared_attention_workspace_size(ctypes.byref(dims)))
+
+
+def lr_shared_attention(Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len, *, rope_theta: float,
+                        softmax_scale: float = 0.0, O=None, lse=None, want_lse: bool = False,
+                        workspace=None, stream=None):
+    """Attention over the shared base cache plus one agent's LR cache (Sec. 3.1).
+
+    Shapes: ``Q [B, n_tok, n_q, d]``; ``K_base, V_base [B|1, s_cap, n_kv, d]``;
+    ``L_k, L_v [B|1, s_cap, r]`` or None; ``B_k, B_v [B|1, n_kv*d, r]`` or None
+    (stored transposed); ``positions [B, n_tok]`` and ``kv_len [B]`` int32.
+    Returns ``(O, lse)`` (``lse`` None unless requested).
+    """
+    for name, t, nd in (("Q", Q, 4), ("K_base", K_base, 4), ("V_base", V_base, 4), ("L_k", L_k, 3),
+                        ("L_v", L_v, 3), ("B_k", B_k, 3), ("B_v", B_v, 3)):
+        _bf16(name, t, nd)
+    for name, t in (("Q", Q), ("K_base", K_base), ("V_base", V_base)):
+        if not t[0].is_contiguous():
+            raise ValueError(f"{name} must be contiguous within a request")
+    if K_base.shape != V_base.shape or K_base.stride() != V_base.stride():
+        raise ValueError("K_base and V_base must share shape and strides")
+    if L_k is not None and L_v is not None and (L_k.shape != L_v.shape or L_k.stride() != L_v.stride()):
+        raise ValueError("L_k and L_v must share shape and strides")
+    if B_k is not None and B_v is not None and (B_k.shape != B_v.shape or B_k.stride() != B_v.stride()):
+        raise ValueError("B_k and B_v must share shape and strides")
+    dims = make_dims(Q, K_base, L_k, L_v, B_k, B_v, rope_theta, softmax_scale)
+    if positions.dtype != torch.int32 or kv_len.dtype != torch.int32:
+        raise TypeError("positions and kv_len must be int32")
+    if tuple(positions.shape) != tuple(Q.shape[:2]) or not positions.is_contiguous():
+        raise ValueError("positions must be a contiguous [B, n_tok] tensor")
+    if tuple(kv_len.shape) != (Q.shape[0],):
+        raise ValueError("kv_len must be a [B] tensor")
+    if O is None:
+        O = torch.empty_like(Q)
+    if lse is None and want_lse:
+        lse = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device)
+    need = workspace_size(dims)
+    if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=Q.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib().lr_shared_attention(ctypes.byref(dims), _ptr(Q), _ptr(K_base), _ptr(V_base), _ptr(L_k),
+                                   _ptr(L_v), _ptr(B_k), _ptr(B_v), _ptr(positions), _ptr(kv_len), _ptr(O),
+                                   _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream))
+    _check("lr_shared_attention", st)
+    return O, lse
+
+
+def materialize_agent_kv(K_base, V_base, L_k, L_v, B_k, B_v, kv_len, *, rope_theta: float, K_full=None,
+                         V_full=None, stream=None):
+    """Write each request's full per-agent K/V (the materialise-then-attend reference point)."""
+    for name, t, nd in (("K_base", K_base, 4), ("V_base", V_base, 4), ("L_k", L_k, 3), ("L_v", L_v, 3),
+                        ("B_k", B_k, 3), ("B_v", B_v, 3)):
+        _bf16(name, t, nd)
+    batch = kv_len.shape[0]
+    dims = make_dims(None, K_base, L_k, L_v, B_k, B_v, rope_theta, batch=batch, n_q=K_base.shape[2])
+    shape = (batch,) + tuple(K_base.shape[1:])
+    if K_full is None:
+        K_full = torch.empty(shape, dtype=torch.bfloat16, device=K_base.device)
+    if V_full is None:
+        V_full = torch.empty(shape, dtype=torch.bfloat16, device=K_base.device)
+    if tuple(K_full.shape) != shape or not K_full.is_contiguous() or not V_full.is_contiguous():
+        raise ValueError("K_full/V_full must be contiguous [B, s_cap, n_kv, d]")
+    st = lib().materialize_agent_kv(ctypes.byref(dims), _ptr(K_base), _ptr(V_base), _ptr(L_k), _ptr(L_v),
+                                    _ptr(B_k), _ptr(B_v), _ptr(kv_len), _ptr(K_full), _ptr(V_full),
+                                    _stream(stream))
+    _check("materialize_agent_kv", st)
+    return K_full, V_full

@@ -1,0 +1,261 @@
+// C ABI of the PreLRShared hot path: host-side validation and dispatch.
+//
+// Every argument check runs on the host before any HIP call, so each error
+// status can be produced (and tested) without a GPU.  The semantics of each
+// entry point are documented in include/precache.h.
+#include "precache.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "kernels.hpp"
+
+#define PRC_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local std::string g_err;
+
+prc_status fail(prc_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+prc_status ok() {
+  g_err.clear();
+  return PRC_OK;
+}
+
+bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
+bool rank_ok(int64_t r) { return r == 8 || r == 16 || r == 32 || r == 64; }
+
+prc_status launch_status(hipError_t e, const char* what) {
+  if (e != hipSuccess) return fail(PRC_ELAUNCH, "%s: HIP launch failed: %s", what, hipGetErrorString(e));
+  return ok();
+}
+
+// Validated view of an attention/materialise call.
+struct Checked {
+  prc::AttnArgs a;
+  bool empty;
+};
+
+prc_status check_attention(const lrsa_dims* dims, const uint16_t* Q, const uint16_t* K_base,
+                           const uint16_t* V_base, const uint16_t* L_k, const uint16_t* L_v,
+                           const uint16_t* B_k, const uint16_t* B_v, const int32_t* positions,
+                           const int32_t* kv_len, bool need_q, Checked* out) {
+  if (dims == nullptr) return fail(PRC_EINVAL, "dims is NULL");
+  const lrsa_dims& d = *dims;
+  if (d.batch < 0 || d.batch > 65535) return fail(PRC_EINVAL, "batch=%d outside [0, 65535]", d.batch);
+  if (d.n_tok < 0) return fail(PRC_EINVAL, "n_tok=%d is negative", d.n_tok);
+  if (d.n_q_heads < 1 || d.n_kv_heads < 1 || d.n_kv_heads > 65535)
+    return fail(PRC_EINVAL, "n_q_heads=%d, n_kv_heads=%d must be positive", d.n_q_heads, d.n_kv_heads);
+  if (d.n_q_heads % d.n_kv_heads != 0)
+    return fail(PRC_ESHAPE, "n_q_heads=%d is not a multiple of n_kv_heads=%d", d.n_q_heads, d.n_kv_heads);
+  const int group = d.n_q_heads / d.n_kv_heads;
+  if (group > 8) return fail(PRC_EUNSUPPORTED, "GQA group n_q/n_kv=%d > 8 is not built", group);
+  if (d.head_dim != 64 && d.head_dim != 128)
+    return fail(PRC_EUNSUPPORTED, "head_dim=%d (built: 64, 128)", d.head_dim);
+  if (d.s_cap < 1 || d.s_cap > INT32_MAX) return fail(PRC_EINVAL, "s_cap=%lld outside [1, 2^31-1]", (long long)d.s_cap);
+  if ((int64_t)d.n_tok * group > INT32_MAX / 2) return fail(PRC_EINVAL, "n_tok * group too large");
+  if (!(d.rope_theta > 0.0) || !std::isfinite(d.rope_theta))
+    return fail(PRC_EINVAL, "rope_theta=%g must be positive and finite", d.rope_theta);
+  if (!std::isfinite(d.softmax_scale)) return fail(PRC_EINVAL, "softmax_scale is not finite");
+  if (d.reserved0 != 0.f) return fail(PRC_EINVAL, "reserved0 must be 0");
+  if ((L_k == nullptr) != (B_k == nullptr))
+    return fail(PRC_EINVAL, "L_k and B_k must both be given or both be NULL");
+  if ((L_v == nullptr) != (B_v == nullptr))
+    return fail(PRC_EINVAL, "L_v and B_v must both be given or both be NULL");
+  const bool has_lr = L_k != nullptr || L_v != nullptr;
+  if (has_lr && !rank_ok(d.rank)) return fail(PRC_EUNSUPPORTED, "rank=%d (built: 8, 16, 32, 64)", d.rank);
+  const int64_t dd = d.head_dim, r = has_lr ? d.rank : 8;
+  const int64_t kv_need = d.s_cap * d.n_kv_heads * dd;
+  if (d.kv_req_stride != 0 && d.kv_req_stride < kv_need && d.batch > 1)
+    return fail(PRC_ESHAPE, "kv_req_stride=%lld < s_cap*n_kv*d=%lld", (long long)d.kv_req_stride, (long long)kv_need);
+  if (d.kv_req_stride < 0 || d.l_req_stride < 0 || d.b_req_stride < 0)
+    return fail(PRC_EINVAL, "request strides must be >= 0");
+  if (has_lr && d.l_req_stride != 0 && d.l_req_stride < d.s_cap * r && d.batch > 1)
+    return fail(PRC_ESHAPE, "l_req_stride=%lld < s_cap*rank", (long long)d.l_req_stride);
+  if (has_lr && d.b_req_stride != 0 && d.b_req_stride < d.n_kv_heads * dd * r && d.batch > 1)
+    return fail(PRC_ESHAPE, "b_req_stride=%lld < n_kv*d*rank", (long long)d.b_req_stride);
+  if (d.kv_req_stride % 8 || d.l_req_stride % 8 || d.b_req_stride % 8)
+    return fail(PRC_EALIGN, "request strides must be multiples of 8 elements (16 bytes)");
+
+  out->empty = d.batch == 0 || (need_q && d.n_tok == 0);
+  if (out->empty) return ok();
+  if (need_q && Q == nullptr) return fail(PRC_EINVAL, "Q is NULL");
+  if (K_base == nullptr || V_base == nullptr) return fail(PRC_EINVAL, "K_base/V_base is NULL");
+  if (kv_len == nullptr) return fail(PRC_EINVAL, "kv_len is NULL");
+  if (need_q && positions == nullptr) return fail(PRC_EINVAL, "positions is NULL");
+  const void* bf[] = {Q, K_base, V_base, L_k, L_v, B_k, B_v};
+  const char* names[] = {"Q", "K_base", "V_base", "L_k", "L_v", "B_k", "B_v"};
+  for (int i = 0; i < 7; ++i)
+    if (bf[i] != nullptr && !aligned(bf[i], 16)) return fail(PRC_EALIGN, "%s is not 16-byte aligned", names[i]);
+  if (!aligned(kv_len, 4) || (positions != nullptr && !aligned(positions, 4)))
+    return fail(PRC_EALIGN, "positions/kv_len are not 4-byte aligned");
+
+  prc::AttnArgs& a = out->a;
+  a = prc::AttnArgs{};
+  a.Q = Q;
+  a.Kb = K_base;
+  a.Vb = V_base;
+  a.Lk = L_k;
+  a.Lv = L_v;
+  a.Bk = B_k;
+  a.Bv = B_v;
+  a.positions = positions;
+  a.kv_len = kv_len;
+  a.s_cap = d.s_cap;
+  a.kv_stride = d.kv_req_stride;
+  a.l_stride = d.l_req_stride;
+  a.b_stride = d.b_req_stride;
+  a.batch = d.batch;
+  a.n_tok = d.n_tok;
+  a.n_q = d.n_q_heads;
+  a.n_kv = d.n_kv_heads;
+  a.group = group;
+  a.head_dim = d.head_dim;
+  a.rank = (int32_t)r;
+  const double scale = d.softmax_scale > 0.f ? (double)d.softmax_scale : 1.0 / std::sqrt((double)d.head_dim);
+  a.scale_log2 = (float)(scale * 1.4426950408889634);
+  // RoPE frequencies omega_j = theta^(-2j/d), passed as revolutions per
+  // position, omega_j / (2 pi), in fp64.
+  for (int j = 0; j < d.head_dim / 2; ++j)
+    a.w2pi[j] = std::pow(d.rope_theta, -2.0 * j / (double)d.head_dim) / (2.0 * M_PI);
+  return ok();
+}
+
+}  // namespace
+
+PRC_API const char* prc_last_error(void) { return g_err.c_str(); }
+
+PRC_API const char* prc_status_string(prc_status s) {
+  switch (s) {
+    case PRC_OK: return "PRC_OK";
+    case PRC_EINVAL: return "PRC_EINVAL";
+    case PRC_ESHAPE: return "PRC_ESHAPE";
+    case PRC_EALIGN: return "PRC_EALIGN";
+    case PRC_EUNSUPPORTED: return "PRC_EUNSUPPORTED";
+    case PRC_EWORKSPACE: return "PRC_EWORKSPACE";
+    case PRC_ELAUNCH: return "PRC_ELAUNCH";
+    case PRC_EDEVICE: return "PRC_EDEVICE";
+  }
+  return "PRC_UNKNOWN";
+}
+
+PRC_API const char* prc_version(void) { return "0.1.0"; }
+
+PRC_API prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
+                                       const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                       int32_t rank, uint16_t* L_out, int64_t s_cap, int64_t tok_offset,
+                                       void* stream) {
+  if (T < 0) return fail(PRC_EINVAL, "T=%lld is negative", (long long)T);
+  if (d_in < 1 || d_in % 8) return fail(PRC_EUNSUPPORTED, "d_in=%lld must be a positive multiple of 8", (long long)d_in);
+  if (ld_x < d_in) return fail(PRC_ESHAPE, "ld_x=%lld < d_in=%lld", (long long)ld_x, (long long)d_in);
+  if (ld_x % 8) return fail(PRC_EALIGN, "ld_x=%lld is not a multiple of 8 elements", (long long)ld_x);
+  if (n_proj < 1 || n_agents < 1) return fail(PRC_EINVAL, "n_proj=%d, n_agents=%d must be positive", n_proj, n_agents);
+  if (!rank_ok(rank)) return fail(PRC_EUNSUPPORTED, "rank=%d (built: 8, 16, 32, 64)", rank);
+  const int64_t n_cols = (int64_t)n_proj * n_agents * rank;
+  if (n_cols > 65535LL * 64) return fail(PRC_EINVAL, "n_proj*n_agents*rank=%lld too large", (long long)n_cols);
+  if (s_cap < 1) return fail(PRC_EINVAL, "s_cap=%lld must be positive", (long long)s_cap);
+  if (tok_offset < 0 || tok_offset + T > s_cap)
+    return fail(PRC_ESHAPE, "rows [%lld, %lld) fall outside s_cap=%lld", (long long)tok_offset,
+                (long long)(tok_offset + T), (long long)s_cap);
+  if (T == 0) return ok();
+  if (T > (int64_t)INT32_MAX * 64) return fail(PRC_EINVAL, "T too large");
+  if (X == nullptr || A_rows == nullptr || L_out == nullptr) return fail(PRC_EINVAL, "X/A_rows/L_out is NULL");
+  if (!aligned(X, 16) || !aligned(A_rows, 16) || !aligned(L_out, 16))
+    return fail(PRC_EALIGN, "X/A_rows/L_out must be 16-byte aligned");
+  prc::PrecomputeArgs a{};
+  a.X = X;
+  a.A = A_rows;
+  a.L = L_out;
+  a.T = T;
+  a.d_in = d_in;
+  a.ld_x = ld_x;
+  a.s_cap = s_cap;
+  a.tok_offset = tok_offset;
+  a.n_cols = (int32_t)n_cols;
+  a.rank = rank;
+  return launch_status(prc::launch_precompute(a, static_cast<hipStream_t>(stream)), "precompute_lr_cache");
+}
+
+PRC_API size_t lr_shared_attention_workspace_size(const lrsa_dims* dims) {
+  if (dims == nullptr || dims->n_tok != 1 || dims->batch < 1 || dims->n_kv_heads < 1 || dims->s_cap < 1)
+    return 0;
+  const int r = rank_ok(dims->rank) ? dims->rank : 8;
+  int n_splits = 0, split_tiles = 0;
+  prc::decode_plan(dims->s_cap, dims->batch, dims->n_kv_heads, &n_splits, &split_tiles);
+  return prc::decode_workspace_bytes(dims->batch, dims->n_q_heads, n_splits, dims->head_dim, r);
+}
+
+PRC_API prc_status lr_shared_attention(const lrsa_dims* dims, const uint16_t* Q, const uint16_t* K_base,
+                                       const uint16_t* V_base, const uint16_t* L_k, const uint16_t* L_v,
+                                       const uint16_t* B_k, const uint16_t* B_v, const int32_t* positions,
+                                       const int32_t* kv_len, uint16_t* O, float* lse, void* workspace,
+                                       size_t workspace_bytes, void* stream) {
+  Checked c;
+  prc_status s = check_attention(dims, Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len, true, &c);
+  if (s != PRC_OK || c.empty) return s;
+  if (O == nullptr) return fail(PRC_EINVAL, "O is NULL");
+  if (!aligned(O, 16)) return fail(PRC_EALIGN, "O is not 16-byte aligned");
+  if (lse != nullptr && !aligned(lse, 4)) return fail(PRC_EALIGN, "lse is not 4-byte aligned");
+  prc::AttnArgs& a = c.a;
+  a.O = O;
+  a.lse = lse;
+  // A rank outside the built set is only legal without LR; keep the size
+  // query and the launch on the same effective rank.
+  if (!rank_ok(dims->rank)) a.rank = 8;
+  else a.rank = dims->rank;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (dims->n_tok == 1) {
+    const size_t need = lr_shared_attention_workspace_size(dims);
+    if (workspace == nullptr || workspace_bytes < need)
+      return fail(PRC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace == nullptr ? 0 : workspace_bytes,
+                  need);
+    if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
+    prc::decode_plan(a.s_cap, a.batch, a.n_kv, &a.n_splits, &a.split_tiles);
+    a.ws = static_cast<float*>(workspace);
+    return launch_status(prc::launch_decode(a, st), "lr_shared_attention (decode)");
+  }
+  return launch_status(prc::launch_prefill(a, st), "lr_shared_attention (prefill)");
+}
+
+PRC_API prc_status materialize_agent_kv(const lrsa_dims* dims, const uint16_t* K_base, const uint16_t* V_base,
+                                        const uint16_t* L_k, const uint16_t* L_v, const uint16_t* B_k,
+                                        const uint16_t* B_v, const int32_t* kv_len, uint16_t* K_full,
+                                        uint16_t* V_full, void* stream) {
+  Checked c;
+  prc_status s = check_attention(dims, nullptr, K_base, V_base, L_k, L_v, B_k, B_v, nullptr, kv_len, false, &c);
+  if (s != PRC_OK || c.empty) return s;
+  if (K_full == nullptr || V_full == nullptr) return fail(PRC_EINVAL, "K_full/V_full is NULL");
+  if (!aligned(K_full, 16) || !aligned(V_full, 16)) return fail(PRC_EALIGN, "K_full/V_full not 16-byte aligned");
+  // Outputs must not overlap any input (each is [B, s_cap, n_kv, d]).
+  const uintptr_t bytes = (uintptr_t)dims->batch * dims->s_cap * dims->n_kv_heads * dims->head_dim * 2;
+  const uint16_t* ins[] = {K_base, V_base, L_k, L_v, B_k, B_v};
+  for (const uint16_t* o : {static_cast<const uint16_t*>(K_full), static_cast<const uint16_t*>(V_full)}) {
+    const uintptr_t o0 = reinterpret_cast<uintptr_t>(o), o1 = o0 + bytes;
+    for (const uint16_t* in : ins) {
+      if (in == nullptr) continue;
+      const uintptr_t i0 = reinterpret_cast<uintptr_t>(in);
+      if (i0 >= o0 && i0 < o1) return fail(PRC_EINVAL, "K_full/V_full overlap an input");
+    }
+  }
+  {
+    const uintptr_t k0 = reinterpret_cast<uintptr_t>(K_full), v0 = reinterpret_cast<uintptr_t>(V_full);
+    if ((k0 >= v0 && k0 < v0 + bytes) || (v0 >= k0 && v0 < k0 + bytes))
+      return fail(PRC_EINVAL, "K_full and V_full overlap");
+  }
+  c.a.Kout = K_full;
+  c.a.Vout = V_full;
+  return launch_status(prc::launch_materialize(c.a, static_cast<hipStream_t>(stream)), "materialize_agent_kv");
+}

@@ -1,0 +1,74 @@
+// Internal interface between the C ABI layer (abi.cpp) and the kernel files.
+// Everything here runs after host-side validation has passed.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace prc {
+
+constexpr int kMaxHalfDim = 64;  // head_dim <= 128
+
+// Arguments of one attention (or materialise) launch.  Strides are in
+// elements; `kv_stride` etc. may be 0 (all requests share one buffer).
+struct AttnArgs {
+  const uint16_t* Q;
+  const uint16_t* Kb;
+  const uint16_t* Vb;
+  const uint16_t* Lk;   // nullptr: key projection not adapted
+  const uint16_t* Lv;   // nullptr: value projection not adapted
+  const uint16_t* Bk;   // [n_kv*d, r] per request
+  const uint16_t* Bv;
+  const int32_t* positions;
+  const int32_t* kv_len;
+  uint16_t* O;
+  float* lse;
+  float* ws;            // decode split partials
+  uint16_t* Kout;       // materialise outputs
+  uint16_t* Vout;
+  int64_t s_cap;
+  int64_t kv_stride;
+  int64_t l_stride;
+  int64_t b_stride;
+  int32_t batch;
+  int32_t n_tok;
+  int32_t n_q;
+  int32_t n_kv;
+  int32_t group;        // n_q / n_kv
+  int32_t head_dim;
+  int32_t rank;
+  int32_t n_splits;     // decode: KV splits per request
+  int32_t split_tiles;  // decode: KV tiles per split
+  float scale_log2;     // softmax scale * log2(e)
+  double w2pi[kMaxHalfDim];  // RoPE omega_j / (2 pi), fp64
+};
+
+// Decode (one query token per request): split-KV partials + merge.
+int decode_tile_tokens();
+void decode_plan(int64_t s_cap, int batch, int n_kv, int* n_splits, int* split_tiles);
+size_t decode_workspace_bytes(int batch, int n_q, int n_splits, int head_dim, int rank);
+hipError_t launch_decode(const AttnArgs& a, hipStream_t stream);
+
+// Prefill (several query tokens per request): causal flash attention.
+hipError_t launch_prefill(const AttnArgs& a, hipStream_t stream);
+
+// Reference point: write the full per-agent K/V.
+hipError_t launch_materialize(const AttnArgs& a, hipStream_t stream);
+
+// LR-cache precompute GEMM.
+struct PrecomputeArgs {
+  const uint16_t* X;
+  const uint16_t* A;    // [n_cols, d_in]
+  uint16_t* L;          // [n_cols / r][s_cap][r]
+  int64_t T;
+  int64_t d_in;
+  int64_t ld_x;
+  int64_t s_cap;
+  int64_t tok_offset;
+  int32_t n_cols;
+  int32_t rank;
+};
+hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t stream);
+
+}  // namespace prc

@@ -1,0 +1,151 @@
+// On-chip rebuild of an agent's keys/values from the shared base cache and the
+// agent's LR cache (Eq. 1; App. D.2: the key-side term is expanded from rank r
+// and then rotated):
+//     K[t] = K_base[t] + RoPE(L_k[t] B_k, t),     V[t] = V_base[t] + L_v[t] B_v.
+//
+// Register layout shared by every kernel that rebuilds (decode, prefill,
+// materialise).  A wave handles 16 tokens of one KV head; lane l holds token
+// l%16 and, with q = l/16, the head dims
+//     [q*QPG, (q+1)*QPG)  and  [HALF + q*QPG, HALF + (q+1)*QPG),   QPG = d/8,
+// so both elements of every RoPE pair (j, j + d/2) sit in the same lane.
+// These dims are kept as D/32 "chunks" of 8 consecutive bf16 (u32x4):
+// chunk kk starts at chunk_dim(kk, q).
+//
+// The rank-r expansion is E^T = B^T L^T on 16x16x16 MFMAs, one per 16-dim
+// block.  Row m of block blk is head dim blk_dim(blk, m), which makes result
+// row 4q+i of block blk land on element (blk&1)*4+i of chunk blk>>1 -- the
+// chunk layout above.  Blocks blk < D/32 cover the low RoPE half and pair
+// with block blk + D/32.
+#pragma once
+
+#include "common.hpp"
+
+namespace prc {
+
+// Number of 16-wide rank chunks of the expansion (r = 8 pads to 16).
+constexpr int RCH(int r) { return r < 16 ? 1 : r / 16; }
+
+template <int D, int R>
+struct Rb {
+  static constexpr int HALF = D / 2;
+  static constexpr int NB = D / 32;    // 16-dim blocks per RoPE half
+  static constexpr int NBLK = D / 16;  // 16-dim blocks
+  static constexpr int NCH = D / 32;   // 8-dim chunks per lane
+  static constexpr int QPG = D / 8;    // dims per lane group per half
+  static constexpr int RC = R < 16 ? 1 : R / 16;  // 16-wide rank chunks
+};
+
+// First head dim of chunk kk for lane group q.
+template <int D>
+__device__ __forceinline__ int chunk_dim(int kk, int q) {
+  constexpr int HALF = D / 2, NB = D / 32, QPG = D / 8;
+  return ((2 * kk) / NB) * HALF + q * QPG + ((2 * kk) % NB) * 4;
+}
+
+// Head dim of row m in 16-dim block blk.
+template <int D>
+__device__ __forceinline__ int blk_dim(int blk, int m) {
+  constexpr int HALF = D / 2, NB = D / 32, QPG = D / 8;
+  return (blk / NB) * HALF + (m >> 2) * QPG + (blk % NB) * 4 + (m & 3);
+}
+
+// B^T fragments (A operand of the expansion) of one KV head.  `bhead` points
+// at the head's first row of an up-projection stored [n_kv*d, r].
+template <int D, int R>
+__device__ __forceinline__ void load_bt_frags(i16x4 (&f)[D / 16][RCH(R)], const uint16_t* bhead,
+                                              bool ok, int lane) {
+  const int c16 = lane & 15, q = lane >> 4;
+#pragma unroll
+  for (int blk = 0; blk < D / 16; ++blk) {
+    const int dim = blk_dim<D>(blk, c16);
+#pragma unroll
+    for (int rc = 0; rc < RCH(R); ++rc) {
+      const int r0 = rc * 16 + q * 4;
+      const bool v = ok && r0 < R;
+      f[blk][rc] = as_i16x4(ld8(v ? bhead + (int64_t)dim * R + r0 : nullptr, v));
+    }
+  }
+}
+
+// One LR row as the B operand of the expansion (k = rank index).
+template <int R>
+__device__ __forceinline__ void load_lr_frag(u32x2 (&l)[RCH(R)], const uint16_t* lrow, bool ok,
+                                             int lane) {
+  const int q = lane >> 4;
+#pragma unroll
+  for (int rc = 0; rc < RCH(R); ++rc) {
+    const int r0 = rc * 16 + q * 4;
+    const bool v = ok && r0 < R;
+    l[rc] = ld8(v ? lrow + r0 : nullptr, v);
+  }
+}
+
+// Base row of this lane's token in chunk layout.
+template <int D>
+__device__ __forceinline__ void load_chunks(u32x4 (&x)[D / 32], const uint16_t* head_row, bool ok, int lane) {
+  const int q = lane >> 4;
+#pragma unroll
+  for (int kk = 0; kk < D / 32; ++kk) x[kk] = ld16(head_row + chunk_dim<D>(kk, q), ok);
+}
+
+template <int D>
+__device__ __forceinline__ void store_chunks(uint16_t* head_row, const u32x4 (&x)[D / 32], int lane) {
+  const int q = lane >> 4;
+#pragma unroll
+  for (int kk = 0; kk < D / 32; ++kk) *reinterpret_cast<u32x4*>(head_row + chunk_dim<D>(kk, q)) = x[kk];
+}
+
+__device__ __forceinline__ float chunk_get(const u32x4& c, int el) {
+  const uint32_t u = c[el >> 1];
+  return (el & 1) ? bf_hi(u) : bf_lo(u);
+}
+
+// x += L B (value side), rounded back to bf16.
+template <int D, int R>
+__device__ __forceinline__ void add_expansion(u32x4 (&x)[D / 32], const i16x4 (&bf)[D / 16][RCH(R)],
+                                              const u32x2 (&l)[RCH(R)]) {
+#pragma unroll
+  for (int blk = 0; blk < D / 16; ++blk) {
+    f32x4 e = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int rc = 0; rc < RCH(R); ++rc) e = mfma16x16x16(bf[blk][rc], as_i16x4(l[rc]), e);
+    const int kk = blk >> 1, w0 = (blk & 1) * 2;
+    float v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = chunk_get(x[kk], (blk & 1) * 4 + i) + e[i];
+    x[kk][w0] = pack_bf16(v[0], v[1]);
+    x[kk][w0 + 1] = pack_bf16(v[2], v[3]);
+  }
+}
+
+// x += RoPE(L B) (key side), rounded back to bf16.  c[blk][i], s[blk][i] are
+// cos/sin of the token's angle at frequency q*QPG + blk*4 + i.
+template <int D, int R>
+__device__ __forceinline__ void add_rotated_expansion(u32x4 (&x)[D / 32], const i16x4 (&bf)[D / 16][RCH(R)],
+                                                      const u32x2 (&l)[RCH(R)],
+                                                      const float (&c)[D / 32][4], const float (&s)[D / 32][4]) {
+  constexpr int NB = D / 32;
+#pragma unroll
+  for (int blk = 0; blk < NB; ++blk) {
+    f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int rc = 0; rc < RCH(R); ++rc) {
+      elo = mfma16x16x16(bf[blk][rc], as_i16x4(l[rc]), elo);
+      ehi = mfma16x16x16(bf[blk + NB][rc], as_i16x4(l[rc]), ehi);
+    }
+    const int klo = blk >> 1, khi = (blk + NB) >> 1, w0 = (blk & 1) * 2;
+    float vlo[4], vhi[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int el = (blk & 1) * 4 + i;
+      vlo[i] = chunk_get(x[klo], el) + elo[i] * c[blk][i] - ehi[i] * s[blk][i];
+      vhi[i] = chunk_get(x[khi], el) + ehi[i] * c[blk][i] + elo[i] * s[blk][i];
+    }
+    x[klo][w0] = pack_bf16(vlo[0], vlo[1]);
+    x[klo][w0 + 1] = pack_bf16(vlo[2], vlo[3]);
+    x[khi][w0] = pack_bf16(vhi[0], vhi[1]);
+    x[khi][w0 + 1] = pack_bf16(vhi[2], vhi[3]);
+  }
+}
+
+}  // namespace prc
