@@ -1,0 +1,270 @@
+"""GPU parity of every entry point against the fp64 oracle, at sizes the oracle
+finishes in seconds (several tiles, ragged tails, GQA groups 1/4/5/8, ranks
+8-64, head dims 64/128, every LR wiring), plus edge cases."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_34054_amd as prc
+from gpu_cases import (ATOL_MAX, ATOL_MEAN, LR_SENS, LSE_ATOL, PRE_REL, attn_errors, b_paper, f64,
+                       gpu_attention, lse_error, oracle_attention, to_dev)
+from workload import CONFIGS, Config, attention_case, precompute_case
+from workload.gen import normal_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def mk_cfg(idx, n_q, n_kv, d, r, theta=1e4, hidden=256, n_agents=1):
+    return Config(idx, "parity", hidden=hidden, n_q=n_q, n_kv=n_kv, head_dim=d, theta=theta,
+                  n_agents=n_agents, rank=r, context=0, prefill_tokens=0, decode_batch=0, precompute_rows=0)
+
+
+# ----------------------------------------------------------------- precompute
+PRE_CASES = [
+    # id, T, d_in, n_proj, N, r, tok_offset, s_cap
+    ("tiny_c1", 528, 256, 2, 3, 8, 0, 528),
+    ("ragged_tail", 77, 264, 2, 2, 16, 5, 100),
+    ("r32_single_proj", 130, 512, 1, 5, 32, 3, 200),
+    ("r64", 64, 128, 2, 1, 64, 0, 64),
+    ("one_row", 1, 4096, 2, 8, 16, 31, 32),
+    ("c2_chunk", 512, 4096, 2, 4, 16, 8192, 8704),
+    ("c3_segment", 4096, 4096, 2, 8, 16, 32768, 36864),
+    ("c4_chunk", 2048, 5120, 2, 6, 64, 0, 2048),
+]
+
+
+@pytest.mark.parametrize("cid,T,d_in,n_proj,N,r,off,s_cap", PRE_CASES, ids=[c[0] for c in PRE_CASES])
+def test_precompute(cid, T, d_in, n_proj, N, r, off, s_cap):
+    print(f"precompute {cid}", flush=True)
+    cfg = mk_cfg(7, 4, 4, 64, r, hidden=d_in, n_agents=N)
+    cfg = Config(**{**cfg.__dict__, "n_proj": n_proj})
+    pc = precompute_case(cfg, T, seed_base=T)
+    sentinel = 3.0
+    L = torch.full((n_proj, N, s_cap, r), sentinel, dtype=torch.bfloat16, device="cuda")
+    prc.precompute_lr_cache(pc["X"].cuda(), pc["A_rows"].cuda(), n_proj, N, r, L, tok_offset=off)
+    torch.cuda.synchronize()
+    ref = oracle.precompute_lr_cache(f64(pc["X"]), f64(pc["A_rows"]).T, n_proj, N, r)
+    got = f64(L)
+    rel = np.linalg.norm(got[:, :, off:off + T] - ref) / np.linalg.norm(ref)
+    assert rel <= PRE_REL, rel
+    # Rows outside the segment are untouched.
+    assert (got[:, :, :off] == sentinel).all() and (got[:, :, off + T:] == sentinel).all()
+
+
+def test_precompute_strided_rows():
+    """X rows with a row stride larger than d_in (a view into a wider buffer)."""
+    cfg = mk_cfg(8, 4, 4, 64, 16, hidden=256, n_agents=2)
+    pc = precompute_case(cfg, 100)
+    wide = torch.zeros(100, 384, dtype=torch.bfloat16)
+    wide[:, :256] = pc["X"]
+    L = torch.zeros((2, 2, 100, 16), dtype=torch.bfloat16, device="cuda")
+    prc.precompute_lr_cache(wide.cuda()[:, :256], pc["A_rows"].cuda(), 2, 2, 16, L)
+    torch.cuda.synchronize()
+    ref = oracle.precompute_lr_cache(f64(pc["X"]), f64(pc["A_rows"]).T, 2, 2, 16)
+    assert np.linalg.norm(f64(L) - ref) / np.linalg.norm(ref) <= PRE_REL
+
+
+# ------------------------------------------------------------------ attention
+# id, d, r, n_q, n_kv, n_tok, kv_lens, s_cap, lr ("kv"|"v"|"k"|"none"), q_std, pos ("end"|"mid")
+ATTN_CASES = [
+    ("c1_prefill", 64, 8, 4, 4, 16, [528], 544, "kv", 1.0, "end"),
+    ("c1_decode", 64, 8, 4, 4, 1, [528], 544, "kv", 1.0, "end"),
+    ("g4_r16_prefill_ragged", 128, 16, 8, 2, 70, [300, 233], 320, "kv", 1.0, "end"),
+    ("g4_r16_decode_ragged", 128, 16, 8, 2, 1, [1000, 77, 1], 1024, "kv", 1.0, "end"),
+    ("g4_r16_decode_long", 128, 16, 8, 2, 1, [5000], 5000, "kv", 1.0, "end"),
+    ("g5_r64_prefill", 128, 64, 10, 2, 37, [200, 150], 256, "kv", 1.0, "end"),
+    ("g5_r64_decode", 128, 64, 10, 2, 1, [700, 64], 704, "kv", 1.0, "end"),
+    ("g8_r32_prefill", 128, 32, 16, 2, 20, [150], 160, "kv", 1.0, "end"),
+    ("g8_r32_decode", 128, 32, 16, 2, 1, [333], 340, "kv", 1.0, "end"),
+    ("g1_d64_r16_prefill_2tiles", 64, 16, 4, 4, 130, [400], 400, "kv", 1.0, "end"),
+    ("g1_d128_r8_decode", 128, 8, 2, 2, 1, [129], 136, "kv", 1.0, "end"),
+    ("d64_g4_r32_prefill", 64, 32, 8, 2, 33, [97], 104, "kv", 1.0, "end"),
+    ("qv_prefill", 128, 16, 8, 2, 40, [256], 256, "v", 1.0, "end"),
+    ("qv_decode", 128, 16, 8, 2, 1, [512, 300], 512, "v", 1.0, "end"),
+    ("k_only_prefill", 128, 16, 8, 2, 24, [128], 136, "k", 1.0, "end"),
+    ("k_only_decode", 64, 8, 4, 2, 1, [90], 96, "k", 1.0, "end"),
+    ("plain_prefill", 128, 16, 8, 2, 50, [300], 304, "none", 1.0, "end"),
+    ("plain_decode", 128, 16, 8, 2, 1, [2000, 1], 2000, "none", 1.0, "end"),
+    # Sharper softmax (q std 2): the sharpest setting at which bf16 storage of
+    # the agent's rebuilt keys -- what any bf16 KV cache, the materialised
+    # reference included, holds -- stays inside the gate with margin.
+    ("sharp_prefill", 128, 16, 8, 2, 64, [512], 512, "kv", 2.0, "end"),
+    ("sharp_prefill_long", 128, 16, 8, 2, 16, [4096], 4096, "kv", 2.0, "end"),
+    ("sharp_decode", 128, 16, 8, 2, 1, [3000, 2999], 3008, "kv", 2.0, "end"),
+    ("mid_positions_prefill", 128, 16, 8, 2, 12, [300], 304, "kv", 1.0, "mid"),
+    ("mid_positions_decode", 128, 16, 8, 2, 1, [300, 500], 512, "kv", 1.0, "mid"),
+    ("many_requests_decode", 64, 16, 8, 8, 1, [64, 65, 63, 1, 17, 200, 31, 128], 256, "kv", 1.0, "end"),
+]
+
+
+def _positions(kv_lens, n_tok, mode):
+    pos = []
+    for kl in kv_lens:
+        end = kl if mode == "end" else max(n_tok, kl // 2)
+        pos.append(list(range(end - n_tok, end)))
+    return pos
+
+
+def _case(cid, d, r, n_q, n_kv, n_tok, kv_lens, s_cap, lr, q_std, pos_mode, seed=0):
+    cfg = mk_cfg(10 + len(cid), n_q, n_kv, d, r)
+    return cfg, attention_case(cfg, batch=len(kv_lens), n_tok=n_tok, kv_len=kv_lens,
+                               positions=_positions(kv_lens, n_tok, pos_mode), s_cap=s_cap,
+                               seed_base=seed + 100 * len(cid), lr_k=lr in ("kv", "k"), lr_v=lr in ("kv", "v"),
+                               q_std=q_std)
+
+
+@pytest.mark.parametrize("case", ATTN_CASES, ids=[c[0] for c in ATTN_CASES])
+def test_attention(case):
+    print(f"attention {case[0]}", flush=True)
+    cfg, c = _case(*case)
+    O, lse = gpu_attention(to_dev(c), cfg.theta)
+    Oref, lref = oracle_attention(c, cfg.theta)
+    mx, mean = attn_errors(O, Oref)
+    assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (mx, mean)
+    assert lse_error(lse, lref) <= LSE_ATOL
+
+
+@pytest.mark.parametrize("cid", ["c1_prefill", "g4_r16_decode_ragged", "g5_r64_prefill", "sharp_decode"])
+def test_lr_sensitivity(cid):
+    """The LR term's contribution, O - O(B=0), is reproduced (a kernel that drops
+    or mis-rotates the LR term fails this even when O itself is small)."""
+    case = next(c for c in ATTN_CASES if c[0] == cid)
+    cfg, c = _case(*case)
+    g = to_dev(c)
+    O, _ = gpu_attention(g, cfg.theta)
+    z = dict(g)
+    z["Bk_rows"] = torch.zeros_like(g["Bk_rows"])
+    z["Bv_rows"] = torch.zeros_like(g["Bv_rows"])
+    O0, _ = gpu_attention(z, cfg.theta)
+    Oref, _ = oracle_attention(c, cfg.theta)
+    O0ref, _ = oracle_attention(c, cfg.theta, zero_b=True)
+    dg, dr = f64(O) - f64(O0), Oref - O0ref
+    rel = np.linalg.norm(dg - dr) / np.linalg.norm(dr)
+    assert rel <= LR_SENS, rel
+
+
+def test_absent_lr_equals_zero_up_projection():
+    cfg, c = _case("qv_decode", 128, 16, 8, 2, 1, [512, 300], 512, "kv", 1.0, "end")
+    g = to_dev(c)
+    for n_tok in (1,):
+        zk = dict(g, Bk_rows=torch.zeros_like(g["Bk_rows"]))
+        nk = dict(g, L_k=None, Bk_rows=None)
+        Oz, lz = gpu_attention(zk, cfg.theta)
+        On, ln = gpu_attention(nk, cfg.theta)
+        assert torch.equal(Oz, On) and torch.equal(lz, ln)
+
+
+def test_deterministic():
+    for case in (ATTN_CASES[2], ATTN_CASES[4]):
+        cfg, c = _case(*case)
+        g = to_dev(c)
+        O1, l1 = gpu_attention(g, cfg.theta)
+        O2, l2 = gpu_attention(g, cfg.theta)
+        assert torch.equal(O1, O2) and torch.equal(l1, l2)
+
+
+def test_rows_without_visible_keys():
+    """kv_len = 0 or a position before the first key: O = 0, lse = -inf."""
+    cfg = mk_cfg(40, 8, 2, 128, 16)
+    for n_tok in (1, 3):
+        c = attention_case(cfg, batch=2, n_tok=n_tok, kv_len=[0, 50], positions=[[5] * n_tok, [-1] * n_tok],
+                           s_cap=64, poison_tail=False)
+        O, lse = gpu_attention(to_dev(c), cfg.theta)
+        assert (f64(O) == 0).all()
+        assert np.isneginf(f64(lse)).all()
+
+
+def test_shared_buffers_across_requests():
+    """Stride-0 base cache, LR plane and up-projection shared by every request."""
+    cfg = mk_cfg(41, 8, 2, 128, 16)
+    c = attention_case(cfg, batch=1, n_tok=1, kv_len=[400], positions=[[399]], s_cap=400)
+    g = to_dev(c)
+    B = 3
+    Q = normal_bf16((B, 1, 8, 128), 1.0, 4242).cuda()
+    pos = torch.tensor([[399], [250], [10]], dtype=torch.int32, device="cuda")
+    kvl = torch.tensor([400, 251, 11], dtype=torch.int32, device="cuda")
+    O, _ = prc.lr_shared_attention(Q, g["K_base"], g["V_base"], g["L_k"], g["L_v"], g["Bk_rows"], g["Bv_rows"],
+                                   pos, kvl, rope_theta=cfg.theta)
+    torch.cuda.synchronize()
+    for b in range(B):
+        n = int(kvl[b])
+        Oref, _ = oracle.lr_shared_attention(f64(Q[b:b + 1]), f64(c["K_base"])[:, :n], f64(c["V_base"])[:, :n],
+                                             f64(c["L_k"])[:, :n], f64(c["L_v"])[:, :n], b_paper(c["Bk_rows"]),
+                                             b_paper(c["Bv_rows"]), pos[b:b + 1].cpu().numpy(), [n], cfg.theta)
+        mx, mean = attn_errors(O[b:b + 1], Oref)
+        assert mx <= ATOL_MAX and mean <= ATOL_MEAN
+
+
+def test_custom_softmax_scale():
+    cfg, c = _case("plain_prefill", 128, 16, 8, 2, 9, [100], 104, "kv", 1.0, "end")
+    O, _ = gpu_attention(to_dev(c), cfg.theta, softmax_scale=0.05)
+    Q = f64(c["Q"])
+    Ks, Vs = oracle.materialize_agent_kv(f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]), f64(c["L_v"]),
+                                         b_paper(c["Bk_rows"]), b_paper(c["Bv_rows"]), [100], cfg.theta)
+    Oref, _ = oracle.attention(Q[0], Ks[0], Vs[0], c["positions"].numpy()[0], 100, scale=0.05)
+    mx, mean = attn_errors(O[0], Oref)
+    assert mx <= ATOL_MAX and mean <= ATOL_MEAN
+
+
+# ---------------------------------------------------------------- materialise
+@pytest.mark.parametrize("cid", ["c1_prefill", "g5_r64_decode", "qv_decode", "k_only_decode"])
+def test_materialize(cid):
+    case = next(c for c in ATTN_CASES if c[0] == cid)
+    cfg, c = _case(*case)
+    g = to_dev(c)
+    Kf, Vf = prc.materialize_agent_kv(g["K_base"], g["V_base"], g["L_k"], g["L_v"], g["Bk_rows"], g["Bv_rows"],
+                                      g["kv_len"], rope_theta=cfg.theta)
+    torch.cuda.synchronize()
+    Ks, Vs = oracle.materialize_agent_kv(f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]), f64(c["L_v"]),
+                                         b_paper(c["Bk_rows"]), b_paper(c["Bv_rows"]), c["kv_len"].numpy(),
+                                         cfg.theta)
+    for b, n in enumerate(c["kv_len"].tolist()):
+        for got, ref in ((f64(Kf)[b, :n], Ks[b]), (f64(Vf)[b, :n], Vs[b])):
+            # One bf16 rounding of the rebuilt value: |err| <= 2^-8 |x| (+ fp32 slack).
+            assert (np.abs(got - ref) <= np.abs(ref) * 2.0 ** -8 + 1e-3).all()
+    # Materialise-then-attend matches the oracle too, and the fused path.
+    O_m, _ = prc.lr_shared_attention(g["Q"], Kf, Vf, None, None, None, None, g["positions"], g["kv_len"],
+                                     rope_theta=cfg.theta)
+    O_f, _ = gpu_attention(g, cfg.theta)
+    Oref, _ = oracle_attention(c, cfg.theta)
+    mx, mean = attn_errors(O_m, Oref)
+    assert mx <= ATOL_MAX and mean <= ATOL_MEAN
+    assert (f64(O_m) - f64(O_f)).__abs__().max() <= ATOL_MAX
+
+
+# ------------------------------------------------- the tiny workload, end to end
+def test_tiny_workload_full_chain():
+    """Hidden states -> frozen projections (oracle) -> LR precompute (GPU) ->
+    LR-shared attention (GPU) for every agent, against the all-fp64 chain:
+    this is Eq. 1 checked end to end on the GPU."""
+    cfg = CONFIGS[1]
+    from workload import lora_case
+    S = cfg.context + cfg.prefill_tokens
+    lc = lora_case(cfg, S)
+    X, N, r, d = f64(lc["X"]), cfg.n_agents, cfg.rank, cfg.head_dim
+    t = np.arange(S)
+    Kb = oracle.rope((X @ f64(lc["W_k"])).reshape(S, cfg.n_kv, d), t[:, None], cfg.theta)
+    Vb = (X @ f64(lc["W_v"])).reshape(S, cfg.n_kv, d)
+    Q_all = oracle.rope((X @ f64(lc["W_q"])).reshape(S, cfg.n_q, d), t[:, None], cfg.theta)
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(torch.bfloat16)
+    Kb_t, Vb_t, Q_t = bf(Kb)[None], bf(Vb)[None], bf(Q_all)
+    L = torch.zeros((2, N, S, r), dtype=torch.bfloat16, device="cuda")
+    prc.precompute_lr_cache(lc["X"].cuda(), lc["A_rows"].cuda(), 2, N, r, L)
+    L_or = oracle.precompute_lr_cache(X, f64(lc["A_rows"]).T, 2, N, r)
+    for n_tok in (cfg.prefill_tokens, 1):
+        q_t = Q_t[S - n_tok:][None]
+        pos = torch.arange(S - n_tok, S, dtype=torch.int32)[None]
+        kvl = torch.tensor([S], dtype=torch.int32)
+        for a in range(N):
+            O, _ = prc.lr_shared_attention(q_t.cuda(), Kb_t.cuda(), Vb_t.cuda(), L[0, a][None], L[1, a][None],
+                                           lc["Bk_rows"][a][None].cuda(), lc["Bv_rows"][a][None].cuda(),
+                                           pos.cuda(), kvl.cuda(), rope_theta=cfg.theta)
+            torch.cuda.synchronize()
+            Oref, _ = oracle.lr_shared_attention(f64(q_t), f64(Kb_t), f64(Vb_t), L_or[0, a][None], L_or[1, a][None],
+                                                 b_paper(lc["Bk_rows"][a][None]), b_paper(lc["Bv_rows"][a][None]),
+                                                 pos.numpy(), kvl.numpy(), cfg.theta)
+            mx, mean = attn_errors(O, Oref)
+            assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (n_tok, a, mx, mean)
