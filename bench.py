@@ -1,0 +1,383 @@
+"""Benchmark of the PreLRShared hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input at
+the 32k-context, 8B-shaped layer (hidden 4096, 32 q / 8 KV heads, head dim 128,
+8 agents, LoRA rank 16 on k and v):
+  1. LR-cache precompute of a new 4096-token segment for all 8 agents
+     (X[4096x4096] . A_stack[4096x256] -> 16 LR planes);
+  2. prefill of that segment: 4096 queries at positions 32768..36863 over the
+     shared base cache plus the agent's LR cache (kv_len 36864);
+  3. decode of 16 concurrent agent requests, each with its own 32768-token base
+     cache, LR cache and up-projections.
+Inputs are resident in HBM before the timed region.  Each stage is timed with
+HIP events on the stream the kernels run on.
+
+The reported value is decode HBM throughput (algorithmic bytes / decode time);
+prefill and precompute throughput (algorithmic flop / time) sit beside it, with
+a roofline per stage.  The materialise-then-attend reference (write each
+request's full per-agent K/V, then run plain attention) is timed on the same
+inputs.  The fp64 oracle is timed on a bounded sample of the same workload on
+the host cores (rank 0, N = 1 only).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "LR-shared attention decode HBM GB/s + prefill TFLOP/s at 32k ctx, 1 GPU"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+
+
+# --------------------------------------------------------------- the workload
+def workload_dims():
+    from workload import CONFIGS
+    cfg = CONFIGS[3]
+    S = cfg.context
+    return cfg, dict(
+        S=S, seg=cfg.precompute_rows, n_pre=cfg.prefill_tokens, B=cfg.decode_batch,
+        hidden=cfg.hidden, n_q=cfg.n_q, n_kv=cfg.n_kv, d=cfg.head_dim, r=cfg.rank, N=cfg.n_agents,
+        theta=cfg.theta)
+
+
+def algorithmic_work(w):
+    """Bytes and flops the method must move/do (each counted once)."""
+    S, d, n_q, n_kv, r, B = w["S"], w["d"], w["n_q"], w["n_kv"], w["r"], w["B"]
+    # Decode: read each request's base K and V and its agent's L_k, L_v rows
+    # once, plus Q, B_k, B_v, and write O.
+    dec_bytes_req = (S * n_kv * d * 2 * 2 + S * r * 2 * 2 + n_q * d * 2 + 2 * n_kv * d * r * 2 + n_q * d * 2)
+    dec_flops_req = (4 * n_q * d * S            # Q K^T and P V
+                     + 2 * r * d * n_kv * S     # key-side expansion L_k B_k
+                     + 2 * n_q * r * S          # P L_v
+                     + 2 * n_q * r * d)         # (P L_v) B_v
+    # Prefill: 4096 queries at positions S..S+n-1, causal.
+    n = w["n_pre"]
+    kv = S + n
+    vis = sum(S + i + 1 for i in range(n))
+    pre_flops = 4 * n_q * d * vis + 2 * 2 * r * d * n_kv * kv
+    pre_bytes = kv * n_kv * d * 2 * 2 + kv * r * 2 * 2 + 2 * n * n_q * d * 2 + 2 * n_kv * d * r * 2
+    # Precompute: X[seg x hidden] . A[hidden x 2Nr].
+    cols = 2 * w["N"] * r
+    pc_flops = 2 * w["seg"] * w["hidden"] * cols
+    pc_bytes = (w["seg"] * w["hidden"] + cols * w["hidden"] + w["seg"] * cols) * 2
+    return dict(decode_bytes=B * dec_bytes_req, decode_flops=B * dec_flops_req, decode_bytes_per_request=dec_bytes_req,
+                prefill_flops=pre_flops, prefill_bytes=pre_bytes, precompute_flops=pc_flops,
+                precompute_bytes=pc_bytes)
+
+
+def make_inputs(w, dev, seed=3000):
+    """Seeded synthetic inputs, generated directly in HBM."""
+    import torch
+    g = torch.Generator(device=dev).manual_seed(seed)
+
+    def nrm(shape, std=1.0):
+        x = torch.randn(*shape, generator=g, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            x.mul_(std)
+        return x.to(torch.bfloat16)
+
+    S, d, n_q, n_kv, r, B, N = w["S"], w["d"], w["n_q"], w["n_kv"], w["r"], w["B"], w["N"]
+    bstd = math.sqrt(0.02)
+    kv_pre = S + w["n_pre"]
+    x = {}
+    # Precompute: 4 rotating segment buffers so every step reads X from HBM.
+    x["X"] = [nrm((w["seg"], w["hidden"])) for _ in range(4)]
+    x["A_rows"] = nrm((2 * N * r, w["hidden"]), 1.0 / math.sqrt(w["hidden"]))
+    x["L_planes"] = torch.zeros((2, N, kv_pre, r), dtype=torch.bfloat16, device=dev)
+    # Prefill: one request (agent 0) over the shared trajectory.
+    x["pre"] = dict(
+        Q=nrm((1, w["n_pre"], n_q, d)), K_base=nrm((1, kv_pre, n_kv, d)), V_base=nrm((1, kv_pre, n_kv, d)),
+        L_k=nrm((1, kv_pre, r)), L_v=nrm((1, kv_pre, r)),
+        Bk_rows=nrm((1, n_kv * d, r), bstd), Bv_rows=nrm((1, n_kv * d, r), bstd),
+        positions=torch.arange(S, kv_pre, dtype=torch.int32, device=dev)[None],
+        kv_len=torch.tensor([kv_pre], dtype=torch.int32, device=dev))
+    # Decode: 16 requests, each its own base cache, LR plane (agent b mod N)
+    # and up-projections.
+    x["dec"] = dict(
+        Q=nrm((B, 1, n_q, d)), K_base=nrm((B, S, n_kv, d)), V_base=nrm((B, S, n_kv, d)),
+        L_k=nrm((B, S, r)), L_v=nrm((B, S, r)),
+        Bk_rows=nrm((B, n_kv * d, r), bstd), Bv_rows=nrm((B, n_kv * d, r), bstd),
+        positions=torch.full((B, 1), S - 1, dtype=torch.int32, device=dev),
+        kv_len=torch.full((B,), S, dtype=torch.int32, device=dev))
+    return x
+
+
+# ------------------------------------------------------------ GPU timing loop
+def attn(prc, c, theta, O, ws):
+    return prc.lr_shared_attention(c["Q"], c["K_base"], c["V_base"], c["L_k"], c["L_v"], c["Bk_rows"],
+                                   c["Bv_rows"], c["positions"], c["kv_len"], rope_theta=theta, O=O,
+                                   workspace=ws)
+
+
+def run_fused(prc, x, w, steps, warmup):
+    import torch
+    theta = w["theta"]
+    O_pre = torch.empty_like(x["pre"]["Q"])
+    O_dec = torch.empty_like(x["dec"]["Q"])
+    dims = prc.make_dims(x["dec"]["Q"], x["dec"]["K_base"], x["dec"]["L_k"], x["dec"]["L_v"], x["dec"]["Bk_rows"],
+                         x["dec"]["Bv_rows"], theta)
+    ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=O_dec.device)
+
+    def step(i, ev=None):
+        if ev is not None:
+            ev[0].record()
+        prc.precompute_lr_cache(x["X"][i % 4], x["A_rows"], 2, w["N"], w["r"], x["L_planes"], tok_offset=w["S"])
+        if ev is not None:
+            ev[1].record()
+        attn(prc, x["pre"], theta, O_pre, None)
+        if ev is not None:
+            ev[2].record()
+        attn(prc, x["dec"], theta, O_dec, ws)
+        if ev is not None:
+            ev[3].record()
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    stage = {"precompute": 0.0, "prefill": 0.0, "decode": 0.0}
+    for e in evs:
+        stage["precompute"] += e[0].elapsed_time(e[1])
+        stage["prefill"] += e[1].elapsed_time(e[2])
+        stage["decode"] += e[2].elapsed_time(e[3])
+    total = sum(evs[i][0].elapsed_time(evs[i][3]) for i in range(steps))
+    return {k: v / steps for k, v in stage.items()}, total / steps, wall / steps * 1e3
+
+
+def run_materialized(prc, x, w, steps, warmup):
+    """Reference point: materialise each request's full K/V, then attend."""
+    import torch
+    theta = w["theta"]
+    p, dcs = x["pre"], x["dec"]
+    Kp = torch.empty_like(p["K_base"]); Vp = torch.empty_like(p["V_base"])
+    Kd = torch.empty_like(dcs["K_base"]); Vd = torch.empty_like(dcs["V_base"])
+    O_pre = torch.empty_like(p["Q"]); O_dec = torch.empty_like(dcs["Q"])
+    plain_pre = dict(p, K_base=Kp, V_base=Vp, L_k=None, L_v=None, Bk_rows=None, Bv_rows=None)
+    plain_dec = dict(dcs, K_base=Kd, V_base=Vd, L_k=None, L_v=None, Bk_rows=None, Bv_rows=None)
+    dims = prc.make_dims(dcs["Q"], Kd, None, None, None, None, theta)
+    ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=O_dec.device)
+
+    def step(i, ev=None):
+        if ev is not None:
+            ev[0].record()
+        prc.precompute_lr_cache(x["X"][i % 4], x["A_rows"], 2, w["N"], w["r"], x["L_planes"], tok_offset=w["S"])
+        if ev is not None:
+            ev[1].record()
+        prc.materialize_agent_kv(p["K_base"], p["V_base"], p["L_k"], p["L_v"], p["Bk_rows"], p["Bv_rows"],
+                                 p["kv_len"], rope_theta=theta, K_full=Kp, V_full=Vp)
+        attn(prc, plain_pre, theta, O_pre, None)
+        if ev is not None:
+            ev[2].record()
+        prc.materialize_agent_kv(dcs["K_base"], dcs["V_base"], dcs["L_k"], dcs["L_v"], dcs["Bk_rows"],
+                                 dcs["Bv_rows"], dcs["kv_len"], rope_theta=theta, K_full=Kd, V_full=Vd)
+        attn(prc, plain_dec, theta, O_dec, ws)
+        if ev is not None:
+            ev[3].record()
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+    for i in range(steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    stage = {"precompute": 0.0, "prefill": 0.0, "decode": 0.0}
+    for e in evs:
+        stage["precompute"] += e[0].elapsed_time(e[1])
+        stage["prefill"] += e[1].elapsed_time(e[2])
+        stage["decode"] += e[2].elapsed_time(e[3])
+    return {k: v / steps for k, v in stage.items()}
+
+
+# ------------------------------------------------------------- CPU baseline
+def cpu_baseline(w, budget_s=20.0):
+    """Time the fp64 oracle on a bounded sample of the same workload.
+
+    Sample: decode of whole requests (all 32 q heads, full 32768-token context)
+    until about half the budget is spent, then prefill of query tokens (all
+    heads, over their full causal range) for the rest.  Reported in the
+    metric's unit (GB/s of the decode's algorithmic bytes), with the prefill
+    rate in TFLOP/s beside it.
+    """
+    import numpy as np
+    import oracle
+    from workload import attention_case
+    cfg, _ = workload_dims()
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    f64 = lambda t: None if t is None else t.double().numpy()
+    tr = lambda t: None if t is None else np.swapaxes(f64(t), -1, -2)
+    S, work = w["S"], algorithmic_work(w)
+    dec_t, dec_n = 0.0, 0
+    while dec_t < budget_s / 2 and dec_n < w["B"]:
+        c = attention_case(cfg, batch=1, n_tok=1, kv_len=[S], positions=[[S - 1]], s_cap=S,
+                           seed_base=50_000 + dec_n, poison_tail=False)
+        t0 = time.perf_counter()
+        oracle.lr_shared_attention(f64(c["Q"]), f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]),
+                                   f64(c["L_v"]), tr(c["Bk_rows"]), tr(c["Bv_rows"]), c["positions"].numpy(),
+                                   c["kv_len"].numpy(), cfg.theta)
+        dec_t += time.perf_counter() - t0
+        dec_n += 1
+    # Prefill sample: n_s query tokens at the end of the segment.
+    n_s = 32
+    kv = S + w["n_pre"]
+    pos = list(range(kv - n_s, kv))
+    c = attention_case(cfg, batch=1, n_tok=n_s, kv_len=[kv], positions=[pos], s_cap=kv, seed_base=60_000,
+                       poison_tail=False)
+    t0 = time.perf_counter()
+    oracle.lr_shared_attention(f64(c["Q"]), f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]), f64(c["L_v"]),
+                               tr(c["Bk_rows"]), tr(c["Bv_rows"]), c["positions"].numpy(), c["kv_len"].numpy(),
+                               cfg.theta)
+    pre_t = time.perf_counter() - t0
+    pre_flops = 4 * w["n_q"] * w["d"] * sum(p + 1 for p in pos)
+    return {
+        "value": round(dec_n * work["decode_bytes_per_request"] / dec_t / 1e9, 4),
+        "unit": "GB/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"decode of {dec_n} of {w['B']} requests (32 q heads, {S}-token context) in {dec_t:.1f} s; "
+                   f"prefill of the last {n_s} of {w['n_pre']} queries (over {kv} keys) in {pre_t:.1f} s"),
+        "prefill_tflops": round(pre_flops / pre_t / 1e12, 6),
+        "host_cpus": os.cpu_count(),
+    }
+
+
+def source_digest(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2609_34054_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kernel_file, launches_per_stage=1):
+    """HBM bytes per launch from the committed counter summary, if it was taken
+    on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path)).get(kernel_file)
+    except Exception:
+        return None
+    if not rec or rec.get("source_digest") != source_digest(kernel_file, "common.hpp", "rebuild.hpp"):
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-materialize", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the multi-GPU sharding of the path is described in DESIGN.md).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_34054_amd as prc
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    prc.lib()
+    dev = torch.device("cuda:0")
+    cfg, w = workload_dims()
+    work = algorithmic_work(w)
+    print(f"bench: generating inputs ({w['B']} x {w['S']}-token decode caches)", file=sys.stderr, flush=True)
+    x = make_inputs(w, dev)
+    torch.cuda.synchronize()
+    print("bench: timing fused path", file=sys.stderr, flush=True)
+    stage, ms_step, wall_ms = run_fused(prc, x, w, args.steps, args.warmup)
+
+    dec_gbs = work["decode_bytes"] / (stage["decode"] * 1e-3) / 1e9
+    pre_tf = work["prefill_flops"] / (stage["prefill"] * 1e-3) / 1e12
+    pc_tf = work["precompute_flops"] / (stage["precompute"] * 1e-3) / 1e12
+    pc_gbs = work["precompute_bytes"] / (stage["precompute"] * 1e-3) / 1e9
+
+    def roof(bound, achieved, peak, unit, traffic):
+        return {"bound": bound, "achieved": round(achieved, 3), "peak": peak, "unit": unit,
+                "frac": round(achieved / peak, 4), "traffic": traffic}
+
+    rooflines = {
+        "decode": dict(roof("hbm", dec_gbs, HBM_PEAK_GBS, "GB/s", traffic_for("lrsa_decode.hip")),
+                       kernel="lrsa_decode_kernel + lrsa_merge_kernel", ms=round(stage["decode"], 4),
+                       algorithmic_bytes=work["decode_bytes"]),
+        "prefill": dict(roof("mfma", pre_tf, MFMA_BF16_PEAK_TFLOPS, "TFLOP/s", None),
+                        kernel="lrsa_prefill_kernel", ms=round(stage["prefill"], 4),
+                        algorithmic_flops=work["prefill_flops"]),
+        "precompute": dict(roof("hbm", pc_gbs, HBM_PEAK_GBS, "GB/s", traffic_for("precompute_gemm.hip")),
+                           kernel="precompute_kernel", ms=round(stage["precompute"], 4),
+                           algorithmic_bytes=work["precompute_bytes"], tflops=round(pc_tf, 3),
+                           mfma_frac=round(pc_tf / MFMA_BF16_PEAK_TFLOPS, 4)),
+    }
+    dominant = max(("decode", "prefill", "precompute"), key=lambda k: stage[k])
+    out = {
+        "metric": METRIC,
+        "value": round(dec_gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": ("8B-shaped layer at 32k context: precompute of a 4096-token segment for 8 agents "
+                         "(rank 16, k and v); prefill of 4096 queries at positions 32768-36863; decode of 16 "
+                         "requests at 32768 tokens"),
+            "hidden": w["hidden"], "n_q_heads": w["n_q"], "n_kv_heads": w["n_kv"], "head_dim": w["d"],
+            "agents": w["N"], "rank": w["r"], "context": w["S"], "decode_batch": w["B"],
+            "prefill_tokens": w["n_pre"], "rope_theta": w["theta"],
+        },
+        "prefill_tflops": round(pre_tf, 3),
+        "precompute_tflops": round(pc_tf, 3),
+        "stages_ms": {k: round(v, 4) for k, v in stage.items()},
+        "roofline": dict(rooflines[dominant], stage=dominant),
+        "rooflines": rooflines,
+        "host_ms_per_step": round(wall_ms, 4),
+    }
+    if not args.no_materialize:
+        print("bench: timing materialise-then-attend reference", file=sys.stderr, flush=True)
+        ref = run_materialized(prc, x, w, max(3, args.steps // 2), args.warmup)
+        out["materialize_baseline"] = {
+            "stages_ms": {k: round(v, 4) for k, v in ref.items()},
+            "speedup_decode": round(ref["decode"] / stage["decode"], 3),
+            "speedup_prefill": round(ref["prefill"] / stage["prefill"], 3),
+            "speedup_step": round(sum(ref.values()) / sum(stage.values()), 3),
+        }
+    del x
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        print("bench: timing the fp64 oracle on a host sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
