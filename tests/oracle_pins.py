@@ -25,6 +25,7 @@ independently written route to the same number:
                        whole range (the identity split-KV decoding relies on).
 * pin_precompute       Sec. 3.1 precompute: each agent's block equals X A_a, by a
                        naive triple loop.
+* pin_golden           hand-derived worked cases (tests/golden/worked_cases.json).
 """
 from __future__ import annotations
 
@@ -284,6 +285,25 @@ def pin_precompute(orc, seed=9, T=7, d_in=5, n_proj=2, N=3, r=2):
                     assert abs(L[p, a, t, j] - ref) <= 1e-12, "precompute block mismatch"
 
 
-ALL_PINS = [pin_merged_weights, pin_plain_attention, pin_softmax_rows, pin_rope,
+def pin_golden(orc):
+    """Hand-derived worked cases (tests/golden/worked_cases.json)."""
+    import json
+    import os
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "worked_cases.json")
+    for c in json.load(open(path))["cases"]:
+        if "Q" in c:
+            Bk = np.array([c["B_k_unit"]]) * (math.sqrt(2.0) * math.log(3.0))
+            O, lse = orc.lr_shared_attention(
+                np.array(c["Q"])[None], np.array(c["K_base"])[None], np.array(c["V_base"])[None],
+                np.array(c["L_k"])[None], np.array(c["L_v"])[None], Bk[None], np.array(c["B_v"])[None],
+                np.array([c["positions"]]), [len(c["K_base"])], c["theta"])
+            assert np.allclose(O[0], c["expected_O"], atol=1e-12), c["name"]
+            assert np.allclose(lse[0], c["expected_lse"], atol=1e-12), c["name"]
+        else:
+            L = orc.precompute_lr_cache(np.array(c["X"]), np.array(c["A_stack"]), 1, 2, 1)
+            assert np.array_equal(L, np.array(c["expected_L"])), c["name"]
+
+
+ALL_PINS = [pin_golden, pin_merged_weights, pin_plain_attention, pin_softmax_rows, pin_rope,
             pin_value_assoc, pin_closed_forms, pin_permutation, pin_split_merge,
             pin_precompute]
