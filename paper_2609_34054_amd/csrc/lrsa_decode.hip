@@ -5,26 +5,30 @@
 // K = K_base + RoPE(L_k B_k), with the rank-r expansion done before RoPE
 // (App. D.2).  Values use the associativity of App. D.2:
 //     P (V_base + L_v B_v) = P V_base + (P L_v) B_v,
-// so only an r-wide accumulator is carried per head and B_v is applied once.
+// so only an r-wide accumulator is carried per head and B_v is applied once,
+// in the merge.
 //
 // Work split (flash-decoding): one workgroup per (request, KV-range split,
-// group of up to 8 KV heads); one wavefront per KV head.  Each wave keeps the
-// whole GQA group of its KV head in one 16-row MFMA tile.  The waves of a
-// workgroup walk the same tokens, so the RoPE cos/sin table of each KV tile is
-// built once in LDS and shared by all 8 heads.  The LR rows are per token and
-// shared by all heads, so they are read through the same L1 lines.  A second
-// kernel merges the split partials with log-sum-exp weights.
+// group of up to 8 KV heads); one wavefront per KV head.  The waves of a
+// workgroup walk the same tokens, so the RoPE cos/sin table of each 32-token
+// tile is built once in LDS for all heads, and the per-token LR rows are read
+// through shared L1 lines.  A second kernel merges the split partials with
+// log-sum-exp weights.
 //
-// Per 16-token sub-block, each wave:
-//   1. loads L_k rows and expands E^T = B_k^T L_k^T with 16x16x16 MFMAs;
-//      lane l then holds token l%16 and 32 head dims, both RoPE halves of
-//      every pair in the same lane;
-//   2. rotates E at the token's position, adds K_base and rounds to bf16;
-//      the result is already the B operand of the QK^T MFMA;
-//   3. computes S = Q K^T with 16x16x32 MFMAs (rows = q heads of the group).
-//   4. updates the online softmax (exp2, per-head running max and sum);
-//   5. passes P through a wave-private LDS block, then runs P V_base and
-//      P L_v on the vector ALUs (fp32 P), reading V in its natural layout.
+// Per 16-token sub-block, each wave (lane l: query head l%16 of the group,
+// q = l/16):
+//   1. scores S^T = K Q^T on 16x16x32 MFMAs in two parts: the raw bf16
+//      K_base rows (no rounding) plus bf16(RoPE(E)), where E^T = B_k^T L_k^T
+//      comes from 16x16x16 MFMAs whose result layout holds both halves of
+//      every RoPE pair in one lane;
+//   2. online softmax per head (lane l%16), exp2 domain;
+//   3. O^T += V^T P^T and (P L_v)^T += L_v^T P^T on 16x16x16 MFMAs.  V and
+//      L_v rows pass through a wave-private LDS tile and come back through
+//      the transposing LDS read (ds_read_b64_tr_b16), so P, already in B
+//      operand layout, needs no shuffles and the softmax rescale is a
+//      per-lane scalar.
+// The loads of the next sub-block are issued before the current one is
+// consumed.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
@@ -34,44 +38,78 @@ namespace {
 
 constexpr int TK = 32;        // tokens per KV tile (one LDS table, one barrier)
 constexpr int NSB = TK / 16;  // 16-token sub-blocks per tile
-constexpr int MAXW = 8;       // waves (KV heads) per workgroup
+constexpr int NW = 8;         // waves per workgroup (KV heads)
+constexpr int NT = NW * 64;   // threads per workgroup
 
-template <int D, int R, int GM>
+template <int D, int R>
 struct Dec {
   static constexpr int HALF = D / 2;
   static constexpr int NB = D / 32;           // 16-dim blocks per RoPE half
   static constexpr int NBLK = D / 16;         // 16-dim blocks
-  static constexpr int QPG = HALF / 4;        // dims per lane group per half
-  static constexpr int NKK = D / 32;          // 16x16x32 k-chunks over d
-  static constexpr int RC = R < 16 ? 1 : R / 16;  // 16-wide rank chunks
+  static constexpr int NCH = D / 32;          // 8-dim chunks per lane
+  static constexpr int QPG = D / 8;           // dims per lane group per half
+  static constexpr int RC = RCH(R);           // 16-wide rank chunks
   static constexpr int CS_ROW = HALF + 2;     // float2 per table row (padded)
-  static constexpr int PG = GM <= 4 ? 4 : 8;  // floats per token row of P
-  static constexpr int LPR = D / 8;           // lanes per V row (8 dims each)
+  static constexpr int EPT = TK * HALF / NT;  // table entries per thread
+  static constexpr int V_ROW = D + 16;        // bf16 per V row in LDS
+  static constexpr int LV_ROW = 16 * RC + 16; // bf16 per L_v row in LDS
+  static constexpr int LPR = D / 8;           // lanes per V row (16 bytes each)
   static constexpr int RPL = 64 / LPR;        // V rows per wave load
   static constexpr int NVL = 16 / RPL;        // V loads per sub-block
   static constexpr int PS = 4 + D + R;        // floats per split partial
-  static constexpr int LRG = 64 / R;          // token groups of the P L_v layout
-  static constexpr int LTK = 16 / LRG;        // P L_v tokens per lane per sub-block
 };
 
-template <int D, int R, int GM>
-__global__ void __launch_bounds__(512)
+// Transposing LDS read: lane j of each 16-lane group points at 4 consecutive
+// bf16; lane i receives element i%4 of lanes i/4, i/4+4, i/4+8, i/4+12.
+__device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((v4s __attribute__((address_space(3)))*)(p));
+  return __builtin_bit_cast(i16x4, v);
+}
+
+template <int D, int R>
+struct Stage {
+  u32x4 kb[D / 32];               // K_base chunks of token l%16
+  u32x2 lk[RCH(R)];               // L_k row fragment of token l%16
+  u32x4 v[Dec<D, R>::NVL];        // V rows, natural layout
+  u32x2 lv[RCH(R)];               // L_v row fragment of token l%16
+};
+
+template <int D, int R>
+__device__ __forceinline__ void stage_load(Stage<D, R>& s, const uint16_t* Kb, const uint16_t* Vb,
+                                           const uint16_t* Lk, const uint16_t* Lv, int64_t row, int64_t t0,
+                                           int64_t t_end, int lane) {
+  using C = Dec<D, R>;
+  const int c16 = lane & 15;
+  const int64_t t = t0 + c16;
+  const bool ok = t < t_end;
+  load_chunks<D>(s.kb, Kb + t * row, ok, lane);
+  if (Lk != nullptr) load_lr_frag<R>(s.lk, Lk + t * R, ok, lane);
+  if (Lv != nullptr) load_lr_frag<R>(s.lv, Lv + t * R, ok, lane);
+  const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
+#pragma unroll
+  for (int iv = 0; iv < C::NVL; ++iv) {
+    const int64_t tv = t0 + vrow + C::RPL * iv;
+    s.v[iv] = ld16(Vb + tv * row + vdim, tv < t_end);
+  }
+}
+
+template <int D, int R>
+__global__ void __launch_bounds__(NT)
 lrsa_decode_kernel(const AttnArgs a) {
-  using C = Dec<D, R, GM>;
+  using C = Dec<D, R>;
   __shared__ float2 cs_lds[2][TK * C::CS_ROW];
-  __shared__ __attribute__((aligned(16))) float p_lds[MAXW][16 * C::PG];
-  __shared__ double w_lds[C::HALF];
+  __shared__ float2 base_lds[2][C::HALF];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[NW][16 * C::V_ROW];
+  __shared__ __attribute__((aligned(16))) uint16_t lv_lds[NW][16 * C::LV_ROW];
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int nthreads = blockDim.x;
   const int split = blockIdx.x, b = blockIdx.z;
-  const int g = blockIdx.y * MAXW + w;
+  const int g = blockIdx.y * NW + w;
   const bool active = g < a.n_kv;
   const int G = a.group;
   const int q = lane >> 4, c16 = lane & 15;
   const bool has_lk = a.Lk != nullptr, has_lv = a.Lv != nullptr;
-
-  for (int j = tid; j < C::HALF; j += nthreads) w_lds[j] = a.w2pi[j];
 
   // Keys this request may see: t < kv_len (clamped into the buffer) and
   // t <= position of its query token.
@@ -85,191 +123,202 @@ lrsa_decode_kernel(const AttnArgs a) {
   if (t_end > vis) t_end = vis;
   const int n_tiles = t_end > t_begin ? (int)((t_end - t_begin + TK - 1) / TK) : 0;
 
+  // RoPE table entries this thread builds every tile, by angle addition from
+  // the exact base angle of the tile and exact per-entry offset angles.
+  float cdl[C::EPT], sdl[C::EPT];
+  int ej[C::EPT], eidx[C::EPT];
+#pragma unroll
+  for (int k = 0; k < C::EPT; ++k) {
+    const int e = tid + NT * k, tok = e / C::HALF;
+    ej[k] = e - tok * C::HALF;
+    eidx[k] = tok * C::CS_ROW + ej[k];
+    cdl[k] = 1.f;
+    sdl[k] = 0.f;
+    if (has_lk) rope_cs(tok, a.w2pi[ej[k]], cdl[k], sdl[k]);
+  }
+  if (has_lk && tid < C::HALF && n_tiles > 0) {
+    float c, s;
+    rope_cs((int)t_begin, a.w2pi[tid], c, s);
+    base_lds[0][tid] = make_float2(c, s);
+  }
+  // L_v tile columns past the rank stay zero (rank 8 pads to 16).
+  for (int i = lane; i < 16 * C::LV_ROW; i += 64) lv_lds[w][i] = 0;
+
   const int64_t row = (int64_t)a.n_kv * D;  // elements between tokens
   const uint16_t* Kb = a.Kb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Lk = has_lk ? a.Lk + (int64_t)b * a.l_stride : nullptr;
   const uint16_t* Lv = has_lv ? a.Lv + (int64_t)b * a.l_stride : nullptr;
+  const int64_t t_end_w = active ? t_end : t_begin;  // inactive waves load nothing
 
-  // Q of the group as the A operand (rows = q heads, zero rows past G).
-  bf16x8 qf[C::NKK];
+  // Q^T of the group as the B operand (cols = q heads, zero past G).
+  bf16x8 qf[C::NCH];
   {
     const bool ok = active && c16 < G;
     const uint16_t* qp = a.Q + ((int64_t)b * a.n_tok * a.n_q + (int64_t)g * G + c16) * D;
 #pragma unroll
-    for (int kk = 0; kk < C::NKK; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
+    for (int kk = 0; kk < C::NCH; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
   }
-  // B_k^T of this KV head as the A operand of the expansion.
   i16x4 bkf[C::NBLK][C::RC];
   load_bt_frags<D, R>(bkf, has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr,
                       has_lk && active, lane);
 
-  float m_run[4], l_run[4];
+  float m_run = -INFINITY, l_part = 0.f;
+  f32x4 acc[C::NBLK];   // O^T: dims blk*16 + 4q + i, head l%16
+  f32x4 accl[C::RC];    // (P L_v)^T: rank rc*16 + 4q + i, head l%16
 #pragma unroll
-  for (int i = 0; i < 4; ++i) { m_run[i] = -INFINITY; l_run[i] = 0.f; }
-  float acc[GM][8];
-  float accl[GM];  // value-side LR accumulator: lane holds rank index lane % R
+  for (int blk = 0; blk < C::NBLK; ++blk) acc[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int h = 0; h < GM; ++h) {
-#pragma unroll
-    for (int c = 0; c < 8; ++c) acc[h][c] = 0.f;
-    accl[h] = 0.f;
-  }
-  const int lr_j = lane % R, lr_g = lane / R;  // rank index, token group
-  const int vrow0 = lane / C::LPR, vdim0 = (lane % C::LPR) * 8;
-  float* pl = p_lds[w];
+  for (int rc = 0; rc < C::RC; ++rc) accl[rc] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  __syncthreads();  // w_lds ready
+  uint16_t* vl = v_lds[w];
+  uint16_t* lvl = lv_lds[w];
+  const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
+  // Transposing-read addresses: lane j of group l/16 reads row
+  // 4*(l/16) + (j/4), columns 4*(j%4) .. +3 of a 16-column block.
+  const int tr_row = 4 * q + (c16 >> 2), tr_col = 4 * (c16 & 3);
+
+  Stage<D, R> st[2];
+  if (n_tiles > 0) stage_load<D, R>(st[0], Kb, Vb, Lk, Lv, row, t_begin, t_end_w, lane);
+
+  __syncthreads();  // base angles of the first tile, zeroed L_v tiles
 
   for (int tile = 0; tile < n_tiles; ++tile) {
     const int64_t t0 = t_begin + (int64_t)tile * TK;
     float2* cs = cs_lds[tile & 1];
     if (has_lk) {
-      for (int e = tid; e < TK * C::HALF; e += nthreads) {
-        const int tok = e / C::HALF, j = e - tok * C::HALF;
+      const float2* base = base_lds[tile & 1];
+#pragma unroll
+      for (int k = 0; k < C::EPT; ++k) {
+        const float2 bc = base[ej[k]];
+        cs[eidx[k]] = make_float2(bc.x * cdl[k] - bc.y * sdl[k], bc.y * cdl[k] + bc.x * sdl[k]);
+      }
+      if (tid < C::HALF && tile + 1 < n_tiles) {
         float c, s;
-        rope_cs((int)(t0 + tok), w_lds[j], c, s);
-        cs[tok * C::CS_ROW + j] = make_float2(c, s);
+        rope_cs((int)(t0 + TK), a.w2pi[tid], c, s);
+        base_lds[(tile + 1) & 1][tid] = make_float2(c, s);
       }
     }
-    __syncthreads();  // table of this tile ready; double buffering keeps the
-                      // previous tile's table intact for slower waves.
+    __syncthreads();  // this tile's table is ready; double buffering keeps
+                      // the previous tile's table intact for slower waves.
     if (!active) continue;
 
-#pragma unroll 1
-    for (int sb = 0; sb < NSB; ++sb) {
-      // ---- 1-3: rebuild K for 16 tokens and score them -------------------
-      const int64_t t = t0 + sb * 16 + c16;
-      const bool ok = t < t_end;
-      u32x4 kb[C::NKK];
-      load_chunks<D>(kb, Kb + t * row, ok, lane);
-      bf16x8 kf[C::NKK];
-      if (has_lk) {
-        u32x2 lk[C::RC];
-        load_lr_frag<R>(lk, Lk + t * R, ok, lane);
-        const float2* csr = cs + (sb * 16 + c16) * C::CS_ROW + q * C::QPG;
-        float cc[C::NB][4], ss[C::NB][4];
 #pragma unroll
-        for (int blk = 0; blk < C::NB; ++blk)
+    for (int sb = 0; sb < NSB; ++sb) {
+      Stage<D, R>& cur = st[sb & 1];
+      Stage<D, R>& nxt = st[(sb + 1) & 1];
+      const int64_t ts = t0 + sb * 16;
+      // A sub-block past the split end holds no visible key (and its stage
+      // buffer was never loaded).
+      if (ts >= t_end) break;
+      // Issue the next sub-block's loads before consuming this one.
+      if (ts + 16 < t_end) stage_load<D, R>(nxt, Kb, Vb, Lk, Lv, row, ts + 16, t_end_w, lane);
+
+      // ---- V and L_v rows into the wave's LDS tile ------------------------
+#pragma unroll
+      for (int iv = 0; iv < C::NVL; ++iv)
+        *reinterpret_cast<u32x4*>(vl + (vrow + C::RPL * iv) * C::V_ROW + vdim) = cur.v[iv];
+      if (has_lv) {
+#pragma unroll
+        for (int rc = 0; rc < C::RC; ++rc)
+          if (rc * 16 + q * 4 < R) *reinterpret_cast<u32x2*>(lvl + c16 * C::LV_ROW + rc * 16 + q * 4) = cur.lv[rc];
+      }
+
+      // ---- scores S^T = K_base Q^T + bf16(RoPE(E)) Q^T --------------------
+      f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int kk = 0; kk < C::NCH; ++kk) sc = mfma16x16x32(as_bf16x8(cur.kb[kk]), qf[kk], sc);
+      if (has_lk) {
+        const float2* csr = cs + (sb * 16 + c16) * C::CS_ROW + q * C::QPG;
+        u32x4 ek[C::NCH];
+#pragma unroll
+        for (int blk = 0; blk < C::NB; ++blk) {
+          f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int rc = 0; rc < C::RC; ++rc) {
+            elo = mfma16x16x16(bkf[blk][rc], as_i16x4(cur.lk[rc]), elo);
+            ehi = mfma16x16x16(bkf[blk + C::NB][rc], as_i16x4(cur.lk[rc]), ehi);
+          }
+          float rlo[4], rhi[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const float2 r = csr[blk * 4 + i];
-            cc[blk][i] = r.x;
-            ss[blk][i] = r.y;
+            rlo[i] = elo[i] * r.x - ehi[i] * r.y;
+            rhi[i] = ehi[i] * r.x + elo[i] * r.y;
           }
-        add_rotated_expansion<D, R>(kb, bkf, lk, cc, ss);
+          const int klo = blk >> 1, khi = (blk + C::NB) >> 1, w0 = (blk & 1) * 2;
+          ek[klo][w0] = pack_bf16(rlo[0], rlo[1]);
+          ek[klo][w0 + 1] = pack_bf16(rlo[2], rlo[3]);
+          ek[khi][w0] = pack_bf16(rhi[0], rhi[1]);
+          ek[khi][w0 + 1] = pack_bf16(rhi[2], rhi[3]);
+        }
+#pragma unroll
+        for (int kk = 0; kk < C::NCH; ++kk) sc = mfma16x16x32(as_bf16x8(ek[kk]), qf[kk], sc);
       }
-#pragma unroll
-      for (int kk = 0; kk < C::NKK; ++kk) kf[kk] = as_bf16x8(kb[kk]);
-      f32x4 sc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int kk = 0; kk < C::NKK; ++kk) sc = mfma16x16x32(qf[kk], kf[kk], sc);
 
-      // ---- online softmax over these 16 tokens ---------------------------
-      // Lanes of group q hold q heads 4q..4q+3, one token per lane.
-      float alpha[4], p[4];
+      // ---- online softmax: lane l%16 is a head, 4 tokens per lane ---------
+      float s2[4];
+      float mx = -INFINITY;
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float s2 = ok ? sc[i] * a.scale_log2 : -INFINITY;
-        const float mx = max16(s2);
-        const float mn = fmaxf(m_run[i], mx);
-        const float ms = (mn == -INFINITY) ? 0.f : mn;
-        alpha[i] = fast_exp2(m_run[i] - ms);
-        p[i] = fast_exp2(s2 - ms);
-        l_run[i] = l_run[i] * alpha[i] + p[i];
-        m_run[i] = mn;
+        s2[i] = (ts + q * 4 + i < t_end) ? sc[i] * a.scale_log2 : -INFINITY;
+        mx = fmaxf(mx, s2[i]);
       }
-      if (q * 4 < G)
-        *reinterpret_cast<float4*>(&pl[c16 * C::PG + q * 4]) = make_float4(p[0], p[1], p[2], p[3]);
+      mx = fmaxf(mx, shfl_xor(mx, 16));
+      mx = fmaxf(mx, shfl_xor(mx, 32));
+      const float mn = fmaxf(m_run, mx);
+      const float ms = (mn == -INFINITY) ? 0.f : mn;
+      const float alpha = fast_exp2(m_run - ms);
+      m_run = mn;
+      float p[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p[i] = fast_exp2(s2[i] - ms);
+      l_part = l_part * alpha + (p[0] + p[1]) + (p[2] + p[3]);
+      u32x2 pw;
+      pw[0] = pack_bf16(p[0], p[1]);
+      pw[1] = pack_bf16(p[2], p[3]);
+      const i16x4 pb = as_i16x4(pw);
+      // Rescale only when some head's running max moved (exact either way).
+      if (__ballot(alpha != 1.f)) {
+#pragma unroll
+        for (int blk = 0; blk < C::NBLK; ++blk) acc[blk] *= alpha;
+#pragma unroll
+        for (int rc = 0; rc < C::RC; ++rc) accl[rc] *= alpha;
+      }
       __builtin_amdgcn_wave_barrier();
-      float al[GM];
-#pragma unroll
-      for (int h = 0; h < GM; ++h) al[h] = readlane_f(alpha[h & 3], (h >> 2) * 16);
 
-      // ---- P V_base on the vector ALUs, V in its natural layout ----------
+      // ---- O^T += V^T P^T, (P L_v)^T += L_v^T P^T -----------------------
 #pragma unroll
-      for (int h = 0; h < GM; ++h)
-#pragma unroll
-        for (int c = 0; c < 8; ++c) acc[h][c] *= al[h];
-#pragma unroll
-      for (int iv = 0; iv < C::NVL; ++iv) {
-        const int tok = vrow0 + C::RPL * iv;
-        const int64_t tv = t0 + sb * 16 + tok;
-        const u32x4 v = ld16(Vb + tv * row + vdim0, tv < t_end);
-        float vf[8];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) { vf[2 * c] = bf_lo(v[c]); vf[2 * c + 1] = bf_hi(v[c]); }
-        const float* pr = pl + tok * C::PG;
-#pragma unroll
-        for (int h = 0; h < GM; ++h) {
-          const float ph = pr[h];
-#pragma unroll
-          for (int c = 0; c < 8; ++c) acc[h][c] += ph * vf[c];
-        }
-      }
-      // ---- P L_v (value-side LR accumulator) ------------------------------
-      // Lane l owns rank index l % R and the tokens congruent to l / R modulo
-      // 64 / R, so each load instruction reads 64 consecutive bf16.
+      for (int blk = 0; blk < C::NBLK; ++blk)
+        acc[blk] = mfma16x16x16(lds_read_tr(vl + tr_row * C::V_ROW + blk * 16 + tr_col), pb, acc[blk]);
       if (has_lv) {
 #pragma unroll
-        for (int h = 0; h < GM; ++h) accl[h] *= al[h];
-#pragma unroll
-        for (int k = 0; k < C::LTK; ++k) {
-          const int tok = lr_g + C::LRG * k;
-          const int64_t tl = t0 + sb * 16 + tok;
-          const float lv = tl < t_end ? __uint_as_float((uint32_t)Lv[tl * R + lr_j] << 16) : 0.f;
-          const float* pr = pl + tok * C::PG;
-#pragma unroll
-          for (int h = 0; h < GM; ++h) accl[h] += pr[h] * lv;
-        }
+        for (int rc = 0; rc < C::RC; ++rc)
+          accl[rc] = mfma16x16x16(lds_read_tr(lvl + tr_row * C::LV_ROW + rc * 16 + tr_col), pb, accl[rc]);
       }
       __builtin_amdgcn_wave_barrier();
     }
-    __builtin_amdgcn_wave_barrier();
   }
 
   if (!active) return;
-  // Cross-lane reductions, then one partial per (request, q head, split).
+  // One partial per (request, q head, split): lane l%16 is the head; lanes
+  // l, l^16, l^32, l^48 share it and hold different dims of O^T.
+  l_part += shfl_xor(l_part, 16);
+  l_part += shfl_xor(l_part, 32);
+  if (c16 >= G) return;
+  const int64_t hstride = (int64_t)a.n_splits * C::PS;
+  float* wsb = a.ws + ((int64_t)b * a.n_q + (int64_t)g * G + c16) * hstride + (int64_t)split * C::PS;
+  if (q == 0) {
+    wsb[0] = m_run;
+    wsb[1] = l_part;
+  }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) l_run[i] = sum16(l_run[i]);
-#pragma unroll
-  for (int h = 0; h < GM; ++h)
-#pragma unroll
-    for (int c = 0; c < 8; ++c)
-#pragma unroll
-      for (int x = C::LPR; x < 64; x <<= 1) acc[h][c] += shfl_xor(acc[h][c], x);
+  for (int blk = 0; blk < C::NBLK; ++blk)
+    *reinterpret_cast<f32x4*>(wsb + 4 + blk * 16 + q * 4) = acc[blk];
   if (has_lv) {
 #pragma unroll
-    for (int h = 0; h < GM; ++h)
-#pragma unroll
-      for (int x = R; x < 64; x <<= 1) accl[h] += shfl_xor(accl[h], x);
-  }
-  const int64_t hstride = (int64_t)a.n_splits * C::PS;
-  float* wsb = a.ws + ((int64_t)b * a.n_q + (int64_t)g * G) * hstride + (int64_t)split * C::PS;
-  if (c16 == 0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int hh = q * 4 + i;
-      if (hh < G) {
-        wsb[hh * hstride + 0] = m_run[i];
-        wsb[hh * hstride + 1] = l_run[i];
-      }
-    }
-  }
-  if (lane < C::LPR) {
-#pragma unroll
-    for (int h = 0; h < GM; ++h) {
-      if (h < G) {
-        float* dst = wsb + h * hstride + 4 + vdim0;
-        *reinterpret_cast<float4*>(dst) = make_float4(acc[h][0], acc[h][1], acc[h][2], acc[h][3]);
-        *reinterpret_cast<float4*>(dst + 4) = make_float4(acc[h][4], acc[h][5], acc[h][6], acc[h][7]);
-      }
-    }
-  }
-  if (has_lv && lane < R) {
-#pragma unroll
-    for (int h = 0; h < GM; ++h)
-      if (h < G) wsb[h * hstride + 4 + D + lr_j] = accl[h];
+    for (int rc = 0; rc < C::RC; ++rc)
+      if (rc * 16 + q * 4 < R) *reinterpret_cast<f32x4*>(wsb + 4 + D + rc * 16 + q * 4) = accl[rc];
   }
 }
 
@@ -330,32 +379,23 @@ lrsa_merge_kernel(const AttnArgs a) {
     a.lse[(int64_t)b * a.n_tok * a.n_q + h] = L > 0.f ? (M + __log2f(L)) * kLn2 : -INFINITY;
 }
 
-template <int D, int R, int GM>
+template <int D, int R>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
-  const int hg = (a.n_kv + MAXW - 1) / MAXW;
-  const int waves = a.n_kv < MAXW ? a.n_kv : MAXW;
-  hipLaunchKernelGGL((lrsa_decode_kernel<D, R, GM>), dim3(a.n_splits, hg, a.batch), dim3(64 * waves),
-                     0, st, a);
+  const int hg = (a.n_kv + NW - 1) / NW;
+  hipLaunchKernelGGL((lrsa_decode_kernel<D, R>), dim3(a.n_splits, hg, a.batch), dim3(NT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 
-template <int D, int R>
-hipError_t launch_g(const AttnArgs& a, hipStream_t st) {
-  if (a.group == 1) return launch_t<D, R, 1>(a, st);
-  if (a.group <= 4) return launch_t<D, R, 4>(a, st);
-  return launch_t<D, R, 8>(a, st);
-}
-
 template <int D>
 hipError_t launch_r(const AttnArgs& a, hipStream_t st) {
   switch (a.rank) {
-    case 8: return launch_g<D, 8>(a, st);
-    case 16: return launch_g<D, 16>(a, st);
-    case 32: return launch_g<D, 32>(a, st);
-    case 64: return launch_g<D, 64>(a, st);
+    case 8: return launch_t<D, 8>(a, st);
+    case 16: return launch_t<D, 16>(a, st);
+    case 32: return launch_t<D, 32>(a, st);
+    case 64: return launch_t<D, 64>(a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -366,7 +406,7 @@ int decode_tile_tokens() { return TK; }
 
 void decode_plan(int64_t s_cap, int batch, int n_kv, int* n_splits, int* split_tiles) {
   const int64_t tiles = (s_cap + TK - 1) / TK;
-  const int64_t hg = (n_kv + MAXW - 1) / MAXW;
+  const int64_t hg = (n_kv + NW - 1) / NW;
   const int64_t groups = (int64_t)(batch > 0 ? batch : 1) * hg;
   const int64_t target_wgs = 1024;  // about four workgroups per CU
   int64_t ns = (target_wgs + groups - 1) / groups;
