@@ -1,27 +1,33 @@
 // LR-shared attention, prefill (many query tokens per request), gfx950.
 //
 // Causal flash attention of a chunk of new query tokens over the shared base
-// cache plus the current agent's LR cache (Sec. 3.1, reuse step).  Each KV
-// tile is rebuilt in LDS before use (App. D.2 order: rank-r expansion, then
-// RoPE on the key side):
-//     K_tile = K_base + RoPE(L_k B_k),   V_tile = V_base + L_v B_v.
+// cache plus the current agent's LR cache (Sec. 3.1, reuse step).
+//   keys:   each KV tile is rebuilt in LDS, K = K_base + RoPE(L_k B_k), with
+//           the rank-r expansion before RoPE (App. D.2);
+//   values: associativity (App. D.2), O = P V_base + (P L_v) B_v: V_base and
+//           L_v tiles go to LDS unchanged, P L_v is accumulated beside P V_base
+//           and B_v is applied once in the epilogue.
 //
-// Work split: one workgroup (4 waves) per (request, KV head, 128 query rows).
-// A query row is a (token, q head of the GQA group) pair, so the group's
-// heads share every rebuilt tile.  Each wave owns 32 rows.
-//
-// Per 64-token KV tile:
-//   rebuild   wave w rebuilds tokens 16w..16w+15: E^T = B^T L^T with 16x16x16
-//             MFMAs (lane l: token l%16, both RoPE halves of 16 pairs), RoPE
-//             by angle addition (exact per-tile base angle in LDS, exact
-//             per-lane offset angles in registers), + base, bf16, stored as
-//             K[tok][dim] and V^T[dim][tok] in LDS;
-//   scores    S^T = K Q^T with 32x32x16 MFMAs: lane l holds row l%32 and 32
-//             of the tile's tokens, so softmax statistics are per lane;
-//   softmax   online, exp2 domain, running max shared by lanes l and l^32;
-//   PV        O^T += V^T P^T with 32x32x16 MFMAs; P is already in the B
-//             operand layout, O^T keeps one row per lane, so the rescale by
-//             the softmax correction is a per-lane scalar.
+// Work split: one workgroup per (request, KV head, 128 query rows).  A query
+// row is a (token, q head of the GQA group) pair, so the group's heads share
+// every rebuilt tile.  The workgroup's 8 waves specialise:
+//   producers (waves 4-7) load KV tile k+2 from HBM while rebuilding tile k+1
+//             into LDS: E^T = B_k^T L_k^T on 16x16x16 MFMAs (lane l: token
+//             l%16, both RoPE halves of each pair in the same lane), RoPE by
+//             angle addition (exact per-tile base angle in LDS, exact per-lane
+//             offsets in registers), + base, bf16, stored as K[tok][dim];
+//             V_base and L_v rows are stored as they are;
+//   consumers (waves 0-3, 32 rows each) attend over tile k:
+//     scores  S^T = K Q^T on 32x32x16 MFMAs: lane l holds row l%32 and 32 of
+//             the tile's tokens, so softmax statistics are per lane;
+//     softmax online, exp2 domain, running max shared by lanes l and l^32;
+//             the causal mask is applied only on tiles that cross it;
+//     PV      O^T += V^T P^T and (P L_v)^T += L_v^T P^T on 32x32x16 MFMAs;
+//             V^T and L_v^T come from row-major LDS tiles through the
+//             transposing LDS read, P is already in the B operand layout,
+//             and the softmax rescale is a per-lane scalar.
+// LDS is double-buffered with one barrier per tile; a producer and a consumer
+// share each SIMD, so the rebuild's vector work overlaps the MFMAs.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
@@ -30,65 +36,212 @@ namespace prc {
 namespace {
 
 constexpr int TKV = 64;      // KV tokens per tile
-constexpr int NWAVE = 4;     // waves per workgroup
-constexpr int WROWS = 32;    // query rows per wave
-constexpr int BROWS = NWAVE * WROWS;
+constexpr int NCONS = 4;     // consumer waves (32 query rows each)
+constexpr int NPROD = 4;     // producer waves (16 rebuilt tokens each)
+constexpr int NTHR = 64 * (NCONS + NPROD);
+constexpr int WROWS = 32;    // query rows per consumer wave
+constexpr int BROWS = NCONS * WROWS;
 
 template <int D, int R>
 struct Pre {
   static constexpr int HALF = D / 2;
-  static constexpr int NB = D / 32;        // 16-dim blocks per RoPE half
+  static constexpr int NB = D / 32;          // 16-dim blocks per RoPE half
   static constexpr int NBLK = D / 16;
-  static constexpr int QPG = HALF / 4;     // dims per lane group per half
-  static constexpr int RC = R < 16 ? 1 : R / 16;
-  static constexpr int NKQ = D / 16;       // 32x32x16 k-chunks over d
-  static constexpr int NDB = D / 32;       // 32-dim blocks of O^T
-  static constexpr int K_ROW = D + 8;      // bf16 per K row in LDS (padded)
-  static constexpr int VT_ROW = TKV + 8;   // bf16 per V^T row in LDS (padded)
+  static constexpr int NCH = D / 32;         // 8-dim chunks per lane (rebuild)
+  static constexpr int QPG = D / 8;          // dims per lane group per half
+  static constexpr int RC = RCH(R);          // 16-wide rank chunks
+  static constexpr int RB = (R + 31) / 32;   // 32-row blocks of (P L_v)^T
+  static constexpr int NKQ = D / 16;         // 32x32x16 k-chunks over d
+  static constexpr int NDB = D / 32;         // 32-dim blocks of O^T
+  static constexpr int K_ROW = D + 8;        // bf16 per K row in LDS
+  static constexpr int V_ROW = D + 16;       // bf16 per V row in LDS
+  static constexpr int LV_ROW = 32 * RB + 16;  // bf16 per L_v row in LDS
+  static constexpr int LPR = D / 8;          // lanes per V row (16 bytes each)
+  static constexpr int RPL = 64 / LPR;       // V rows per wave load
+  static constexpr int NVL = 16 / RPL;       // V loads per wave per tile
+};
+
+__device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((v4s __attribute__((address_space(3)))*)(p));
+  return __builtin_bit_cast(i16x4, v);
+}
+
+// 32x32x16 A operand [32 rows x 16 tokens] from a row-major [token][col] LDS
+// tile, in the token order of the P fragments: k = 8h + i is token
+// 16m + 4h + i (i < 4) or 16m + 8 + 4h + (i - 4) (i >= 4), h = l/32.
+__device__ __forceinline__ bf16x8 lds_tr_a32(const uint16_t* tile, int row_stride, int m, int col0, int lane) {
+  const int gg = lane >> 4, j = lane & 15, h = lane >> 5;
+  const uint16_t* p = tile + (16 * m + 4 * h + (j >> 2)) * row_stride + col0 + 16 * (gg & 1) + 4 * (j & 3);
+  const i16x4 lo = lds_read_tr(p);
+  const i16x4 hi = lds_read_tr(p + 8 * row_stride);
+  typedef short v8s __attribute__((ext_vector_type(8)));
+  v8s v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+template <int D, int R>
+struct TileRegs {
+  u32x4 kb[D / 32];          // K_base chunks of this lane's rebuild token
+  u32x2 lk[RCH(R)];          // L_k fragment of that token
+  u32x4 v[Pre<D, R>::NVL];   // V_base rows of the wave's 16 tokens
+  u32x2 lv[RCH(R)];          // L_v fragment of this lane's rebuild token
 };
 
 template <int D, int R>
-__global__ void __launch_bounds__(256)
+__device__ __forceinline__ void tile_load(TileRegs<D, R>& x, const uint16_t* Kb, const uint16_t* Vb,
+                                          const uint16_t* Lk, const uint16_t* Lv, int64_t row_el, int64_t t0w,
+                                          int64_t kv_hi, int lane) {
+  using C = Pre<D, R>;
+  const int64_t t = t0w + (lane & 15);
+  const bool ok = t < kv_hi;
+  load_chunks<D>(x.kb, Kb + t * row_el, ok, lane);
+  if (Lk != nullptr) load_lr_frag<R>(x.lk, Lk + t * R, ok, lane);
+  if (Lv != nullptr) load_lr_frag<R>(x.lv, Lv + t * R, ok, lane);
+  const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
+#pragma unroll
+  for (int iv = 0; iv < C::NVL; ++iv) {
+    const int64_t tv = t0w + vrow + C::RPL * iv;
+    x.v[iv] = ld16(Vb + tv * row_el + vdim, tv < kv_hi);
+  }
+}
+
+template <int D, int R>
+__global__ void __launch_bounds__(NTHR)
 lrsa_prefill_kernel(const AttnArgs a) {
   using C = Pre<D, R>;
-  __shared__ __attribute__((aligned(16))) uint16_t k_lds[TKV * C::K_ROW];
-  __shared__ __attribute__((aligned(16))) uint16_t vt_lds[D * C::VT_ROW];
-  __shared__ float2 base_cs[C::HALF];
-  __shared__ double w_lds[C::HALF];
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][TKV * C::K_ROW];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][TKV * C::V_ROW];
+  __shared__ __attribute__((aligned(16))) uint16_t lv_lds[2][TKV * C::LV_ROW];
+  __shared__ float2 base_cs[2][C::HALF];
   __shared__ int s_maxpos;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int rtile = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  // Heaviest row tiles (latest positions, most keys) are dispatched first.
+  const int rtile = gridDim.x - 1 - blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int G = a.group;
   const int n_rows = a.n_tok * G;
-  const int q = lane >> 4, c16 = lane & 15;
-  const int l32 = lane & 31, h32 = lane >> 5;
+  const bool consumer = w < NCONS;
   const bool has_lk = a.Lk != nullptr, has_lv = a.Lv != nullptr;
 
-  for (int j = tid; j < C::HALF; j += blockDim.x) w_lds[j] = a.w2pi[j];
   if (tid == 0) s_maxpos = -1;
+  // L_v columns past the rank stay zero in both buffers.
+  for (int i = tid; i < 2 * TKV * C::LV_ROW; i += NTHR) (&lv_lds[0][0])[i] = 0;
 
   int64_t kvl = a.kv_len[b];
   kvl = kvl < 0 ? 0 : (kvl > a.s_cap ? a.s_cap : kvl);
 
-  // This lane's query row (the same row for lanes l and l^32).
+  // Consumer lane's query row (the same row for lanes l and l^32).
+  const int l32 = lane & 31, h32 = lane >> 5;
   const int row = rtile * BROWS + w * WROWS + l32;
-  const bool row_ok = row < n_rows;
+  const bool row_ok = consumer && row < n_rows;
   const int qi = row_ok ? row / G : 0, hh = row_ok ? row - qi * G : 0;
   const int pos = row_ok ? a.positions[(int64_t)b * a.n_tok + qi] : -1;
-  // Last key this row may see.
-  const int64_t last = (int64_t)pos < kvl - 1 ? (int64_t)pos : kvl - 1;
+  const int64_t last = (int64_t)pos < kvl - 1 ? (int64_t)pos : kvl - 1;  // last visible key
 
   __syncthreads();
   if (row_ok && last >= 0) atomicMax(&s_maxpos, (int)last);
-  // Wave-level bound, to skip tiles no row of this wave can see.
-  int wave_last = (int)last;
+  __syncthreads();
+  const int64_t kv_hi = (int64_t)s_maxpos + 1;  // keys [0, kv_hi) are needed
+  const int n_tiles = (int)((kv_hi + TKV - 1) / TKV);
+
+  const int64_t row_el = (int64_t)a.n_kv * D;
+  const uint16_t* Kb = a.Kb + (int64_t)b * a.kv_stride + (int64_t)g * D;
+  const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
+  const uint16_t* Lk = has_lk ? a.Lk + (int64_t)b * a.l_stride : nullptr;
+  const uint16_t* Lv = has_lv ? a.Lv + (int64_t)b * a.l_stride : nullptr;
+
+  if (!consumer) {
+    // ======================= producer waves ================================
+    const int pw_ = w - NCONS;             // 0..3: tokens 16*pw_ .. +15 of a tile
+    const int ptid = tid - 64 * NCONS;     // 0..255
+    const int q = lane >> 4, c16 = lane & 15;
+    const int delta = pw_ * 16 + c16;      // this lane's rebuild token in a tile
+    const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
+    i16x4 bkf[C::NBLK][C::RC];
+    load_bt_frags<D, R>(bkf, has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr, has_lk,
+                        lane);
+    // RoPE offsets of token `delta` for this lane's D/8 frequencies, exact in
+    // fp64 once per kernel.
+    float cd[C::NB][4], sd[C::NB][4];
 #pragma unroll
-  for (int x = 1; x < 64; x <<= 1) {
-    const int o = __shfl_xor(wave_last, x, 64);
-    wave_last = o > wave_last ? o : wave_last;
+    for (int blk = 0; blk < C::NB; ++blk)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        cd[blk][i] = 1.f;
+        sd[blk][i] = 0.f;
+        if (has_lk) rope_cs(delta, a.w2pi[q * C::QPG + blk * 4 + i], cd[blk][i], sd[blk][i]);
+      }
+    auto rebuild = [&](const TileRegs<D, R>& x, int buf) {
+      u32x4 kb[C::NCH];
+#pragma unroll
+      for (int kk = 0; kk < C::NCH; ++kk) kb[kk] = x.kb[kk];
+      if (has_lk) {
+        float cc[C::NB][4], ss[C::NB][4];
+#pragma unroll
+        for (int blk = 0; blk < C::NB; ++blk)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float2 bc = base_cs[buf][q * C::QPG + blk * 4 + i];
+            cc[blk][i] = bc.x * cd[blk][i] - bc.y * sd[blk][i];
+            ss[blk][i] = bc.y * cd[blk][i] + bc.x * sd[blk][i];
+          }
+        add_rotated_expansion<D, R>(kb, bkf, x.lk, cc, ss);
+      }
+      store_chunks<D>(k_lds[buf] + delta * C::K_ROW, kb, lane);
+#pragma unroll
+      for (int iv = 0; iv < C::NVL; ++iv)
+        *reinterpret_cast<u32x4*>(v_lds[buf] + (pw_ * 16 + vrow + C::RPL * iv) * C::V_ROW + vdim) = x.v[iv];
+      if (has_lv) {
+#pragma unroll
+        for (int rc = 0; rc < C::RC; ++rc)
+          if (rc * 16 + q * 4 < R)
+            *reinterpret_cast<u32x2*>(lv_lds[buf] + delta * C::LV_ROW + rc * 16 + q * 4) = x.lv[rc];
+      }
+    };
+    auto base_angles = [&](int64_t t0, int buf) {
+      if (has_lk && ptid < C::HALF) {
+        float c, s;
+        rope_cs((int)t0, a.w2pi[ptid], c, s);
+        base_cs[buf][ptid] = make_float2(c, s);
+      }
+    };
+    // Prologue: tile 0 into LDS buffer 0, tile 1 in flight.
+    TileRegs<D, R> x;
+    if (n_tiles > 0) {
+      tile_load<D, R>(x, Kb, Vb, Lk, Lv, row_el, pw_ * 16, kv_hi, lane);
+      base_angles(0, 0);
+    }
+    __syncthreads();  // [P1] base angles of tile 0
+    if (n_tiles > 0) rebuild(x, 0);
+    if (n_tiles > 1) {
+      tile_load<D, R>(x, Kb, Vb, Lk, Lv, row_el, TKV + pw_ * 16, kv_hi, lane);
+      base_angles(TKV, 1);
+    }
+    __syncthreads();  // [P2] tile 0 in LDS
+    for (int tile = 0; tile < n_tiles; ++tile) {
+      const int buf = tile & 1;
+      const int64_t t0 = (int64_t)tile * TKV;
+      if (tile + 1 < n_tiles) rebuild(x, buf ^ 1);
+      if (tile + 2 < n_tiles) {
+        tile_load<D, R>(x, Kb, Vb, Lk, Lv, row_el, t0 + 2 * TKV + pw_ * 16, kv_hi, lane);
+        base_angles(t0 + 2 * TKV, buf);
+      }
+      __syncthreads();  // [T] tile+1 in LDS; tile consumed
+    }
+    return;
   }
 
+  // ========================= consumer waves ================================
+  // Wave bounds: skip tiles no row of this wave sees; mask only tiles that
+  // reach past some row's last visible key.
+  int wave_last = (int)last, wave_first = row_ok ? (int)last : INT32_MAX;
+#pragma unroll
+  for (int x = 1; x < 64; x <<= 1) {
+    const int o1 = __shfl_xor(wave_last, x, 64), o2 = __shfl_xor(wave_first, x, 64);
+    wave_last = o1 > wave_last ? o1 : wave_last;
+    wave_first = o2 < wave_first ? o2 : wave_first;
+  }
   // Q^T as the B operand of S^T = K Q^T: lane col = row l%32,
   // k = (l/32)*8 + 0..7 within each 16-dim chunk.
   bf16x8 qf[C::NKQ];
@@ -97,121 +250,59 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
     for (int kk = 0; kk < C::NKQ; ++kk) qf[kk] = as_bf16x8(ld16(qp + kk * 16 + h32 * 8, row_ok));
   }
-
-  // Expansion operands B^T of this KV head (A operand of 16x16x16).
-  i16x4 bkf[C::NBLK][C::RC], bvf[C::NBLK][C::RC];
-  {
-    const int64_t off = (int64_t)b * a.b_stride + (int64_t)g * D * R;
-    load_bt_frags<D, R>(bkf, has_lk ? a.Bk + off : nullptr, has_lk, lane);
-    load_bt_frags<D, R>(bvf, has_lv ? a.Bv + off : nullptr, has_lv, lane);
-  }
-
-  __syncthreads();  // w_lds, s_maxpos ready
-  const int64_t kv_hi = (int64_t)s_maxpos + 1;  // keys [0, kv_hi) are needed
-
-  // RoPE offsets of this lane's rebuild token (tile offset 16w + l%16) for its
-  // 16 (or 8) frequencies, exact in fp64 once per kernel.
-  const int delta = w * 16 + c16;
-  float cd[C::NB][4], sd[C::NB][4];
-#pragma unroll
-  for (int blk = 0; blk < C::NB; ++blk)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) rope_cs(delta, w_lds[q * C::QPG + blk * 4 + i], cd[blk][i], sd[blk][i]);
-
-  const int64_t row_el = (int64_t)a.n_kv * D;
-  const uint16_t* Kb = a.Kb + (int64_t)b * a.kv_stride + (int64_t)g * D;
-  const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
-  const uint16_t* Lk = has_lk ? a.Lk + (int64_t)b * a.l_stride : nullptr;
-  const uint16_t* Lv = has_lv ? a.Lv + (int64_t)b * a.l_stride : nullptr;
-
-  f32x16 acc[C::NDB];
+  f32x16 acc[C::NDB];   // O^T: lane col = row l%32
+  f32x16 accl[C::RB];   // (P L_v)^T
 #pragma unroll
   for (int db = 0; db < C::NDB; ++db)
 #pragma unroll
     for (int j = 0; j < 16; ++j) acc[db][j] = 0.f;
+#pragma unroll
+  for (int rb = 0; rb < C::RB; ++rb)
+#pragma unroll
+    for (int j = 0; j < 16; ++j) accl[rb][j] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  for (int64_t t0 = 0; t0 < kv_hi; t0 += TKV) {
-    // ---- exact base angles of this tile --------------------------------
-    if (has_lk && tid < C::HALF) {
-      float c, s;
-      rope_cs((int)t0, w_lds[tid], c, s);
-      base_cs[tid] = make_float2(c, s);
-    }
-    __syncthreads();
-
-    // ---- rebuild 16 tokens per wave ------------------------------------
-    {
-      const int64_t t = t0 + delta;
-      const bool ok = t < kv_hi;
-      u32x4 kb[Rb<D, R>::NCH], vb[Rb<D, R>::NCH];
-      load_chunks<D>(kb, Kb + t * row_el, ok, lane);
-      load_chunks<D>(vb, Vb + t * row_el, ok, lane);
-      if (has_lk) {
-        u32x2 lk[C::RC];
-        load_lr_frag<R>(lk, Lk + t * R, ok, lane);
-        // Angle addition: (t0 + delta) * omega from the exact tile base and
-        // the exact per-lane offset.
-        float cc[C::NB][4], ss[C::NB][4];
-#pragma unroll
-        for (int blk = 0; blk < C::NB; ++blk)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float2 bc = base_cs[q * C::QPG + blk * 4 + i];
-            cc[blk][i] = bc.x * cd[blk][i] - bc.y * sd[blk][i];
-            ss[blk][i] = bc.y * cd[blk][i] + bc.x * sd[blk][i];
-          }
-        add_rotated_expansion<D, R>(kb, bkf, lk, cc, ss);
-      }
-      store_chunks<D>(k_lds + delta * C::K_ROW, kb, lane);
-      if (has_lv) {
-        u32x2 lv[C::RC];
-        load_lr_frag<R>(lv, Lv + t * R, ok, lane);
-        add_expansion<D, R>(vb, bvf, lv);
-      }
-      // V stored transposed, V^T[dim][token], for the PV operand.
-#pragma unroll
-      for (int kk = 0; kk < Rb<D, R>::NCH; ++kk) {
-        const int d0 = chunk_dim<D>(kk, q);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t u = vb[kk][e >> 1];
-          vt_lds[(d0 + e) * C::VT_ROW + delta] = (uint16_t)((e & 1) ? (u >> 16) : (u & 0xffffu));
-        }
-      }
-    }
-    __syncthreads();
-
-    // ---- scores, softmax and PV for this wave's 32 rows ----------------
+  __syncthreads();  // [P1]
+  __syncthreads();  // [P2]
+  for (int tile = 0; tile < n_tiles; ++tile) {
+    const int buf = tile & 1;
+    const int64_t t0 = (int64_t)tile * TKV;
     if (t0 <= (int64_t)wave_last) {
+      const uint16_t* kl = k_lds[buf];
       f32x16 s[2];
-#pragma unroll
-      for (int tb = 0; tb < 2; ++tb) {
-#pragma unroll
-        for (int j = 0; j < 16; ++j) s[tb][j] = 0.f;
-        const uint16_t* kr = k_lds + (tb * 32 + l32) * C::K_ROW + h32 * 8;
-#pragma unroll
-        for (int kk = 0; kk < C::NKQ; ++kk) {
-          const bf16x8 kfrag = as_bf16x8(*reinterpret_cast<const u32x4*>(kr + kk * 16));
-          s[tb] = mfma32x32x16(kfrag, qf[kk], s[tb]);
-        }
-      }
-      float mx = -INFINITY;
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int64_t t = t0 + tb * 32 + (j >> 2) * 8 + h32 * 4 + (j & 3);
-          const float v = t <= last ? s[tb][j] * a.scale_log2 : -INFINITY;
-          s[tb][j] = v;
-          mx = fmaxf(mx, v);
-        }
-      mx = fmaxf(mx, shfl_xor(mx, 32));
+        for (int j = 0; j < 16; ++j) s[tb][j] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < C::NKQ; ++kk)
+#pragma unroll
+        for (int tb = 0; tb < 2; ++tb)
+          s[tb] = mfma32x32x16(as_bf16x8(*reinterpret_cast<const u32x4*>(kl + (tb * 32 + l32) * C::K_ROW +
+                                                                          kk * 16 + h32 * 8)),
+                               qf[kk], s[tb]);
+      if (t0 + TKV - 1 > (int64_t)wave_first) {  // tile crosses some row's causal limit
+#pragma unroll
+        for (int tb = 0; tb < 2; ++tb)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) {
+            const int64_t t = t0 + tb * 32 + (j >> 2) * 8 + h32 * 4 + (j & 3);
+            if (t > last) s[tb][j] = -INFINITY;
+          }
+      }
+      float mx0 = s[0][0], mx1 = s[1][0];
+#pragma unroll
+      for (int j = 1; j < 16; ++j) {
+        mx0 = fmaxf(mx0, s[0][j]);
+        mx1 = fmaxf(mx1, s[1][j]);
+      }
+      float mx = fmaxf(mx0, mx1);
+      mx = fmaxf(mx, shfl_xor(mx, 32)) * a.scale_log2;
       const float mn = fmaxf(m_run, mx);
       const float ms = (mn == -INFINITY) ? 0.f : mn;
       const float alpha = fast_exp2(m_run - ms);
       m_run = mn;
-      float ls = 0.f;
+      float ls0 = 0.f, ls1 = 0.f;
       u32x4 pw[2][2];  // bf16 P: [token block][half of its 16 registers]
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb)
@@ -219,34 +310,66 @@ lrsa_prefill_kernel(const AttnArgs a) {
         for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
-            const float p0 = fast_exp2(s[tb][hf * 8 + 2 * c] - ms);
-            const float p1 = fast_exp2(s[tb][hf * 8 + 2 * c + 1] - ms);
-            ls += p0 + p1;
+            const float p0 = fast_exp2(__builtin_fmaf(s[tb][hf * 8 + 2 * c], a.scale_log2, -ms));
+            const float p1 = fast_exp2(__builtin_fmaf(s[tb][hf * 8 + 2 * c + 1], a.scale_log2, -ms));
+            ls0 += p0;
+            ls1 += p1;
             pw[tb][hf][c] = pack_bf16(p0, p1);
           }
-      l_run = l_run * alpha + ls;
+      l_run = l_run * alpha + (ls0 + ls1);
+      if (__ballot(alpha != 1.f)) {
 #pragma unroll
-      for (int db = 0; db < C::NDB; ++db)
+        for (int db = 0; db < C::NDB; ++db) acc[db] *= alpha;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) acc[db][j] *= alpha;
-      // O^T[dims x rows] += V^T[dims x 16 tok] P^T[16 tok x rows], 4 chunks.
+        for (int rb = 0; rb < C::RB; ++rb) accl[rb] *= alpha;
+      }
+      // O^T[dims x rows] += V^T[dims x 16 tok] P^T[16 tok x rows], 4 chunks;
+      // (P L_v)^T likewise with L_v^T.
+      const uint16_t* vt = v_lds[buf];
+      const uint16_t* lvt = lv_lds[buf];
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
         const bf16x8 pb = as_bf16x8(pw[m >> 1][m & 1]);
 #pragma unroll
-        for (int db = 0; db < C::NDB; ++db) {
-          const uint16_t* vr = vt_lds + (db * 32 + l32) * C::VT_ROW + m * 16 + h32 * 4;
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
-          const u32x2 hi = *reinterpret_cast<const u32x2*>(vr + 8);
-          const u32x4 va = {lo[0], lo[1], hi[0], hi[1]};
-          acc[db] = mfma32x32x16(as_bf16x8(va), pb, acc[db]);
+        for (int db = 0; db < C::NDB; ++db)
+          acc[db] = mfma32x32x16(lds_tr_a32(vt, C::V_ROW, m, db * 32, lane), pb, acc[db]);
+        if (has_lv) {
+#pragma unroll
+          for (int rb = 0; rb < C::RB; ++rb)
+            accl[rb] = mfma32x32x16(lds_tr_a32(lvt, C::LV_ROW, m, rb * 32, lane), pb, accl[rb]);
         }
       }
     }
-    __syncthreads();
+    __syncthreads();  // [T]
   }
 
-  // ---- epilogue: O = acc / l, lse -----------------------------------------
+  // ---- epilogue: O^T += B_v^T (P L_v)^T, then O = acc / l, lse -------------
+  if (has_lv) {
+    // (P L_v)^T registers of rank chunk jc (16 ranks) are the B operand in
+    // the same k order as P; split into bf16 hi + lo to keep fp32 accuracy.
+#pragma unroll
+    for (int jc = 0; jc < C::RC; ++jc) {
+      const int rb = jc >> 1, j0 = 8 * (jc & 1);
+      u32x4 hi, lo;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const float x0 = accl[rb][j0 + 2 * c], x1 = accl[rb][j0 + 2 * c + 1];
+        hi[c] = pack_bf16(x0, x1);
+        lo[c] = pack_bf16(x0 - bf_lo(hi[c]), x1 - bf_hi(hi[c]));
+      }
+      const int r0 = 16 * jc + 4 * h32;
+#pragma unroll
+      for (int db = 0; db < C::NDB; ++db) {
+        const int dim = db * 32 + l32;
+        const uint16_t* bv = a.Bv + (int64_t)b * a.b_stride + ((int64_t)g * D + dim) * R;
+        const u32x2 b0 = ld8(bv + r0, r0 < R);
+        const u32x2 b1 = ld8(bv + r0 + 8, r0 + 8 < R);
+        const u32x4 bw = {b0[0], b0[1], b1[0], b1[1]};
+        acc[db] = mfma32x32x16(as_bf16x8(bw), as_bf16x8(hi), acc[db]);
+        acc[db] = mfma32x32x16(as_bf16x8(bw), as_bf16x8(lo), acc[db]);
+      }
+    }
+  }
   const float l_tot = l_run + shfl_xor(l_run, 32);
   if (!row_ok) return;
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -270,8 +393,7 @@ template <int D, int R>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const int n_rows = a.n_tok * a.group;
   const int tiles = (n_rows + BROWS - 1) / BROWS;
-  hipLaunchKernelGGL((lrsa_prefill_kernel<D, R>), dim3(tiles, a.n_kv, a.batch), dim3(64 * NWAVE), 0,
-                     st, a);
+  hipLaunchKernelGGL((lrsa_prefill_kernel<D, R>), dim3(tiles, a.n_kv, a.batch), dim3(NTHR), 0, st, a);
   return hipGetLastError();
 }
 
