@@ -324,26 +324,38 @@ lrsa_decode_kernel(const AttnArgs a) {
 
 // Merge the split partials of one (request, q head): log-sum-exp weights,
 // then the deferred up-projection O += (sum_s w_s P_s L_v) B_v, then 1/l.
+// Four waves each fold a quarter of the splits (independent loads in flight),
+// and the four partial sums meet in LDS.
+constexpr int MW = 4;  // waves per merge workgroup
+
 template <int D, int R>
-__global__ void __launch_bounds__(64)
+__global__ void __launch_bounds__(64 * MW)
 lrsa_merge_kernel(const AttnArgs a) {
   constexpr int PS = 4 + D + R, DPL = D / 64;
-  __shared__ float accl_s[64];
-  const int h = blockIdx.x, b = blockIdx.y, lane = threadIdx.x;
+  __shared__ float red_acc[MW][D];
+  __shared__ float red_lr[MW][64];
+  __shared__ float red_l[MW];
+  __shared__ float red_m[MW];
+  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int g = h / a.group;
   const bool has_lv = a.Lv != nullptr;
   const float* base = a.ws + ((int64_t)b * a.n_q + h) * (int64_t)a.n_splits * PS;
 
   float M = -INFINITY;
-  for (int s = lane; s < a.n_splits; s += 64) M = fmaxf(M, base[(int64_t)s * PS]);
+  for (int s = tid; s < a.n_splits; s += 64 * MW) M = fmaxf(M, base[(int64_t)s * PS]);
 #pragma unroll
   for (int x = 1; x < 64; x <<= 1) M = fmaxf(M, shfl_xor(M, x));
+  if (lane == 0) red_m[w] = M;
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < MW; ++i) M = fmaxf(M, red_m[i]);
   const float Ms = (M == -INFINITY) ? 0.f : M;
 
   float L = 0.f, accl = 0.f, acc[DPL];
 #pragma unroll
   for (int dd = 0; dd < DPL; ++dd) acc[dd] = 0.f;
-  for (int s = 0; s < a.n_splits; ++s) {
+#pragma unroll 4
+  for (int s = w; s < a.n_splits; s += MW) {
     const float* p = base + (int64_t)s * PS;
     const float wgt = fast_exp2(p[0] - Ms);
     L += wgt * p[1];
@@ -351,9 +363,29 @@ lrsa_merge_kernel(const AttnArgs a) {
     for (int dd = 0; dd < DPL; ++dd) acc[dd] += wgt * p[4 + lane + 64 * dd];
     if (has_lv && lane < R) accl += wgt * p[4 + D + lane];
   }
+#pragma unroll
+  for (int dd = 0; dd < DPL; ++dd) red_acc[w][lane + 64 * dd] = acc[dd];
+  red_lr[w][lane] = accl;
+  if (lane == 0) red_l[w] = L;
+  __syncthreads();
+  if (w != 0) return;
+#pragma unroll
+  for (int dd = 0; dd < DPL; ++dd) {
+    acc[dd] = 0.f;
+#pragma unroll
+    for (int i = 0; i < MW; ++i) acc[dd] += red_acc[i][lane + 64 * dd];
+  }
+  L = 0.f;
+#pragma unroll
+  for (int i = 0; i < MW; ++i) L += red_l[i];
   if (has_lv) {
-    if (lane < R) accl_s[lane] = accl;
-    __syncthreads();
+    // The four waves' P L_v sums, added in lane order into red_lr[0].
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < MW; ++i) t += red_lr[i][lane];
+    __builtin_amdgcn_wave_barrier();
+    red_lr[0][lane] = t;
+    __builtin_amdgcn_wave_barrier();
 #pragma unroll
     for (int dd = 0; dd < DPL; ++dd) {
       const int dim = lane + 64 * dd;
@@ -363,7 +395,8 @@ lrsa_merge_kernel(const AttnArgs a) {
       for (int j = 0; j < R; j += 8) {
         const u32x4 u = *reinterpret_cast<const u32x4*>(bv + j);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) sum += accl_s[j + 2 * c] * bf_lo(u[c]) + accl_s[j + 2 * c + 1] * bf_hi(u[c]);
+        for (int c = 0; c < 4; ++c)
+          sum += red_lr[0][j + 2 * c] * bf_lo(u[c]) + red_lr[0][j + 2 * c + 1] * bf_hi(u[c]);
       }
       acc[dd] += sum;
     }
@@ -385,7 +418,7 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((lrsa_decode_kernel<D, R>), dim3(a.n_splits, hg, a.batch), dim3(NT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch), dim3(64), 0, st, a);
+  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch), dim3(64 * MW), 0, st, a);
   return hipGetLastError();
 }
 
