@@ -51,8 +51,11 @@ struct Dec {
   static constexpr int RC = RCH(R);           // 16-wide rank chunks
   static constexpr int CS_ROW = HALF + 2;     // float2 per table row (padded)
   static constexpr int EPT = TK * HALF / NT;  // table entries per thread
-  static constexpr int V_ROW = D + 16;        // bf16 per V row in LDS
-  static constexpr int LV_ROW = 16 * RC + 16; // bf16 per L_v row in LDS
+  // Row strides of the tiles read with ds_read_b64_tr_b16: the two 16-lane
+  // groups serviced together read 8 consecutive rows of 32 bytes, which land
+  // on disjoint banks when the stride is an odd multiple of 8 dwords mod 64.
+  static constexpr int V_ROW = D + 16;                          // 72 / 40 dwords
+  static constexpr int LV_ROW = RC == 1 ? 16 : (RC == 2 ? 48 : 80);  // 8 / 24 / 40 dwords
   static constexpr int LPR = D / 8;           // lanes per V row (16 bytes each)
   static constexpr int RPL = 64 / LPR;        // V rows per wave load
   static constexpr int NVL = 16 / RPL;        // V loads per sub-block

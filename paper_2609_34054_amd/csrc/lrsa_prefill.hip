@@ -8,16 +8,17 @@
 //           L_v tiles go to LDS unchanged, P L_v is accumulated beside P V_base
 //           and B_v is applied once in the epilogue.
 //
-// Work split: one workgroup per (request, KV head, 128 query rows).  A query
-// row is a (token, q head of the GQA group) pair, so the group's heads share
-// every rebuilt tile.  The workgroup's 8 waves specialise:
-//   producers (waves 4-7) load KV tile k+2 from HBM while rebuilding tile k+1
+// Work split: one workgroup per (request, KV head, 32 * NCONS query rows).  A
+// query row is a (token, q head of the GQA group) pair, so the group's heads
+// share every rebuilt tile.  The workgroup's NCONS + 4 waves specialise:
+//   producers (last 4 waves) load KV tile k+2 from HBM while rebuilding tile k+1
 //             into LDS: E^T = B_k^T L_k^T on 16x16x16 MFMAs (lane l: token
 //             l%16, both RoPE halves of each pair in the same lane), RoPE by
 //             angle addition (exact per-tile base angle in LDS, exact per-lane
 //             offsets in registers), + base, bf16, stored as K[tok][dim];
 //             V_base and L_v rows are stored as they are;
-//   consumers (waves 0-3, 32 rows each) attend over tile k:
+//   consumers (first NCONS waves, 32 rows each) attend over tile k, in two
+//             halves of 32 tokens:
 //     scores  S^T = K Q^T on 32x32x16 MFMAs: lane l holds row l%32 and 32 of
 //             the tile's tokens, so softmax statistics are per lane;
 //     softmax online, exp2 domain, running max shared by lanes l and l^32;
@@ -26,8 +27,9 @@
 //             V^T and L_v^T come from row-major LDS tiles through the
 //             transposing LDS read, P is already in the B operand layout,
 //             and the softmax rescale is a per-lane scalar.
-// LDS is double-buffered with one barrier per tile; a producer and a consumer
-// share each SIMD, so the rebuild's vector work overlaps the MFMAs.
+// LDS is double-buffered with one barrier per tile; producers and consumers
+// share each SIMD, so the rebuild's vector work overlaps the MFMAs, and with
+// 8 consumers each rebuilt tile serves 256 query rows.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
@@ -36,14 +38,17 @@ namespace prc {
 namespace {
 
 constexpr int TKV = 64;      // KV tokens per tile
-constexpr int NCONS = 4;     // consumer waves (32 query rows each)
 constexpr int NPROD = 4;     // producer waves (16 rebuilt tokens each)
-constexpr int NTHR = 64 * (NCONS + NPROD);
 constexpr int WROWS = 32;    // query rows per consumer wave
-constexpr int BROWS = NCONS * WROWS;
 
 template <int D, int R>
 struct Pre {
+  // Consumer waves (32 query rows each).  Eight fit three workgroup-waves per
+  // SIMD within the register file; the widest accumulators (d = 128 with
+  // rank >= 32) need the registers of two per SIMD, so they take four.
+  static constexpr int NCONS = (D == 128 && R >= 32) ? 4 : 8;
+  static constexpr int NTHR = 64 * (NCONS + NPROD);
+  static constexpr int BROWS = NCONS * WROWS;
   static constexpr int HALF = D / 2;
   static constexpr int NB = D / 32;          // 16-dim blocks per RoPE half
   static constexpr int NBLK = D / 16;
@@ -54,8 +59,12 @@ struct Pre {
   static constexpr int NKQ = D / 16;         // 32x32x16 k-chunks over d
   static constexpr int NDB = D / 32;         // 32-dim blocks of O^T
   static constexpr int K_ROW = D + 8;        // bf16 per K row in LDS
-  static constexpr int V_ROW = D + 16;       // bf16 per V row in LDS
-  static constexpr int LV_ROW = 32 * RB + 16;  // bf16 per L_v row in LDS
+  // Row strides of the tiles read with ds_read_b64_tr_b16: the two 16-lane
+  // groups serviced together read the same 4 rows at column offsets 8 dwords
+  // apart, which land on disjoint banks when the stride is 16 or 48 dwords
+  // mod 64.
+  static constexpr int V_ROW = D + 32;                   // 80 / 48 dwords
+  static constexpr int LV_ROW = RB == 1 ? 32 : 96;       // 16 / 48 dwords
   static constexpr int LPR = D / 8;          // lanes per V row (16 bytes each)
   static constexpr int RPL = 64 / LPR;       // V rows per wave load
   static constexpr int NVL = 16 / RPL;       // V loads per wave per tile
@@ -107,7 +116,7 @@ __device__ __forceinline__ void tile_load(TileRegs<D, R>& x, const uint16_t* Kb,
 }
 
 template <int D, int R>
-__global__ void __launch_bounds__(NTHR)
+__global__ void __launch_bounds__((Pre<D, R>::NTHR))
 lrsa_prefill_kernel(const AttnArgs a) {
   using C = Pre<D, R>;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][TKV * C::K_ROW];
@@ -121,19 +130,19 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int rtile = gridDim.x - 1 - blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int G = a.group;
   const int n_rows = a.n_tok * G;
-  const bool consumer = w < NCONS;
+  const bool consumer = w < C::NCONS;
   const bool has_lk = a.Lk != nullptr, has_lv = a.Lv != nullptr;
 
   if (tid == 0) s_maxpos = -1;
   // L_v columns past the rank stay zero in both buffers.
-  for (int i = tid; i < 2 * TKV * C::LV_ROW; i += NTHR) (&lv_lds[0][0])[i] = 0;
+  for (int i = tid; i < 2 * TKV * C::LV_ROW; i += C::NTHR) (&lv_lds[0][0])[i] = 0;
 
   int64_t kvl = a.kv_len[b];
   kvl = kvl < 0 ? 0 : (kvl > a.s_cap ? a.s_cap : kvl);
 
   // Consumer lane's query row (the same row for lanes l and l^32).
   const int l32 = lane & 31, h32 = lane >> 5;
-  const int row = rtile * BROWS + w * WROWS + l32;
+  const int row = rtile * C::BROWS + w * WROWS + l32;
   const bool row_ok = consumer && row < n_rows;
   const int qi = row_ok ? row / G : 0, hh = row_ok ? row - qi * G : 0;
   const int pos = row_ok ? a.positions[(int64_t)b * a.n_tok + qi] : -1;
@@ -153,8 +162,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
 
   if (!consumer) {
     // ======================= producer waves ================================
-    const int pw_ = w - NCONS;             // 0..3: tokens 16*pw_ .. +15 of a tile
-    const int ptid = tid - 64 * NCONS;     // 0..255
+    const int pw_ = w - C::NCONS;            // 0..3: tokens 16*pw_ .. +15 of a tile
+    const int ptid = tid - 64 * C::NCONS;    // 0..255
     const int q = lane >> 4, c16 = lane & 15;
     const int delta = pw_ * 16 + c16;      // this lane's rebuild token in a tile
     const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
@@ -267,55 +276,46 @@ lrsa_prefill_kernel(const AttnArgs a) {
   for (int tile = 0; tile < n_tiles; ++tile) {
     const int buf = tile & 1;
     const int64_t t0 = (int64_t)tile * TKV;
-    if (t0 <= (int64_t)wave_last) {
-      const uint16_t* kl = k_lds[buf];
-      f32x16 s[2];
+    // The tile is consumed as two 32-token halves, each with its own online
+    // softmax update (half the live score and P registers of a whole tile).
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb)
+    for (int tb = 0; tb < 2; ++tb) {
+      const int64_t th = t0 + tb * 32;  // first token of this half
+      if (th > (int64_t)wave_last) break;
+      const uint16_t* kl = k_lds[buf] + (tb * 32 + l32) * C::K_ROW + h32 * 8;
+      f32x16 s;
 #pragma unroll
-        for (int j = 0; j < 16; ++j) s[tb][j] = 0.f;
+      for (int j = 0; j < 16; ++j) s[j] = 0.f;
 #pragma unroll
       for (int kk = 0; kk < C::NKQ; ++kk)
+        s = mfma32x32x16(as_bf16x8(*reinterpret_cast<const u32x4*>(kl + kk * 16)), qf[kk], s);
+      if (th + 31 > (int64_t)wave_first) {  // this half crosses some row's causal limit
+        // Positions fit in 32 bits (s_cap < 2^31): key t is masked iff t > last.
+        const int rel = (int)last - (int)th - h32 * 4;  // last - (first token of this lane)
 #pragma unroll
-        for (int tb = 0; tb < 2; ++tb)
-          s[tb] = mfma32x32x16(as_bf16x8(*reinterpret_cast<const u32x4*>(kl + (tb * 32 + l32) * C::K_ROW +
-                                                                          kk * 16 + h32 * 8)),
-                               qf[kk], s[tb]);
-      if (t0 + TKV - 1 > (int64_t)wave_first) {  // tile crosses some row's causal limit
-#pragma unroll
-        for (int tb = 0; tb < 2; ++tb)
-#pragma unroll
-          for (int j = 0; j < 16; ++j) {
-            const int64_t t = t0 + tb * 32 + (j >> 2) * 8 + h32 * 4 + (j & 3);
-            if (t > last) s[tb][j] = -INFINITY;
-          }
+        for (int j = 0; j < 16; ++j)
+          if ((j >> 2) * 8 + (j & 3) > rel) s[j] = -INFINITY;
       }
-      float mx0 = s[0][0], mx1 = s[1][0];
+      float mx = s[0];
 #pragma unroll
-      for (int j = 1; j < 16; ++j) {
-        mx0 = fmaxf(mx0, s[0][j]);
-        mx1 = fmaxf(mx1, s[1][j]);
-      }
-      float mx = fmaxf(mx0, mx1);
+      for (int j = 1; j < 16; ++j) mx = fmaxf(mx, s[j]);
       mx = fmaxf(mx, shfl_xor(mx, 32)) * a.scale_log2;
       const float mn = fmaxf(m_run, mx);
       const float ms = (mn == -INFINITY) ? 0.f : mn;
       const float alpha = fast_exp2(m_run - ms);
       m_run = mn;
       float ls0 = 0.f, ls1 = 0.f;
-      u32x4 pw[2][2];  // bf16 P: [token block][half of its 16 registers]
+      u32x4 pw[2];  // bf16 P of this half, one per 16-token chunk
 #pragma unroll
-      for (int tb = 0; tb < 2; ++tb)
+      for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-          for (int c = 0; c < 4; ++c) {
-            const float p0 = fast_exp2(__builtin_fmaf(s[tb][hf * 8 + 2 * c], a.scale_log2, -ms));
-            const float p1 = fast_exp2(__builtin_fmaf(s[tb][hf * 8 + 2 * c + 1], a.scale_log2, -ms));
-            ls0 += p0;
-            ls1 += p1;
-            pw[tb][hf][c] = pack_bf16(p0, p1);
-          }
+        for (int c = 0; c < 4; ++c) {
+          const float p0 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c], a.scale_log2, -ms));
+          const float p1 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c + 1], a.scale_log2, -ms));
+          ls0 += p0;
+          ls1 += p1;
+          pw[hf][c] = pack_bf16(p0, p1);
+        }
       l_run = l_run * alpha + (ls0 + ls1);
       if (__ballot(alpha != 1.f)) {
 #pragma unroll
@@ -323,13 +323,14 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
         for (int rb = 0; rb < C::RB; ++rb) accl[rb] *= alpha;
       }
-      // O^T[dims x rows] += V^T[dims x 16 tok] P^T[16 tok x rows], 4 chunks;
-      // (P L_v)^T likewise with L_v^T.
+      // O^T[dims x rows] += V^T[dims x 16 tok] P^T[16 tok x rows] for the two
+      // 16-token chunks of this half; (P L_v)^T likewise with L_v^T.
       const uint16_t* vt = v_lds[buf];
       const uint16_t* lvt = lv_lds[buf];
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const bf16x8 pb = as_bf16x8(pw[m >> 1][m & 1]);
+      for (int hf = 0; hf < 2; ++hf) {
+        const int m = 2 * tb + hf;
+        const bf16x8 pb = as_bf16x8(pw[hf]);
 #pragma unroll
         for (int db = 0; db < C::NDB; ++db)
           acc[db] = mfma32x32x16(lds_tr_a32(vt, C::V_ROW, m, db * 32, lane), pb, acc[db]);
@@ -392,8 +393,9 @@ lrsa_prefill_kernel(const AttnArgs a) {
 template <int D, int R>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const int n_rows = a.n_tok * a.group;
-  const int tiles = (n_rows + BROWS - 1) / BROWS;
-  hipLaunchKernelGGL((lrsa_prefill_kernel<D, R>), dim3(tiles, a.n_kv, a.batch), dim3(NTHR), 0, st, a);
+  using C = Pre<D, R>;
+  const int tiles = (n_rows + C::BROWS - 1) / C::BROWS;
+  hipLaunchKernelGGL((lrsa_prefill_kernel<D, R>), dim3(tiles, a.n_kv, a.batch), dim3(C::NTHR), 0, st, a);
   return hipGetLastError();
 }
 
