@@ -8,28 +8,28 @@
 //           L_v tiles go to LDS unchanged, P L_v is accumulated beside P V_base
 //           and B_v is applied once in the epilogue.
 //
-// Work split: one workgroup per (request, KV head, 32 * NCONS query rows).  A
-// query row is a (token, q head of the GQA group) pair, so the group's heads
-// share every rebuilt tile.  The workgroup's NCONS + 4 waves specialise:
-//   producers (last 4 waves) load KV tile k+2 from HBM while rebuilding tile k+1
-//             into LDS: E^T = B_k^T L_k^T on 16x16x16 MFMAs (lane l: token
-//             l%16, both RoPE halves of each pair in the same lane), RoPE by
-//             angle addition (exact per-tile base angle in LDS, exact per-lane
-//             offsets in registers), + base, bf16, stored as K[tok][dim];
-//             V_base and L_v rows are stored as they are;
-//   consumers (first NCONS waves, 32 rows each) attend over tile k, in two
-//             halves of 32 tokens:
-//     scores  S^T = K Q^T on 32x32x16 MFMAs: lane l holds row l%32 and 32 of
-//             the tile's tokens, so softmax statistics are per lane;
-//     softmax online, exp2 domain, running max shared by lanes l and l^32;
-//             the causal mask is applied only on tiles that cross it;
+// Work split: one workgroup of 8 waves per (request, KV head, 256 query rows).
+// A query row is a (token, q head of the GQA group) pair, so the group's heads
+// share every rebuilt tile.  Every wave both builds and attends:
+//   build   wave w rebuilds 16 tokens (w % 4) x half of the RoPE pair blocks
+//           (w / 4) of the next KV tile: E^T = B_k^T L_k^T on 16x16x16 MFMAs
+//           (lane l: token l%16, both halves of each pair in the same lane),
+//           RoPE by angle addition (exact per-tile base angle in LDS, exact
+//           per-lane offsets in registers), + base, bf16 into LDS; it also
+//           copies 8 rows of V_base and L_v.  Its global loads for the tile
+//           after next are in flight meanwhile;
+//   attend  over 32 query rows (lanes l and l^32 share row l%32), in two
+//           halves of 32 tokens:
+//     scores  S^T = K Q^T on 32x32x16 MFMAs, so softmax statistics are per
+//             lane; causal mask only on halves that cross it;
+//     softmax online, exp2 domain, lazily rescaled;
 //     PV      O^T += V^T P^T and (P L_v)^T += L_v^T P^T on 32x32x16 MFMAs;
 //             V^T and L_v^T come from row-major LDS tiles through the
-//             transposing LDS read, P is already in the B operand layout,
-//             and the softmax rescale is a per-lane scalar.
-// LDS is double-buffered with one barrier per tile; producers and consumers
-// share each SIMD, so the rebuild's vector work overlaps the MFMAs, and with
-// 8 consumers each rebuilt tile serves 256 query rows.
+//             transposing LDS read, one MFMA ahead; P is already in the B
+//             operand layout.
+// The two waves that share a SIMD run the two jobs in opposite order, so one
+// wave's rebuild (vector ALU) overlaps the other's MFMAs.  LDS is
+// double-buffered with one barrier per tile.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
@@ -37,22 +37,19 @@
 namespace prc {
 namespace {
 
-constexpr int TKV = 64;      // KV tokens per tile
-constexpr int NPROD = 4;     // producer waves (16 rebuilt tokens each)
-constexpr int WROWS = 32;    // query rows per consumer wave
+constexpr int TKV = 64;              // KV tokens per tile
+constexpr int NW = 8;                // waves per workgroup
+constexpr int NTHR = 64 * NW;
+constexpr int WROWS = 32;            // query rows per wave
+constexpr int BROWS = NW * WROWS;    // query rows per workgroup
+constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (log2 domain)
 
 template <int D, int R>
 struct Pre {
-  // Consumer waves (32 query rows each).  Eight fit three workgroup-waves per
-  // SIMD within the register file; the widest accumulators (d = 128 with
-  // rank >= 32) need the registers of two per SIMD, so they take four.
-  static constexpr int NCONS = (D == 128 && R >= 32) ? 4 : 8;
-  static constexpr int NTHR = 64 * (NCONS + NPROD);
-  static constexpr int BROWS = NCONS * WROWS;
   static constexpr int HALF = D / 2;
   static constexpr int NB = D / 32;          // 16-dim blocks per RoPE half
-  static constexpr int NBLK = D / 16;
-  static constexpr int NCH = D / 32;         // 8-dim chunks per lane (rebuild)
+  static constexpr int NBW = NB / 2;         // low blocks rebuilt per wave
+  static constexpr int SEG = 4 * NBW;        // contiguous dims per lane and half
   static constexpr int QPG = D / 8;          // dims per lane group per half
   static constexpr int RC = RCH(R);          // 16-wide rank chunks
   static constexpr int RB = (R + 31) / 32;   // 32-row blocks of (P L_v)^T
@@ -65,10 +62,45 @@ struct Pre {
   // mod 64.
   static constexpr int V_ROW = D + 32;                   // 80 / 48 dwords
   static constexpr int LV_ROW = RB == 1 ? 32 : 96;       // 16 / 48 dwords
-  static constexpr int LPR = D / 8;          // lanes per V row (16 bytes each)
-  static constexpr int RPL = 64 / LPR;       // V rows per wave load
-  static constexpr int NVL = 16 / RPL;       // V loads per wave per tile
+  static constexpr int VLPR = D / 8;         // lanes per V row (16 bytes each)
+  static constexpr int VRPL = 64 / VLPR;     // V rows per wave load
+  static constexpr int NVL = 8 / VRPL;       // V loads per wave per tile (8 rows)
+  static constexpr int LVW = R < 16 ? 1 : R / 16;  // L_v words per lane (8 rows)
 };
+
+// SEG consecutive bf16 of one row.
+template <int SEG>
+struct Seg {
+  uint32_t w[SEG / 2];
+};
+template <int SEG>
+__device__ __forceinline__ Seg<SEG> ld_seg(const uint16_t* p, bool ok) {
+  Seg<SEG> s;
+  if constexpr (SEG == 8) {
+    const u32x4 v = ld16(p, ok);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s.w[i] = v[i];
+  } else {
+    const u32x2 v = ld8(p, ok);
+    s.w[0] = v[0];
+    s.w[1] = v[1];
+  }
+  return s;
+}
+template <int SEG>
+__device__ __forceinline__ void st_seg(uint16_t* p, const Seg<SEG>& s) {
+  if constexpr (SEG == 8) {
+    const u32x4 v = {s.w[0], s.w[1], s.w[2], s.w[3]};
+    *reinterpret_cast<u32x4*>(p) = v;
+  } else {
+    const u32x2 v = {s.w[0], s.w[1]};
+    *reinterpret_cast<u32x2*>(p) = v;
+  }
+}
+template <int SEG>
+__device__ __forceinline__ float seg_get(const Seg<SEG>& s, int e) {
+  return (e & 1) ? bf_hi(s.w[e >> 1]) : bf_lo(s.w[e >> 1]);
+}
 
 __device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) {
   typedef short v4s __attribute__((ext_vector_type(4)));
@@ -89,40 +121,27 @@ __device__ __forceinline__ bf16x8 lds_tr_a32(const uint16_t* tile, int row_strid
   return __builtin_bit_cast(bf16x8, v);
 }
 
+// Global data one wave stages for one KV tile.
 template <int D, int R>
-struct TileRegs {
-  u32x4 kb[D / 32];          // K_base chunks of this lane's rebuild token
-  u32x2 lk[RCH(R)];          // L_k fragment of that token
-  u32x4 v[Pre<D, R>::NVL];   // V_base rows of the wave's 16 tokens
-  u32x2 lv[RCH(R)];          // L_v fragment of this lane's rebuild token
+struct Unit {
+  Seg<Pre<D, R>::SEG> klo, khi;   // K_base of the lane's rebuild token, both halves
+  u32x2 lk[RCH(R)];               // L_k row of that token (expansion B operand)
+  u32x4 v[Pre<D, R>::NVL];        // V_base rows 8w .. 8w+7
+  uint32_t lv[Pre<D, R>::LVW];    // L_v rows 8w .. 8w+7
 };
 
-template <int D, int R>
-__device__ __forceinline__ void tile_load(TileRegs<D, R>& x, const uint16_t* Kb, const uint16_t* Vb,
-                                          const uint16_t* Lk, const uint16_t* Lv, int64_t row_el, int64_t t0w,
-                                          int64_t kv_hi, int lane) {
-  using C = Pre<D, R>;
-  const int64_t t = t0w + (lane & 15);
-  const bool ok = t < kv_hi;
-  load_chunks<D>(x.kb, Kb + t * row_el, ok, lane);
-  if (Lk != nullptr) load_lr_frag<R>(x.lk, Lk + t * R, ok, lane);
-  if (Lv != nullptr) load_lr_frag<R>(x.lv, Lv + t * R, ok, lane);
-  const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
-#pragma unroll
-  for (int iv = 0; iv < C::NVL; ++iv) {
-    const int64_t tv = t0w + vrow + C::RPL * iv;
-    x.v[iv] = ld16(Vb + tv * row_el + vdim, tv < kv_hi);
-  }
-}
-
-template <int D, int R>
-__global__ void __launch_bounds__((Pre<D, R>::NTHR))
+template <int D, int R, bool LK, bool LV>
+__global__ void __launch_bounds__(NTHR)
 lrsa_prefill_kernel(const AttnArgs a) {
   using C = Pre<D, R>;
+  constexpr bool ones_sum = LV && R < 32;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][TKV * C::K_ROW];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][TKV * C::V_ROW];
   __shared__ __attribute__((aligned(16))) uint16_t lv_lds[2][TKV * C::LV_ROW];
-  __shared__ float2 base_cs[2][C::HALF];
+  __shared__ __attribute__((aligned(16))) float2 base_cs[2][C::HALF];
+  // cos/sin of each build lane's in-tile offset at its SEG frequencies,
+  // [wave][pair of frequencies][lane] (one 16-byte read per pair).
+  __shared__ __attribute__((aligned(16))) f32x4 off_cs[LK ? NW : 1][C::SEG / 2][64];
   __shared__ int s_maxpos;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -130,20 +149,23 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int rtile = gridDim.x - 1 - blockIdx.x, g = blockIdx.y, b = blockIdx.z;
   const int G = a.group;
   const int n_rows = a.n_tok * G;
-  const bool consumer = w < C::NCONS;
-  const bool has_lk = a.Lk != nullptr, has_lv = a.Lv != nullptr;
 
   if (tid == 0) s_maxpos = -1;
-  // L_v columns past the rank stay zero in both buffers.
-  for (int i = tid; i < 2 * TKV * C::LV_ROW; i += C::NTHR) (&lv_lds[0][0])[i] = 0;
+  // L_v columns past the rank stay zero in both buffers, except that with
+  // rank < 32 column `rank` holds ones: the (P L_v)^T product then carries the
+  // softmax row sums in its spare row for free.
+  if constexpr (LV) {
+    for (int i = tid; i < 2 * TKV * C::LV_ROW; i += NTHR)
+      (&lv_lds[0][0])[i] = (ones_sum && i % C::LV_ROW == R) ? (uint16_t)0x3F80 : (uint16_t)0;
+  }
 
   int64_t kvl = a.kv_len[b];
   kvl = kvl < 0 ? 0 : (kvl > a.s_cap ? a.s_cap : kvl);
 
-  // Consumer lane's query row (the same row for lanes l and l^32).
+  // This lane's query row (the same row for lanes l and l^32).
   const int l32 = lane & 31, h32 = lane >> 5;
-  const int row = rtile * C::BROWS + w * WROWS + l32;
-  const bool row_ok = consumer && row < n_rows;
+  const int row = rtile * BROWS + w * WROWS + l32;
+  const bool row_ok = row < n_rows;
   const int qi = row_ok ? row / G : 0, hh = row_ok ? row - qi * G : 0;
   const int pos = row_ok ? a.positions[(int64_t)b * a.n_tok + qi] : -1;
   const int64_t last = (int64_t)pos < kvl - 1 ? (int64_t)pos : kvl - 1;  // last visible key
@@ -157,91 +179,112 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int64_t row_el = (int64_t)a.n_kv * D;
   const uint16_t* Kb = a.Kb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
-  const uint16_t* Lk = has_lk ? a.Lk + (int64_t)b * a.l_stride : nullptr;
-  const uint16_t* Lv = has_lv ? a.Lv + (int64_t)b * a.l_stride : nullptr;
+  const uint16_t* Lk = LK ? a.Lk + (int64_t)b * a.l_stride : nullptr;
+  const uint16_t* Lv = LV ? a.Lv + (int64_t)b * a.l_stride : nullptr;
 
-  if (!consumer) {
-    // ======================= producer waves ================================
-    const int pw_ = w - C::NCONS;            // 0..3: tokens 16*pw_ .. +15 of a tile
-    const int ptid = tid - 64 * C::NCONS;    // 0..255
-    const int q = lane >> 4, c16 = lane & 15;
-    const int delta = pw_ * 16 + c16;      // this lane's rebuild token in a tile
-    const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
-    i16x4 bkf[C::NBLK][C::RC];
-    load_bt_frags<D, R>(bkf, has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr, has_lk,
-                        lane);
-    // RoPE offsets of token `delta` for this lane's D/8 frequencies, exact in
-    // fp64 once per kernel.
-    float cd[C::NB][4], sd[C::NB][4];
+  // ---- build role: 16 tokens x SEG pair dims, 8 V rows, 8 L_v rows --------
+  const int q = lane >> 4, c16 = lane & 15;
+  const int tg = w & 3, ph = w >> 2;
+  const int blk0 = ph * C::NBW;                    // first low 16-dim block
+  const int lo_dim0 = q * C::QPG + blk0 * 4;       // first low dim of this lane
+  const int delta = 16 * tg + c16;                 // rebuild token within a tile
+  const int vrow = lane / C::VLPR, vdim = (lane % C::VLPR) * 8;
+  i16x4 bkf[2 * C::NBW][C::RC];  // B_k^T fragments: low blocks, then their partners
+  if constexpr (LK) {
+    const uint16_t* bhead = a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R;
 #pragma unroll
-    for (int blk = 0; blk < C::NB; ++blk)
+    for (int i = 0; i < 2 * C::NBW; ++i) {
+      const int blk = blk0 + (i % C::NBW) + (i / C::NBW) * C::NB;
+      const int dim = blk_dim<D>(blk, c16);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        cd[blk][i] = 1.f;
-        sd[blk][i] = 0.f;
-        if (has_lk) rope_cs(delta, a.w2pi[q * C::QPG + blk * 4 + i], cd[blk][i], sd[blk][i]);
+      for (int rc = 0; rc < C::RC; ++rc) {
+        const int r0 = rc * 16 + q * 4;
+        bkf[i][rc] = as_i16x4(ld8(bhead + (int64_t)dim * R + (r0 < R ? r0 : 0), r0 < R));
       }
-    auto rebuild = [&](const TileRegs<D, R>& x, int buf) {
-      u32x4 kb[C::NCH];
-#pragma unroll
-      for (int kk = 0; kk < C::NCH; ++kk) kb[kk] = x.kb[kk];
-      if (has_lk) {
-        float cc[C::NB][4], ss[C::NB][4];
-#pragma unroll
-        for (int blk = 0; blk < C::NB; ++blk)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float2 bc = base_cs[buf][q * C::QPG + blk * 4 + i];
-            cc[blk][i] = bc.x * cd[blk][i] - bc.y * sd[blk][i];
-            ss[blk][i] = bc.y * cd[blk][i] + bc.x * sd[blk][i];
-          }
-        add_rotated_expansion<D, R>(kb, bkf, x.lk, cc, ss);
-      }
-      store_chunks<D>(k_lds[buf] + delta * C::K_ROW, kb, lane);
-#pragma unroll
-      for (int iv = 0; iv < C::NVL; ++iv)
-        *reinterpret_cast<u32x4*>(v_lds[buf] + (pw_ * 16 + vrow + C::RPL * iv) * C::V_ROW + vdim) = x.v[iv];
-      if (has_lv) {
-#pragma unroll
-        for (int rc = 0; rc < C::RC; ++rc)
-          if (rc * 16 + q * 4 < R)
-            *reinterpret_cast<u32x2*>(lv_lds[buf] + delta * C::LV_ROW + rc * 16 + q * 4) = x.lv[rc];
-      }
-    };
-    auto base_angles = [&](int64_t t0, int buf) {
-      if (has_lk && ptid < C::HALF) {
-        float c, s;
-        rope_cs((int)t0, a.w2pi[ptid], c, s);
-        base_cs[buf][ptid] = make_float2(c, s);
-      }
-    };
-    // Prologue: tile 0 into LDS buffer 0, tile 1 in flight.
-    TileRegs<D, R> x;
-    if (n_tiles > 0) {
-      tile_load<D, R>(x, Kb, Vb, Lk, Lv, row_el, pw_ * 16, kv_hi, lane);
-      base_angles(0, 0);
     }
-    __syncthreads();  // [P1] base angles of tile 0
-    if (n_tiles > 0) rebuild(x, 0);
-    if (n_tiles > 1) {
-      tile_load<D, R>(x, Kb, Vb, Lk, Lv, row_el, TKV + pw_ * 16, kv_hi, lane);
-      base_angles(TKV, 1);
+#pragma unroll
+    for (int e = 0; e < C::SEG; e += 2) {
+      float c0, s0, c1, s1;
+      rope_cs(delta, a.w2pi[lo_dim0 + e], c0, s0);
+      rope_cs(delta, a.w2pi[lo_dim0 + e + 1], c1, s1);
+      off_cs[w][e / 2][lane] = f32x4{c0, s0, c1, s1};
     }
-    __syncthreads();  // [P2] tile 0 in LDS
-    for (int tile = 0; tile < n_tiles; ++tile) {
-      const int buf = tile & 1;
-      const int64_t t0 = (int64_t)tile * TKV;
-      if (tile + 1 < n_tiles) rebuild(x, buf ^ 1);
-      if (tile + 2 < n_tiles) {
-        tile_load<D, R>(x, Kb, Vb, Lk, Lv, row_el, t0 + 2 * TKV + pw_ * 16, kv_hi, lane);
-        base_angles(t0 + 2 * TKV, buf);
-      }
-      __syncthreads();  // [T] tile+1 in LDS; tile consumed
-    }
-    return;
   }
+  auto load_unit = [&](Unit<D, R>& u, int64_t t0) {
+    const int64_t tk = t0 + delta;
+    const bool ok = tk < kv_hi;
+    u.klo = ld_seg<C::SEG>(Kb + tk * row_el + lo_dim0, ok);
+    u.khi = ld_seg<C::SEG>(Kb + tk * row_el + C::HALF + lo_dim0, ok);
+    if constexpr (LK) load_lr_frag<R>(u.lk, Lk + (ok ? tk : 0) * R, ok, lane);
+#pragma unroll
+    for (int iv = 0; iv < C::NVL; ++iv) {
+      const int64_t tv = t0 + 8 * w + vrow + C::VRPL * iv;
+      u.v[iv] = ld16(Vb + (tv < kv_hi ? tv : 0) * row_el + vdim, tv < kv_hi);
+    }
+    if constexpr (LV) {
+#pragma unroll
+      for (int j = 0; j < C::LVW; ++j) {
+        const int i = lane + 64 * j, r = i / (R / 2), c = i % (R / 2);
+        const int64_t tv = t0 + 8 * w + r;
+        const bool okv = i < 4 * R && tv < kv_hi;
+        u.lv[j] = okv ? reinterpret_cast<const uint32_t*>(Lv + tv * R)[c] : 0u;
+      }
+    }
+  };
+  auto rebuild = [&](const Unit<D, R>& u, int buf) {
+    Seg<C::SEG> lo = u.klo, hi = u.khi;
+    if constexpr (LK) {
+#pragma unroll
+      for (int i = 0; i < C::NBW; ++i) {
+        f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int rc = 0; rc < C::RC; ++rc) {
+          elo = mfma16x16x16(bkf[i][rc], as_i16x4(u.lk[rc]), elo);
+          ehi = mfma16x16x16(bkf[C::NBW + i][rc], as_i16x4(u.lk[rc]), ehi);
+        }
+        float vlo[4], vhi[4];
+        const f32x4 od0 = off_cs[w][2 * i][lane], od1 = off_cs[w][2 * i + 1][lane];
+        const float cd[4] = {od0[0], od0[2], od1[0], od1[2]}, sd[4] = {od0[1], od0[3], od1[1], od1[3]};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int e = 4 * i + j;
+          const float2 bc = base_cs[buf][lo_dim0 + e];
+          const float c = bc.x * cd[j] - bc.y * sd[j];
+          const float s = bc.y * cd[j] + bc.x * sd[j];
+          vlo[j] = seg_get(u.klo, e) + elo[j] * c - ehi[j] * s;
+          vhi[j] = seg_get(u.khi, e) + ehi[j] * c + elo[j] * s;
+        }
+        lo.w[2 * i] = pack_bf16(vlo[0], vlo[1]);
+        lo.w[2 * i + 1] = pack_bf16(vlo[2], vlo[3]);
+        hi.w[2 * i] = pack_bf16(vhi[0], vhi[1]);
+        hi.w[2 * i + 1] = pack_bf16(vhi[2], vhi[3]);
+      }
+    }
+    st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + lo_dim0, lo);
+    st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + C::HALF + lo_dim0, hi);
+#pragma unroll
+    for (int iv = 0; iv < C::NVL; ++iv)
+      *reinterpret_cast<u32x4*>(v_lds[buf] + (8 * w + vrow + C::VRPL * iv) * C::V_ROW + vdim) = u.v[iv];
+    if constexpr (LV) {
+#pragma unroll
+      for (int j = 0; j < C::LVW; ++j) {
+        const int i = lane + 64 * j, r = i / (R / 2), c = i % (R / 2);
+        if (i < 4 * R) reinterpret_cast<uint32_t*>(lv_lds[buf] + (8 * w + r) * C::LV_ROW)[c] = u.lv[j];
+      }
+    }
+  };
+  // RoPE of each tile's first token, exact in fp64, by the last wave.
+  auto base_angles = [&](int64_t t0, int buf) {
+    if constexpr (LK) {
+      if (w == NW - 1 && lane < C::HALF) {
+        float c, s;
+        rope_cs((int)t0, a.w2pi[lane], c, s);
+        base_cs[buf][lane] = make_float2(c, s);
+      }
+    }
+  };
 
-  // ========================= consumer waves ================================
+  // ---- attend role ----------------------------------------------------------
   // Wave bounds: skip tiles no row of this wave sees; mask only tiles that
   // reach past some row's last visible key.
   int wave_last = (int)last, wave_first = row_ok ? (int)last : INT32_MAX;
@@ -271,81 +314,132 @@ lrsa_prefill_kernel(const AttnArgs a) {
     for (int j = 0; j < 16; ++j) accl[rb][j] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  __syncthreads();  // [P1]
-  __syncthreads();  // [P2]
+
+  // The two waves of a SIMD (w and w + 4, or w and w ^ 1, depending on how the
+  // workgroup is laid out) take the two jobs in opposite order.
+  const bool build_first = ((w >> 2) ^ w) & 1;
+
+  // Prologue: tile 0 into LDS buffer 0, tile 1 in flight.
+  Unit<D, R> u;
+  if (n_tiles > 0) {
+    load_unit(u, 0);
+    base_angles(0, 0);
+  }
+  __syncthreads();
+  if (n_tiles > 0) rebuild(u, 0);
+  if (n_tiles > 1) {
+    load_unit(u, TKV);
+    base_angles(TKV, 1);
+  }
+  __syncthreads();
+
   for (int tile = 0; tile < n_tiles; ++tile) {
     const int buf = tile & 1;
     const int64_t t0 = (int64_t)tile * TKV;
-    // The tile is consumed as two 32-token halves, each with its own online
-    // softmax update (half the live score and P registers of a whole tile).
+    // Build tile + 1 (its data arrived during the previous tile) and start
+    // the loads of tile + 2.
+    auto build = [&]() {
+      if (tile + 1 < n_tiles) rebuild(u, buf ^ 1);
+      if (tile + 2 < n_tiles) load_unit(u, t0 + 2 * TKV);
+    };
+    if (build_first) build();
+    if (t0 <= (int64_t)wave_last) {
+      // K fragments (A operand of S^T = K Q^T) of one half, all in flight at once.
+      bf16x8 kf[C::NKQ];
+      auto load_k = [&](int tb) {
+        const uint16_t* kl = k_lds[buf] + (tb * 32 + l32) * C::K_ROW + h32 * 8;
 #pragma unroll
-    for (int tb = 0; tb < 2; ++tb) {
-      const int64_t th = t0 + tb * 32;  // first token of this half
-      if (th > (int64_t)wave_last) break;
-      const uint16_t* kl = k_lds[buf] + (tb * 32 + l32) * C::K_ROW + h32 * 8;
-      f32x16 s;
+        for (int kk = 0; kk < C::NKQ; ++kk) kf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(kl + kk * 16));
+      };
+      // The tile is consumed as two 32-token halves, each with its own online
+      // softmax update (half the live score and P registers of a whole tile).
 #pragma unroll
-      for (int j = 0; j < 16; ++j) s[j] = 0.f;
+      for (int tb = 0; tb < 2; ++tb) {
+        const int64_t th = t0 + tb * 32;  // first token of this half
+        if (th > (int64_t)wave_last) break;
+        if (tb == 0) load_k(0);
+        f32x16 s;
 #pragma unroll
-      for (int kk = 0; kk < C::NKQ; ++kk)
-        s = mfma32x32x16(as_bf16x8(*reinterpret_cast<const u32x4*>(kl + kk * 16)), qf[kk], s);
-      if (th + 31 > (int64_t)wave_first) {  // this half crosses some row's causal limit
-        // Positions fit in 32 bits (s_cap < 2^31): key t is masked iff t > last.
-        const int rel = (int)last - (int)th - h32 * 4;  // last - (first token of this lane)
+        for (int j = 0; j < 16; ++j) s[j] = 0.f;
 #pragma unroll
-        for (int j = 0; j < 16; ++j)
-          if ((j >> 2) * 8 + (j & 3) > rel) s[j] = -INFINITY;
-      }
-      float mx = s[0];
+        for (int kk = 0; kk < C::NKQ; ++kk) s = mfma32x32x16(kf[kk], qf[kk], s);
+        // The next half's K fragments are read while this half finishes.
+        if (tb == 0 && t0 + 32 <= (int64_t)wave_last) load_k(1);
+        if (th + 31 > (int64_t)wave_first) {  // this half crosses some row's causal limit
+          // Positions fit in 32 bits (s_cap < 2^31): key t is masked iff t > last.
+          const int rel = (int)last - (int)th - h32 * 4;  // last - (first token of this lane)
 #pragma unroll
-      for (int j = 1; j < 16; ++j) mx = fmaxf(mx, s[j]);
-      mx = fmaxf(mx, shfl_xor(mx, 32)) * a.scale_log2;
-      const float mn = fmaxf(m_run, mx);
-      const float ms = (mn == -INFINITY) ? 0.f : mn;
-      const float alpha = fast_exp2(m_run - ms);
-      m_run = mn;
-      float ls0 = 0.f, ls1 = 0.f;
-      u32x4 pw[2];  // bf16 P of this half, one per 16-token chunk
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const float p0 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c], a.scale_log2, -ms));
-          const float p1 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c + 1], a.scale_log2, -ms));
-          ls0 += p0;
-          ls1 += p1;
-          pw[hf][c] = pack_bf16(p0, p1);
+          for (int j = 0; j < 16; ++j)
+            if ((j >> 2) * 8 + (j & 3) > rel) s[j] = -INFINITY;
         }
-      l_run = l_run * alpha + (ls0 + ls1);
-      if (__ballot(alpha != 1.f)) {
+        float mx = s[0];
 #pragma unroll
-        for (int db = 0; db < C::NDB; ++db) acc[db] *= alpha;
+        for (int j = 1; j < 16; ++j) mx = fmaxf(mx, s[j]);
+        mx = max_xor32(mx) * a.scale_log2;
+        // Lazy rescale: the reference maximum m_run only moves when some row's
+        // maximum exceeds it by more than 2^8, so P stays below 256 and the
+        // accumulators are rescaled a handful of times per row.
+        if (__ballot(mx > m_run + kRescaleLog2)) {
+          const float mn = fmaxf(m_run, mx);
+          const float alpha = fast_exp2(m_run - (mn == -INFINITY ? 0.f : mn));
 #pragma unroll
-        for (int rb = 0; rb < C::RB; ++rb) accl[rb] *= alpha;
-      }
-      // O^T[dims x rows] += V^T[dims x 16 tok] P^T[16 tok x rows] for the two
-      // 16-token chunks of this half; (P L_v)^T likewise with L_v^T.
-      const uint16_t* vt = v_lds[buf];
-      const uint16_t* lvt = lv_lds[buf];
+          for (int db = 0; db < C::NDB; ++db) acc[db] *= alpha;
 #pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const int m = 2 * tb + hf;
-        const bf16x8 pb = as_bf16x8(pw[hf]);
+          for (int rb = 0; rb < C::RB; ++rb) accl[rb] *= alpha;
+          l_run *= alpha;
+          m_run = mn;
+        }
+        const float ms = (m_run == -INFINITY) ? 0.f : m_run;
+        float ls0 = 0.f, ls1 = 0.f;
+        u32x4 pw[2];  // bf16 P of this half, one per 16-token chunk
 #pragma unroll
-        for (int db = 0; db < C::NDB; ++db)
-          acc[db] = mfma32x32x16(lds_tr_a32(vt, C::V_ROW, m, db * 32, lane), pb, acc[db]);
-        if (has_lv) {
+        for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-          for (int rb = 0; rb < C::RB; ++rb)
-            accl[rb] = mfma32x32x16(lds_tr_a32(lvt, C::LV_ROW, m, rb * 32, lane), pb, accl[rb]);
+          for (int c = 0; c < 4; ++c) {
+            const float p0 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c], a.scale_log2, -ms));
+            const float p1 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c + 1], a.scale_log2, -ms));
+            if constexpr (!ones_sum) {
+              ls0 += p0;
+              ls1 += p1;
+            }
+            pw[hf][c] = pack_bf16(p0, p1);
+          }
+        if constexpr (!ones_sum) l_run += ls0 + ls1;
+        // O^T[dims x rows] += V^T[dims x 16 tok] P^T[16 tok x rows] for the two
+        // 16-token chunks of this half; (P L_v)^T likewise with L_v^T.
+        const uint16_t* vt = v_lds[buf];
+        const uint16_t* lvt = lv_lds[buf];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          const int m = 2 * tb + hf;
+          const bf16x8 pb = as_bf16x8(pw[hf]);
+          // A fragments are read one MFMA ahead; the L_v ones at the chunk start.
+          bf16x8 lvf[C::RB];
+          if constexpr (LV) {
+#pragma unroll
+            for (int rb = 0; rb < C::RB; ++rb) lvf[rb] = lds_tr_a32(lvt, C::LV_ROW, m, rb * 32, lane);
+          }
+          bf16x8 fa = lds_tr_a32(vt, C::V_ROW, m, 0, lane);
+#pragma unroll
+          for (int db = 0; db < C::NDB; ++db) {
+            const bf16x8 fn = db + 1 < C::NDB ? lds_tr_a32(vt, C::V_ROW, m, (db + 1) * 32, lane) : fa;
+            acc[db] = mfma32x32x16(fa, pb, acc[db]);
+            fa = fn;
+          }
+          if constexpr (LV) {
+#pragma unroll
+            for (int rb = 0; rb < C::RB; ++rb) accl[rb] = mfma32x32x16(lvf[rb], pb, accl[rb]);
+          }
         }
       }
     }
-    __syncthreads();  // [T]
+    if (!build_first) build();
+    if (tile + 2 < n_tiles) base_angles(t0 + 2 * TKV, buf);
+    __syncthreads();  // tile + 1 in LDS; tile consumed by every wave
   }
 
   // ---- epilogue: O^T += B_v^T (P L_v)^T, then O = acc / l, lse -------------
-  if (has_lv) {
+  if constexpr (LV) {
     // (P L_v)^T registers of rank chunk jc (16 ranks) are the B operand in
     // the same k order as P; split into bf16 hi + lo to keep fp32 accuracy.
 #pragma unroll
@@ -371,7 +465,15 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
     }
   }
-  const float l_tot = l_run + shfl_xor(l_run, 32);
+  // Row sum: from the ones row of (P L_v)^T (row R: register 4 (R/8) + R%4 of
+  // block 0 in lanes (R%8)/4*32 .. +31), else from the per-lane partial sums.
+  float l_tot;
+  if constexpr (ones_sum) {
+    constexpr int jr = 4 * ((R % 32) / 8) + (R % 4);
+    l_tot = __shfl(accl[0][jr], l32 + 32 * ((R % 8) / 4), 64);
+  } else {
+    l_tot = sum_xor32(l_run);
+  }
   if (!row_ok) return;
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   uint16_t* op = a.O + (((int64_t)b * a.n_tok + qi) * a.n_q + (int64_t)g * G + hh) * D;
@@ -390,22 +492,30 @@ lrsa_prefill_kernel(const AttnArgs a) {
         l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
 }
 
-template <int D, int R>
+template <int D, int R, bool LK, bool LV>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const int n_rows = a.n_tok * a.group;
-  using C = Pre<D, R>;
-  const int tiles = (n_rows + C::BROWS - 1) / C::BROWS;
-  hipLaunchKernelGGL((lrsa_prefill_kernel<D, R>), dim3(tiles, a.n_kv, a.batch), dim3(C::NTHR), 0, st, a);
+  const int tiles = (n_rows + BROWS - 1) / BROWS;
+  hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV>), dim3(tiles, a.n_kv, a.batch), dim3(NTHR), 0, st, a);
   return hipGetLastError();
+}
+
+template <int D, int R>
+hipError_t launch_lr(const AttnArgs& a, hipStream_t st) {
+  const bool lk = a.Lk != nullptr, lv = a.Lv != nullptr;
+  if (lk && lv) return launch_t<D, R, true, true>(a, st);
+  if (lk) return launch_t<D, R, true, false>(a, st);
+  if (lv) return launch_t<D, R, false, true>(a, st);
+  return launch_t<D, 8, false, false>(a, st);  // no LR: the rank is irrelevant
 }
 
 template <int D>
 hipError_t launch_r(const AttnArgs& a, hipStream_t st) {
   switch (a.rank) {
-    case 8: return launch_t<D, 8>(a, st);
-    case 16: return launch_t<D, 16>(a, st);
-    case 32: return launch_t<D, 32>(a, st);
-    case 64: return launch_t<D, 64>(a, st);
+    case 8: return launch_lr<D, 8>(a, st);
+    case 16: return launch_lr<D, 16>(a, st);
+    case 32: return launch_lr<D, 32>(a, st);
+    case 64: return launch_lr<D, 64>(a, st);
     default: return hipErrorInvalidValue;
   }
 }
