@@ -102,6 +102,21 @@ __device__ __forceinline__ float seg_get(const Seg<SEG>& s, int e) {
   return (e & 1) ? bf_hi(s.w[e >> 1]) : bf_lo(s.w[e >> 1]);
 }
 
+// Buffer resource over `bytes` bytes from `base`: loads at offsets at or past
+// the end return zeros (raw buffer, stride 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base, int32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, bytes, 0x00020000);
+}
+__device__ __forceinline__ u32x4 buf_ld16(__amdgpu_buffer_rsrc_t r, int32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ u32x2 buf_ld8(__amdgpu_buffer_rsrc_t r, int32_t off) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+}
+__device__ __forceinline__ uint32_t buf_ld4(__amdgpu_buffer_rsrc_t r, int32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+
 __device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) {
   typedef short v4s __attribute__((ext_vector_type(4)));
   v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((v4s __attribute__((address_space(3)))*)(p));
@@ -210,25 +225,51 @@ lrsa_prefill_kernel(const AttnArgs a) {
       off_cs[w][e / 2][lane] = f32x4{c0, s0, c1, s1};
     }
   }
+  // Per-lane byte offsets of the staged data within a tile (constant); the
+  // tile itself is addressed by buffer resources built per tile, whose
+  // range check returns zeros for rows at or beyond kv_hi.
+  const int32_t offk = delta * (int32_t)(row_el * 2) + lo_dim0 * 2;
+  const int32_t offlk = delta * R * 2 + q * 8;
+  int32_t offv[C::NVL];
+#pragma unroll
+  for (int iv = 0; iv < C::NVL; ++iv) offv[iv] = (8 * w + vrow + C::VRPL * iv) * (int32_t)(row_el * 2) + vdim * 2;
+  int32_t offlv[C::LVW];
+#pragma unroll
+  for (int j = 0; j < C::LVW; ++j) {
+    const int i = lane + 64 * j;
+    offlv[j] = i < 4 * R ? (8 * w + i / (R / 2)) * R * 2 + (i % (R / 2)) * 4 : INT32_MIN;
+  }
   auto load_unit = [&](Unit<D, R>& u, int64_t t0) {
-    const int64_t tk = t0 + delta;
-    const bool ok = tk < kv_hi;
-    u.klo = ld_seg<C::SEG>(Kb + tk * row_el + lo_dim0, ok);
-    u.khi = ld_seg<C::SEG>(Kb + tk * row_el + C::HALF + lo_dim0, ok);
-    if constexpr (LK) load_lr_frag<R>(u.lk, Lk + (ok ? tk : 0) * R, ok, lane);
+    const int rows = (int)(kv_hi - t0 < TKV ? kv_hi - t0 : TKV);  // valid rows of this tile (> 0)
+    const int32_t kv_bytes = (rows - 1) * (int32_t)(row_el * 2) + D * 2;
+    const auto rk = make_rsrc(Kb + t0 * row_el, kv_bytes);
+    const auto rv = make_rsrc(Vb + t0 * row_el, kv_bytes);
+    if constexpr (C::SEG == 8) {
+      const u32x4 lo = buf_ld16(rk, offk), hi = buf_ld16(rk, offk + C::HALF * 2);
 #pragma unroll
-    for (int iv = 0; iv < C::NVL; ++iv) {
-      const int64_t tv = t0 + 8 * w + vrow + C::VRPL * iv;
-      u.v[iv] = ld16(Vb + (tv < kv_hi ? tv : 0) * row_el + vdim, tv < kv_hi);
-    }
-    if constexpr (LV) {
-#pragma unroll
-      for (int j = 0; j < C::LVW; ++j) {
-        const int i = lane + 64 * j, r = i / (R / 2), c = i % (R / 2);
-        const int64_t tv = t0 + 8 * w + r;
-        const bool okv = i < 4 * R && tv < kv_hi;
-        u.lv[j] = okv ? reinterpret_cast<const uint32_t*>(Lv + tv * R)[c] : 0u;
+      for (int i = 0; i < 4; ++i) {
+        u.klo.w[i] = lo[i];
+        u.khi.w[i] = hi[i];
       }
+    } else {
+      const u32x2 lo = buf_ld8(rk, offk), hi = buf_ld8(rk, offk + C::HALF * 2);
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        u.klo.w[i] = lo[i];
+        u.khi.w[i] = hi[i];
+      }
+    }
+    if constexpr (LK) {
+      const auto rl = make_rsrc(Lk + t0 * R, rows * R * 2);
+#pragma unroll
+      for (int rc = 0; rc < C::RC; ++rc) u.lk[rc] = rc * 16 + q * 4 < R ? buf_ld8(rl, offlk + rc * 32) : u32x2{0u, 0u};
+    }
+#pragma unroll
+    for (int iv = 0; iv < C::NVL; ++iv) u.v[iv] = buf_ld16(rv, offv[iv]);
+    if constexpr (LV) {
+      const auto rl = make_rsrc(Lv + t0 * R, rows * R * 2);
+#pragma unroll
+      for (int j = 0; j < C::LVW; ++j) u.lv[j] = buf_ld4(rl, offlv[j]);
     }
   };
   auto rebuild = [&](const Unit<D, R>& u, int buf) {
