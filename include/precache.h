@@ -81,8 +81,9 @@ const char* prc_version(void);
  *            [tok_offset, tok_offset + T) of every plane are overwritten;
  *            nothing else is touched.
  * Arithmetic: bf16 inputs, fp32 accumulation, round-to-nearest-even to bf16.
- * Requires d_in % 8 == 0, ld_x % 8 == 0, r in {8, 16, 32, 64},
- * 0 <= tok_offset and tok_offset + T <= s_cap.  T == 0 is a no-op.
+ * Requires d_in % 8 == 0, ld_x % 8 == 0, d_in <= ld_x < 2^24 (PRC_EUNSUPPORTED
+ * otherwise), r in {8, 16, 32, 64}, 0 <= tok_offset and tok_offset + T <= s_cap.
+ * T == 0 is a no-op.
  */
 prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
                                const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,

@@ -162,6 +162,8 @@ PRC_API prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_i
   if (d_in < 1 || d_in % 8) return fail(PRC_EUNSUPPORTED, "d_in=%lld must be a positive multiple of 8", (long long)d_in);
   if (ld_x < d_in) return fail(PRC_ESHAPE, "ld_x=%lld < d_in=%lld", (long long)ld_x, (long long)d_in);
   if (ld_x % 8) return fail(PRC_EALIGN, "ld_x=%lld is not a multiple of 8 elements", (long long)ld_x);
+  // Tiles of 64 rows are addressed with 32-bit byte offsets.
+  if (ld_x >= (1LL << 24)) return fail(PRC_EUNSUPPORTED, "ld_x=%lld must be below 2^24", (long long)ld_x);
   if (n_proj < 1 || n_agents < 1) return fail(PRC_EINVAL, "n_proj=%d, n_agents=%d must be positive", n_proj, n_agents);
   if (!rank_ok(rank)) return fail(PRC_EUNSUPPORTED, "rank=%d (built: 8, 16, 32, 64)", rank);
   const int64_t n_cols = (int64_t)n_proj * n_agents * rank;

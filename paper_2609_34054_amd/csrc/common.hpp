@@ -46,6 +46,26 @@ __device__ __forceinline__ u32x2 ld8(const uint16_t* p, bool ok) {
   return ok ? *reinterpret_cast<const u32x2*>(p) : z;
 }
 
+// ------------------------------------------------------- buffer loads ----
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+// Raw buffer resource over `bytes` bytes from `base` (stride 0): loads at
+// offsets at or past `bytes` return zeros.
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, int32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  return i32x4{(int)(uint32_t)b, (int)(uint32_t)(b >> 32), bytes, 0x00020000};
+}
+// Direct global->LDS load of 16 bytes per lane: lane i's data lands at
+// lds + 16 i.  Issued through inline assembly so that the compiler does not
+// treat every later LDS read as dependent on it; the caller waits with
+// s_waitcnt vmcnt before publishing the data (barrier) and reading it.
+__device__ __forceinline__ void lds_dma16(i32x4 rsrc, const void* lds, int32_t voff, int32_t soff) {
+  const uint32_t m = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const void*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds" ::"s"(m), "v"(voff), "s"(rsrc),
+               "s"(soff)
+               : "memory", "m0");
+}
+
 // ---------------------------------------------------------------- MFMA ----
 // 16x16x32 bf16: lane l holds A[m = l%16][k = (l/16)*8 + 0..7],
 // B[k = (l/16)*8 + 0..7][n = l%16]; C[m = (l/16)*4 + i][n = l%16].

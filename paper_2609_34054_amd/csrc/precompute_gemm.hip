@@ -6,15 +6,18 @@
 // i.e. one GEMM  X[T x d_in] . A_stack[d_in x n_cols]  whose n_cols = n_proj*N*r
 // output columns are scattered into per-agent planes [s_cap][r].
 //
-// Both operands are contiguous along d_in (A is stored as rows), so MFMA
-// fragments are read straight from global memory in operand layout.  The
-// kernel computes the transposed product C^T = A_rows . X^T with 16x16x32 bf16
-// MFMAs: the result layout gives each lane 4 consecutive output columns of one
-// token, i.e. 4 consecutive rank entries of one plane row (an 8-byte store).
-//
-// Workgroup tile: 64 columns x 64 tokens.  Each of the 4 waves computes the
-// whole tile over a quarter of d_in (16 MFMAs per 8 fragment loads, loads of
-// the next k-step in flight), and the partial tiles are summed through LDS.
+// The kernel computes the transposed product C^T = A_rows . X^T, so both
+// operands are rows contiguous along d_in.  Workgroup tile: 64 columns x 64
+// tokens, 4 waves, each owning a 32 x 32 quadrant on 32x32x16 MFMAs.  The
+// operand tiles are staged in LDS, 64 k (128 bytes per row) per stage, in a
+// ring of NST stages filled by direct global->LDS buffer loads: every load
+// instruction brings 8 whole 128-byte rows, so the texture path sees full
+// cache lines and no VGPRs are spent on staging.  Inside a stage each row's
+// eight 16-byte chunks are XOR-swizzled by the row index so that the MFMA
+// fragment reads are free of bank conflicts.  Rows past the matrix and k past
+// d_in read as zeros (buffer range check / out-of-range offsets).  The result
+// layout gives each lane 4 consecutive output columns of one token: 4
+// consecutive rank entries of one plane row, one 8-byte store.
 // Block order is XCD-aware: the column tiles that share rows of X run on the
 // same XCD, so X is fetched into each L2 once.
 #include "common.hpp"
@@ -23,21 +26,40 @@
 namespace prc {
 namespace {
 
-constexpr int TC = 64;  // output columns per workgroup
-constexpr int TT = 64;  // tokens per workgroup
-constexpr int KS = 32;  // k per MFMA
-constexpr int NXCD = 8; // XCDs of an MI355X
+constexpr int TC = 64;   // output columns per workgroup
+constexpr int TT = 64;   // tokens per workgroup
+constexpr int KST = 64;  // k per stage (128 bytes of a row)
+constexpr int NST = 4;   // stages in the LDS ring
+constexpr int NXCD = 8;  // XCDs of an MI355X
 
-struct Frag {
-  u32x4 a[4];  // A rows: columns 16i + l%16, k chunk (l/16)*8
-  u32x4 x[4];  // X rows: tokens 16j + l%16, same k chunk
-};
+// Physical 16-byte chunk of logical chunk c in row r of a stage tile.  Rows
+// r and r + 1 differ in bank half (64-dword rows hold two 128-byte rows); the
+// XOR with r / 2 makes the 16 rows read together by one fragment load hit
+// distinct banks.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 
-__global__ void __launch_bounds__(256)
-precompute_kernel(const PrecomputeArgs a, int n_ct, int n_tt) {
-  __shared__ __attribute__((aligned(16))) float red[3][TC * TT];
+// s_waitcnt vmcnt(n) for a wave-uniform n in {0, 4, ..., 4 (NST - 2)}, other
+// counters not waited on.  gfx9 encoding: vmcnt bits [3:0] and [15:14],
+// expcnt [6:4] = 7, lgkmcnt [11:8] = 15.  The immediate must be a constant,
+// so the cases are spelled out.
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+__device__ __forceinline__ void wait_vmcnt_le(int n) {
+  static_assert(4 * (NST - 2) <= 24, "vmcnt cases");
+  switch (n) {
+    case 24: __builtin_amdgcn_s_waitcnt(vmcnt_imm(24)); break;
+    case 20: __builtin_amdgcn_s_waitcnt(vmcnt_imm(20)); break;
+    case 16: __builtin_amdgcn_s_waitcnt(vmcnt_imm(16)); break;
+    case 12: __builtin_amdgcn_s_waitcnt(vmcnt_imm(12)); break;
+    case 8: __builtin_amdgcn_s_waitcnt(vmcnt_imm(8)); break;
+    case 4: __builtin_amdgcn_s_waitcnt(vmcnt_imm(4)); break;
+    default: __builtin_amdgcn_s_waitcnt(vmcnt_imm(0)); break;
+  }
+}
+
+__global__ void __launch_bounds__(256) precompute_kernel(const PrecomputeArgs a, int n_ct, int n_tt) {
+  // [stage][A tile, X tile][64 rows x 128 bytes]
+  __shared__ __attribute__((aligned(1024))) uint16_t tiles[NST][2][64 * KST];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int c16 = lane & 15, q = lane >> 4;
   // XCD-aware tile order: workgroup L runs on XCD L % 8; consecutive slots of
   // one XCD walk the column tiles of one token tile.
   const int L = blockIdx.x, xcd = L % NXCD, slot = L / NXCD;
@@ -46,82 +68,88 @@ precompute_kernel(const PrecomputeArgs a, int n_ct, int n_tt) {
   if (tt >= n_tt) return;  // padding of the grid (uniform over the workgroup)
   const int col0 = ct * TC;
   const int64_t tok0 = (int64_t)tt * TT;
+  const int cols = a.n_cols - col0 < TC ? a.n_cols - col0 : TC;          // valid rows of the A tile
+  const int toks = (int)(a.T - tok0 < TT ? a.T - tok0 : (int64_t)TT);    // valid rows of the X tile
 
-  const uint16_t* ap[4];
-  const uint16_t* xp[4];
-  bool aok[4], xok[4];
+  // Buffer resources over the valid rows of each operand tile (k included).
+  const i32x4 ra = buffer_rsrc(a.A + (int64_t)col0 * a.d_in, (int32_t)((cols - 1) * a.d_in * 2 + a.d_in * 2));
+  const i32x4 rx = buffer_rsrc(a.X + tok0 * a.ld_x, (int32_t)((toks - 1) * a.ld_x * 2 + a.d_in * 2));
+
+  // Loader: each wave fills 16 of the 64 rows of both tiles per stage, two
+  // instructions per tile, each writing 1 KB (8 rows x 128 bytes) at
+  // consecutive lane positions.  Lane i of instruction j holds physical chunk
+  // i % 8 of row 16 w + 8 j + i / 8, i.e. logical chunk swz(row, i % 8).
+  int32_t offa[2], offx[2], kch[2];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = col0 + i * 16 + c16;
-    aok[i] = c < a.n_cols;
-    ap[i] = a.A + (int64_t)(aok[i] ? c : 0) * a.d_in + q * 8;
-    const int64_t t = tok0 + i * 16 + c16;
-    xok[i] = t < a.T;
-    xp[i] = a.X + (xok[i] ? t : 0) * a.ld_x + q * 8;
+  for (int j = 0; j < 2; ++j) {
+    const int row = 16 * w + 8 * j + (lane >> 3);
+    const int c = swz(row, lane & 7);
+    kch[j] = c * 8;  // first k of this lane's chunk within a stage
+    offa[j] = row * (int32_t)(a.d_in * 2) + c * 16;
+    offx[j] = row * (int32_t)(a.ld_x * 2) + c * 16;
   }
-  // This wave's share of d_in, in whole k-steps of 32.
-  const int64_t nk = (a.d_in + KS - 1) / KS;
-  const int64_t k_begin = (nk * w / 4) * KS, k_end = (nk * (w + 1) / 4) * KS;
-
-  f32x4 acc[4][4];
+  const int nstage = (int)((a.d_in + KST - 1) / KST);
+  // Each token tile walks the k stages from its own starting point (the
+  // column tiles that share its X rows use the same one), so that at any
+  // moment the workgroups read rows at different k offsets: with row strides
+  // that are multiples of 4 KB, equal offsets would all hit the same few L2
+  // channels.
+  const int rot = (int)(((int64_t)tt * nstage) / n_tt);
+  auto issue = [&](int s) {
+    const int sl = s % NST;
+    const int ks = s + rot < nstage ? s + rot : s + rot - nstage;
+    const int32_t k0 = ks * KST;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  auto load = [&](Frag& f, int64_t k0) {
-    const bool kok = k0 + q * 8 < a.d_in;  // d_in is a multiple of 8
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      f.a[i] = ld16(ap[i] + k0, aok[i] && kok);
-      f.x[i] = ld16(xp[i] + k0, xok[i] && kok);
+    for (int j = 0; j < 2; ++j) {
+      // Chunks wholly past d_in (d_in is a multiple of 8) read as zeros.
+      const bool kok = k0 + kch[j] < a.d_in;
+      const int32_t oa = kok ? offa[j] : INT32_MIN, ox = kok ? offx[j] : INT32_MIN;
+      lds_dma16(ra, &tiles[sl][0][(16 * w + 8 * j) * KST], oa, k0 * 2);
+      lds_dma16(rx, &tiles[sl][1][(16 * w + 8 * j) * KST], ox, k0 * 2);
     }
   };
-  auto mma = [&](const Frag& f) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[i][j] = mfma16x16x32(as_bf16x8(f.a[i]), as_bf16x8(f.x[j]), acc[i][j]);
-  };
 
-  Frag f0, f1;
-  int64_t k0 = k_begin;
-  if (k0 < k_end) load(f0, k0);
-  for (; k0 + 2 * KS <= k_end; k0 += 2 * KS) {
-    load(f1, k0 + KS);
-    mma(f0);
-    if (k0 + 2 * KS < k_end) load(f0, k0 + 2 * KS);
-    mma(f1);
-  }
-  if (k0 < k_end) mma(f0);
+  // Compute: wave w owns columns 32 (w & 1) .. +31 and tokens 32 (w >> 1) .. +31.
+  // 32x32x16 fragments: lane l holds row l % 32, k = (l / 32) * 8 + 0..7.
+  const int l32 = lane & 31, h = lane >> 5;
+  const int ra_row = 32 * (w & 1) + l32, rx_row = 32 * (w >> 1) + l32;
+  f32x16 acc;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) acc[j] = 0.f;
 
-  // Sum the 4 partial tiles: waves 1-3 park theirs in LDS, wave 0 adds them.
-  // acc[i][j][e]: column col0 + 16i + 4q + e, token tok0 + 16j + l%16.
-  if (w > 0) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+  for (int s = 0; s < NST - 1; ++s)
+    if (s < nstage) issue(s);
+  for (int s = 0; s < nstage; ++s) {
+    // Stage s has landed once at most the loads of the stages after it (up to
+    // NST - 2 of them, 4 instructions each) are still in flight.
+    const int ahead = nstage - 1 - s < NST - 2 ? nstage - 1 - s : NST - 2;
+    wait_vmcnt_le(4 * ahead);
+    __syncthreads();  // stage s visible to all waves; stage s - 1 consumed by all
+    if (s + NST - 1 < nstage) issue(s + NST - 1);
+    const uint16_t* ta = tiles[s % NST][0] + ra_row * KST;
+    const uint16_t* tx = tiles[s % NST][1] + rx_row * KST;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        *reinterpret_cast<f32x4*>(&red[w - 1][((i * 4 + j) * 64 + lane) * 4]) = acc[i][j];
+    for (int kk = 0; kk < KST / 16; ++kk) {
+      const int c = 2 * kk + h;  // logical chunk of this lane's 8 k
+      const u32x4 fa = *reinterpret_cast<const u32x4*>(ta + swz(ra_row, c) * 8);
+      const u32x4 fx = *reinterpret_cast<const u32x4*>(tx + swz(rx_row, c) * 8);
+      acc = mfma32x32x16(as_bf16x8(fa), as_bf16x8(fx), acc);
+    }
   }
-  __syncthreads();
-  if (w > 0) return;
+
+  // acc[j]: column 32 (w & 1) + (j / 4) * 8 + h * 4 + j % 4, token 32 (w >> 1) + l32.
+  const int64_t t = tok0 + 32 * (w >> 1) + l32;
+  if (t >= a.T) return;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = col0 + i * 16 + q * 4;
+  for (int jg = 0; jg < 4; ++jg) {
+    const int c = col0 + 32 * (w & 1) + jg * 8 + h * 4;
+    if (c >= a.n_cols) continue;
     const int plane = c / a.rank, jr = c - plane * a.rank;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      f32x4 v = acc[i][j];
-#pragma unroll
-      for (int p = 0; p < 3; ++p) v += *reinterpret_cast<const f32x4*>(&red[p][((i * 4 + j) * 64 + lane) * 4]);
-      const int64_t t = tok0 + j * 16 + c16;
-      if (c >= a.n_cols || t >= a.T) continue;
-      u32x2 o;
-      o[0] = pack_bf16(v[0], v[1]);
-      o[1] = pack_bf16(v[2], v[3]);
-      *reinterpret_cast<u32x2*>(a.L + ((int64_t)plane * a.s_cap + a.tok_offset + t) * a.rank + jr) = o;
-    }
+    u32x2 o;
+    o[0] = pack_bf16(acc[4 * jg + 0], acc[4 * jg + 1]);
+    o[1] = pack_bf16(acc[4 * jg + 2], acc[4 * jg + 3]);
+    *reinterpret_cast<u32x2*>(a.L + ((int64_t)plane * a.s_cap + a.tok_offset + t) * a.rank + jr) = o;
   }
 }
 

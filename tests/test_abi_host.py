@@ -53,6 +53,7 @@ def _pc(X=A16, T=64, d_in=256, ld_x=256, A=A16, n_proj=2, N=3, r=8, L=A16, s_cap
     (dict(d_in=0), EUNSUP),
     (dict(ld_x=128), ESHAPE),
     (dict(ld_x=260), EALIGN),
+    (dict(ld_x=1 << 24), EUNSUP),
     (dict(n_proj=0), EINVAL),
     (dict(N=0), EINVAL),
     (dict(r=12), EUNSUP),
