@@ -394,24 +394,39 @@ lrsa_prefill_kernel(const AttnArgs a) {
       };
       // The tile is consumed as two 32-token halves, each with its own online
       // softmax update (half the live score and P registers of a whole tile).
+      const bool half1 = t0 + 32 <= (int64_t)wave_last;
+      f32x16 s_next;
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb) {
         const int64_t th = t0 + tb * 32;  // first token of this half
         if (th > (int64_t)wave_last) break;
-        if (tb == 0) load_k(0);
         f32x16 s;
+        if (tb == 0) {
+          load_k(0);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) s[j] = 0.f;
+          for (int j = 0; j < 16; ++j) s[j] = 0.f;
 #pragma unroll
-        for (int kk = 0; kk < C::NKQ; ++kk) s = mfma32x32x16(kf[kk], qf[kk], s);
-        // The next half's K fragments are read while this half finishes.
-        if (tb == 0 && t0 + 32 <= (int64_t)wave_last) load_k(1);
+          for (int kk = 0; kk < C::NKQ; ++kk) s = mfma32x32x16(kf[kk], qf[kk], s);
+          // The second half's K fragments are read while the first half's
+          // scores finish.
+          if (half1) load_k(1);
+        } else {
+          s = s_next;
+        }
         if (th + 31 > (int64_t)wave_first) {  // this half crosses some row's causal limit
           // Positions fit in 32 bits (s_cap < 2^31): key t is masked iff t > last.
           const int rel = (int)last - (int)th - h32 * 4;  // last - (first token of this lane)
 #pragma unroll
           for (int j = 0; j < 16; ++j)
             if ((j >> 2) * 8 + (j & 3) > rel) s[j] = -INFINITY;
+        }
+        // The second half's scores are issued before the first half's
+        // softmax, so their MFMAs run beside its vector work.
+        if (tb == 0 && half1) {
+#pragma unroll
+          for (int j = 0; j < 16; ++j) s_next[j] = 0.f;
+#pragma unroll
+          for (int kk = 0; kk < C::NKQ; ++kk) s_next = mfma32x32x16(kf[kk], qf[kk], s_next);
         }
         float mx = s[0];
 #pragma unroll
