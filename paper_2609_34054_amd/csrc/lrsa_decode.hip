@@ -78,23 +78,64 @@ struct Stage {
   u32x2 lv[RCH(R)];               // L_v row fragment of token l%16
 };
 
+// Buffer resource over `bytes` bytes from `base` (raw, stride 0): loads at
+// offsets at or past the end return zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base, int32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, bytes, 0x00020000);
+}
+
+// Per-lane byte offsets of one 16-token sub-block's data (constant over the
+// kernel): the sub-block itself is addressed by resources built per
+// sub-block, whose range check zero-fills tokens at or past the split end.
+// The loads are branch-free, so the compiler can keep the next sub-block's
+// loads in flight while the current one is consumed.
 template <int D, int R>
-__device__ __forceinline__ void stage_load(Stage<D, R>& s, const uint16_t* Kb, const uint16_t* Vb,
-                                           const uint16_t* Lk, const uint16_t* Lv, int64_t row, int64_t t0,
-                                           int64_t t_end, int lane) {
+struct StageOffsets {
+  int32_t kb[D / 32], lr[RCH(R)], v[Dec<D, R>::NVL];
+};
+
+template <int D, int R>
+__device__ __forceinline__ StageOffsets<D, R> stage_offsets(int64_t row, int lane) {
   using C = Dec<D, R>;
-  const int c16 = lane & 15;
-  const int64_t t = t0 + c16;
-  const bool ok = t < t_end;
-  load_chunks<D>(s.kb, Kb + t * row, ok, lane);
-  if (Lk != nullptr) load_lr_frag<R>(s.lk, Lk + t * R, ok, lane);
-  if (Lv != nullptr) load_lr_frag<R>(s.lv, Lv + t * R, ok, lane);
+  StageOffsets<D, R> o;
+  const int c16 = lane & 15, q = lane >> 4;
+#pragma unroll
+  for (int kk = 0; kk < C::NCH; ++kk) o.kb[kk] = c16 * (int32_t)(row * 2) + chunk_dim<D>(kk, q) * 2;
+#pragma unroll
+  for (int rc = 0; rc < C::RC; ++rc) {
+    const int r0 = rc * 16 + q * 4;
+    o.lr[rc] = r0 < R ? c16 * R * 2 + r0 * 2 : INT32_MIN;  // ranks past r read as zeros
+  }
   const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
 #pragma unroll
-  for (int iv = 0; iv < C::NVL; ++iv) {
-    const int64_t tv = t0 + vrow + C::RPL * iv;
-    s.v[iv] = ld16(Vb + tv * row + vdim, tv < t_end);
+  for (int iv = 0; iv < C::NVL; ++iv) o.v[iv] = (vrow + C::RPL * iv) * (int32_t)(row * 2) + vdim * 2;
+  return o;
+}
+
+template <int D, int R>
+__device__ __forceinline__ void stage_load(Stage<D, R>& s, const StageOffsets<D, R>& o, const uint16_t* Kb,
+                                           const uint16_t* Vb, const uint16_t* Lk, const uint16_t* Lv,
+                                           int64_t row, int64_t t0, int64_t t_end) {
+  using C = Dec<D, R>;
+  // Valid tokens of the sub-block (none past the end: every load reads zeros).
+  const int64_t n = t_end - t0 < 0 ? 0 : (t_end - t0 < 16 ? t_end - t0 : 16);
+  const int32_t kv_bytes = n > 0 ? (int32_t)((n - 1) * row * 2 + D * 2) : 0;
+  const auto rk = make_rsrc(Kb + t0 * row, kv_bytes);
+  const auto rv = make_rsrc(Vb + t0 * row, kv_bytes);
+  // Absent LR caches get empty resources (loads read zeros, touch nothing).
+  const auto rlk = make_rsrc(Lk != nullptr ? Lk + t0 * R : Kb, Lk != nullptr ? (int32_t)(n * R * 2) : 0);
+  const auto rlv = make_rsrc(Lv != nullptr ? Lv + t0 * R : Kb, Lv != nullptr ? (int32_t)(n * R * 2) : 0);
+#pragma unroll
+  for (int kk = 0; kk < C::NCH; ++kk)
+    s.kb[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, o.kb[kk], 0, 0));
+#pragma unroll
+  for (int rc = 0; rc < C::RC; ++rc) {
+    s.lk[rc] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rlk, o.lr[rc], 0, 0));
+    s.lv[rc] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rlv, o.lr[rc], 0, 0));
   }
+#pragma unroll
+  for (int iv = 0; iv < C::NVL; ++iv)
+    s.v[iv] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, o.v[iv], 0, 0));
 }
 
 template <int D, int R>
@@ -106,7 +147,9 @@ lrsa_decode_kernel(const AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[NW][16 * C::V_ROW];
   __shared__ __attribute__((aligned(16))) uint16_t lv_lds[NW][16 * C::LV_ROW];
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // The wave index is made visibly wave-uniform, so that everything derived
+  // from it (the KV head and its buffer resources) lives in scalar registers.
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int split = blockIdx.x, b = blockIdx.z;
   const int g = blockIdx.y * NW + w;
   const bool active = g < a.n_kv;
@@ -139,6 +182,8 @@ lrsa_decode_kernel(const AttnArgs a) {
     sdl[k] = 0.f;
     if (has_lk) rope_cs(tok, a.w2pi[ej[k]], cdl[k], sdl[k]);
   }
+  // This thread's frequency for the per-tile base angles, read once.
+  const double w2pi_t = a.w2pi[tid < C::HALF ? tid : 0];
   if (has_lk && tid < C::HALF && n_tiles > 0) {
     float c, s;
     rope_cs((int)t_begin, a.w2pi[tid], c, s);
@@ -181,8 +226,9 @@ lrsa_decode_kernel(const AttnArgs a) {
   // 4*(l/16) + (j/4), columns 4*(j%4) .. +3 of a 16-column block.
   const int tr_row = 4 * q + (c16 >> 2), tr_col = 4 * (c16 & 3);
 
+  const StageOffsets<D, R> so = stage_offsets<D, R>(row, lane);
   Stage<D, R> st[2];
-  if (n_tiles > 0) stage_load<D, R>(st[0], Kb, Vb, Lk, Lv, row, t_begin, t_end_w, lane);
+  stage_load<D, R>(st[0], so, Kb, Vb, Lk, Lv, row, t_begin, t_end_w);
 
   __syncthreads();  // base angles of the first tile, zeroed L_v tiles
 
@@ -198,7 +244,7 @@ lrsa_decode_kernel(const AttnArgs a) {
       }
       if (tid < C::HALF && tile + 1 < n_tiles) {
         float c, s;
-        rope_cs((int)(t0 + TK), a.w2pi[tid], c, s);
+        rope_cs((int)(t0 + TK), w2pi_t, c, s);
         base_lds[(tile + 1) & 1][tid] = make_float2(c, s);
       }
     }
@@ -214,8 +260,9 @@ lrsa_decode_kernel(const AttnArgs a) {
       // A sub-block past the split end holds no visible key (and its stage
       // buffer was never loaded).
       if (ts >= t_end) break;
-      // Issue the next sub-block's loads before consuming this one.
-      if (ts + 16 < t_end) stage_load<D, R>(nxt, Kb, Vb, Lk, Lv, row, ts + 16, t_end_w, lane);
+      // Issue the next sub-block's loads before consuming this one (past the
+      // split end they read zeros and touch no memory).
+      stage_load<D, R>(nxt, so, Kb, Vb, Lk, Lv, row, ts + 16, t_end_w);
 
       // ---- V and L_v rows into the wave's LDS tile ------------------------
 #pragma unroll
