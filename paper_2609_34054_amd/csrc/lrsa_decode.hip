@@ -491,7 +491,7 @@ void decode_plan(int64_t s_cap, int batch, int n_kv, int* n_splits, int* split_t
   const int64_t tiles = (s_cap + TK - 1) / TK;
   const int64_t hg = (n_kv + NW - 1) / NW;
   const int64_t groups = (int64_t)(batch > 0 ? batch : 1) * hg;
-  const int64_t target_wgs = 1024;  // about four workgroups per CU
+  const int64_t target_wgs = 512;  // about two rounds of one workgroup per CU (measured best)
   int64_t ns = (target_wgs + groups - 1) / groups;
   if (ns < 1) ns = 1;
   if (ns > tiles) ns = tiles > 0 ? tiles : 1;
