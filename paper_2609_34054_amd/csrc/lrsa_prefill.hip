@@ -314,12 +314,15 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
     }
   };
-  // RoPE of each tile's first token, exact in fp64, by the last wave.
+  // RoPE of each tile's first token, exact in fp64, by the last wave.  Its
+  // lane's frequency is read once, outside the tile loop (a load in the loop
+  // would make the compiler wait for the tile loads in flight).
+  const double w2pi_lane = a.w2pi[lane < C::HALF ? lane : 0];
   auto base_angles = [&](int64_t t0, int buf) {
     if constexpr (LK) {
       if (w == NW - 1 && lane < C::HALF) {
         float c, s;
-        rope_cs((int)t0, a.w2pi[lane], c, s);
+        rope_cs((int)t0, w2pi_lane, c, s);
         base_cs[buf][lane] = make_float2(c, s);
       }
     }
@@ -343,6 +346,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
     for (int kk = 0; kk < C::NKQ; ++kk) qf[kk] = as_bf16x8(ld16(qp + kk * 16 + h32 * 8, row_ok));
   }
+  // Let these one-time loads (Q, B_k) land before the tile loop: across the
+  // loop's back edge the compiler could not tell them from the tile loads in
+  // flight and would wait for all of those at the first score MFMA.
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   f32x16 acc[C::NDB];   // O^T: lane col = row l%32
   f32x16 accl[C::RB];   // (P L_v)^T
 #pragma unroll
