@@ -5,8 +5,8 @@
 //   keys:   each KV tile is rebuilt in LDS, K = K_base + RoPE(L_k B_k), with
 //           the rank-r expansion before RoPE (App. D.2);
 //   values: associativity (App. D.2), O = P V_base + (P L_v) B_v: V_base and
-//           L_v tiles go to LDS unchanged, P L_v is accumulated beside P V_base
-//           and B_v is applied once in the epilogue.
+//           L_v go to LDS unchanged in value, P L_v is accumulated beside
+//           P V_base and B_v is applied once in the epilogue.
 //
 // Work split: one workgroup of 8 waves per (request, KV head, 256 query rows).
 // A query row is a (token, q head of the GQA group) pair, so the group's heads
@@ -15,24 +15,31 @@
 //           (w / 4) of the next KV tile: E^T = B_k^T L_k^T on 16x16x16 MFMAs
 //           (lane l: token l%16, both halves of each pair in the same lane),
 //           RoPE by angle addition (exact per-tile base angle in LDS, exact
-//           per-lane offsets in registers), + base, bf16 into LDS; it also
-//           copies 8 rows of V_base and L_v.  Its global loads for the tile
-//           after next are in flight meanwhile;
+//           per-lane offsets), + base, bf16 into LDS.  It also transposes a
+//           32-token block of V_base (and, for the first waves, of L_v) on
+//           the MFMA against a shifted identity, which writes them to LDS
+//           directly in the PV A-fragment layout.  Its global loads for the
+//           tile after next are in flight meanwhile;
 //   attend  over 32 query rows (lanes l and l^32 share row l%32), in two
 //           halves of 32 tokens:
 //     scores  S^T = K Q^T on 32x32x16 MFMAs, so softmax statistics are per
 //             lane; causal mask only on halves that cross it;
 //     softmax online, exp2 domain, lazily rescaled;
-//     PV      O^T += V^T P^T and (P L_v)^T += L_v^T P^T on 32x32x16 MFMAs;
-//             V^T and L_v^T come from row-major LDS tiles through the
-//             transposing LDS read, one MFMA ahead; P is already in the B
-//             operand layout.
-// The two waves that share a SIMD run the two jobs in opposite order, so one
-// wave's rebuild (vector ALU) overlaps the other's MFMAs.  LDS is
+//     PV      O^T += V^T P^T and (P L_v)^T += L_v^T P^T on 32x32x16 MFMAs,
+//             one conflict-free 16-byte LDS read per A fragment; P is
+//             already in the B operand layout.
+// LDS instructions, not bytes, bound the tile rate here (each costs the CU
+// about 4 cycles whatever its width), hence the fragment layouts above and
+// the register-resident identities and small-rank B_k fragments.  The two
+// waves that share a SIMD run the two jobs in opposite order.  LDS is
 // double-buffered with one barrier per tile.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
+
+#ifndef SGB
+#define SGB 0
+#endif
 
 namespace prc {
 namespace {
@@ -46,6 +53,7 @@ constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (log2 domain)
 
 template <int D, int R>
 struct Pre {
+  static_assert(D == 64 || D == 128, "head dims 64 and 128");
   static constexpr int HALF = D / 2;
   static constexpr int NB = D / 32;          // 16-dim blocks per RoPE half
   static constexpr int NBW = NB / 2;         // low blocks rebuilt per wave
@@ -56,16 +64,16 @@ struct Pre {
   static constexpr int NKQ = D / 16;         // 32x32x16 k-chunks over d
   static constexpr int NDB = D / 32;         // 32-dim blocks of O^T
   static constexpr int K_ROW = D + 8;        // bf16 per K row in LDS
-  // Row strides of the tiles read with ds_read_b64_tr_b16: the two 16-lane
-  // groups serviced together read the same 4 rows at column offsets 8 dwords
-  // apart, which land on disjoint banks when the stride is 16 or 48 dwords
-  // mod 64.
-  static constexpr int V_ROW = D + 32;                   // 80 / 48 dwords
-  static constexpr int LV_ROW = RB == 1 ? 32 : 96;       // 16 / 48 dwords
-  static constexpr int VLPR = D / 8;         // lanes per V row (16 bytes each)
-  static constexpr int VRPL = 64 / VLPR;     // V rows per wave load
-  static constexpr int NVL = 8 / VRPL;       // V loads per wave per tile (8 rows)
-  static constexpr int LVW = R < 16 ? 1 : R / 16;  // L_v words per lane (8 rows)
+  // V^T is kept in LDS as ready-made PV A fragments: fragment (m, db) holds,
+  // for lane l, dims 32 db + l%32 at the 8 tokens of 16-token chunk m in P's
+  // k order.  The tile is 2 x (D/16) half blocks of 32 tokens x 16 dims; each
+  // wave transposes NHB of them.
+  static constexpr int NHB = D / 64;         // half blocks per wave (8 waves)
+  // L_v^T likewise, fragment (m, rb) for ranks 32 rb + l%32: waves
+  // 0 .. 2 RB - 1 each transpose 32 tokens x 32 ranks, in NLP 16-rank halves.
+  static constexpr int NLP = R >= 32 ? 2 : 1;
+  // B_k^T fragments of small ranks stay in registers, larger ones in LDS.
+  static constexpr bool BK_REG = R <= 16;
 };
 
 // SEG consecutive bf16 of one row.
@@ -117,32 +125,13 @@ __device__ __forceinline__ uint32_t buf_ld4(__amdgpu_buffer_rsrc_t r, int32_t of
   return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
 }
 
-__device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) {
-  typedef short v4s __attribute__((ext_vector_type(4)));
-  v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((v4s __attribute__((address_space(3)))*)(p));
-  return __builtin_bit_cast(i16x4, v);
-}
-
-// 32x32x16 A operand [32 rows x 16 tokens] from a row-major [token][col] LDS
-// tile, in the token order of the P fragments: k = 8h + i is token
-// 16m + 4h + i (i < 4) or 16m + 8 + 4h + (i - 4) (i >= 4), h = l/32.
-__device__ __forceinline__ bf16x8 lds_tr_a32(const uint16_t* tile, int row_stride, int m, int col0, int lane) {
-  const int gg = lane >> 4, j = lane & 15, h = lane >> 5;
-  const uint16_t* p = tile + (16 * m + 4 * h + (j >> 2)) * row_stride + col0 + 16 * (gg & 1) + 4 * (j & 3);
-  const i16x4 lo = lds_read_tr(p);
-  const i16x4 hi = lds_read_tr(p + 8 * row_stride);
-  typedef short v8s __attribute__((ext_vector_type(8)));
-  v8s v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-  return __builtin_bit_cast(bf16x8, v);
-}
-
 // Global data one wave stages for one KV tile.
 template <int D, int R>
 struct Unit {
   Seg<Pre<D, R>::SEG> klo, khi;   // K_base of the lane's rebuild token, both halves
   u32x2 lk[RCH(R)];               // L_k row of that token (expansion B operand)
-  u32x4 v[Pre<D, R>::NVL];        // V_base rows 8w .. 8w+7
-  uint32_t lv[Pre<D, R>::LVW];    // L_v rows 8w .. 8w+7
+  u32x4 v[Pre<D, R>::NHB];        // V_base half blocks (32 tokens x 16 dims, A layout)
+  u32x4 lv[Pre<D, R>::NLP];       // L_v half blocks (32 tokens x 16 ranks, A layout)
 };
 
 template <int D, int R, bool LK, bool LV>
@@ -151,12 +140,14 @@ lrsa_prefill_kernel(const AttnArgs a) {
   using C = Pre<D, R>;
   constexpr bool ones_sum = LV && R < 32;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][TKV * C::K_ROW];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][TKV * C::V_ROW];
-  __shared__ __attribute__((aligned(16))) uint16_t lv_lds[2][TKV * C::LV_ROW];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][TKV * D];  // V^T fragments
+  __shared__ __attribute__((aligned(16))) uint16_t lv_lds[LV ? 2 : 1][LV ? TKV * 32 * C::RB : 8];  // L_v^T fragments
   __shared__ __attribute__((aligned(16))) float2 base_cs[2][C::HALF];
   // cos/sin of each build lane's in-tile offset at its SEG frequencies,
   // [wave][pair of frequencies][lane] (one 16-byte read per pair).
   __shared__ __attribute__((aligned(16))) f32x4 off_cs[LK ? NW : 1][C::SEG / 2][64];
+  // B_k of this KV head, [d][r] as stored (the expansion's A fragments).
+  __shared__ __attribute__((aligned(16))) uint16_t bk_lds[LK && !C::BK_REG ? D * R : 8];
   __shared__ int s_maxpos;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -166,14 +157,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int n_rows = a.n_tok * G;
 
   if (tid == 0) s_maxpos = -1;
-  // L_v columns past the rank stay zero in both buffers, except that with
-  // rank < 32 column `rank` holds ones: the (P L_v)^T product then carries the
-  // softmax row sums in its spare row for free.
-  if constexpr (LV) {
-    for (int i = tid; i < 2 * TKV * C::LV_ROW; i += NTHR)
-      (&lv_lds[0][0])[i] = (ones_sum && i % C::LV_ROW == R) ? (uint16_t)0x3F80 : (uint16_t)0;
+  if constexpr (LK && !C::BK_REG) {
+    const u32x4* src = reinterpret_cast<const u32x4*>(a.Bk + (int64_t)blockIdx.z * a.b_stride + (int64_t)blockIdx.y * D * R);
+    for (int i = tid; i < D * R / 8; i += NTHR) reinterpret_cast<u32x4*>(bk_lds)[i] = src[i];
   }
-
   int64_t kvl = a.kv_len[b];
   kvl = kvl < 0 ? 0 : (kvl > a.s_cap ? a.s_cap : kvl);
 
@@ -203,20 +190,45 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int blk0 = ph * C::NBW;                    // first low 16-dim block
   const int lo_dim0 = q * C::QPG + blk0 * 4;       // first low dim of this lane
   const int delta = 16 * tg + c16;                 // rebuild token within a tile
-  const int vrow = lane / C::VLPR, vdim = (lane % C::VLPR) * 8;
-  i16x4 bkf[2 * C::NBW][C::RC];  // B_k^T fragments: low blocks, then their partners
-  if constexpr (LK) {
-    const uint16_t* bhead = a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R;
+  // V half blocks of this wave: token block vtb, dim block vdb, 16-dim halves
+  // vp0 .. vp0 + NHB - 1 of it.
+  const int vtb = w & 1, vdb = (w >> 1) % C::NDB, vp0 = C::NHB == 2 ? 0 : w / (2 * C::NDB);
+  // Shifted identities (B operands): half p moves column 16p + k of a 16-wide
+  // chunk to output column 16p + k, so the 32x32x16 product of a half block
+  // of V or L_v rows (A operand: lane l = token l%32, columns (l/32)*8 + 0..7)
+  // lands transposed, lane = column, in exactly the PV fragment order (exact
+  // in bf16).
+  u32x4 vid[2];
 #pragma unroll
-    for (int i = 0; i < 2 * C::NBW; ++i) {
-      const int blk = blk0 + (i % C::NBW) + (i / C::NBW) * C::NB;
-      const int dim = blk_dim<D>(blk, c16);
+  for (int p = 0; p < 2; ++p)
 #pragma unroll
-      for (int rc = 0; rc < C::RC; ++rc) {
-        const int r0 = rc * 16 + q * 4;
-        bkf[i][rc] = as_i16x4(ld8(bhead + (int64_t)dim * R + (r0 < R ? r0 : 0), r0 < R));
-      }
+    for (int c = 0; c < 4; ++c) {
+      const int i0 = (lane & 31) - 16 * p - (lane >> 5) * 8 - 2 * c;  // element index of the 1
+      vid[p][c] = (i0 == 0 ? 0x3F80u : 0u) | (i0 == 1 ? 0x3F800000u : 0u);
     }
+  // L_v half blocks of this wave (waves < 2 RB): tokens 32 ltb.., ranks 32 lrb..
+  const int ltb = w & 1, lrb = w >> 1;
+  const bool lv_wave = LV && w < 2 * C::RB;
+  // B_k^T fragment (16x16x16 A operand) of low block i (i < NBW) or of its
+  // RoPE partner (i >= NBW), rank chunk rc: lane = dim row, 4 ranks from q*4.
+  const uint16_t* bhead = LK ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr;
+  auto bk_frag_at = [&](const uint16_t* base, int i, int rc) -> u32x2 {
+    const int blk = blk0 + (i % C::NBW) + (i / C::NBW) * C::NB;
+    const int r0 = rc * 16 + q * 4;
+    return *reinterpret_cast<const u32x2*>(base + blk_dim<D>(blk, c16) * R + (r0 < R ? r0 : 0));
+  };
+  u32x2 bkr[C::BK_REG && LK ? 2 * C::NBW : 1][C::RC];
+  if constexpr (C::BK_REG && LK) {
+#pragma unroll
+    for (int i = 0; i < 2 * C::NBW; ++i)
+#pragma unroll
+      for (int rc = 0; rc < C::RC; ++rc) bkr[i][rc] = bk_frag_at(bhead, i, rc);
+  }
+  auto bk_frag = [&](int i, int rc) -> i16x4 {
+    const u32x2 v = C::BK_REG ? bkr[i][rc] : bk_frag_at(bk_lds, i, rc);
+    return as_i16x4(rc * 16 + q * 4 < R ? v : u32x2{0u, 0u});
+  };
+  if constexpr (LK) {
 #pragma unroll
     for (int e = 0; e < C::SEG; e += 2) {
       float c0, s0, c1, s1;
@@ -230,14 +242,15 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // range check returns zeros for rows at or beyond kv_hi.
   const int32_t offk = delta * (int32_t)(row_el * 2) + lo_dim0 * 2;
   const int32_t offlk = delta * R * 2 + q * 8;
-  int32_t offv[C::NVL];
+  int32_t offv[C::NHB];
 #pragma unroll
-  for (int iv = 0; iv < C::NVL; ++iv) offv[iv] = (8 * w + vrow + C::VRPL * iv) * (int32_t)(row_el * 2) + vdim * 2;
-  int32_t offlv[C::LVW];
+  for (int hb = 0; hb < C::NHB; ++hb)
+    offv[hb] = (32 * vtb + (lane & 31)) * (int32_t)(row_el * 2) + (32 * vdb + 16 * (vp0 + hb) + (lane >> 5) * 8) * 2;
+  int32_t offlv[C::NLP];
 #pragma unroll
-  for (int j = 0; j < C::LVW; ++j) {
-    const int i = lane + 64 * j;
-    offlv[j] = i < 4 * R ? (8 * w + i / (R / 2)) * R * 2 + (i % (R / 2)) * 4 : INT32_MIN;
+  for (int p = 0; p < C::NLP; ++p) {
+    const int r0 = 32 * lrb + 16 * p + (lane >> 5) * 8;
+    offlv[p] = r0 < R ? (32 * ltb + (lane & 31)) * R * 2 + r0 * 2 : INT32_MIN;
   }
   auto load_unit = [&](Unit<D, R>& u, int64_t t0) {
     const int rows = (int)(kv_hi - t0 < TKV ? kv_hi - t0 : TKV);  // valid rows of this tile (> 0)
@@ -265,11 +278,11 @@ lrsa_prefill_kernel(const AttnArgs a) {
       for (int rc = 0; rc < C::RC; ++rc) u.lk[rc] = rc * 16 + q * 4 < R ? buf_ld8(rl, offlk + rc * 32) : u32x2{0u, 0u};
     }
 #pragma unroll
-    for (int iv = 0; iv < C::NVL; ++iv) u.v[iv] = buf_ld16(rv, offv[iv]);
+    for (int hb = 0; hb < C::NHB; ++hb) u.v[hb] = buf_ld16(rv, offv[hb]);
     if constexpr (LV) {
       const auto rl = make_rsrc(Lv + t0 * R, rows * R * 2);
 #pragma unroll
-      for (int j = 0; j < C::LVW; ++j) u.lv[j] = buf_ld4(rl, offlv[j]);
+      for (int p = 0; p < C::NLP; ++p) u.lv[p] = lv_wave ? buf_ld16(rl, offlv[p]) : u32x4{0u, 0u, 0u, 0u};
     }
   };
   auto rebuild = [&](const Unit<D, R>& u, int buf) {
@@ -280,8 +293,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
         f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int rc = 0; rc < C::RC; ++rc) {
-          elo = mfma16x16x16(bkf[i][rc], as_i16x4(u.lk[rc]), elo);
-          ehi = mfma16x16x16(bkf[C::NBW + i][rc], as_i16x4(u.lk[rc]), ehi);
+          elo = mfma16x16x16(bk_frag(i, rc), as_i16x4(u.lk[rc]), elo);
+          ehi = mfma16x16x16(bk_frag(C::NBW + i, rc), as_i16x4(u.lk[rc]), ehi);
         }
         float vlo[4], vhi[4];
         const f32x4 od0 = off_cs[w][2 * i][lane], od1 = off_cs[w][2 * i + 1][lane];
@@ -303,14 +316,42 @@ lrsa_prefill_kernel(const AttnArgs a) {
     }
     st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + lo_dim0, lo);
     st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + C::HALF + lo_dim0, hi);
+    {
+      // Transpose the V half blocks on the MFMA and store them as fragments
+      // (2 vtb, vdb) and (2 vtb + 1, vdb).
+      f32x16 t;
 #pragma unroll
-    for (int iv = 0; iv < C::NVL; ++iv)
-      *reinterpret_cast<u32x4*>(v_lds[buf] + (8 * w + vrow + C::VRPL * iv) * C::V_ROW + vdim) = u.v[iv];
-    if constexpr (LV) {
+      for (int j = 0; j < 16; ++j) t[j] = 0.f;
 #pragma unroll
-      for (int j = 0; j < C::LVW; ++j) {
-        const int i = lane + 64 * j, r = i / (R / 2), c = i % (R / 2);
-        if (i < 4 * R) reinterpret_cast<uint32_t*>(lv_lds[buf] + (8 * w + r) * C::LV_ROW)[c] = u.lv[j];
+      for (int hb = 0; hb < C::NHB; ++hb) t = mfma32x32x16(as_bf16x8(u.v[hb]), as_bf16x8(vid[vp0 + hb]), t);
+      // With one half block per wave (d = 64) the wave owns only its 16 dims
+      // of each fragment; the other half's lanes are written by another wave.
+      if (C::NHB == 2 || (lane & 31) / 16 == vp0) {
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+          u32x4 f;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) f[c] = pack_bf16(t[8 * hf + 2 * c], t[8 * hf + 2 * c + 1]);
+          *reinterpret_cast<u32x4*>(v_lds[buf] + (((2 * vtb + hf) * C::NDB + vdb) * 64 + lane) * 8) = f;
+        }
+      }
+    }
+    if (lv_wave) {
+      // L_v^T fragments (2 ltb + hf, lrb).  With rank < 32, rank row `rank`
+      // holds ones: the (P L_v)^T product then carries the softmax row sums in
+      // its spare row for free.
+      f32x16 t;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) t[j] = 0.f;
+#pragma unroll
+      for (int p = 0; p < C::NLP; ++p) t = mfma32x32x16(as_bf16x8(u.lv[p]), as_bf16x8(vid[p]), t);
+      const bool ones = ones_sum && (lane & 31) == R;
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        u32x4 f;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) f[c] = ones ? 0x3F803F80u : pack_bf16(t[8 * hf + 2 * c], t[8 * hf + 2 * c + 1]);
+        *reinterpret_cast<u32x4*>(lv_lds[buf] + (((2 * ltb + hf) * C::RB + lrb) * 64 + lane) * 8) = f;
       }
     }
   };
@@ -392,48 +433,40 @@ lrsa_prefill_kernel(const AttnArgs a) {
     };
     if (build_first) build();
     if (t0 <= (int64_t)wave_last) {
-      // K fragments (A operand of S^T = K Q^T) of one half, all in flight at once.
+      // K fragments (A operand of S^T = K Q^T) of one half.
       bf16x8 kf[C::NKQ];
-      auto load_k = [&](int tb) {
-        const uint16_t* kl = k_lds[buf] + (tb * 32 + l32) * C::K_ROW + h32 * 8;
-#pragma unroll
-        for (int kk = 0; kk < C::NKQ; ++kk) kf[kk] = as_bf16x8(*reinterpret_cast<const u32x4*>(kl + kk * 16));
+      auto k_frag = [&](int tb, int kk) {
+        return as_bf16x8(*reinterpret_cast<const u32x4*>(k_lds[buf] + (tb * 32 + l32) * C::K_ROW + h32 * 8 + kk * 16));
       };
+      // Scores of the first half.  Each second-half K fragment is read as
+      // soon as the first half's MFMA has taken its register (harmless when
+      // that half is unused).
+      f32x16 s, s_next;
+#pragma unroll
+      for (int kk = 0; kk < C::NKQ; ++kk) kf[kk] = k_frag(0, kk);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) s[j] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < C::NKQ; ++kk) {
+        s = mfma32x32x16(kf[kk], qf[kk], s);
+        kf[kk] = k_frag(1, kk);
+      }
       // The tile is consumed as two 32-token halves, each with its own online
-      // softmax update (half the live score and P registers of a whole tile).
-      const bool half1 = t0 + 32 <= (int64_t)wave_last;
-      f32x16 s_next;
+      // softmax update.  Per half: mask and row maximum, the (rare) rescale,
+      // then one straight-line block in which the exponentials run beside
+      // MFMAs: the second half's scores during the first half's softmax, and
+      // each 16-token chunk's PV beside the next chunk's exponentials.
 #pragma unroll
       for (int tb = 0; tb < 2; ++tb) {
         const int64_t th = t0 + tb * 32;  // first token of this half
         if (th > (int64_t)wave_last) break;
-        f32x16 s;
-        if (tb == 0) {
-          load_k(0);
-#pragma unroll
-          for (int j = 0; j < 16; ++j) s[j] = 0.f;
-#pragma unroll
-          for (int kk = 0; kk < C::NKQ; ++kk) s = mfma32x32x16(kf[kk], qf[kk], s);
-          // The second half's K fragments are read while the first half's
-          // scores finish.
-          if (half1) load_k(1);
-        } else {
-          s = s_next;
-        }
+        if (tb == 1) s = s_next;
         if (th + 31 > (int64_t)wave_first) {  // this half crosses some row's causal limit
           // Positions fit in 32 bits (s_cap < 2^31): key t is masked iff t > last.
           const int rel = (int)last - (int)th - h32 * 4;  // last - (first token of this lane)
 #pragma unroll
           for (int j = 0; j < 16; ++j)
             if ((j >> 2) * 8 + (j & 3) > rel) s[j] = -INFINITY;
-        }
-        // The second half's scores are issued before the first half's
-        // softmax, so their MFMAs run beside its vector work.
-        if (tb == 0 && half1) {
-#pragma unroll
-          for (int j = 0; j < 16; ++j) s_next[j] = 0.f;
-#pragma unroll
-          for (int kk = 0; kk < C::NKQ; ++kk) s_next = mfma32x32x16(kf[kk], qf[kk], s_next);
         }
         float mx = s[0];
 #pragma unroll
@@ -453,6 +486,27 @@ lrsa_prefill_kernel(const AttnArgs a) {
           m_run = mn;
         }
         const float ms = (m_run == -INFINITY) ? 0.f : m_run;
+        // PV A fragments of this half.
+        const uint16_t* vt = v_lds[buf];
+        const uint16_t* lvt = lv_lds[buf];
+        bf16x8 vf[2][C::NDB], lvf[2][C::RB];
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) {
+#pragma unroll
+          for (int db = 0; db < C::NDB; ++db)
+            vf[hf][db] = as_bf16x8(*reinterpret_cast<const u32x4*>(vt + (((2 * tb + hf) * C::NDB + db) * 64 + lane) * 8));
+          if constexpr (LV) {
+#pragma unroll
+            for (int rb = 0; rb < C::RB; ++rb)
+              lvf[hf][rb] = as_bf16x8(*reinterpret_cast<const u32x4*>(lvt + (((2 * tb + hf) * C::RB + rb) * 64 + lane) * 8));
+          }
+        }
+        if (tb == 0) {
+#pragma unroll
+          for (int j = 0; j < 16; ++j) s_next[j] = 0.f;
+#pragma unroll
+          for (int kk = 0; kk < C::NKQ; ++kk) s_next = mfma32x32x16(kf[kk], qf[kk], s_next);
+        }
         float ls0 = 0.f, ls1 = 0.f;
         u32x4 pw[2];  // bf16 P of this half, one per 16-token chunk
 #pragma unroll
@@ -470,30 +524,38 @@ lrsa_prefill_kernel(const AttnArgs a) {
         if constexpr (!ones_sum) l_run += ls0 + ls1;
         // O^T[dims x rows] += V^T[dims x 16 tok] P^T[16 tok x rows] for the two
         // 16-token chunks of this half; (P L_v)^T likewise with L_v^T.
-        const uint16_t* vt = v_lds[buf];
-        const uint16_t* lvt = lv_lds[buf];
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
-          const int m = 2 * tb + hf;
           const bf16x8 pb = as_bf16x8(pw[hf]);
-          // A fragments are read one MFMA ahead; the L_v ones at the chunk start.
-          bf16x8 lvf[C::RB];
+#pragma unroll
+          for (int db = 0; db < C::NDB; ++db) acc[db] = mfma32x32x16(vf[hf][db], pb, acc[db]);
           if constexpr (LV) {
 #pragma unroll
-            for (int rb = 0; rb < C::RB; ++rb) lvf[rb] = lds_tr_a32(lvt, C::LV_ROW, m, rb * 32, lane);
-          }
-          bf16x8 fa = lds_tr_a32(vt, C::V_ROW, m, 0, lane);
-#pragma unroll
-          for (int db = 0; db < C::NDB; ++db) {
-            const bf16x8 fn = db + 1 < C::NDB ? lds_tr_a32(vt, C::V_ROW, m, (db + 1) * 32, lane) : fa;
-            acc[db] = mfma32x32x16(fa, pb, acc[db]);
-            fa = fn;
-          }
-          if constexpr (LV) {
-#pragma unroll
-            for (int rb = 0; rb < C::RB; ++rb) accl[rb] = mfma32x32x16(lvf[rb], pb, accl[rb]);
+            for (int rb = 0; rb < C::RB; ++rb) accl[rb] = mfma32x32x16(lvf[hf][rb], pb, accl[rb]);
           }
         }
+#if SGB
+        // Issue order of the block: LDS reads first, then (first half only)
+        // one score MFMA per 5 vector instructions, then the PV MFMAs of
+        // chunk 0 interleaved with the rest of the vector work.
+        constexpr int NPV = C::NDB + (LV ? C::RB : 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2 * NPV + (LV ? 2 * C::RB : 0), 0);
+        if (tb == 0) {
+#pragma unroll
+          for (int i = 0; i < C::NKQ; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x402, 3, 0);
+          }
+        } else {
+          __builtin_amdgcn_sched_group_barrier(0x402, 20, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < NPV; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x402, 4, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, NPV, 0);
+#endif
       }
     }
     if (!build_first) build();
