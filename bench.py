@@ -50,22 +50,26 @@ def workload_dims():
         theta=cfg.theta)
 
 
-def algorithmic_work(w):
-    """Bytes and flops the method must move/do (each counted once)."""
+def algorithmic_work(w, lk=True, lv=True):
+    """Bytes and flops the method must move/do (each counted once); lk / lv
+    say which projections carry an LR part (both for the k-and-v workload,
+    only lv for the paper's QV setting)."""
     S, d, n_q, n_kv, r, B = w["S"], w["d"], w["n_q"], w["n_kv"], w["r"], w["B"]
+    n_lr = int(lk) + int(lv)
     # Decode: read each request's base K and V and its agent's L_k, L_v rows
     # once, plus Q, B_k, B_v, and write O.
-    dec_bytes_req = (S * n_kv * d * 2 * 2 + S * r * 2 * 2 + n_q * d * 2 + 2 * n_kv * d * r * 2 + n_q * d * 2)
-    dec_flops_req = (4 * n_q * d * S            # Q K^T and P V
-                     + 2 * r * d * n_kv * S     # key-side expansion L_k B_k
-                     + 2 * n_q * r * S          # P L_v
-                     + 2 * n_q * r * d)         # (P L_v) B_v
+    dec_bytes_req = (S * n_kv * d * 2 * 2 + S * r * 2 * n_lr + n_q * d * 2 + n_lr * n_kv * d * r * 2
+                     + n_q * d * 2)
+    dec_flops_req = (4 * n_q * d * S                        # Q K^T and P V
+                     + int(lk) * 2 * r * d * n_kv * S       # key-side expansion L_k B_k
+                     + int(lv) * 2 * n_q * r * S            # P L_v
+                     + int(lv) * 2 * n_q * r * d)           # (P L_v) B_v
     # Prefill: 4096 queries at positions S..S+n-1, causal.
     n = w["n_pre"]
     kv = S + n
     vis = sum(S + i + 1 for i in range(n))
-    pre_flops = 4 * n_q * d * vis + 2 * 2 * r * d * n_kv * kv
-    pre_bytes = kv * n_kv * d * 2 * 2 + kv * r * 2 * 2 + 2 * n * n_q * d * 2 + 2 * n_kv * d * r * 2
+    pre_flops = 4 * n_q * d * vis + n_lr * 2 * r * d * n_kv * kv
+    pre_bytes = kv * n_kv * d * 2 * 2 + kv * r * 2 * n_lr + 2 * n * n_q * d * 2 + n_lr * n_kv * d * r * 2
     # Precompute: X[seg x hidden] . A[hidden x 2Nr].
     cols = 2 * w["N"] * r
     pc_flops = 2 * w["seg"] * w["hidden"] * cols
@@ -306,6 +310,74 @@ def traffic_for(kernel_file, launches_per_stage=1):
     return rec.get("hbm_bytes_per_launch")
 
 
+def rank_sweep(prc, w, dev, steps, warmup):
+    """Throughput of the fused prefill and decode over LoRA ranks 8..64, with
+    LR on k and v (the workload's setting) and on v only (the paper's QV
+    setting), plus plain attention over the base cache; one JSON line each.
+    Same shapes as the main workload; only the rank and the adapted
+    projections change."""
+    import torch
+    g = torch.Generator(device=dev).manual_seed(4000)
+
+    def nrm(shape, std=1.0):
+        x = torch.randn(*shape, generator=g, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            x.mul_(std)
+        return x.to(torch.bfloat16)
+
+    S, d, n_q, n_kv, B = w["S"], w["d"], w["n_q"], w["n_kv"], w["B"]
+    kv_pre = S + w["n_pre"]
+    base = dict(
+        pre=dict(Q=nrm((1, w["n_pre"], n_q, d)), K_base=nrm((1, kv_pre, n_kv, d)), V_base=nrm((1, kv_pre, n_kv, d)),
+                 positions=torch.arange(S, kv_pre, dtype=torch.int32, device=dev)[None],
+                 kv_len=torch.tensor([kv_pre], dtype=torch.int32, device=dev)),
+        dec=dict(Q=nrm((B, 1, n_q, d)), K_base=nrm((B, S, n_kv, d)), V_base=nrm((B, S, n_kv, d)),
+                 positions=torch.full((B, 1), S - 1, dtype=torch.int32, device=dev),
+                 kv_len=torch.full((B,), S, dtype=torch.int32, device=dev)))
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    runs = [("plain", 16, False, False)] + [(m, r, m == "kv", True) for m in ("qv", "kv") for r in (8, 16, 32, 64)]
+    bstd = math.sqrt(0.02)
+    for mode, r, lk, lv in runs:
+        cases = {}
+        for st, nb, ntok in (("pre", 1, kv_pre), ("dec", B, S)):
+            c = dict(base[st])
+            c["L_k"] = nrm((nb, ntok, r)) if lk else None
+            c["L_v"] = nrm((nb, ntok, r)) if lv else None
+            c["Bk_rows"] = nrm((nb, n_kv * d, r), bstd) if lk else None
+            c["Bv_rows"] = nrm((nb, n_kv * d, r), bstd) if lv else None
+            cases[st] = c
+        O_pre = torch.empty_like(cases["pre"]["Q"])
+        O_dec = torch.empty_like(cases["dec"]["Q"])
+        cd = cases["dec"]
+        dims = prc.make_dims(cd["Q"], cd["K_base"], cd["L_k"], cd["L_v"], cd["Bk_rows"], cd["Bv_rows"], w["theta"])
+        ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
+        t_pre = timed(lambda: attn(prc, cases["pre"], w["theta"], O_pre, None))
+        t_dec = timed(lambda: attn(prc, cases["dec"], w["theta"], O_dec, ws))
+        work = algorithmic_work(dict(w, r=r), lk, lv)
+        pre_tf = work["prefill_flops"] / (t_pre * 1e-3) / 1e12
+        dec_gbs = work["decode_bytes"] / (t_dec * 1e-3) / 1e9
+        print(json.dumps({"sweep": "rank", "mode": mode, "rank": r if (lk or lv) else 0,
+                          "prefill_ms": round(t_pre, 4), "prefill_tflops": round(pre_tf, 2),
+                          "prefill_mfma_frac": round(pre_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                          "decode_ms": round(t_dec, 4), "decode_gbs": round(dec_gbs, 1),
+                          "decode_hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+                          "decode_bytes": work["decode_bytes"], "prefill_flops": work["prefill_flops"]}),
+              flush=True)
+        del cases, O_pre, O_dec, ws
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -317,6 +389,9 @@ def main():
     ap.add_argument("--pmc-pass", action="store_true",
                     help="for hardware-counter runs: one 1 GiB calibration copy, then exactly one launch of "
                          "each hot-path kernel, no timing")
+    ap.add_argument("--rank-sweep", action="store_true",
+                    help="instead of the step: prefill and decode throughput over ranks 8..64 with LR on k and v "
+                         "and on v only (the paper's QV setting), one JSON line each")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -331,6 +406,9 @@ def main():
     prc.lib()
     dev = torch.device("cuda:0")
     cfg, w = workload_dims()
+    if args.rank_sweep:
+        rank_sweep(prc, w, dev, max(3, args.steps // 2), args.warmup)
+        return
     work = algorithmic_work(w)
     print(f"bench: generating inputs ({w['B']} x {w['S']}-token decode caches)", file=sys.stderr, flush=True)
     x = make_inputs(w, dev)

@@ -46,7 +46,7 @@ struct AttnArgs {
 
 // Decode (one query token per request): split-KV partials + merge.
 int decode_tile_tokens();
-void decode_plan(int64_t s_cap, int batch, int n_kv, int* n_splits, int* split_tiles);
+void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, int* n_splits, int* split_tiles);
 size_t decode_workspace_bytes(int batch, int n_q, int n_splits, int head_dim, int rank);
 hipError_t launch_decode(const AttnArgs& a, hipStream_t stream);
 

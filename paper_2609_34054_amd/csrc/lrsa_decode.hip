@@ -38,11 +38,16 @@ namespace {
 
 constexpr int TK = 32;        // tokens per KV tile (one LDS table, one barrier)
 constexpr int NSB = TK / 16;  // 16-token sub-blocks per tile
-constexpr int NW = 8;         // waves per workgroup (KV heads)
-constexpr int NT = NW * 64;   // threads per workgroup
+// Waves per workgroup (one KV head each).  Rank 64 keeps its B_k^T
+// fragments (64 VGPRs) in registers by running one wave per SIMD, which
+// gives each wave the whole register file (architected plus accumulation
+// registers) instead of spilling to scratch.
+constexpr int dec_waves(int rank) { return rank >= 64 ? 4 : 8; }
 
 template <int D, int R>
 struct Dec {
+  static constexpr int NW = dec_waves(R);    // waves per workgroup (KV heads)
+  static constexpr int NT = NW * 64;         // threads per workgroup
   static constexpr int HALF = D / 2;
   static constexpr int NB = D / 32;           // 16-dim blocks per RoPE half
   static constexpr int NBLK = D / 16;         // 16-dim blocks
@@ -139,9 +144,10 @@ __device__ __forceinline__ void stage_load(Stage<D, R>& s, const StageOffsets<D,
 }
 
 template <int D, int R>
-__global__ void __launch_bounds__(NT)
+__global__ void __launch_bounds__(dec_waves(R) * 64, dec_waves(R) / 4)
 lrsa_decode_kernel(const AttnArgs a) {
   using C = Dec<D, R>;
+  constexpr int NW = C::NW, NT = C::NT;
   __shared__ float2 cs_lds[2][TK * C::CS_ROW];
   __shared__ float2 base_lds[2][C::HALF];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[NW][16 * C::V_ROW];
@@ -464,8 +470,9 @@ lrsa_merge_kernel(const AttnArgs a) {
 
 template <int D, int R>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
-  const int hg = (a.n_kv + NW - 1) / NW;
-  hipLaunchKernelGGL((lrsa_decode_kernel<D, R>), dim3(a.n_splits, hg, a.batch), dim3(NT), 0, st, a);
+  using C = Dec<D, R>;
+  const int hg = (a.n_kv + C::NW - 1) / C::NW;
+  hipLaunchKernelGGL((lrsa_decode_kernel<D, R>), dim3(a.n_splits, hg, a.batch), dim3(C::NT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch), dim3(64 * MW), 0, st, a);
@@ -487,11 +494,13 @@ hipError_t launch_r(const AttnArgs& a, hipStream_t st) {
 
 int decode_tile_tokens() { return TK; }
 
-void decode_plan(int64_t s_cap, int batch, int n_kv, int* n_splits, int* split_tiles) {
+void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, int* n_splits, int* split_tiles) {
   const int64_t tiles = (s_cap + TK - 1) / TK;
-  const int64_t hg = (n_kv + NW - 1) / NW;
+  const int nw = dec_waves(rank);
+  const int64_t hg = (n_kv + nw - 1) / nw;
   const int64_t groups = (int64_t)(batch > 0 ? batch : 1) * hg;
-  const int64_t target_wgs = 512;  // about two rounds of one workgroup per CU (measured best)
+  // About two rounds of one workgroup per CU (measured best), in waves.
+  const int64_t target_wgs = 512 * 8 / nw;
   int64_t ns = (target_wgs + groups - 1) / groups;
   if (ns < 1) ns = 1;
   if (ns > tiles) ns = tiles > 0 ? tiles : 1;

@@ -146,8 +146,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // cos/sin of each build lane's in-tile offset at its SEG frequencies,
   // [wave][pair of frequencies][lane] (one 16-byte read per pair).
   __shared__ __attribute__((aligned(16))) f32x4 off_cs[LK ? NW : 1][C::SEG / 2][64];
-  // B_k of this KV head, [d][r] as stored (the expansion's A fragments).
-  __shared__ __attribute__((aligned(16))) uint16_t bk_lds[LK && !C::BK_REG ? D * R : 8];
+  // B_k^T fragments of this KV head for ranks > 16, [RoPE half ph][block i]
+  // [lane][rank chunk]: each lane's RC fragments are contiguous, so a block's
+  // set comes in RC / 2 16-byte reads.
+  __shared__ __attribute__((aligned(16))) u32x2 bk_lds[LK && !C::BK_REG ? 2 * 2 * C::NBW * 64 * C::RC : 2];
   __shared__ int s_maxpos;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -158,8 +160,14 @@ lrsa_prefill_kernel(const AttnArgs a) {
 
   if (tid == 0) s_maxpos = -1;
   if constexpr (LK && !C::BK_REG) {
-    const u32x4* src = reinterpret_cast<const u32x4*>(a.Bk + (int64_t)blockIdx.z * a.b_stride + (int64_t)blockIdx.y * D * R);
-    for (int i = tid; i < D * R / 8; i += NTHR) reinterpret_cast<u32x4*>(bk_lds)[i] = src[i];
+    const uint16_t* bh = a.Bk + (int64_t)blockIdx.z * a.b_stride + (int64_t)blockIdx.y * D * R;
+    for (int e = tid; e < 2 * 2 * C::NBW * 64 * C::RC; e += NTHR) {
+      const int rc = e % C::RC, l = (e / C::RC) % 64, i = (e / (C::RC * 64)) % (2 * C::NBW);
+      const int phe = e / (C::RC * 64 * 2 * C::NBW);
+      const int blk = phe * C::NBW + (i % C::NBW) + (i / C::NBW) * C::NB;
+      const int r0 = rc * 16 + (l >> 4) * 4;
+      bk_lds[e] = r0 < R ? *reinterpret_cast<const u32x2*>(bh + blk_dim<D>(blk, l & 15) * R + r0) : u32x2{0u, 0u};
+    }
   }
   int64_t kvl = a.kv_len[b];
   kvl = kvl < 0 ? 0 : (kvl > a.s_cap ? a.s_cap : kvl);
@@ -222,11 +230,25 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
     for (int i = 0; i < 2 * C::NBW; ++i)
 #pragma unroll
-      for (int rc = 0; rc < C::RC; ++rc) bkr[i][rc] = bk_frag_at(bhead, i, rc);
+      for (int rc = 0; rc < C::RC; ++rc) {
+        const u32x2 v = bk_frag_at(bhead, i, rc);
+        bkr[i][rc] = rc * 16 + q * 4 < R ? v : u32x2{0u, 0u};
+      }
   }
-  auto bk_frag = [&](int i, int rc) -> i16x4 {
-    const u32x2 v = C::BK_REG ? bkr[i][rc] : bk_frag_at(bk_lds, i, rc);
-    return as_i16x4(rc * 16 + q * 4 < R ? v : u32x2{0u, 0u});
+  // The RC fragments of block set i (registers, or 16-byte LDS reads).
+  auto bk_set = [&](int i, u32x2 (&f)[C::RC]) {
+    if constexpr (C::BK_REG) {
+#pragma unroll
+      for (int rc = 0; rc < C::RC; ++rc) f[rc] = bkr[i][rc];
+    } else {
+      const u32x4* p = reinterpret_cast<const u32x4*>(bk_lds + ((ph * 2 * C::NBW + i) * 64 + lane) * C::RC);
+#pragma unroll
+      for (int j = 0; j < C::RC / 2; ++j) {
+        const u32x4 v = p[j];
+        f[2 * j] = u32x2{v[0], v[1]};
+        f[2 * j + 1] = u32x2{v[2], v[3]};
+      }
+    }
   };
   if constexpr (LK) {
 #pragma unroll
@@ -291,10 +313,13 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < C::NBW; ++i) {
         f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
+        u32x2 fl[C::RC], fh[C::RC];
+        bk_set(i, fl);
+        bk_set(C::NBW + i, fh);
 #pragma unroll
         for (int rc = 0; rc < C::RC; ++rc) {
-          elo = mfma16x16x16(bk_frag(i, rc), as_i16x4(u.lk[rc]), elo);
-          ehi = mfma16x16x16(bk_frag(C::NBW + i, rc), as_i16x4(u.lk[rc]), ehi);
+          elo = mfma16x16x16(as_i16x4(fl[rc]), as_i16x4(u.lk[rc]), elo);
+          ehi = mfma16x16x16(as_i16x4(fh[rc]), as_i16x4(u.lk[rc]), ehi);
         }
         float vlo[4], vhi[4];
         const f32x4 od0 = off_cs[w][2 * i][lane], od1 = off_cs[w][2 * i + 1][lane];

@@ -84,6 +84,12 @@ ATTN_CASES = [
     ("d64_g4_r32_prefill", 64, 32, 8, 2, 33, [97], 104, "kv", 1.0, "end"),
     ("qv_prefill", 128, 16, 8, 2, 40, [256], 256, "v", 1.0, "end"),
     ("qv_decode", 128, 16, 8, 2, 1, [512, 300], 512, "v", 1.0, "end"),
+    # The paper's QV setting over its rank range (value LR only).
+    ("qv_r8_prefill", 128, 8, 8, 2, 45, [190], 192, "v", 1.0, "end"),
+    ("qv_r32_decode", 128, 32, 8, 2, 1, [700, 129], 704, "v", 1.0, "end"),
+    ("qv_r64_prefill", 128, 64, 8, 2, 33, [260], 264, "v", 1.0, "end"),
+    ("qv_r64_decode", 128, 64, 8, 2, 1, [333], 336, "v", 1.0, "end"),
+    ("qv_d64_r32_prefill", 64, 32, 4, 4, 70, [140], 144, "v", 1.0, "end"),
     ("k_only_prefill", 128, 16, 8, 2, 24, [128], 136, "k", 1.0, "end"),
     ("k_only_decode", 64, 8, 4, 2, 1, [90], 96, "k", 1.0, "end"),
     ("plain_prefill", 128, 16, 8, 2, 50, [300], 304, "none", 1.0, "end"),
