@@ -378,6 +378,64 @@ def rank_sweep(prc, w, dev, steps, warmup):
         del cases, O_pre, O_dec, ws
 
 
+def shared_base_decode(prc, w, dev, steps, warmup):
+    """Decode of all N agents at the end of one shared 32k-token trajectory:
+    one base cache, each agent its own LR plane, up-projections and query.
+    The shared-base kernel reads every base tile once for all agents; the
+    reference is the per-request kernel over per-agent copies of the base
+    (what decoding the agents as independent requests costs).  One JSON line."""
+    import torch
+    g = torch.Generator(device=dev).manual_seed(5000)
+
+    def nrm(shape, std=1.0):
+        x = torch.randn(*shape, generator=g, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            x.mul_(std)
+        return x.to(torch.bfloat16)
+
+    S, d, n_q, n_kv, r, N = w["S"], w["d"], w["n_q"], w["n_kv"], w["r"], w["N"]
+    bstd = math.sqrt(0.02)
+    c = dict(Q=nrm((N, 1, n_q, d)), K_base=nrm((1, S, n_kv, d)), V_base=nrm((1, S, n_kv, d)),
+             L_k=nrm((N, S, r)), L_v=nrm((N, S, r)), Bk_rows=nrm((N, n_kv * d, r), bstd),
+             Bv_rows=nrm((N, n_kv * d, r), bstd),
+             positions=torch.full((N, 1), S - 1, dtype=torch.int32, device=dev),
+             kv_len=torch.full((N,), S, dtype=torch.int32, device=dev))
+    O = torch.empty_like(c["Q"])
+
+    def timed(case):
+        dims = prc.make_dims(case["Q"], case["K_base"], case["L_k"], case["L_v"], case["Bk_rows"],
+                             case["Bv_rows"], w["theta"])
+        ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
+        for _ in range(warmup):
+            attn(prc, case, w["theta"], O, ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            attn(prc, case, w["theta"], O, ws)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps, O.clone()
+
+    t_shared, O_shared = timed(c)
+    rep = dict(c, K_base=c["K_base"].expand(N, -1, -1, -1).contiguous(),
+               V_base=c["V_base"].expand(N, -1, -1, -1).contiguous())
+    t_rep, O_rep = timed(rep)
+    diff = (O_shared.float() - O_rep.float()).abs().max().item()
+    base_bytes = S * n_kv * d * 2 * 2
+    lr_bytes = N * (S * r * 2 * 2 + 2 * n_kv * d * r * 2 + 2 * n_q * d * 2)
+    algo = base_bytes + lr_bytes
+    gbs = algo / (t_shared * 1e-3) / 1e9
+    print(json.dumps({
+        "bench": "shared_base_decode", "agents": N, "context": S, "rank": r,
+        "workload": (f"decode of {N} agents at position {S - 1} over one shared {S}-token base cache "
+                     f"({n_q} q / {n_kv} KV heads, d {d}), each with its own rank-{r} k and v LR plane"),
+        "ms": round(t_shared, 4), "algorithmic_bytes": algo, "gbs": round(gbs, 1),
+        "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
+        "per_request_copies_ms": round(t_rep, 4), "speedup_vs_per_request_copies": round(t_rep / t_shared, 3),
+        "max_abs_diff_vs_per_request": diff}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -392,6 +450,9 @@ def main():
     ap.add_argument("--rank-sweep", action="store_true",
                     help="instead of the step: prefill and decode throughput over ranks 8..64 with LR on k and v "
                          "and on v only (the paper's QV setting), one JSON line each")
+    ap.add_argument("--shared-base", action="store_true",
+                    help="instead of the step: decode of all agents over one shared base cache, against the "
+                         "same agents decoded as independent requests over per-agent copies")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -408,6 +469,9 @@ def main():
     cfg, w = workload_dims()
     if args.rank_sweep:
         rank_sweep(prc, w, dev, max(3, args.steps // 2), args.warmup)
+        return
+    if args.shared_base:
+        shared_base_decode(prc, w, dev, args.steps, args.warmup)
         return
     work = algorithmic_work(w)
     print(f"bench: generating inputs ({w['B']} x {w['S']}-token decode caches)", file=sys.stderr, flush=True)

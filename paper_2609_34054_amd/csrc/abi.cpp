@@ -196,7 +196,8 @@ PRC_API size_t lr_shared_attention_workspace_size(const lrsa_dims* dims) {
     return 0;
   const int r = rank_ok(dims->rank) ? dims->rank : 8;
   int n_splits = 0, split_tiles = 0;
-  prc::decode_plan(dims->s_cap, dims->batch, dims->n_kv_heads, r, &n_splits, &split_tiles);
+  prc::decode_plan(dims->s_cap, dims->batch, dims->n_kv_heads, r,
+                   prc::decode_shares_base(dims->batch, dims->kv_req_stride), &n_splits, &split_tiles);
   return prc::decode_workspace_bytes(dims->batch, dims->n_q_heads, n_splits, dims->head_dim, r);
 }
 
@@ -225,7 +226,8 @@ PRC_API prc_status lr_shared_attention(const lrsa_dims* dims, const uint16_t* Q,
       return fail(PRC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace == nullptr ? 0 : workspace_bytes,
                   need);
     if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
-    prc::decode_plan(a.s_cap, a.batch, a.n_kv, a.rank, &a.n_splits, &a.split_tiles);
+    prc::decode_plan(a.s_cap, a.batch, a.n_kv, a.rank, prc::decode_shares_base(a.batch, a.kv_stride), &a.n_splits,
+                     &a.split_tiles);
     a.ws = static_cast<float*>(workspace);
     return launch_status(prc::launch_decode(a, st), "lr_shared_attention (decode)");
   }

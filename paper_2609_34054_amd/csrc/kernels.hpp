@@ -46,7 +46,11 @@ struct AttnArgs {
 
 // Decode (one query token per request): split-KV partials + merge.
 int decode_tile_tokens();
-void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, int* n_splits, int* split_tiles);
+// A decode batch whose requests all read one base cache (request stride 0)
+// runs the shared-base kernel: each base tile is read once for all of them.
+bool decode_shares_base(int batch, int64_t kv_req_stride);
+void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base, int* n_splits,
+                 int* split_tiles);
 size_t decode_workspace_bytes(int batch, int n_q, int n_splits, int head_dim, int rank);
 hipError_t launch_decode(const AttnArgs& a, hipStream_t stream);
 

@@ -468,6 +468,305 @@ lrsa_merge_kernel(const AttnArgs a) {
     a.lse[(int64_t)b * a.n_tok * a.n_q + h] = L > 0.f ? (M + __log2f(L)) * kLn2 : -INFINITY;
 }
 
+// ---------------------------------------------------------------------------
+// Decode over one base cache shared by every request (kv_req_stride == 0):
+// several agents' queries over the same trajectory, each with its own LR
+// plane, up-projections, query and position.  One workgroup per (split, KV
+// head, group of NW requests); wave w serves request group*NW + w.  Each
+// 64-token step of the head's K_base/V_base rows is read from memory once,
+// staged in LDS, and used by every wave: base bytes are paid once for all
+// agents, and only the agents' LR rows (a few per cent of the base bytes)
+// are read per request.  One barrier per step; within a step each wave runs
+// the per-request kernel's 16-token sub-block work four times.  The partials
+// go to the same workspace and the same merge.
+template <int D, int R>
+__global__ void __launch_bounds__(dec_waves(R) * 64, dec_waves(R) / 4)
+lrsa_decode_shared_kernel(const AttnArgs a) {
+  using C = Dec<D, R>;
+  constexpr int NW = C::NW, NT = C::NT;
+  constexpr int SB = 16;                    // tokens per sub-block
+  constexpr int NSS = 4;                    // sub-blocks per step
+  constexpr int STEP = SB * NSS;            // tokens per step (one barrier)
+  constexpr int K_ROW = D + 8;              // conflict-free 16-byte row reads
+  constexpr int EPS = SB * C::HALF / NT;    // RoPE table entries per thread per sub-block
+  constexpr int CPR = D / 8;                // 16-byte chunks per base row
+  constexpr int NBC = 2 * STEP * CPR;       // base chunks (K rows, then V rows) per step
+  constexpr int NCK = (NBC + NT - 1) / NT;  // base chunks per thread per step
+  static_assert(EPS >= 1 && SB * C::HALF % NT == 0 && NSS * C::HALF <= NT, "step sizes");
+  __shared__ float2 cs_lds[2][NSS][SB * C::CS_ROW];
+  __shared__ float2 base_lds[2][NSS][C::HALF];
+  __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][STEP * K_ROW];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][STEP * C::V_ROW];
+  __shared__ __attribute__((aligned(16))) uint16_t lv_lds[NW][16 * C::LV_ROW];
+
+  const int tid = threadIdx.x, lane = tid & 63, w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int split = blockIdx.x, g = blockIdx.y;
+  const int b = blockIdx.z * NW + w;
+  const bool active = b < a.batch;
+  const int G = a.group;
+  const int q = lane >> 4, c16 = lane & 15;
+  const bool has_lk = a.Lk != nullptr, has_lv = a.Lv != nullptr;
+  const int64_t t_begin = (int64_t)split * a.split_tiles * TK;
+  const int64_t t_cap = t_begin + (int64_t)a.split_tiles * TK;
+
+  // Keys request r may see: t < min(kv_len, position + 1), within the split.
+  auto req_end = [&](int r) -> int64_t {
+    int64_t kvl = a.kv_len[r];
+    kvl = kvl < 0 ? 0 : (kvl > a.s_cap ? a.s_cap : kvl);
+    const int64_t pos = a.positions[(int64_t)r * a.n_tok];
+    int64_t vis = pos + 1 < kvl ? pos + 1 : kvl;
+    if (vis < t_begin) vis = t_begin;
+    return vis < t_cap ? vis : t_cap;
+  };
+  const int64_t t_end = active ? req_end(b) : t_begin;
+  // The workgroup walks up to the furthest end among its requests.
+  int64_t t_end_wg = t_begin;
+  for (int r = blockIdx.z * NW; r < blockIdx.z * NW + NW && r < a.batch; ++r) {
+    const int64_t e = req_end(r);
+    t_end_wg = e > t_end_wg ? e : t_end_wg;
+  }
+  const int n_steps = __builtin_amdgcn_readfirstlane((int)((t_end_wg - t_begin + STEP - 1) / STEP));
+
+  // RoPE table entries of this thread within a sub-block (token, frequency j),
+  // and the sub-block base angle it computes (sub-block tid / HALF, j).
+  float cdl[EPS], sdl[EPS];
+  int ej[EPS], eidx[EPS];
+#pragma unroll
+  for (int k = 0; k < EPS; ++k) {
+    const int e = tid + NT * k, tok = e / C::HALF;
+    ej[k] = e - tok * C::HALF;
+    eidx[k] = tok * C::CS_ROW + ej[k];
+    cdl[k] = 1.f;
+    sdl[k] = 0.f;
+    if (has_lk) rope_cs(tok, a.w2pi[ej[k]], cdl[k], sdl[k]);
+  }
+  const int bsb = tid / C::HALF, bj = tid % C::HALF;  // base angle this thread computes
+  const bool base_thread = has_lk && tid < NSS * C::HALF;
+  const double w2pi_t = a.w2pi[bj];
+  auto base_angles = [&](int64_t t0s, int buf) {
+    if (base_thread) {
+      float c, s;
+      rope_cs((int)(t0s + bsb * SB), w2pi_t, c, s);
+      base_lds[buf][bsb][bj] = make_float2(c, s);
+    }
+  };
+  if (n_steps > 0) base_angles(t_begin, 0);
+  for (int i = lane; i < 16 * C::LV_ROW; i += 64) lv_lds[w][i] = 0;
+
+  const int64_t row = (int64_t)a.n_kv * D;
+  const uint16_t* Kb = a.Kb + (int64_t)g * D;
+  const uint16_t* Vb = a.Vb + (int64_t)g * D;
+  const uint16_t* Lk = has_lk && active ? a.Lk + (int64_t)b * a.l_stride : nullptr;
+  const uint16_t* Lv = has_lv && active ? a.Lv + (int64_t)b * a.l_stride : nullptr;
+
+  // Base chunks of a step: chunk c < STEP*CPR is K row c / CPR, else V.
+  int32_t boff[NCK];
+#pragma unroll
+  for (int k = 0; k < NCK; ++k) {
+    const int c = (tid + NT * k) % (STEP * CPR);
+    boff[k] = tid + NT * k < NBC ? (c / CPR) * (int32_t)(row * 2) + (c % CPR) * 16 : INT32_MIN;
+  }
+  auto base_load = [&](u32x4 (&r)[NCK], int64_t t0) {
+    const int64_t n = t_end_wg - t0 < 0 ? 0 : (t_end_wg - t0 < STEP ? t_end_wg - t0 : STEP);
+    const int32_t bytes = n > 0 ? (int32_t)((n - 1) * row * 2 + D * 2) : 0;
+    const auto rk = make_rsrc(Kb + t0 * row, bytes), rv = make_rsrc(Vb + t0 * row, bytes);
+#pragma unroll
+    for (int k = 0; k < NCK; ++k) {
+      const bool isk = (tid + NT * k) < STEP * CPR;
+      r[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(isk ? rk : rv, boff[k], 0, 0));
+    }
+  };
+  auto base_store = [&](const u32x4 (&r)[NCK], int buf) {
+#pragma unroll
+    for (int k = 0; k < NCK; ++k) {
+      const int c = tid + NT * k, cc = c % (STEP * CPR), tok = cc / CPR, col = (cc % CPR) * 8;
+      if (c < STEP * CPR)
+        *reinterpret_cast<u32x4*>(k_lds[buf] + tok * K_ROW + col) = r[k];
+      else if (c < NBC)
+        *reinterpret_cast<u32x4*>(v_lds[buf] + tok * C::V_ROW + col) = r[k];
+    }
+  };
+  // This wave's LR rows of a sub-block (rank chunks of token l%16), zero past
+  // its end.
+  struct LrStage {
+    u32x2 lk[C::RC], lv[C::RC];
+  };
+  int32_t lroff[C::RC];
+#pragma unroll
+  for (int rc = 0; rc < C::RC; ++rc) {
+    const int r0 = rc * 16 + q * 4;
+    lroff[rc] = r0 < R ? c16 * R * 2 + r0 * 2 : INT32_MIN;
+  }
+  auto lr_load = [&](LrStage& s, int64_t t0) {
+    const int64_t n = t_end - t0 < 0 ? 0 : (t_end - t0 < SB ? t_end - t0 : SB);
+    const auto rlk = make_rsrc(Lk != nullptr ? Lk + t0 * R : Kb, Lk != nullptr ? (int32_t)(n * R * 2) : 0);
+    const auto rlv = make_rsrc(Lv != nullptr ? Lv + t0 * R : Kb, Lv != nullptr ? (int32_t)(n * R * 2) : 0);
+#pragma unroll
+    for (int rc = 0; rc < C::RC; ++rc) {
+      s.lk[rc] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rlk, lroff[rc], 0, 0));
+      s.lv[rc] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rlv, lroff[rc], 0, 0));
+    }
+  };
+
+  bf16x8 qf[C::NCH];
+  {
+    const bool ok = active && c16 < G;
+    const uint16_t* qp = a.Q + ((int64_t)(active ? b : 0) * a.n_tok * a.n_q + (int64_t)g * G + c16) * D;
+#pragma unroll
+    for (int kk = 0; kk < C::NCH; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
+  }
+  i16x4 bkf[C::NBLK][C::RC];
+  load_bt_frags<D, R>(bkf, has_lk && active ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr,
+                      has_lk && active, lane);
+
+  float m_run = -INFINITY, l_part = 0.f;
+  f32x4 acc[C::NBLK];
+  f32x4 accl[C::RC];
+#pragma unroll
+  for (int blk = 0; blk < C::NBLK; ++blk) acc[blk] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int rc = 0; rc < C::RC; ++rc) accl[rc] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint16_t* lvl = lv_lds[w];
+  const int tr_row = 4 * q + (c16 >> 2), tr_col = 4 * (c16 & 3);
+
+  // The base rows of the next step are in flight during a step; the wave's
+  // LR rows run two sub-blocks ahead in a ring of NSS (static indices).
+  u32x4 breg[NCK];
+  LrStage lr[NSS];
+  base_load(breg, t_begin);
+  lr_load(lr[0], t_begin);
+  lr_load(lr[1], t_begin + SB);
+  __syncthreads();  // base angles of the first step, zeroed L_v tiles
+
+  for (int step = 0; step < n_steps; ++step) {
+    const int buf = step & 1;
+    const int64_t t0s = t_begin + (int64_t)step * STEP;
+    // ---- stage this step (tables, base rows) and start the next one -------
+    if (has_lk) {
+#pragma unroll
+      for (int sb = 0; sb < NSS; ++sb) {
+        const float2* base = base_lds[buf][sb];
+        float2* cs = cs_lds[buf][sb];
+#pragma unroll
+        for (int k = 0; k < EPS; ++k) {
+          const float2 bc = base[ej[k]];
+          cs[eidx[k]] = make_float2(bc.x * cdl[k] - bc.y * sdl[k], bc.y * cdl[k] + bc.x * sdl[k]);
+        }
+      }
+      if (step + 1 < n_steps) base_angles(t0s + STEP, buf ^ 1);
+    }
+    base_store(breg, buf);
+    base_load(breg, t0s + STEP);
+    __syncthreads();  // step's tables and base rows visible; double buffers
+                      // keep the previous step's intact for slower waves
+    const uint16_t* kt = k_lds[buf];
+    const uint16_t* vt = v_lds[buf];
+#pragma unroll
+    for (int sb = 0; sb < NSS; ++sb) {
+      const int64_t ts = t0s + sb * SB;
+      lr_load(lr[(sb + 2) % NSS], ts + 2 * SB);
+      if (!active || ts >= t_end) continue;
+      const LrStage& cur = lr[sb];
+        if (has_lv) {
+#pragma unroll
+          for (int rc = 0; rc < C::RC; ++rc)
+            if (rc * 16 + q * 4 < R) *reinterpret_cast<u32x2*>(lvl + c16 * C::LV_ROW + rc * 16 + q * 4) = cur.lv[rc];
+        }
+        // ---- scores S^T = K_base Q^T + bf16(RoPE(E)) Q^T --------------------
+        f32x4 sc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kk = 0; kk < C::NCH; ++kk)
+          sc = mfma16x16x32(as_bf16x8(*reinterpret_cast<const u32x4*>(kt + (sb * SB + c16) * K_ROW + chunk_dim<D>(kk, q))),
+                            qf[kk], sc);
+        if (has_lk) {
+          const float2* csr = cs_lds[buf][sb] + c16 * C::CS_ROW + q * C::QPG;
+          u32x4 ek[C::NCH];
+#pragma unroll
+          for (int blk = 0; blk < C::NB; ++blk) {
+            f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int rc = 0; rc < C::RC; ++rc) {
+              elo = mfma16x16x16(bkf[blk][rc], as_i16x4(cur.lk[rc]), elo);
+              ehi = mfma16x16x16(bkf[blk + C::NB][rc], as_i16x4(cur.lk[rc]), ehi);
+            }
+            float rlo[4], rhi[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const float2 r = csr[blk * 4 + i];
+              rlo[i] = elo[i] * r.x - ehi[i] * r.y;
+              rhi[i] = ehi[i] * r.x + elo[i] * r.y;
+            }
+            const int klo = blk >> 1, khi = (blk + C::NB) >> 1, w0 = (blk & 1) * 2;
+            ek[klo][w0] = pack_bf16(rlo[0], rlo[1]);
+            ek[klo][w0 + 1] = pack_bf16(rlo[2], rlo[3]);
+            ek[khi][w0] = pack_bf16(rhi[0], rhi[1]);
+            ek[khi][w0 + 1] = pack_bf16(rhi[2], rhi[3]);
+          }
+#pragma unroll
+          for (int kk = 0; kk < C::NCH; ++kk) sc = mfma16x16x32(as_bf16x8(ek[kk]), qf[kk], sc);
+        }
+        // ---- online softmax: lane l%16 is a head, 4 tokens per lane ---------
+        float s2[4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          s2[i] = (ts + q * 4 + i < t_end) ? sc[i] * a.scale_log2 : -INFINITY;
+          mx = fmaxf(mx, s2[i]);
+        }
+        mx = fmaxf(mx, shfl_xor(mx, 16));
+        mx = fmaxf(mx, shfl_xor(mx, 32));
+        const float mn = fmaxf(m_run, mx);
+        const float ms = (mn == -INFINITY) ? 0.f : mn;
+        const float alpha = fast_exp2(m_run - ms);
+        m_run = mn;
+        float p[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[i] = fast_exp2(s2[i] - ms);
+        l_part = l_part * alpha + (p[0] + p[1]) + (p[2] + p[3]);
+        u32x2 pw;
+        pw[0] = pack_bf16(p[0], p[1]);
+        pw[1] = pack_bf16(p[2], p[3]);
+        const i16x4 pb = as_i16x4(pw);
+        if (__ballot(alpha != 1.f)) {
+#pragma unroll
+          for (int blk = 0; blk < C::NBLK; ++blk) acc[blk] *= alpha;
+#pragma unroll
+          for (int rc = 0; rc < C::RC; ++rc) accl[rc] *= alpha;
+        }
+        __builtin_amdgcn_wave_barrier();
+        // ---- O^T += V^T P^T, (P L_v)^T += L_v^T P^T -----------------------
+#pragma unroll
+        for (int blk = 0; blk < C::NBLK; ++blk)
+          acc[blk] = mfma16x16x16(lds_read_tr(vt + (sb * SB + tr_row) * C::V_ROW + blk * 16 + tr_col), pb, acc[blk]);
+        if (has_lv) {
+#pragma unroll
+          for (int rc = 0; rc < C::RC; ++rc)
+            accl[rc] = mfma16x16x16(lds_read_tr(lvl + tr_row * C::LV_ROW + rc * 16 + tr_col), pb, accl[rc]);
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+  }
+
+  if (!active) return;
+  l_part += shfl_xor(l_part, 16);
+  l_part += shfl_xor(l_part, 32);
+  if (c16 >= G) return;
+  const int64_t hstride = (int64_t)a.n_splits * C::PS;
+  float* wsb = a.ws + ((int64_t)b * a.n_q + (int64_t)g * G + c16) * hstride + (int64_t)split * C::PS;
+  if (q == 0) {
+    wsb[0] = m_run;
+    wsb[1] = l_part;
+  }
+#pragma unroll
+  for (int blk = 0; blk < C::NBLK; ++blk)
+    *reinterpret_cast<f32x4*>(wsb + 4 + blk * 16 + q * 4) = acc[blk];
+  if (has_lv) {
+#pragma unroll
+    for (int rc = 0; rc < C::RC; ++rc)
+      if (rc * 16 + q * 4 < R) *reinterpret_cast<f32x4*>(wsb + 4 + D + rc * 16 + q * 4) = accl[rc];
+  }
+}
+
 template <int D, int R>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   using C = Dec<D, R>;
@@ -479,13 +778,24 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int D, int R>
+hipError_t launch_shared_t(const AttnArgs& a, hipStream_t st) {
+  using C = Dec<D, R>;
+  const int rg = (a.batch + C::NW - 1) / C::NW;
+  hipLaunchKernelGGL((lrsa_decode_shared_kernel<D, R>), dim3(a.n_splits, a.n_kv, rg), dim3(C::NT), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch), dim3(64 * MW), 0, st, a);
+  return hipGetLastError();
+}
+
 template <int D>
-hipError_t launch_r(const AttnArgs& a, hipStream_t st) {
+hipError_t launch_r(const AttnArgs& a, hipStream_t st, bool shared) {
   switch (a.rank) {
-    case 8: return launch_t<D, 8>(a, st);
-    case 16: return launch_t<D, 16>(a, st);
-    case 32: return launch_t<D, 32>(a, st);
-    case 64: return launch_t<D, 64>(a, st);
+    case 8: return shared ? launch_shared_t<D, 8>(a, st) : launch_t<D, 8>(a, st);
+    case 16: return shared ? launch_shared_t<D, 16>(a, st) : launch_t<D, 16>(a, st);
+    case 32: return shared ? launch_shared_t<D, 32>(a, st) : launch_t<D, 32>(a, st);
+    case 64: return shared ? launch_shared_t<D, 64>(a, st) : launch_t<D, 64>(a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -494,11 +804,16 @@ hipError_t launch_r(const AttnArgs& a, hipStream_t st) {
 
 int decode_tile_tokens() { return TK; }
 
-void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, int* n_splits, int* split_tiles) {
+bool decode_shares_base(int batch, int64_t kv_req_stride) { return batch > 1 && kv_req_stride == 0; }
+
+void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base, int* n_splits,
+                 int* split_tiles) {
   const int64_t tiles = (s_cap + TK - 1) / TK;
   const int nw = dec_waves(rank);
-  const int64_t hg = (n_kv + nw - 1) / nw;
-  const int64_t groups = (int64_t)(batch > 0 ? batch : 1) * hg;
+  const int64_t nb = batch > 0 ? batch : 1;
+  // Workgroups per split: (request, group of nw KV heads) for the per-request
+  // kernel, (KV head, group of nw requests) when the base cache is shared.
+  const int64_t groups = shared_base ? (int64_t)n_kv * ((nb + nw - 1) / nw) : nb * ((n_kv + nw - 1) / nw);
   // About two rounds of one workgroup per CU (measured best), in waves.
   const int64_t target_wgs = 512 * 8 / nw;
   int64_t ns = (target_wgs + groups - 1) / groups;
@@ -517,8 +832,9 @@ size_t decode_workspace_bytes(int batch, int n_q, int n_splits, int head_dim, in
 }
 
 hipError_t launch_decode(const AttnArgs& a, hipStream_t st) {
-  if (a.head_dim == 64) return launch_r<64>(a, st);
-  if (a.head_dim == 128) return launch_r<128>(a, st);
+  const bool shared = decode_shares_base(a.batch, a.kv_stride);
+  if (a.head_dim == 64) return launch_r<64>(a, st, shared);
+  if (a.head_dim == 128) return launch_r<128>(a, st, shared);
   return hipErrorInvalidValue;
 }
 

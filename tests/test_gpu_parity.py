@@ -204,6 +204,48 @@ def test_shared_buffers_across_requests():
         assert mx <= ATOL_MAX and mean <= ATOL_MEAN
 
 
+# Several agents decoding over one shared base cache (request stride 0), each
+# with its own LR plane, up-projections, query and position: the shared-base
+# decode kernel, which reads each base tile once for all of them.
+# id, d, r, n_q, n_kv, kv_lens, positions (None: kv_len - 1), s_cap, lr
+SHARED_BASE_CASES = [
+    ("sb_d128_r16_kv", 128, 16, 16, 4, [300, 299, 150, 1, 77, 300, 256, 33], None, 304, "kv"),
+    ("sb_d64_r8_kv_two_groups", 64, 8, 8, 4, [90, 13, 64, 65, 1, 200, 199, 31, 128, 100, 7], None, 200, "kv"),
+    ("sb_d128_r64_kv", 128, 64, 8, 2, [400, 390, 17, 256, 399], None, 400, "kv"),
+    ("sb_d128_r32_qv", 128, 32, 16, 2, [130, 64, 1, 129, 100, 33, 64, 65, 128], None, 136, "v"),
+    ("sb_plain", 128, 16, 8, 2, [222, 100, 222, 5], None, 224, "none"),
+    ("sb_mid_positions", 128, 16, 8, 2, [500, 500, 500], [[100], [499], [250]], 512, "kv"),
+    ("sb_long_splits", 128, 16, 8, 2, [5000, 4001, 4999], None, 5008, "kv"),
+]
+
+
+@pytest.mark.parametrize("case", SHARED_BASE_CASES, ids=[c[0] for c in SHARED_BASE_CASES])
+def test_shared_base_decode(case):
+    cid, d, r, n_q, n_kv, kv_lens, pos, s_cap, lr = case
+    print(f"shared-base decode {cid}", flush=True)
+    B = len(kv_lens)
+    pos = [[k - 1] for k in kv_lens] if pos is None else pos
+    cfg = mk_cfg(60 + len(cid), n_q, n_kv, d, r)
+    c = attention_case(cfg, batch=B, n_tok=1, kv_len=kv_lens, positions=pos, s_cap=s_cap, seed_base=7 * len(cid),
+                       lr_k=lr in ("kv", "k"), lr_v=lr in ("kv", "v"), poison_tail=False)
+    # One base cache for every request, valid up to the longest request; each
+    # request's own LR rows past its length are poisoned.
+    top = max(kv_lens)
+    for name in ("K_base", "V_base"):
+        c[name] = c[name][:1].clone()
+        c[name][0, top:] = float("nan")
+    for name in ("L_k", "L_v"):
+        if c[name] is not None:
+            for b in range(B):
+                c[name][b, kv_lens[b]:] = float("nan")
+    g = to_dev(c)
+    O, lse = gpu_attention(g, cfg.theta)
+    Oref, lref = oracle_attention(c, cfg.theta)
+    mx, mean = attn_errors(O, Oref)
+    assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (mx, mean)
+    assert lse_error(lse, lref) <= LSE_ATOL
+
+
 def test_custom_softmax_scale():
     cfg, c = _case("plain_prefill", 128, 16, 8, 2, 9, [100], 104, "kv", 1.0, "end")
     O, _ = gpu_attention(to_dev(c), cfg.theta, softmax_scale=0.05)
