@@ -28,23 +28,27 @@ namespace {
 
 constexpr int TC = 64;   // output columns per workgroup
 constexpr int TT = 64;   // tokens per workgroup
-constexpr int KST = 64;  // k per stage (128 bytes of a row)
-constexpr int NST = 4;   // stages in the LDS ring
+constexpr int KST = 128;        // k per stage (256 bytes of a row)
+constexpr int CPW = KST / 8;    // 16-byte chunks per row and stage
+constexpr int RPI = 64 / CPW;   // rows per load instruction (1 KB)
+constexpr int NI = 16 / RPI;    // load instructions per operand, wave and stage
+constexpr int NST = 4;          // stages in the LDS ring
+constexpr int AHEAD = NST - 2;  // stages in flight beyond the one awaited
 constexpr int NXCD = 8;  // XCDs of an MI355X
 
-// Physical 16-byte chunk of logical chunk c in row r of a stage tile.  Rows
-// r and r + 1 differ in bank half (64-dword rows hold two 128-byte rows); the
-// XOR with r / 2 makes the 16 rows read together by one fragment load hit
-// distinct banks.
-__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
+// Physical 16-byte chunk of logical chunk c in row r of a stage tile.  A row
+// of a stage spans all 64 banks (256 bytes); the XOR with r % 16 makes the 16
+// rows read together by one fragment load hit distinct banks.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ (r & 15); }
+static_assert(CPW == 16, "swizzle written for 256-byte stage rows");
 
-// s_waitcnt vmcnt(n) for a wave-uniform n in {0, 4, ..., 4 (NST - 2)}, other
+// s_waitcnt vmcnt(n) for a wave-uniform n in {0, 4, ..., 24}, other
 // counters not waited on.  gfx9 encoding: vmcnt bits [3:0] and [15:14],
 // expcnt [6:4] = 7, lgkmcnt [11:8] = 15.  The immediate must be a constant,
 // so the cases are spelled out.
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 __device__ __forceinline__ void wait_vmcnt_le(int n) {
-  static_assert(4 * (NST - 2) <= 24, "vmcnt cases");
+  static_assert(2 * NI * AHEAD <= 24 && (2 * NI) % 4 == 0, "vmcnt cases");
   switch (n) {
     case 24: __builtin_amdgcn_s_waitcnt(vmcnt_imm(24)); break;
     case 20: __builtin_amdgcn_s_waitcnt(vmcnt_imm(20)); break;
@@ -56,10 +60,14 @@ __device__ __forceinline__ void wait_vmcnt_le(int n) {
   }
 }
 
-__global__ void __launch_bounds__(256) precompute_kernel(const PrecomputeArgs a, int n_ct, int n_tt) {
+__global__ void __launch_bounds__(512) precompute_kernel(const PrecomputeArgs a, int n_ct, int n_tt) {
   // [stage][A tile, X tile][64 rows x 128 bytes]
   __shared__ __attribute__((aligned(1024))) uint16_t tiles[NST][2][64 * KST];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  // Waves 0-3 compute, waves 4-7 fill the LDS ring: issuing a stage's loads
+  // costs about as long as computing one, and the two now overlap.
+  const int tid = threadIdx.x, lane = tid & 63, wv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool producer = wv >= 4;
+  const int w = wv & 3;
   // XCD-aware tile order: workgroup L runs on XCD L % 8; consecutive slots of
   // one XCD walk the column tiles of one token tile.
   const int L = blockIdx.x, xcd = L % NXCD, slot = L / NXCD;
@@ -75,15 +83,15 @@ __global__ void __launch_bounds__(256) precompute_kernel(const PrecomputeArgs a,
   const i32x4 ra = buffer_rsrc(a.A + (int64_t)col0 * a.d_in, (int32_t)((cols - 1) * a.d_in * 2 + a.d_in * 2));
   const i32x4 rx = buffer_rsrc(a.X + tok0 * a.ld_x, (int32_t)((toks - 1) * a.ld_x * 2 + a.d_in * 2));
 
-  // Loader: each wave fills 16 of the 64 rows of both tiles per stage, two
-  // instructions per tile, each writing 1 KB (8 rows x 128 bytes) at
+  // Loader: each producer wave fills 16 of the 64 rows of both tiles per
+  // stage, NI instructions per tile, each writing 1 KB (RPI rows) at
   // consecutive lane positions.  Lane i of instruction j holds physical chunk
-  // i % 8 of row 16 w + 8 j + i / 8, i.e. logical chunk swz(row, i % 8).
-  int32_t offa[2], offx[2], kch[2];
+  // i % CPW of row 16 w + RPI j + i / CPW, i.e. logical chunk swz(row, i % CPW).
+  int32_t offa[NI], offx[NI], kch[NI];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int row = 16 * w + 8 * j + (lane >> 3);
-    const int c = swz(row, lane & 7);
+  for (int j = 0; j < NI; ++j) {
+    const int row = 16 * w + RPI * j + lane / CPW;
+    const int c = swz(row, lane % CPW);
     kch[j] = c * 8;  // first k of this lane's chunk within a stage
     offa[j] = row * (int32_t)(a.d_in * 2) + c * 16;
     offx[j] = row * (int32_t)(a.ld_x * 2) + c * 16;
@@ -100,12 +108,12 @@ __global__ void __launch_bounds__(256) precompute_kernel(const PrecomputeArgs a,
     const int ks = s + rot < nstage ? s + rot : s + rot - nstage;
     const int32_t k0 = ks * KST;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < NI; ++j) {
       // Chunks wholly past d_in (d_in is a multiple of 8) read as zeros.
       const bool kok = k0 + kch[j] < a.d_in;
       const int32_t oa = kok ? offa[j] : INT32_MIN, ox = kok ? offx[j] : INT32_MIN;
-      lds_dma16(ra, &tiles[sl][0][(16 * w + 8 * j) * KST], oa, k0 * 2);
-      lds_dma16(rx, &tiles[sl][1][(16 * w + 8 * j) * KST], ox, k0 * 2);
+      lds_dma16(ra, &tiles[sl][0][(16 * w + RPI * j) * KST], oa, k0 * 2);
+      lds_dma16(rx, &tiles[sl][1][(16 * w + RPI * j) * KST], ox, k0 * 2);
     }
   };
 
@@ -117,16 +125,25 @@ __global__ void __launch_bounds__(256) precompute_kernel(const PrecomputeArgs a,
 #pragma unroll
   for (int j = 0; j < 16; ++j) acc[j] = 0.f;
 
+  if (producer) {
+    // Stage s + AHEAD goes into the slot of stage s - 2, which the compute
+    // waves finished before the previous barrier, so it is issued before
+    // waiting for stage s: issuing overlaps the wait.
 #pragma unroll
-  for (int s = 0; s < NST - 1; ++s)
-    if (s < nstage) issue(s);
+    for (int s = 0; s < AHEAD; ++s)
+      if (s < nstage) issue(s);
+    for (int s = 0; s < nstage; ++s) {
+      if (s + AHEAD < nstage) issue(s + AHEAD);
+      // Stage s has landed once at most the loads of the stages after it (up
+      // to AHEAD of them, 2 NI instructions each) are still in flight.
+      const int ahead = nstage - 1 - s < AHEAD ? nstage - 1 - s : AHEAD;
+      wait_vmcnt_le(2 * NI * ahead);
+      __syncthreads();  // stage s visible to all waves
+    }
+    return;
+  }
   for (int s = 0; s < nstage; ++s) {
-    // Stage s has landed once at most the loads of the stages after it (up to
-    // NST - 2 of them, 4 instructions each) are still in flight.
-    const int ahead = nstage - 1 - s < NST - 2 ? nstage - 1 - s : NST - 2;
-    wait_vmcnt_le(4 * ahead);
     __syncthreads();  // stage s visible to all waves; stage s - 1 consumed by all
-    if (s + NST - 1 < nstage) issue(s + NST - 1);
     const uint16_t* ta = tiles[s % NST][0] + ra_row * KST;
     const uint16_t* tx = tiles[s % NST][1] + rx_row * KST;
 #pragma unroll
@@ -160,7 +177,7 @@ hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t st) {
   const int n_tt = (int)((a.T + TT - 1) / TT);
   const int groups = (n_tt + NXCD - 1) / NXCD;  // token tiles per XCD
   const int grid = groups * NXCD * n_ct;
-  hipLaunchKernelGGL(precompute_kernel, dim3(grid), dim3(256), 0, st, a, n_ct, n_tt);
+  hipLaunchKernelGGL(precompute_kernel, dim3(grid), dim3(512), 0, st, a, n_ct, n_tt);
   return hipGetLastError();
 }
 
