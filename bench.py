@@ -436,6 +436,61 @@ def shared_base_decode(prc, w, dev, steps, warmup):
         "max_abs_diff_vs_per_request": diff}), flush=True)
 
 
+def fused_projection(prc, w, dev, steps, warmup):
+    """The base projection of a 4096-token segment (K_base with RoPE, V_base)
+    and every agent's LR rows in one GEMM over X, against the base projection
+    and the LR precompute as two calls.  One JSON line."""
+    import torch
+    g = torch.Generator(device=dev).manual_seed(6000)
+
+    def nrm(shape, std=1.0):
+        x = torch.randn(*shape, generator=g, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            x.mul_(std)
+        return x.to(torch.bfloat16)
+
+    S, T, hid, n_kv, d, r, N = w["S"], w["seg"], w["hidden"], w["n_kv"], w["d"], w["r"], w["N"]
+    s_cap = S + T
+    X = nrm((T, hid))
+    W_rows = nrm((2 * n_kv * d, hid), 1.0 / math.sqrt(hid))
+    A_rows = nrm((2 * N * r, hid), 1.0 / math.sqrt(hid))
+    K = torch.empty((s_cap, n_kv, d), dtype=torch.bfloat16, device=dev)
+    V = torch.empty_like(K)
+    L = torch.empty((2, N, s_cap, r), dtype=torch.bfloat16, device=dev)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    th = w["theta"]
+    t_fused = timed(lambda: prc.project_kv_and_lr_cache(X, W_rows, A_rows, n_kv, d, 2, N, r, K, V, L,
+                                                        rope_theta=th, tok_offset=S))
+    t_base = timed(lambda: prc.project_kv_and_lr_cache(X, W_rows, None, n_kv, d, 2, 0, r, K, V, None,
+                                                       rope_theta=th, tok_offset=S))
+    t_pre = timed(lambda: prc.precompute_lr_cache(X, A_rows, 2, N, r, L, tok_offset=S))
+    cols = 2 * n_kv * d + 2 * N * r
+    flops = 2 * T * hid * cols
+    byts = (T * hid + cols * hid + T * cols) * 2
+    tf = flops / (t_fused * 1e-3) / 1e12
+    print(json.dumps({
+        "bench": "fused_projection",
+        "workload": (f"{T}-token segment, hidden {hid}: K_base (RoPE) and V_base for {n_kv} KV heads x {d} plus "
+                     f"rank-{r} k and v LR rows of {N} agents, one GEMM of {cols} columns"),
+        "ms": round(t_fused, 4), "tflops": round(tf, 1), "mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+        "algorithmic_flops": flops, "algorithmic_bytes": byts,
+        "base_projection_alone_ms": round(t_base, 4), "precompute_alone_ms": round(t_pre, 4),
+        "separate_ms": round(t_base + t_pre, 4),
+        "lr_cost_in_fused_ms": round(t_fused - t_base, 4)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -453,6 +508,9 @@ def main():
     ap.add_argument("--shared-base", action="store_true",
                     help="instead of the step: decode of all agents over one shared base cache, against the "
                          "same agents decoded as independent requests over per-agent copies")
+    ap.add_argument("--fused-projection", action="store_true",
+                    help="instead of the step: the base K/V projection and the LR precompute of a segment as "
+                         "one GEMM, against the two as separate calls")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -472,6 +530,9 @@ def main():
         return
     if args.shared_base:
         shared_base_decode(prc, w, dev, args.steps, args.warmup)
+        return
+    if args.fused_projection:
+        fused_projection(prc, w, dev, args.steps, args.warmup)
         return
     work = algorithmic_work(w)
     print(f"bench: generating inputs ({w['B']} x {w['S']}-token decode caches)", file=sys.stderr, flush=True)

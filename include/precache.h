@@ -90,6 +90,39 @@ prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64
                                int32_t rank, uint16_t* L_out, int64_t s_cap,
                                int64_t tok_offset, void* stream);
 
+/*
+ * project_kv_and_lr_cache -- the base projection of a newly processed segment
+ * joined with the LR-cache precompute (Sec. 2.2 base cache X W0 with RoPE on
+ * the key side; Sec. 3.1 LR precompute X A_k for every agent), as one GEMM
+ * over the segment's hidden states, so X is read once for all of it:
+ *     K_base[tok_offset + t][h][:] = RoPE(X[t] . W_k[:, h*d:(h+1)*d], tok_offset + t)
+ *     V_base[tok_offset + t][h][:] = X[t] . W_v[:, h*d:(h+1)*d]
+ *     L[p][a][tok_offset + t][j]  = X[t] . A_rows[(p*N + a)*r + j]
+ * RoPE is the rotate-half form with omega_j = rope_theta^(-2j/d), each token
+ * at its absolute position tok_offset + t (KV token t sits at position t).
+ *
+ *   X        [T, d_in] bf16, row stride ld_x, as for precompute_lr_cache.
+ *   W_rows   [2*n_kv*d, d_in] bf16, contiguous: row h*d + j is column h*d + j
+ *            of W_k (key projection), row n_kv*d + h*d + j that of W_v.
+ *   A_rows   as for precompute_lr_cache.
+ *   K_base, V_base  [s_cap, n_kv, d] bf16, contiguous (one request's base
+ *            cache); rows [tok_offset, tok_offset + T) are overwritten.
+ *   L_out    [n_proj, N, s_cap, r] bf16, contiguous; the same rows of every
+ *            plane are overwritten.  Nothing else is touched.
+ *   n_proj * n_agents == 0 computes the base cache alone; A_rows and L_out
+ *            may then be NULL and rank is ignored.
+ * Arithmetic: bf16 inputs, fp32 accumulation, RoPE in fp32 with angles
+ * reduced in fp64, round-to-nearest-even to bf16.  Requires d in {64, 128},
+ * the precompute_lr_cache limits, 2*n_kv*d*d_in < 2^29 and s_cap < 2^31
+ * (PRC_EUNSUPPORTED / PRC_EINVAL otherwise).  T == 0 is a no-op.
+ */
+prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
+                                   const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
+                                   const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                   int32_t rank, double rope_theta, uint16_t* K_base,
+                                   uint16_t* V_base, uint16_t* L_out, int64_t s_cap,
+                                   int64_t tok_offset, void* stream);
+
 /* Dimensions of one LR-shared attention call (a batch of B requests). */
 typedef struct lrsa_dims {
   int32_t batch;        /* B >= 0 requests                                     */

@@ -9,6 +9,7 @@ from .precache_oracle import (  # noqa: F401
     rope_frequencies,
     rope,
     precompute_lr_cache,
+    project_kv_and_lr,
     rebuild_kv,
     attention_scores,
     attention_probs,

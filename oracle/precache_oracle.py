@@ -102,6 +102,29 @@ def precompute_lr_cache(X, A_stack, n_proj: int, n_agents: int, rank: int) -> np
     return L
 
 
+def project_kv_and_lr(X, W_k, W_v, A_stack, n_kv: int, n_proj: int, n_agents: int, rank: int,
+                      positions, theta: float):
+    """Base cache and every agent's LR cache of one segment of hidden states.
+
+    ``X [T, d_in]``; ``W_k, W_v [d_in, n_kv*d]`` (the base key and value
+    projections, paper orientation); ``A_stack`` as in ``precompute_lr_cache``;
+    ``positions [T]`` the tokens' absolute positions.  Returns
+    ``K_base [T, n_kv, d] = RoPE(X W_k)`` (Sec. 2.2 base cache ``X W0`` on the
+    key side, rotated at each token's position as the keys of a RoPE model
+    are), ``V_base [T, n_kv, d] = X W_v`` and the LR planes of
+    ``precompute_lr_cache`` (Sec. 3.1).
+    """
+    X, W_k, W_v = _f64(X), _f64(W_k), _f64(W_v)
+    T = X.shape[0]
+    if W_k.shape != W_v.shape or W_k.shape[0] != X.shape[1] or W_k.shape[1] % n_kv:
+        raise ValueError(f"W_k {W_k.shape} / W_v {W_v.shape} do not fit X {X.shape} and n_kv={n_kv}")
+    d = W_k.shape[1] // n_kv
+    K = (X @ W_k).reshape(T, n_kv, d)
+    K = rope(K, np.asarray(positions, dtype=np.float64)[:, None], theta)
+    V = (X @ W_v).reshape(T, n_kv, d)
+    return K, V, precompute_lr_cache(X, A_stack, n_proj, n_agents, rank)
+
+
 # ----------------------------------------------------------------------------
 # Per-agent K/V as the method defines them (Eq. 1 + Sec. 2.2 + App. D.2)
 # ----------------------------------------------------------------------------

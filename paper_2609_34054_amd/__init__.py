@@ -13,6 +13,7 @@ from .binding import (  # noqa: F401
     make_dims,
     materialize_agent_kv,
     precompute_lr_cache,
+    project_kv_and_lr_cache,
     workspace_size,
 )
 

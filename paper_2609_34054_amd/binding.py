@@ -20,8 +20,9 @@ _LIB = None
 STATUS_NAMES = {0: "PRC_OK", 1: "PRC_EINVAL", 2: "PRC_ESHAPE", 3: "PRC_EALIGN",
                 4: "PRC_EUNSUPPORTED", 5: "PRC_EWORKSPACE", 6: "PRC_ELAUNCH", 7: "PRC_EDEVICE"}
 
-EXPORTS = ("precompute_lr_cache", "lr_shared_attention", "lr_shared_attention_workspace_size",
-           "materialize_agent_kv", "prc_last_error", "prc_status_string", "prc_version")
+EXPORTS = ("precompute_lr_cache", "project_kv_and_lr_cache", "lr_shared_attention",
+           "lr_shared_attention_workspace_size", "materialize_agent_kv", "prc_last_error", "prc_status_string",
+           "prc_version")
 
 
 class PrecacheError(RuntimeError):
@@ -60,6 +61,9 @@ def lib() -> ctypes.CDLL:
         vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
         L.precompute_lr_cache.argtypes = [vp, i64, i64, i64, vp, i32, i32, i32, vp, i64, i64, vp]
         L.precompute_lr_cache.restype = ctypes.c_int
+        L.project_kv_and_lr_cache.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, i32, i32, i32, ctypes.c_double,
+                                              vp, vp, vp, i64, i64, vp]
+        L.project_kv_and_lr_cache.restype = ctypes.c_int
         L.lr_shared_attention.argtypes = [ctypes.POINTER(LrsaDims), vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                           vp, vp, vp, ctypes.c_size_t, vp]
         L.lr_shared_attention.restype = ctypes.c_int
@@ -129,6 +133,40 @@ def precompute_lr_cache(X, A_rows, n_proj: int, n_agents: int, rank: int, L_out,
                                    _ptr(L_out), L_out.shape[2], tok_offset, _stream(stream))
     _check("precompute_lr_cache", st)
     return L_out
+
+
+def project_kv_and_lr_cache(X, W_rows, A_rows, n_kv_heads: int, head_dim: int, n_proj: int, n_agents: int,
+                            rank: int, K_base, V_base, L_out, *, rope_theta: float, tok_offset: int = 0,
+                            stream=None):
+    """Base K/V (RoPE on keys) and every agent's LR rows of one segment in one GEMM
+    over ``X`` (Sec. 2.2 base cache, Sec. 3.1 precompute).
+
+    ``X [T, d_in]`` bf16; ``W_rows [2*n_kv*d, d_in]`` (W_k^T rows, then W_v^T);
+    ``A_rows [n_proj*N*r, d_in]``; ``K_base, V_base [s_cap, n_kv, d]`` and
+    ``L_out [n_proj, N, s_cap, r]`` bf16 contiguous, rows ``tok_offset ..`` written.
+    """
+    _bf16("X", X, 2)
+    _bf16("W_rows", W_rows, 2)
+    _bf16("A_rows", A_rows, 2)
+    _bf16("K_base", K_base, 3)
+    _bf16("V_base", V_base, 3)
+    _bf16("L_out", L_out, 4)
+    for name, t in (("W_rows", W_rows), ("A_rows", A_rows), ("K_base", K_base), ("V_base", V_base),
+                    ("L_out", L_out)):
+        if t is not None and not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    s_cap = K_base.shape[0]
+    if tuple(K_base.shape) != (s_cap, n_kv_heads, head_dim) or K_base.shape != V_base.shape:
+        raise ValueError(f"K_base/V_base shapes {tuple(K_base.shape)}, {tuple(V_base.shape)} are not "
+                         f"(s_cap, {n_kv_heads}, {head_dim})")
+    if n_proj * n_agents and tuple(L_out.shape) != (n_proj, n_agents, s_cap, rank):
+        raise ValueError(f"L_out shape {tuple(L_out.shape)} does not match ({n_proj}, {n_agents}, {s_cap}, {rank})")
+    T, d_in = X.shape
+    st = lib().project_kv_and_lr_cache(_ptr(X), T, d_in, X.stride(0), _ptr(W_rows), n_kv_heads, head_dim,
+                                       _ptr(A_rows), n_proj, n_agents, rank, float(rope_theta), _ptr(K_base),
+                                       _ptr(V_base), _ptr(L_out), s_cap, tok_offset, _stream(stream))
+    _check("project_kv_and_lr_cache", st)
+    return K_base, V_base, L_out
 
 
 def make_dims(Q, K_base, L_k, L_v, B_k, B_v, rope_theta: float, softmax_scale: float = 0.0,

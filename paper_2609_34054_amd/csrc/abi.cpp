@@ -191,6 +191,61 @@ PRC_API prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_i
   return launch_status(prc::launch_precompute(a, static_cast<hipStream_t>(stream)), "precompute_lr_cache");
 }
 
+PRC_API prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
+                                           const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
+                                           const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                           int32_t rank, double rope_theta, uint16_t* K_base, uint16_t* V_base,
+                                           uint16_t* L_out, int64_t s_cap, int64_t tok_offset, void* stream) {
+  if (T < 0) return fail(PRC_EINVAL, "T=%lld is negative", (long long)T);
+  if (d_in < 1 || d_in % 8) return fail(PRC_EUNSUPPORTED, "d_in=%lld must be a positive multiple of 8", (long long)d_in);
+  if (ld_x < d_in) return fail(PRC_ESHAPE, "ld_x=%lld < d_in=%lld", (long long)ld_x, (long long)d_in);
+  if (ld_x % 8) return fail(PRC_EALIGN, "ld_x=%lld is not a multiple of 8 elements", (long long)ld_x);
+  if (ld_x >= (1LL << 24)) return fail(PRC_EUNSUPPORTED, "ld_x=%lld must be below 2^24", (long long)ld_x);
+  if (head_dim != 64 && head_dim != 128) return fail(PRC_EUNSUPPORTED, "head_dim=%d (built: 64, 128)", head_dim);
+  if (n_kv_heads < 1) return fail(PRC_EINVAL, "n_kv_heads=%d must be positive", n_kv_heads);
+  const int64_t nkv = (int64_t)n_kv_heads * head_dim;
+  // Weight rows are addressed with 32-bit byte offsets.
+  if (2 * nkv * d_in * 2 >= (1LL << 31))
+    return fail(PRC_EUNSUPPORTED, "2*n_kv*head_dim*d_in=%lld weights are too many", (long long)(2 * nkv * d_in));
+  // n_proj * n_agents == 0: the base projection alone (no LR planes).
+  if (n_proj < 0 || n_agents < 0) return fail(PRC_EINVAL, "n_proj=%d, n_agents=%d must not be negative", n_proj, n_agents);
+  const bool with_lr = n_proj > 0 && n_agents > 0;
+  if (with_lr && !rank_ok(rank)) return fail(PRC_EUNSUPPORTED, "rank=%d (built: 8, 16, 32, 64)", rank);
+  const int64_t n_cols = with_lr ? (int64_t)n_proj * n_agents * rank : 0;
+  if (2 * nkv + n_cols > 65535LL * 64) return fail(PRC_EINVAL, "too many output columns");
+  if (!(rope_theta > 0.0)) return fail(PRC_EINVAL, "rope_theta must be positive");
+  if (s_cap < 1 || s_cap > INT32_MAX) return fail(PRC_EINVAL, "s_cap=%lld must be in [1, 2^31)", (long long)s_cap);
+  if (tok_offset < 0 || tok_offset + T > s_cap)
+    return fail(PRC_ESHAPE, "rows [%lld, %lld) fall outside s_cap=%lld", (long long)tok_offset,
+                (long long)(tok_offset + T), (long long)s_cap);
+  if (T == 0) return ok();
+  if (X == nullptr || W_rows == nullptr || K_base == nullptr || V_base == nullptr ||
+      (with_lr && (A_rows == nullptr || L_out == nullptr)))
+    return fail(PRC_EINVAL, "X/W_rows/A_rows/K_base/V_base/L_out is NULL");
+  if (!aligned(X, 16) || !aligned(W_rows, 16) || !aligned(K_base, 16) || !aligned(V_base, 16) ||
+      (with_lr && (!aligned(A_rows, 16) || !aligned(L_out, 16))))
+    return fail(PRC_EALIGN, "X/W_rows/A_rows/K_base/V_base/L_out must be 16-byte aligned");
+  prc::PrecomputeArgs a{};
+  a.X = X;
+  a.A = A_rows;
+  a.L = L_out;
+  a.W = W_rows;
+  a.Kout = K_base;
+  a.Vout = V_base;
+  a.T = T;
+  a.d_in = d_in;
+  a.ld_x = ld_x;
+  a.s_cap = s_cap;
+  a.tok_offset = tok_offset;
+  a.n_cols = (int32_t)n_cols;
+  a.rank = with_lr ? rank : 8;
+  a.nkv = (int32_t)nkv;
+  a.head_dim = head_dim;
+  for (int j = 0; j < head_dim / 2; ++j)
+    a.w2pi[j] = std::pow(rope_theta, -2.0 * j / (double)head_dim) / (2.0 * M_PI);
+  return launch_status(prc::launch_precompute(a, static_cast<hipStream_t>(stream)), "project_kv_and_lr_cache");
+}
+
 PRC_API size_t lr_shared_attention_workspace_size(const lrsa_dims* dims) {
   if (dims == nullptr || dims->n_tok != 1 || dims->batch < 1 || dims->n_kv_heads < 1 || dims->s_cap < 1)
     return 0;

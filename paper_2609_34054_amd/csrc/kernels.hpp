@@ -61,10 +61,17 @@ hipError_t launch_prefill(const AttnArgs& a, hipStream_t stream);
 hipError_t launch_materialize(const AttnArgs& a, hipStream_t stream);
 
 // LR-cache precompute GEMM.
+// One GEMM over a segment of hidden states X: output columns
+// [0, nkv) are keys (W rows, RoPE applied at position tok_offset + t),
+// [nkv, 2 nkv) values (W rows), then n_cols LR columns (A rows).  nkv = 0 is
+// the LR precompute alone.
 struct PrecomputeArgs {
   const uint16_t* X;
   const uint16_t* A;    // [n_cols, d_in]
   uint16_t* L;          // [n_cols / r][s_cap][r]
+  const uint16_t* W;    // [2 nkv, d_in]: W_k^T rows, then W_v^T rows (nkv > 0)
+  uint16_t* Kout;       // [s_cap, nkv] (tokens x (head, dim))
+  uint16_t* Vout;
   int64_t T;
   int64_t d_in;
   int64_t ld_x;
@@ -72,6 +79,9 @@ struct PrecomputeArgs {
   int64_t tok_offset;
   int32_t n_cols;
   int32_t rank;
+  int32_t nkv;          // n_kv * head_dim, a multiple of 64 (or 0)
+  int32_t head_dim;
+  double w2pi[kMaxHalfDim];  // RoPE omega_j / (2 pi), fp64
 };
 hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t stream);
 

@@ -285,6 +285,32 @@ def pin_precompute(orc, seed=9, T=7, d_in=5, n_proj=2, N=3, r=2):
                     assert abs(L[p, a, t, j] - ref) <= 1e-12, "precompute block mismatch"
 
 
+def pin_projection(orc, seed=10, T=5, d_in=6, n_kv=2, d=8, n_proj=2, N=2, r=2, theta=50.0, t0=3):
+    """Base K/V of a segment by per-element sums and explicit pair rotations;
+    the LR planes as in pin_precompute."""
+    g = _rng(seed)
+    X = g.standard_normal((T, d_in))
+    W_k = g.standard_normal((d_in, n_kv * d))
+    W_v = g.standard_normal((d_in, n_kv * d))
+    A_stack = g.standard_normal((d_in, n_proj * N * r))
+    pos = np.arange(t0, t0 + T)
+    K, V, L = orc.project_kv_and_lr(X, W_k, W_v, A_stack, n_kv, n_proj, N, r, pos, theta)
+    assert K.shape == (T, n_kv, d) and V.shape == (T, n_kv, d) and L.shape == (n_proj, N, T, r)
+    for t in range(T):
+        for h in range(n_kv):
+            xk = [sum(X[t, k] * W_k[k, h * d + j] for k in range(d_in)) for j in range(d)]
+            xv = [sum(X[t, k] * W_v[k, h * d + j] for k in range(d_in)) for j in range(d)]
+            assert np.allclose(K[t, h], loop_rope(xk, int(pos[t]), theta), atol=1e-12), "key projection"
+            assert np.allclose(V[t, h], xv, atol=1e-12), "value projection"
+    for p in range(n_proj):
+        for a in range(N):
+            col = (p * N + a) * r
+            for t in range(T):
+                for j in range(r):
+                    ref = sum(X[t, k] * A_stack[k, col + j] for k in range(d_in))
+                    assert abs(L[p, a, t, j] - ref) <= 1e-12, "projection LR block"
+
+
 def pin_golden(orc):
     """Hand-derived worked cases (tests/golden/worked_cases.json)."""
     import json
@@ -306,4 +332,4 @@ def pin_golden(orc):
 
 ALL_PINS = [pin_golden, pin_merged_weights, pin_plain_attention, pin_softmax_rows, pin_rope,
             pin_value_assoc, pin_closed_forms, pin_permutation, pin_split_merge,
-            pin_precompute]
+            pin_precompute, pin_projection]

@@ -76,6 +76,51 @@ def test_precompute_empty_segment_is_a_noop():
     assert _pc(T=0, X=None, A=None, L=None) == 0
 
 
+# -------------------------------------------------------- fused projection
+def _pj(X=A16, T=64, d_in=256, ld_x=256, W=A16, n_kv=2, d=128, A=A16, n_proj=2, N=3, r=8, theta=1e4,
+        K=A16, V=A16, L=A16, s_cap=128, off=0):
+    return prc.lib().project_kv_and_lr_cache(X, T, d_in, ld_x, W, n_kv, d, A, n_proj, N, r, theta, K, V, L,
+                                             s_cap, off, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(T=-1), EINVAL),
+    (dict(d_in=12, ld_x=16), EUNSUP),
+    (dict(ld_x=128), ESHAPE),
+    (dict(ld_x=260), EALIGN),
+    (dict(d=96), EUNSUP),
+    (dict(d=32), EUNSUP),
+    (dict(n_kv=0), EINVAL),
+    (dict(n_kv=4096, d_in=65536, ld_x=65536), EUNSUP),
+    (dict(N=-1), EINVAL),
+    (dict(r=12), EUNSUP),
+    (dict(theta=0.0), EINVAL),
+    (dict(theta=-1.0), EINVAL),
+    (dict(s_cap=0), EINVAL),
+    (dict(s_cap=1 << 31), EINVAL),
+    (dict(off=100), ESHAPE),
+    (dict(W=None), EINVAL),
+    (dict(K=None), EINVAL),
+    (dict(V=None), EINVAL),
+    (dict(L=None), EINVAL),
+    (dict(W=A16 + 8), EALIGN),
+    (dict(K=A16 + 2), EALIGN),
+])
+def test_projection_rejects(kw, code):
+    assert _pj(**kw) == code
+    assert prc.lib().prc_last_error().decode()
+
+
+def test_projection_empty_segment_is_a_noop():
+    assert _pj(T=0, X=None, W=None, A=None, K=None, V=None, L=None) == 0
+
+
+def test_projection_without_lr_planes_needs_no_lr_buffers():
+    # Rejected for a host-visible reason after the LR buffers were excused.
+    assert _pj(N=0, A=None, L=None, off=100) == ESHAPE
+    assert _pj(n_proj=0, A=None, L=None, r=12, K=None) == EINVAL
+
+
 # ------------------------------------------------------------------ attention
 def _dims(**kw):
     d = dict(batch=2, n_tok=4, n_q_heads=32, n_kv_heads=8, head_dim=128, rank=16, s_cap=1024,

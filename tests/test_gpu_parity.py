@@ -67,6 +67,73 @@ def test_precompute_strided_rows():
     assert np.linalg.norm(f64(L) - ref) / np.linalg.norm(ref) <= PRE_REL
 
 
+# ------------------------------------------------------- fused projection
+# id, T, d_in, n_kv, d, n_proj, N, r, tok_offset, s_cap, theta
+PROJ_CASES = [
+    ("d128_ragged", 100, 256, 2, 128, 2, 3, 8, 5, 128, 5e5),
+    ("d64_large_positions", 70, 264, 4, 64, 2, 2, 16, 10000, 10100, 1e4),
+    ("single_token_append", 1, 512, 2, 128, 2, 4, 16, 333, 400, 5e5),
+    ("r64_one_proj", 130, 320, 1, 128, 1, 3, 64, 0, 130, 5e5),
+    # Enough 128-wide tiles (16 x 17) for the wide-tile kernel; ragged tokens.
+    ("wide_tiles", 2000, 256, 8, 128, 2, 2, 16, 3, 2003, 5e5),
+]
+
+
+@pytest.mark.parametrize("case", PROJ_CASES, ids=[c[0] for c in PROJ_CASES])
+def test_project_kv_and_lr(case):
+    cid, T, d_in, n_kv, d, n_proj, N, r, off, s_cap, theta = case
+    print(f"projection {cid}", flush=True)
+    g = 900 + len(cid)
+    X = normal_bf16((T, d_in), 1.0, g + 1)
+    W_rows = normal_bf16((2 * n_kv * d, d_in), 1.0 / math.sqrt(d_in), g + 2)
+    A_rows = normal_bf16((n_proj * N * r, d_in), 1.0 / math.sqrt(d_in), g + 3)
+    sentinel = -7.0
+    K = torch.full((s_cap, n_kv, d), sentinel, dtype=torch.bfloat16, device="cuda")
+    V = torch.full_like(K, sentinel)
+    L = torch.full((n_proj, N, s_cap, r), sentinel, dtype=torch.bfloat16, device="cuda")
+    prc.project_kv_and_lr_cache(X.cuda(), W_rows.cuda(), A_rows.cuda(), n_kv, d, n_proj, N, r, K, V, L,
+                                rope_theta=theta, tok_offset=off)
+    torch.cuda.synchronize()
+    Wk, Wv = f64(W_rows[: n_kv * d]).T, f64(W_rows[n_kv * d:]).T
+    Kr, Vr, Lr = oracle.project_kv_and_lr(f64(X), Wk, Wv, f64(A_rows).T, n_kv, n_proj, N, r,
+                                          np.arange(off, off + T), theta)
+    for name, got, ref in (("K", f64(K)[off:off + T], Kr), ("V", f64(V)[off:off + T], Vr),
+                           ("L", f64(L)[:, :, off:off + T], Lr)):
+        rel = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+        assert rel <= PRE_REL, (name, rel)
+        # bf16 output rounding bounds each element by about 2^-8 of its size.
+        assert np.max(np.abs(got - ref) - 2 ** -7 * np.abs(ref)) <= 2e-2, name
+    # Rows outside the segment are untouched.
+    for t in (K, V):
+        out = torch.cat([t[:off], t[off + T:]]).float()
+        assert (out == sentinel).all()
+    out = torch.cat([L[:, :, :off], L[:, :, off + T:]], dim=2).float()
+    assert (out == sentinel).all()
+    # The LR part agrees with the precompute alone to the last bf16 place (the
+    # two may tile the GEMM differently, so the fp32 sums may differ in order).
+    L2 = torch.full_like(L, sentinel)
+    prc.precompute_lr_cache(X.cuda(), A_rows.cuda(), n_proj, N, r, L2, tok_offset=off)
+    torch.cuda.synchronize()
+    assert ((L.float() - L2.float()).abs() <= 2 ** -7 * L2.float().abs()).all()
+
+
+def test_project_base_only():
+    """n_agents = 0: the base projection alone (no LR buffers)."""
+    T, d_in, n_kv, d, off, s_cap, theta = 65, 128, 2, 64, 7, 80, 5e5
+    X = normal_bf16((T, d_in), 1.0, 951)
+    W_rows = normal_bf16((2 * n_kv * d, d_in), 1.0 / math.sqrt(d_in), 952)
+    K = torch.zeros((s_cap, n_kv, d), dtype=torch.bfloat16, device="cuda")
+    V = torch.zeros_like(K)
+    prc.project_kv_and_lr_cache(X.cuda(), W_rows.cuda(), None, n_kv, d, 2, 0, 16, K, V, None, rope_theta=theta,
+                                tok_offset=off)
+    torch.cuda.synchronize()
+    A0 = np.zeros((d_in, 0))
+    Kr, Vr, _ = oracle.project_kv_and_lr(f64(X), f64(W_rows[: n_kv * d]).T, f64(W_rows[n_kv * d:]).T, A0, n_kv,
+                                         2, 0, 16, np.arange(off, off + T), theta)
+    for got, ref in ((f64(K)[off:off + T], Kr), (f64(V)[off:off + T], Vr)):
+        assert np.linalg.norm(got - ref) / np.linalg.norm(ref) <= PRE_REL
+
+
 # ------------------------------------------------------------------ attention
 # id, d, r, n_q, n_kv, n_tok, kv_lens, s_cap, lr ("kv"|"v"|"k"|"none"), q_std, pos ("end"|"mid")
 ATTN_CASES = [

@@ -37,6 +37,10 @@ MUTATIONS = {
     "precompute_agent_major": ("col = (p * n_agents + a) * rank", "col = (a * n_proj + p) * rank"),
     "precompute_transposed_block": ("L[p, a] = X @ A_stack[:, col: col + rank]",
                                     "L[p, a] = X @ A_stack[:, col: col + rank][::-1]"),
+    "projection_value_uses_key_weights": ("V = (X @ W_v).reshape(T, n_kv, d)", "V = (X @ W_k).reshape(T, n_kv, d)"),
+    "projection_key_unrotated": ("K = rope(K, np.asarray(positions, dtype=np.float64)[:, None], theta)", "K = K"),
+    "projection_key_head_split_transposed": ("K = (X @ W_k).reshape(T, n_kv, d)",
+                                             "K = (X @ W_k).reshape(T, d, n_kv).transpose(0, 2, 1)"),
     "merge_unshifted_lse": ("return O, m + np.log(z)", "return O, np.log(z)"),
     "merge_unweighted": ("O = sum(w[i][..., None] * np.asarray(p[0], dtype=np.float64)",
                          "O = sum(np.asarray(p[0], dtype=np.float64)"),
