@@ -38,7 +38,8 @@ that the paper or the mathematics fix (Eq. 1 by brute force with merged
 weights, B = 0 against torch's scaled_dot_product_attention, RoPE closed forms
 and invariants, softmax normalisation, value associativity, closed-form
 attention cases, permutation and split invariance, the precompute against a
-naive triple loop).
+naive triple loop, the base projection against per-element sums and explicit
+pair rotations).
 """
 from __future__ import annotations
 
