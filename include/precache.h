@@ -123,6 +123,40 @@ prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, i
                                    uint16_t* V_base, uint16_t* L_out, int64_t s_cap,
                                    int64_t tok_offset, void* stream);
 
+/*
+ * project_kv_and_lr_cache_paged -- project_kv_and_lr_cache writing into paged
+ * caches (the block-table layout of the paged-KV serving setup, Sec. 4.1 and
+ * App. C.2), so that a trajectory's cache grows one segment (or prefill
+ * chunk) at a time without a contiguous reservation of s_cap tokens, and
+ * trajectories can share blocks.  The trajectory's tokens are cut
+ * into blocks of block_size tokens: token p (its absolute position) lives at
+ * row p % block_size of pool block block_table[p / block_size].  The values
+ * written are those of project_kv_and_lr_cache (RoPE still at position p).
+ *
+ *   block_table  [max_blocks] int32, DEVICE memory: the trajectory's blocks.
+ *                Entries are clamped into [0, n_blocks), so no write leaves
+ *                the pools; a wrong entry writes a wrong block of them.
+ *   K_pool, V_pool  [n_blocks, block_size, n_kv, d] bf16, contiguous.
+ *   L_pool   [n_proj, N, n_blocks, block_size, r] bf16, contiguous: each
+ *            agent's LR plane is a pool indexed by the same block ids as the
+ *            base pools.
+ *   n_kv_heads == 0 writes the LR planes alone (W_rows, K_pool, V_pool may be
+ *            NULL; head_dim and rope_theta are ignored); n_proj * n_agents == 0
+ *            the base pools alone.
+ * Requires block_size a positive multiple of 64, max_blocks and n_blocks >= 1,
+ * their products with block_size below 2^31, and tok_offset + T <=
+ * max_blocks * block_size; other limits as for project_kv_and_lr_cache.
+ * Rows of the pools not addressed by [tok_offset, tok_offset + T) are not
+ * touched.
+ */
+prc_status project_kv_and_lr_cache_paged(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
+                                         const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
+                                         const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                         int32_t rank, double rope_theta, uint16_t* K_pool,
+                                         uint16_t* V_pool, uint16_t* L_pool, const int32_t* block_table,
+                                         int32_t block_size, int32_t max_blocks, int32_t n_blocks,
+                                         int64_t tok_offset, void* stream);
+
 /* Dimensions of one LR-shared attention call (a batch of B requests). */
 typedef struct lrsa_dims {
   int32_t batch;        /* B >= 0 requests                                     */
@@ -187,6 +221,54 @@ prc_status lr_shared_attention(const lrsa_dims* dims, const uint16_t* Q,
 /* Workspace bytes lr_shared_attention needs for `dims` (0 when none, or when
  * dims is invalid; validation errors are reported by the call itself). */
 size_t lr_shared_attention_workspace_size(const lrsa_dims* dims);
+
+/* Block tables of a paged lr_shared_attention_paged call. */
+typedef struct lrsa_paging {
+  const int32_t* kv_block_table; /* [B, max_blocks] int32, DEVICE memory: row b
+                                    lists request b's blocks of the base pools */
+  const int32_t* lr_block_table; /* [B, max_blocks] int32, DEVICE memory, for the
+                                    LR pools; NULL: the same as kv_block_table */
+  int32_t block_size;  /* tokens per block, a positive multiple of 64          */
+  int32_t max_blocks;  /* entries per table row; s_cap = max_blocks*block_size */
+  int32_t n_kv_blocks; /* blocks in (each request's) base pools, >= 1          */
+  int32_t n_lr_blocks; /* blocks in each LR pool, >= 1 when an L is given      */
+} lrsa_paging;
+
+/*
+ * lr_shared_attention_paged -- lr_shared_attention over paged caches (the
+ * block-table layout of the paged-KV serving setup of Sec. 4.1 and App. C.2,
+ * with chunked prefill: the n_tok
+ * queries of a chunk attend over every earlier token plus the chunk itself,
+ * once the chunk has been written with project_kv_and_lr_cache_paged).
+ * Computes exactly what lr_shared_attention computes (bit for bit, given the
+ * same cache contents) with token t of request b read from row
+ * t % block_size of block kv_block_table[b][t / block_size] (base) and
+ * lr_block_table[b][t / block_size] (LR).
+ *
+ *   K_pool, V_pool  [n_kv_blocks, block_size, n_kv, d] bf16; request b's pool
+ *              starts kv_req_stride * b elements in (normally 0: one pool
+ *              shared by all requests, so agents of one trajectory list the
+ *              same blocks).
+ *   L_k, L_v   [n_lr_blocks, block_size, r] bf16 pools; request b's starts
+ *              l_req_stride * b elements in (e.g. its agent's plane of the
+ *              L_pool written by project_kv_and_lr_cache_paged).
+ *   dims.s_cap must equal max_blocks * block_size; strides, when non-zero,
+ *   must cover one request's pools.  Table entries are clamped into the
+ *   pools, so no read leaves them.  Other arguments, the output and the
+ *   arithmetic as for lr_shared_attention.  Decode (n_tok == 1) needs the
+ *   workspace given by lr_shared_attention_paged_workspace_size.
+ */
+prc_status lr_shared_attention_paged(const lrsa_dims* dims, const lrsa_paging* paging,
+                                     const uint16_t* Q, const uint16_t* K_pool,
+                                     const uint16_t* V_pool, const uint16_t* L_k,
+                                     const uint16_t* L_v, const uint16_t* B_k,
+                                     const uint16_t* B_v, const int32_t* positions,
+                                     const int32_t* kv_len, uint16_t* O, float* lse,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes lr_shared_attention_paged needs for `dims` (0 as for
+ * lr_shared_attention_workspace_size). */
+size_t lr_shared_attention_paged_workspace_size(const lrsa_dims* dims);
 
 /*
  * materialize_agent_kv -- the reference point: write out each request's full

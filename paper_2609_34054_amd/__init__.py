@@ -7,13 +7,16 @@ binding.  Torch provides device memory and streams only.
 from .binding import (  # noqa: F401
     EXPORTS,
     LrsaDims,
+    LrsaPaging,
     PrecacheError,
     lib,
     lr_shared_attention,
+    lr_shared_attention_paged,
     make_dims,
     materialize_agent_kv,
     precompute_lr_cache,
     project_kv_and_lr_cache,
+    project_kv_and_lr_cache_paged,
     workspace_size,
 )
 

@@ -20,9 +20,10 @@ _LIB = None
 STATUS_NAMES = {0: "PRC_OK", 1: "PRC_EINVAL", 2: "PRC_ESHAPE", 3: "PRC_EALIGN",
                 4: "PRC_EUNSUPPORTED", 5: "PRC_EWORKSPACE", 6: "PRC_ELAUNCH", 7: "PRC_EDEVICE"}
 
-EXPORTS = ("precompute_lr_cache", "project_kv_and_lr_cache", "lr_shared_attention",
-           "lr_shared_attention_workspace_size", "materialize_agent_kv", "prc_last_error", "prc_status_string",
-           "prc_version")
+EXPORTS = ("precompute_lr_cache", "project_kv_and_lr_cache", "project_kv_and_lr_cache_paged",
+           "lr_shared_attention", "lr_shared_attention_workspace_size", "lr_shared_attention_paged",
+           "lr_shared_attention_paged_workspace_size", "materialize_agent_kv", "prc_last_error",
+           "prc_status_string", "prc_version")
 
 
 class PrecacheError(RuntimeError):
@@ -50,6 +51,17 @@ class LrsaDims(ctypes.Structure):
     ]
 
 
+class LrsaPaging(ctypes.Structure):
+    _fields_ = [
+        ("kv_block_table", ctypes.c_void_p),
+        ("lr_block_table", ctypes.c_void_p),
+        ("block_size", ctypes.c_int32),
+        ("max_blocks", ctypes.c_int32),
+        ("n_kv_blocks", ctypes.c_int32),
+        ("n_lr_blocks", ctypes.c_int32),
+    ]
+
+
 def lib() -> ctypes.CDLL:
     """Load libprecache.so (built in-tree by ``build()``); raise if absent."""
     global _LIB
@@ -64,11 +76,19 @@ def lib() -> ctypes.CDLL:
         L.project_kv_and_lr_cache.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, i32, i32, i32, ctypes.c_double,
                                               vp, vp, vp, i64, i64, vp]
         L.project_kv_and_lr_cache.restype = ctypes.c_int
+        L.project_kv_and_lr_cache_paged.argtypes = [vp, i64, i64, i64, vp, i32, i32, vp, i32, i32, i32,
+                                                    ctypes.c_double, vp, vp, vp, vp, i32, i32, i32, i64, vp]
+        L.project_kv_and_lr_cache_paged.restype = ctypes.c_int
         L.lr_shared_attention.argtypes = [ctypes.POINTER(LrsaDims), vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                           vp, vp, vp, ctypes.c_size_t, vp]
         L.lr_shared_attention.restype = ctypes.c_int
         L.lr_shared_attention_workspace_size.argtypes = [ctypes.POINTER(LrsaDims)]
         L.lr_shared_attention_workspace_size.restype = ctypes.c_size_t
+        L.lr_shared_attention_paged.argtypes = [ctypes.POINTER(LrsaDims), ctypes.POINTER(LrsaPaging), vp, vp, vp,
+                                                vp, vp, vp, vp, vp, vp, vp, vp, vp, ctypes.c_size_t, vp]
+        L.lr_shared_attention_paged.restype = ctypes.c_int
+        L.lr_shared_attention_paged_workspace_size.argtypes = [ctypes.POINTER(LrsaDims)]
+        L.lr_shared_attention_paged_workspace_size.restype = ctypes.c_size_t
         L.materialize_agent_kv.argtypes = [ctypes.POINTER(LrsaDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.materialize_agent_kv.restype = ctypes.c_int
         L.prc_last_error.restype = ctypes.c_char_p
@@ -169,6 +189,45 @@ def project_kv_and_lr_cache(X, W_rows, A_rows, n_kv_heads: int, head_dim: int, n
     return K_base, V_base, L_out
 
 
+def project_kv_and_lr_cache_paged(X, W_rows, A_rows, n_kv_heads: int, head_dim: int, n_proj: int,
+                                  n_agents: int, rank: int, K_pool, V_pool, L_pool, block_table, *,
+                                  rope_theta: float, tok_offset: int = 0, stream=None):
+    """:func:`project_kv_and_lr_cache` writing into paged pools: token ``p`` goes to
+    row ``p % blk`` of block ``block_table[p // blk]``.
+
+    ``K_pool, V_pool [n_blocks, blk, n_kv, d]`` (None with ``n_kv_heads == 0``);
+    ``L_pool [n_proj, N, n_blocks, blk, r]`` (None without LR planes);
+    ``block_table [max_blocks]`` int32, contiguous.
+    """
+    _bf16("X", X, 2)
+    _bf16("W_rows", W_rows, 2)
+    _bf16("A_rows", A_rows, 2)
+    _bf16("K_pool", K_pool, 4)
+    _bf16("V_pool", V_pool, 4)
+    _bf16("L_pool", L_pool, 5)
+    for name, t in (("W_rows", W_rows), ("A_rows", A_rows), ("K_pool", K_pool), ("V_pool", V_pool),
+                    ("L_pool", L_pool), ("block_table", block_table)):
+        if t is not None and not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+    if block_table.dtype != torch.int32 or block_table.dim() != 1:
+        raise TypeError("block_table must be a 1-D int32 tensor")
+    pool = K_pool if n_kv_heads else L_pool[0, 0]
+    n_blocks, blk = pool.shape[0], pool.shape[1]
+    if n_kv_heads and (tuple(K_pool.shape) != (n_blocks, blk, n_kv_heads, head_dim) or K_pool.shape != V_pool.shape):
+        raise ValueError(f"K_pool/V_pool shapes {tuple(K_pool.shape)}, {tuple(V_pool.shape)} are not "
+                         f"(n_blocks, blk, {n_kv_heads}, {head_dim})")
+    if n_proj * n_agents and tuple(L_pool.shape) != (n_proj, n_agents, n_blocks, blk, rank):
+        raise ValueError(f"L_pool shape {tuple(L_pool.shape)} does not match "
+                         f"({n_proj}, {n_agents}, {n_blocks}, {blk}, {rank})")
+    T, d_in = X.shape
+    st = lib().project_kv_and_lr_cache_paged(_ptr(X), T, d_in, X.stride(0), _ptr(W_rows), n_kv_heads, head_dim,
+                                             _ptr(A_rows), n_proj, n_agents, rank, float(rope_theta),
+                                             _ptr(K_pool), _ptr(V_pool), _ptr(L_pool), _ptr(block_table), blk,
+                                             block_table.shape[0], n_blocks, tok_offset, _stream(stream))
+    _check("project_kv_and_lr_cache_paged", st)
+    return K_pool, V_pool, L_pool
+
+
 def make_dims(Q, K_base, L_k, L_v, B_k, B_v, rope_theta: float, softmax_scale: float = 0.0,
               batch=None, n_q=None):
     """The lrsa_dims of a call, from tensor shapes (Q may be None for materialise)."""
@@ -260,3 +319,87 @@ def materialize_agent_kv(K_base, V_base, L_k, L_v, B_k, B_v, kv_len, *, rope_the
                                     _stream(stream))
     _check("materialize_agent_kv", st)
     return K_full, V_full
+
+
+def _pool_stride(t, batch, ndim):
+    """Elements between requests' pools: 0 for one pool (``ndim`` dims) shared by all."""
+    if t is None or t.dim() == ndim:
+        return 0
+    if t.dim() != ndim + 1 or t.shape[0] not in (1, batch):
+        raise ValueError(f"pool shape {tuple(t.shape)}: expected {ndim} dims, or {ndim + 1} with a leading 1 or {batch}")
+    return 0 if t.shape[0] == 1 else t.stride(0)
+
+
+def lr_shared_attention_paged(Q, K_pool, V_pool, L_k, L_v, B_k, B_v, positions, kv_len, kv_block_table, *,
+                              rope_theta: float, lr_block_table=None, softmax_scale: float = 0.0, O=None,
+                              lse=None, want_lse: bool = False, workspace=None, stream=None):
+    """:func:`lr_shared_attention` over paged caches (block tables), e.g. one chunk
+    of a chunked prefill over the tokens written so far.
+
+    ``K_pool, V_pool [n_kv_blocks, blk, n_kv, d]`` (one pool) or
+    ``[B, n_kv_blocks, blk, n_kv, d]`` (a pool per request); ``L_k, L_v
+    [n_lr_blocks, blk, r]`` or ``[B, n_lr_blocks, blk, r]`` or None;
+    ``B_k, B_v [B|1, n_kv*d, r]``; ``kv_block_table`` (and ``lr_block_table``,
+    default: the same) ``[B, max_blocks]`` int32.
+    """
+    for name, t in (("K_pool", K_pool), ("V_pool", V_pool), ("L_k", L_k), ("L_v", L_v)):
+        if t is not None:
+            _bf16(name, t, t.dim())
+            if not t.is_contiguous() and not t[0].is_contiguous():
+                raise ValueError(f"{name} must be contiguous within a request")
+    _bf16("Q", Q, 4)
+    _bf16("B_k", B_k, 3)
+    _bf16("B_v", B_v, 3)
+    batch, n_tok, n_q, d = Q.shape
+    if K_pool.shape != V_pool.shape or K_pool.stride() != V_pool.stride():
+        raise ValueError("K_pool and V_pool must share shape and strides")
+    if L_k is not None and L_v is not None and (L_k.shape != L_v.shape or L_k.stride() != L_v.stride()):
+        raise ValueError("L_k and L_v must share shape and strides")
+    if B_k is not None and B_v is not None and (B_k.shape != B_v.shape or B_k.stride() != B_v.stride()):
+        raise ValueError("B_k and B_v must share shape and strides")
+    n_kv_blocks, blk, n_kv, dk = K_pool.shape[-4:]
+    if dk != d:
+        raise ValueError("head dims of Q and K_pool differ")
+    lr = L_k if L_k is not None else L_v
+    bt = B_k if B_k is not None else B_v
+    rank = lr.shape[-1] if lr is not None else 0
+    n_lr_blocks = lr.shape[-3] if lr is not None else 0
+    if lr is not None and lr.shape[-2] != blk:
+        raise ValueError(f"LR pool blocks hold {lr.shape[-2]} tokens, base pool blocks {blk}")
+    if bt is not None and (bt.shape[-2] != n_kv * d or bt.shape[-1] != rank):
+        raise ValueError(f"up-projection shape {tuple(bt.shape)} is not (.., {n_kv * d}, {rank})")
+    for name, t in (("kv_block_table", kv_block_table), ("lr_block_table", lr_block_table)):
+        if t is None:
+            continue
+        if t.dtype != torch.int32 or t.dim() != 2 or t.shape[0] != batch or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous int32 [B, max_blocks] tensor")
+    max_blocks = kv_block_table.shape[1]
+    if lr_block_table is not None and lr_block_table.shape[1] != max_blocks:
+        raise ValueError("the two block tables must have the same width")
+    dims = LrsaDims(batch=batch, n_tok=n_tok, n_q_heads=n_q, n_kv_heads=n_kv, head_dim=d, rank=rank,
+                    s_cap=max_blocks * blk, kv_req_stride=_pool_stride(K_pool, batch, 4),
+                    l_req_stride=_pool_stride(lr, batch, 3), b_req_stride=_req_stride(bt, batch),
+                    softmax_scale=softmax_scale, reserved0=0.0, rope_theta=rope_theta)
+    paging = LrsaPaging(kv_block_table=kv_block_table.data_ptr(),
+                        lr_block_table=None if lr_block_table is None else lr_block_table.data_ptr(),
+                        block_size=blk, max_blocks=max_blocks, n_kv_blocks=n_kv_blocks, n_lr_blocks=n_lr_blocks)
+    if positions.dtype != torch.int32 or kv_len.dtype != torch.int32:
+        raise TypeError("positions and kv_len must be int32")
+    if tuple(positions.shape) != (batch, n_tok) or not positions.is_contiguous():
+        raise ValueError("positions must be a contiguous [B, n_tok] tensor")
+    if tuple(kv_len.shape) != (batch,):
+        raise ValueError("kv_len must be a [B] tensor")
+    if O is None:
+        O = torch.empty_like(Q)
+    if lse is None and want_lse:
+        lse = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device)
+    need = int(lib().lr_shared_attention_paged_workspace_size(ctypes.byref(dims)))
+    if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=Q.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = lib().lr_shared_attention_paged(ctypes.byref(dims), ctypes.byref(paging), _ptr(Q), _ptr(K_pool),
+                                         _ptr(V_pool), _ptr(L_k), _ptr(L_v), _ptr(B_k), _ptr(B_v),
+                                         _ptr(positions), _ptr(kv_len), _ptr(O), _ptr(lse), _ptr(workspace),
+                                         ws_bytes, _stream(stream))
+    _check("lr_shared_attention_paged", st)
+    return O, lse

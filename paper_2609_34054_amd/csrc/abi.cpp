@@ -52,7 +52,7 @@ struct Checked {
 prc_status check_attention(const lrsa_dims* dims, const uint16_t* Q, const uint16_t* K_base,
                            const uint16_t* V_base, const uint16_t* L_k, const uint16_t* L_v,
                            const uint16_t* B_k, const uint16_t* B_v, const int32_t* positions,
-                           const int32_t* kv_len, bool need_q, Checked* out) {
+                           const int32_t* kv_len, bool need_q, const lrsa_paging* pg, Checked* out) {
   if (dims == nullptr) return fail(PRC_EINVAL, "dims is NULL");
   const lrsa_dims& d = *dims;
   if (d.batch < 0 || d.batch > 65535) return fail(PRC_EINVAL, "batch=%d outside [0, 65535]", d.batch);
@@ -78,13 +78,29 @@ prc_status check_attention(const lrsa_dims* dims, const uint16_t* Q, const uint1
   const bool has_lr = L_k != nullptr || L_v != nullptr;
   if (has_lr && !rank_ok(d.rank)) return fail(PRC_EUNSUPPORTED, "rank=%d (built: 8, 16, 32, 64)", d.rank);
   const int64_t dd = d.head_dim, r = has_lr ? d.rank : 8;
-  const int64_t kv_need = d.s_cap * d.n_kv_heads * dd;
+  // Elements of one request's base and LR caches (paged: of its pools).
+  int64_t kv_need = d.s_cap * d.n_kv_heads * dd, l_need = d.s_cap * r;
+  if (pg != nullptr) {
+    const lrsa_paging& p = *pg;
+    if (p.block_size < 64 || p.block_size % 64)
+      return fail(PRC_EUNSUPPORTED, "block_size=%d must be a positive multiple of 64", p.block_size);
+    if (p.max_blocks < 1 || p.n_kv_blocks < 1 || (has_lr && p.n_lr_blocks < 1))
+      return fail(PRC_EINVAL, "max_blocks=%d, n_kv_blocks=%d, n_lr_blocks=%d must be positive", p.max_blocks,
+                  p.n_kv_blocks, p.n_lr_blocks);
+    if ((int64_t)p.max_blocks * p.block_size != d.s_cap)
+      return fail(PRC_ESHAPE, "s_cap=%lld must equal max_blocks*block_size=%lld", (long long)d.s_cap,
+                  (long long)p.max_blocks * p.block_size);
+    kv_need = (int64_t)p.n_kv_blocks * p.block_size * d.n_kv_heads * dd;
+    l_need = (int64_t)p.n_lr_blocks * p.block_size * r;
+  }
   if (d.kv_req_stride != 0 && d.kv_req_stride < kv_need && d.batch > 1)
-    return fail(PRC_ESHAPE, "kv_req_stride=%lld < s_cap*n_kv*d=%lld", (long long)d.kv_req_stride, (long long)kv_need);
+    return fail(PRC_ESHAPE, "kv_req_stride=%lld < %lld elements of one request's base cache",
+                (long long)d.kv_req_stride, (long long)kv_need);
   if (d.kv_req_stride < 0 || d.l_req_stride < 0 || d.b_req_stride < 0)
     return fail(PRC_EINVAL, "request strides must be >= 0");
-  if (has_lr && d.l_req_stride != 0 && d.l_req_stride < d.s_cap * r && d.batch > 1)
-    return fail(PRC_ESHAPE, "l_req_stride=%lld < s_cap*rank", (long long)d.l_req_stride);
+  if (has_lr && d.l_req_stride != 0 && d.l_req_stride < l_need && d.batch > 1)
+    return fail(PRC_ESHAPE, "l_req_stride=%lld < %lld elements of one request's LR cache", (long long)d.l_req_stride,
+                (long long)l_need);
   if (has_lr && d.b_req_stride != 0 && d.b_req_stride < d.n_kv_heads * dd * r && d.batch > 1)
     return fail(PRC_ESHAPE, "b_req_stride=%lld < n_kv*d*rank", (long long)d.b_req_stride);
   if (d.kv_req_stride % 8 || d.l_req_stride % 8 || d.b_req_stride % 8)
@@ -102,6 +118,11 @@ prc_status check_attention(const lrsa_dims* dims, const uint16_t* Q, const uint1
     if (bf[i] != nullptr && !aligned(bf[i], 16)) return fail(PRC_EALIGN, "%s is not 16-byte aligned", names[i]);
   if (!aligned(kv_len, 4) || (positions != nullptr && !aligned(positions, 4)))
     return fail(PRC_EALIGN, "positions/kv_len are not 4-byte aligned");
+  if (pg != nullptr) {
+    if (pg->kv_block_table == nullptr) return fail(PRC_EINVAL, "kv_block_table is NULL");
+    if (!aligned(pg->kv_block_table, 4) || (pg->lr_block_table != nullptr && !aligned(pg->lr_block_table, 4)))
+      return fail(PRC_EALIGN, "block tables are not 4-byte aligned");
+  }
 
   prc::AttnArgs& a = out->a;
   a = prc::AttnArgs{};
@@ -125,6 +146,14 @@ prc_status check_attention(const lrsa_dims* dims, const uint16_t* Q, const uint1
   a.group = group;
   a.head_dim = d.head_dim;
   a.rank = (int32_t)r;
+  if (pg != nullptr) {
+    a.kv_tbl = pg->kv_block_table;
+    a.lr_tbl = pg->lr_block_table != nullptr ? pg->lr_block_table : pg->kv_block_table;
+    a.blk = pg->block_size;
+    a.max_blk = pg->max_blocks;
+    a.kv_nblk = pg->n_kv_blocks;
+    a.lr_nblk = has_lr ? pg->n_lr_blocks : 1;
+  }
   const double scale = d.softmax_scale > 0.f ? (double)d.softmax_scale : 1.0 / std::sqrt((double)d.head_dim);
   a.scale_log2 = (float)(scale * 1.4426950408889634);
   // RoPE frequencies omega_j = theta^(-2j/d), passed as revolutions per
@@ -191,40 +220,52 @@ PRC_API prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_i
   return launch_status(prc::launch_precompute(a, static_cast<hipStream_t>(stream)), "precompute_lr_cache");
 }
 
-PRC_API prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
-                                           const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
-                                           const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
-                                           int32_t rank, double rope_theta, uint16_t* K_base, uint16_t* V_base,
-                                           uint16_t* L_out, int64_t s_cap, int64_t tok_offset, void* stream) {
+namespace {
+
+// Shared body of the contiguous and paged projection entry points.  Paged:
+// the caches are pools of n_blocks blocks of blk tokens and
+// s_cap is the trajectory's logical capacity max_blocks * blk.
+prc_status project_impl(const char* who, const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
+                        const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim, const uint16_t* A_rows,
+                        int32_t n_proj, int32_t n_agents, int32_t rank, double rope_theta, uint16_t* K_base,
+                        uint16_t* V_base, uint16_t* L_out, int64_t s_cap, int64_t tok_offset, bool paged,
+                        const int32_t* tbl, int32_t blk, int32_t n_blocks, hipStream_t stream) {
   if (T < 0) return fail(PRC_EINVAL, "T=%lld is negative", (long long)T);
   if (d_in < 1 || d_in % 8) return fail(PRC_EUNSUPPORTED, "d_in=%lld must be a positive multiple of 8", (long long)d_in);
   if (ld_x < d_in) return fail(PRC_ESHAPE, "ld_x=%lld < d_in=%lld", (long long)ld_x, (long long)d_in);
   if (ld_x % 8) return fail(PRC_EALIGN, "ld_x=%lld is not a multiple of 8 elements", (long long)ld_x);
   if (ld_x >= (1LL << 24)) return fail(PRC_EUNSUPPORTED, "ld_x=%lld must be below 2^24", (long long)ld_x);
-  if (head_dim != 64 && head_dim != 128) return fail(PRC_EUNSUPPORTED, "head_dim=%d (built: 64, 128)", head_dim);
-  if (n_kv_heads < 1) return fail(PRC_EINVAL, "n_kv_heads=%d must be positive", n_kv_heads);
-  const int64_t nkv = (int64_t)n_kv_heads * head_dim;
+  // Paged calls may leave out the base projection (n_kv_heads == 0).
+  const bool with_base = n_kv_heads != 0 || !paged;
+  if (with_base && head_dim != 64 && head_dim != 128)
+    return fail(PRC_EUNSUPPORTED, "head_dim=%d (built: 64, 128)", head_dim);
+  if (n_kv_heads < 0 || (!paged && n_kv_heads < 1))
+    return fail(PRC_EINVAL, "n_kv_heads=%d must be positive", n_kv_heads);
+  const int64_t nkv = with_base ? (int64_t)n_kv_heads * head_dim : 0;
   // Weight rows are addressed with 32-bit byte offsets.
   if (2 * nkv * d_in * 2 >= (1LL << 31))
     return fail(PRC_EUNSUPPORTED, "2*n_kv*head_dim*d_in=%lld weights are too many", (long long)(2 * nkv * d_in));
   // n_proj * n_agents == 0: the base projection alone (no LR planes).
   if (n_proj < 0 || n_agents < 0) return fail(PRC_EINVAL, "n_proj=%d, n_agents=%d must not be negative", n_proj, n_agents);
   const bool with_lr = n_proj > 0 && n_agents > 0;
+  if (!with_base && !with_lr) return fail(PRC_EINVAL, "neither the base projection nor an LR plane is asked for");
   if (with_lr && !rank_ok(rank)) return fail(PRC_EUNSUPPORTED, "rank=%d (built: 8, 16, 32, 64)", rank);
   const int64_t n_cols = with_lr ? (int64_t)n_proj * n_agents * rank : 0;
   if (2 * nkv + n_cols > 65535LL * 64) return fail(PRC_EINVAL, "too many output columns");
-  if (!(rope_theta > 0.0)) return fail(PRC_EINVAL, "rope_theta must be positive");
+  if (with_base && !(rope_theta > 0.0)) return fail(PRC_EINVAL, "rope_theta must be positive");
   if (s_cap < 1 || s_cap > INT32_MAX) return fail(PRC_EINVAL, "s_cap=%lld must be in [1, 2^31)", (long long)s_cap);
   if (tok_offset < 0 || tok_offset + T > s_cap)
     return fail(PRC_ESHAPE, "rows [%lld, %lld) fall outside s_cap=%lld", (long long)tok_offset,
                 (long long)(tok_offset + T), (long long)s_cap);
   if (T == 0) return ok();
-  if (X == nullptr || W_rows == nullptr || K_base == nullptr || V_base == nullptr ||
+  if (X == nullptr || (with_base && (W_rows == nullptr || K_base == nullptr || V_base == nullptr)) ||
       (with_lr && (A_rows == nullptr || L_out == nullptr)))
     return fail(PRC_EINVAL, "X/W_rows/A_rows/K_base/V_base/L_out is NULL");
-  if (!aligned(X, 16) || !aligned(W_rows, 16) || !aligned(K_base, 16) || !aligned(V_base, 16) ||
+  if (!aligned(X, 16) || (with_base && (!aligned(W_rows, 16) || !aligned(K_base, 16) || !aligned(V_base, 16))) ||
       (with_lr && (!aligned(A_rows, 16) || !aligned(L_out, 16))))
     return fail(PRC_EALIGN, "X/W_rows/A_rows/K_base/V_base/L_out must be 16-byte aligned");
+  if (paged && tbl == nullptr) return fail(PRC_EINVAL, "block_table is NULL");
+  if (paged && !aligned(tbl, 4)) return fail(PRC_EALIGN, "block_table is not 4-byte aligned");
   prc::PrecomputeArgs a{};
   a.X = X;
   a.A = A_rows;
@@ -235,34 +276,71 @@ PRC_API prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t
   a.T = T;
   a.d_in = d_in;
   a.ld_x = ld_x;
-  a.s_cap = s_cap;
+  a.s_cap = paged ? (int64_t)n_blocks * blk : s_cap;
   a.tok_offset = tok_offset;
   a.n_cols = (int32_t)n_cols;
   a.rank = with_lr ? rank : 8;
   a.nkv = (int32_t)nkv;
-  a.head_dim = head_dim;
-  for (int j = 0; j < head_dim / 2; ++j)
-    a.w2pi[j] = std::pow(rope_theta, -2.0 * j / (double)head_dim) / (2.0 * M_PI);
-  return launch_status(prc::launch_precompute(a, static_cast<hipStream_t>(stream)), "project_kv_and_lr_cache");
+  a.head_dim = with_base ? head_dim : 64;
+  a.tbl = paged ? tbl : nullptr;
+  a.blk = blk;
+  a.nblk = n_blocks;
+  if (with_base)
+    for (int j = 0; j < head_dim / 2; ++j)
+      a.w2pi[j] = std::pow(rope_theta, -2.0 * j / (double)head_dim) / (2.0 * M_PI);
+  return launch_status(prc::launch_precompute(a, stream), who);
 }
 
-PRC_API size_t lr_shared_attention_workspace_size(const lrsa_dims* dims) {
+}  // namespace
+
+PRC_API prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
+                                           const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
+                                           const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                           int32_t rank, double rope_theta, uint16_t* K_base, uint16_t* V_base,
+                                           uint16_t* L_out, int64_t s_cap, int64_t tok_offset, void* stream) {
+  return project_impl("project_kv_and_lr_cache", X, T, d_in, ld_x, W_rows, n_kv_heads, head_dim, A_rows, n_proj,
+                      n_agents, rank, rope_theta, K_base, V_base, L_out, s_cap, tok_offset, false, nullptr, 0, 0,
+                      static_cast<hipStream_t>(stream));
+}
+
+PRC_API prc_status project_kv_and_lr_cache_paged(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
+                                                 const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
+                                                 const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                                 int32_t rank, double rope_theta, uint16_t* K_pool,
+                                                 uint16_t* V_pool, uint16_t* L_pool, const int32_t* block_table,
+                                                 int32_t block_size, int32_t max_blocks, int32_t n_blocks,
+                                                 int64_t tok_offset, void* stream) {
+  if (block_size < 64 || block_size % 64)
+    return fail(PRC_EUNSUPPORTED, "block_size=%d must be a positive multiple of 64", block_size);
+  if (max_blocks < 1 || n_blocks < 1)
+    return fail(PRC_EINVAL, "max_blocks=%d, n_blocks=%d must be positive", max_blocks, n_blocks);
+  if ((int64_t)max_blocks * block_size > INT32_MAX || (int64_t)n_blocks * block_size > INT32_MAX)
+    return fail(PRC_EINVAL, "max_blocks or n_blocks times block_size reaches 2^31 tokens");
+  return project_impl("project_kv_and_lr_cache_paged", X, T, d_in, ld_x, W_rows, n_kv_heads, head_dim, A_rows,
+                      n_proj, n_agents, rank, rope_theta, K_pool, V_pool, L_pool,
+                      (int64_t)max_blocks * block_size, tok_offset, true, block_table, block_size,
+                      n_blocks, static_cast<hipStream_t>(stream));
+}
+
+namespace {
+
+size_t workspace_size(const lrsa_dims* dims, bool paged) {
   if (dims == nullptr || dims->n_tok != 1 || dims->batch < 1 || dims->n_kv_heads < 1 || dims->s_cap < 1)
     return 0;
   const int r = rank_ok(dims->rank) ? dims->rank : 8;
   int n_splits = 0, split_tiles = 0;
-  prc::decode_plan(dims->s_cap, dims->batch, dims->n_kv_heads, r,
-                   prc::decode_shares_base(dims->batch, dims->kv_req_stride), &n_splits, &split_tiles);
+  // Paged caches always take the per-request decode kernel.
+  const bool shared = !paged && prc::decode_shares_base(dims->batch, dims->kv_req_stride);
+  prc::decode_plan(dims->s_cap, dims->batch, dims->n_kv_heads, r, shared, &n_splits, &split_tiles);
   return prc::decode_workspace_bytes(dims->batch, dims->n_q_heads, n_splits, dims->head_dim, r);
 }
 
-PRC_API prc_status lr_shared_attention(const lrsa_dims* dims, const uint16_t* Q, const uint16_t* K_base,
-                                       const uint16_t* V_base, const uint16_t* L_k, const uint16_t* L_v,
-                                       const uint16_t* B_k, const uint16_t* B_v, const int32_t* positions,
-                                       const int32_t* kv_len, uint16_t* O, float* lse, void* workspace,
-                                       size_t workspace_bytes, void* stream) {
+prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_paging* pg, const uint16_t* Q,
+                          const uint16_t* K_base, const uint16_t* V_base, const uint16_t* L_k, const uint16_t* L_v,
+                          const uint16_t* B_k, const uint16_t* B_v, const int32_t* positions, const int32_t* kv_len,
+                          uint16_t* O, float* lse, void* workspace, size_t workspace_bytes, void* stream) {
   Checked c;
-  prc_status s = check_attention(dims, Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len, true, &c);
+  prc_status s = check_attention(dims, Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len, true, pg, &c);
   if (s != PRC_OK || c.empty) return s;
   if (O == nullptr) return fail(PRC_EINVAL, "O is NULL");
   if (!aligned(O, 16)) return fail(PRC_EALIGN, "O is not 16-byte aligned");
@@ -275,18 +353,46 @@ PRC_API prc_status lr_shared_attention(const lrsa_dims* dims, const uint16_t* Q,
   if (!rank_ok(dims->rank)) a.rank = 8;
   else a.rank = dims->rank;
   hipStream_t st = static_cast<hipStream_t>(stream);
+  char what[96];
   if (dims->n_tok == 1) {
-    const size_t need = lr_shared_attention_workspace_size(dims);
+    const size_t need = workspace_size(dims, pg != nullptr);
     if (workspace == nullptr || workspace_bytes < need)
       return fail(PRC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace == nullptr ? 0 : workspace_bytes,
                   need);
     if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
-    prc::decode_plan(a.s_cap, a.batch, a.n_kv, a.rank, prc::decode_shares_base(a.batch, a.kv_stride), &a.n_splits,
-                     &a.split_tiles);
+    prc::decode_plan(a.s_cap, a.batch, a.n_kv, a.rank,
+                     pg == nullptr && prc::decode_shares_base(a.batch, a.kv_stride), &a.n_splits, &a.split_tiles);
     a.ws = static_cast<float*>(workspace);
-    return launch_status(prc::launch_decode(a, st), "lr_shared_attention (decode)");
+    snprintf(what, sizeof(what), "%s (decode)", who);
+    return launch_status(prc::launch_decode(a, st), what);
   }
-  return launch_status(prc::launch_prefill(a, st), "lr_shared_attention (prefill)");
+  snprintf(what, sizeof(what), "%s (prefill)", who);
+  return launch_status(prc::launch_prefill(a, st), what);
+}
+
+}  // namespace
+
+PRC_API size_t lr_shared_attention_workspace_size(const lrsa_dims* dims) { return workspace_size(dims, false); }
+
+PRC_API size_t lr_shared_attention_paged_workspace_size(const lrsa_dims* dims) { return workspace_size(dims, true); }
+
+PRC_API prc_status lr_shared_attention(const lrsa_dims* dims, const uint16_t* Q, const uint16_t* K_base,
+                                       const uint16_t* V_base, const uint16_t* L_k, const uint16_t* L_v,
+                                       const uint16_t* B_k, const uint16_t* B_v, const int32_t* positions,
+                                       const int32_t* kv_len, uint16_t* O, float* lse, void* workspace,
+                                       size_t workspace_bytes, void* stream) {
+  return attention_impl("lr_shared_attention", dims, nullptr, Q, K_base, V_base, L_k, L_v, B_k, B_v, positions,
+                        kv_len, O, lse, workspace, workspace_bytes, stream);
+}
+
+PRC_API prc_status lr_shared_attention_paged(const lrsa_dims* dims, const lrsa_paging* paging, const uint16_t* Q,
+                                             const uint16_t* K_pool, const uint16_t* V_pool, const uint16_t* L_k,
+                                             const uint16_t* L_v, const uint16_t* B_k, const uint16_t* B_v,
+                                             const int32_t* positions, const int32_t* kv_len, uint16_t* O,
+                                             float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  if (paging == nullptr) return fail(PRC_EINVAL, "paging is NULL");
+  return attention_impl("lr_shared_attention_paged", dims, paging, Q, K_pool, V_pool, L_k, L_v, B_k, B_v, positions,
+                        kv_len, O, lse, workspace, workspace_bytes, stream);
 }
 
 PRC_API prc_status materialize_agent_kv(const lrsa_dims* dims, const uint16_t* K_base, const uint16_t* V_base,
@@ -294,7 +400,7 @@ PRC_API prc_status materialize_agent_kv(const lrsa_dims* dims, const uint16_t* K
                                         const uint16_t* B_v, const int32_t* kv_len, uint16_t* K_full,
                                         uint16_t* V_full, void* stream) {
   Checked c;
-  prc_status s = check_attention(dims, nullptr, K_base, V_base, L_k, L_v, B_k, B_v, nullptr, kv_len, false, &c);
+  prc_status s = check_attention(dims, nullptr, K_base, V_base, L_k, L_v, B_k, B_v, nullptr, kv_len, false, nullptr, &c);
   if (s != PRC_OK || c.empty) return s;
   if (K_full == nullptr || V_full == nullptr) return fail(PRC_EINVAL, "K_full/V_full is NULL");
   if (!aligned(K_full, 16) || !aligned(V_full, 16)) return fail(PRC_EALIGN, "K_full/V_full not 16-byte aligned");

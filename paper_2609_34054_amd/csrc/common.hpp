@@ -122,6 +122,19 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // The angle is formed in fp64 revolutions, reduced to [0, 1) in fp64, and only
 // then rounded to fp32 for the hardware sin/cos (which take revolutions).  The
 // fp32 error stays near 1e-7 at every position below 2^31.
+// First element of token t0's row in one request's cache: contiguous
+// (tbl == nullptr: base + t0 * stride) or paged in blocks of blk tokens, the
+// block read from the request's row of the block table and clamped into the
+// pool's nblk blocks.  t0 is wave-uniform, so the entry is a scalar load.
+__device__ __forceinline__ const uint16_t* cache_row(const uint16_t* base, const int32_t* tbl, int blk, int nblk,
+                                                     int64_t t0, int64_t stride) {
+  if (tbl == nullptr) return base + t0 * stride;
+  const int64_t q = t0 / blk;
+  int32_t e = tbl[q];
+  e = e < 0 ? 0 : (e >= nblk ? nblk - 1 : e);
+  return base + ((int64_t)e * blk + (t0 - q * blk)) * stride;
+}
+
 __device__ __forceinline__ void rope_cs(int pos, double w2pi, float& c, float& s) {
   double rev = (double)pos * w2pi;
   rev -= __builtin_floor(rev);

@@ -27,6 +27,17 @@ struct AttnArgs {
   float* ws;            // decode split partials
   uint16_t* Kout;       // materialise outputs
   uint16_t* Vout;
+  // Paged caches (block tables): token t of request b sits at row t % blk of
+  // block kv_tbl[b * max_blk + t / blk] of request b's base pools (Kb, Vb +
+  // b * kv_stride: [kv_nblk, blk, n_kv, d]) and of block lr_tbl[...] of its
+  // LR pools (Lk, Lv + b * l_stride: [lr_nblk, blk, r]).  Table entries are
+  // clamped into the pools.  kv_tbl == nullptr: contiguous caches.
+  const int32_t* kv_tbl;
+  const int32_t* lr_tbl;
+  int32_t blk;          // tokens per block (a multiple of 64)
+  int32_t max_blk;      // table entries per request
+  int32_t kv_nblk;      // blocks per base pool
+  int32_t lr_nblk;      // blocks per LR pool
   int64_t s_cap;
   int64_t kv_stride;
   int64_t l_stride;
@@ -81,6 +92,12 @@ struct PrecomputeArgs {
   int32_t rank;
   int32_t nkv;          // n_kv * head_dim, a multiple of 64 (or 0)
   int32_t head_dim;
+  // Paged output (tbl != nullptr): token p = tok_offset + t is written to row
+  // tbl[p / blk] * blk + p % blk of every pool (s_cap = nblk * blk rows per
+  // LR plane); the table entry is clamped into [0, nblk).
+  const int32_t* tbl;
+  int32_t blk;
+  int32_t nblk;
   double w2pi[kMaxHalfDim];  // RoPE omega_j / (2 pi), fp64
 };
 hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t stream);

@@ -120,16 +120,21 @@ __device__ __forceinline__ StageOffsets<D, R> stage_offsets(int64_t row, int lan
 template <int D, int R>
 __device__ __forceinline__ void stage_load(Stage<D, R>& s, const StageOffsets<D, R>& o, const uint16_t* Kb,
                                            const uint16_t* Vb, const uint16_t* Lk, const uint16_t* Lv,
+                                           const int32_t* kvt, const int32_t* lrt, int blk, int kvn, int lrn,
                                            int64_t row, int64_t t0, int64_t t_end) {
   using C = Dec<D, R>;
   // Valid tokens of the sub-block (none past the end: every load reads zeros).
   const int64_t n = t_end - t0 < 0 ? 0 : (t_end - t0 < 16 ? t_end - t0 : 16);
   const int32_t kv_bytes = n > 0 ? (int32_t)((n - 1) * row * 2 + D * 2) : 0;
-  const auto rk = make_rsrc(Kb + t0 * row, kv_bytes);
-  const auto rv = make_rsrc(Vb + t0 * row, kv_bytes);
+  // A sub-block with no valid token reads nothing (and no block table entry:
+  // t0 may lie past the request's last block).
+  const auto rk = make_rsrc(n > 0 ? cache_row(Kb, kvt, blk, kvn, t0, row) : Kb, kv_bytes);
+  const auto rv = make_rsrc(n > 0 ? cache_row(Vb, kvt, blk, kvn, t0, row) : Vb, kv_bytes);
   // Absent LR caches get empty resources (loads read zeros, touch nothing).
-  const auto rlk = make_rsrc(Lk != nullptr ? Lk + t0 * R : Kb, Lk != nullptr ? (int32_t)(n * R * 2) : 0);
-  const auto rlv = make_rsrc(Lv != nullptr ? Lv + t0 * R : Kb, Lv != nullptr ? (int32_t)(n * R * 2) : 0);
+  const auto rlk = make_rsrc(Lk != nullptr && n > 0 ? cache_row(Lk, lrt, blk, lrn, t0, R) : Kb,
+                             Lk != nullptr ? (int32_t)(n * R * 2) : 0);
+  const auto rlv = make_rsrc(Lv != nullptr && n > 0 ? cache_row(Lv, lrt, blk, lrn, t0, R) : Kb,
+                             Lv != nullptr ? (int32_t)(n * R * 2) : 0);
 #pragma unroll
   for (int kk = 0; kk < C::NCH; ++kk)
     s.kb[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, o.kb[kk], 0, 0));
@@ -199,6 +204,10 @@ lrsa_decode_kernel(const AttnArgs a) {
   for (int i = lane; i < 16 * C::LV_ROW; i += 64) lv_lds[w][i] = 0;
 
   const int64_t row = (int64_t)a.n_kv * D;  // elements between tokens
+  // This request's caches (or pools, paged through its rows of the block
+  // tables).
+  const int32_t* kvt = a.kv_tbl != nullptr ? a.kv_tbl + (int64_t)b * a.max_blk : nullptr;
+  const int32_t* lrt = a.lr_tbl != nullptr ? a.lr_tbl + (int64_t)b * a.max_blk : nullptr;
   const uint16_t* Kb = a.Kb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Lk = has_lk ? a.Lk + (int64_t)b * a.l_stride : nullptr;
@@ -234,7 +243,7 @@ lrsa_decode_kernel(const AttnArgs a) {
 
   const StageOffsets<D, R> so = stage_offsets<D, R>(row, lane);
   Stage<D, R> st[2];
-  stage_load<D, R>(st[0], so, Kb, Vb, Lk, Lv, row, t_begin, t_end_w);
+  stage_load<D, R>(st[0], so, Kb, Vb, Lk, Lv, kvt, lrt, a.blk, a.kv_nblk, a.lr_nblk, row, t_begin, t_end_w);
 
   __syncthreads();  // base angles of the first tile, zeroed L_v tiles
 
@@ -268,7 +277,7 @@ lrsa_decode_kernel(const AttnArgs a) {
       if (ts >= t_end) break;
       // Issue the next sub-block's loads before consuming this one (past the
       // split end they read zeros and touch no memory).
-      stage_load<D, R>(nxt, so, Kb, Vb, Lk, Lv, row, ts + 16, t_end_w);
+      stage_load<D, R>(nxt, so, Kb, Vb, Lk, Lv, kvt, lrt, a.blk, a.kv_nblk, a.lr_nblk, row, ts + 16, t_end_w);
 
       // ---- V and L_v rows into the wave's LDS tile ------------------------
 #pragma unroll
@@ -832,7 +841,9 @@ size_t decode_workspace_bytes(int batch, int n_q, int n_splits, int head_dim, in
 }
 
 hipError_t launch_decode(const AttnArgs& a, hipStream_t st) {
-  const bool shared = decode_shares_base(a.batch, a.kv_stride);
+  // Paged caches go through the per-request kernel (requests may share some
+  // blocks and not others).
+  const bool shared = a.kv_tbl == nullptr && decode_shares_base(a.batch, a.kv_stride);
   if (a.head_dim == 64) return launch_r<64>(a, st, shared);
   if (a.head_dim == 128) return launch_r<128>(a, st, shared);
   return hipErrorInvalidValue;

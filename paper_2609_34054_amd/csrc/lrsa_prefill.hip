@@ -187,6 +187,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int n_tiles = (int)((kv_hi + TKV - 1) / TKV);
 
   const int64_t row_el = (int64_t)a.n_kv * D;
+  // This request's caches (or pools, paged through its rows of the block
+  // tables).
+  const int32_t* kvt = a.kv_tbl != nullptr ? a.kv_tbl + (int64_t)b * a.max_blk : nullptr;
+  const int32_t* lrt = a.lr_tbl != nullptr ? a.lr_tbl + (int64_t)b * a.max_blk : nullptr;
   const uint16_t* Kb = a.Kb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Lk = LK ? a.Lk + (int64_t)b * a.l_stride : nullptr;
@@ -277,8 +281,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
   auto load_unit = [&](Unit<D, R>& u, int64_t t0) {
     const int rows = (int)(kv_hi - t0 < TKV ? kv_hi - t0 : TKV);  // valid rows of this tile (> 0)
     const int32_t kv_bytes = (rows - 1) * (int32_t)(row_el * 2) + D * 2;
-    const auto rk = make_rsrc(Kb + t0 * row_el, kv_bytes);
-    const auto rv = make_rsrc(Vb + t0 * row_el, kv_bytes);
+    const auto rk = make_rsrc(cache_row(Kb, kvt, a.blk, a.kv_nblk, t0, row_el), kv_bytes);
+    const auto rv = make_rsrc(cache_row(Vb, kvt, a.blk, a.kv_nblk, t0, row_el), kv_bytes);
     if constexpr (C::SEG == 8) {
       const u32x4 lo = buf_ld16(rk, offk), hi = buf_ld16(rk, offk + C::HALF * 2);
 #pragma unroll
@@ -295,14 +299,14 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
     }
     if constexpr (LK) {
-      const auto rl = make_rsrc(Lk + t0 * R, rows * R * 2);
+      const auto rl = make_rsrc(cache_row(Lk, lrt, a.blk, a.lr_nblk, t0, R), rows * R * 2);
 #pragma unroll
       for (int rc = 0; rc < C::RC; ++rc) u.lk[rc] = rc * 16 + q * 4 < R ? buf_ld8(rl, offlk + rc * 32) : u32x2{0u, 0u};
     }
 #pragma unroll
     for (int hb = 0; hb < C::NHB; ++hb) u.v[hb] = buf_ld16(rv, offv[hb]);
     if constexpr (LV) {
-      const auto rl = make_rsrc(Lv + t0 * R, rows * R * 2);
+      const auto rl = make_rsrc(cache_row(Lv, lrt, a.blk, a.lr_nblk, t0, R), rows * R * 2);
 #pragma unroll
       for (int p = 0; p < C::NLP; ++p) u.lv[p] = lv_wave ? buf_ld16(rl, offlv[p]) : u32x4{0u, 0u, 0u, 0u};
     }

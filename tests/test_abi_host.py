@@ -121,6 +121,45 @@ def test_projection_without_lr_planes_needs_no_lr_buffers():
     assert _pj(n_proj=0, A=None, L=None, r=12, K=None) == EINVAL
 
 
+# ----------------------------------------------------- paged fused projection
+def _pjp(X=A16, T=64, d_in=256, ld_x=256, W=A16, n_kv=2, d=128, A=A16, n_proj=2, N=3, r=8, theta=1e4,
+         K=A16, V=A16, L=A16, tbl=A16, blk=128, max_blocks=4, n_blocks=16, off=0):
+    return prc.lib().project_kv_and_lr_cache_paged(X, T, d_in, ld_x, W, n_kv, d, A, n_proj, N, r, theta, K, V,
+                                                   L, tbl, blk, max_blocks, n_blocks, off, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(blk=0), EUNSUP),
+    (dict(blk=96), EUNSUP),
+    (dict(blk=-64), EUNSUP),
+    (dict(max_blocks=0), EINVAL),
+    (dict(n_blocks=0), EINVAL),
+    (dict(max_blocks=1 << 25), EINVAL),   # max_blocks * blk reaches 2^31
+    (dict(n_blocks=1 << 25), EINVAL),
+    (dict(off=500), ESHAPE),              # 500 + 64 > 4 * 128
+    (dict(tbl=None), EINVAL),
+    (dict(tbl=A16 + 2), EALIGN),
+    (dict(n_kv=-1), EINVAL),
+    (dict(n_kv=0, N=0), EINVAL),          # nothing asked for
+    (dict(d=96), EUNSUP),
+    (dict(K=None), EINVAL),
+    (dict(L=None), EINVAL),
+    (dict(r=12), EUNSUP),
+])
+def test_paged_projection_rejects(kw, code):
+    assert _pjp(**kw) == code
+    assert prc.lib().prc_last_error().decode()
+
+
+def test_paged_projection_lr_only_and_base_only_excuse_buffers():
+    # LR planes alone: no weights, no base pools, head_dim and theta unused.
+    # Each call stops at a host check placed after the excused buffers.
+    assert _pjp(n_kv=0, W=None, K=None, V=None, d=0, theta=0.0, off=500) == ESHAPE
+    assert _pjp(n_kv=0, W=None, K=None, V=None, d=0, theta=0.0, tbl=A16 + 2) == EALIGN
+    assert _pjp(N=0, A=None, L=None, r=12, tbl=A16 + 2) == EALIGN
+    assert _pjp(T=0, X=None, W=None, A=None, K=None, V=None, L=None, tbl=None) == 0
+
+
 # ------------------------------------------------------------------ attention
 def _dims(**kw):
     d = dict(batch=2, n_tok=4, n_q_heads=32, n_kv_heads=8, head_dim=128, rank=16, s_cap=1024,
@@ -206,6 +245,71 @@ def test_decode_workspace_query_and_check():
     # contexts.
     big = L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=1, batch=16, s_cap=32768)))
     assert big >= 16 * 32 * (4 + 128 + 16) * 4
+
+
+# ------------------------------------------------------------ paged attention
+def _paging(**kw):
+    from paper_2609_34054_amd.binding import LrsaPaging
+    p = dict(kv_block_table=A16, lr_block_table=None, block_size=128, max_blocks=8, n_kv_blocks=64,
+             n_lr_blocks=16)
+    p.update(kw)
+    return LrsaPaging(**p)
+
+
+def _pdims(**kw):
+    d = dict(s_cap=1024, kv_req_stride=0, l_req_stride=16 * 128 * 16)
+    d.update(kw)
+    return _dims(**d)
+
+
+def _pattn(dims, paging, Q=A16, K=A16, V=A16, Lk=A16, Lv=A16, Bk=A16, Bv=A16, pos=A16, kvl=A16, O=A16,
+           lse=None, ws=None, ws_bytes=0):
+    pg = None if paging is None else ctypes.byref(paging)
+    return prc.lib().lr_shared_attention_paged(ctypes.byref(dims), pg, Q, K, V, Lk, Lv, Bk, Bv, pos, kvl, O,
+                                               lse, ws, ws_bytes, None)
+
+
+@pytest.mark.parametrize("dkw,pkw,code", [
+    (dict(), dict(block_size=0), EUNSUP),
+    (dict(), dict(block_size=100), EUNSUP),
+    (dict(), dict(max_blocks=0), EINVAL),
+    (dict(), dict(n_kv_blocks=0), EINVAL),
+    (dict(), dict(n_lr_blocks=0), EINVAL),
+    (dict(s_cap=2048), dict(), ESHAPE),                  # s_cap != max_blocks * block_size
+    (dict(kv_req_stride=64 * 128 * 8 * 128 - 8), dict(), ESHAPE),  # < one request's pools
+    (dict(l_req_stride=16 * 128 * 16 - 8), dict(), ESHAPE),
+    (dict(), dict(kv_block_table=None), EINVAL),
+    (dict(), dict(kv_block_table=A16 + 2), EALIGN),
+    (dict(), dict(lr_block_table=A16 + 2), EALIGN),
+    (dict(head_dim=96), dict(), EUNSUP),
+])
+def test_paged_attention_rejects(dkw, pkw, code):
+    assert _pattn(_pdims(**dkw), _paging(**pkw)) == code
+    assert prc.lib().prc_last_error().decode()
+
+
+def test_paged_attention_needs_paging_and_lr_pools_only_with_lr():
+    assert _pattn(_pdims(), None) == EINVAL
+    # Without LR caches the LR pool size is never looked at.  The call then
+    # stops at the first missing piece of a decode call, the workspace.
+    d = _pdims(n_tok=1)
+    assert _pattn(d, _paging(n_lr_blocks=0), Lk=None, Lv=None, Bk=None, Bv=None) == EWS
+    assert _pattn(_pdims(batch=0), _paging(kv_block_table=None), Q=None, K=None, V=None, pos=None, kvl=None,
+                  O=None) == 0
+
+
+def test_paged_decode_workspace_is_the_per_request_plan():
+    L = prc.lib()
+    # One base pool shared by all requests (kv_req_stride 0): the contiguous
+    # call would take the shared-base kernel; the paged one never does, and
+    # sizes its workspace for the per-request split plan.
+    d = _pdims(n_tok=1, batch=16, s_cap=32768)
+    need = L.lr_shared_attention_paged_workspace_size(ctypes.byref(d))
+    assert need > 0
+    assert need == L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=1, batch=16, s_cap=32768)))
+    pg = _paging(max_blocks=256)
+    assert _pattn(d, pg, ws=A16, ws_bytes=need - 1) == EWS
+    assert _pattn(d, pg, ws=A16 + 4, ws_bytes=need) == EALIGN
 
 
 # ---------------------------------------------------------------- materialise

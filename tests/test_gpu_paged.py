@@ -1,0 +1,260 @@
+"""Paged caches (block tables, the paged-KV serving setup of Sec. 4.1 and
+App. C.2): attention over pools whose blocks are scattered in a random order
+equals, bit for bit, attention over the same caches laid out contiguously,
+and matches the fp64 oracle; the paged projection writes exactly the rows the
+contiguous one writes; and a chunked prefill that grows a paged trajectory
+chunk by chunk, followed by a decode step, matches the oracle run over the
+whole trajectory at once."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2609_34054_amd as prc
+from gpu_cases import ATOL_MAX, ATOL_MEAN, LSE_ATOL, PRE_REL, attn_errors, b_paper, f64, lse_error, \
+    oracle_attention
+from workload import Config, attention_case
+from workload.gen import normal_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def mk_cfg(idx, n_q, n_kv, d, r, theta=1e4):
+    return Config(idx, "paged", hidden=256, n_q=n_q, n_kv=n_kv, head_dim=d, theta=theta, n_agents=1, rank=r,
+                  context=0, prefill_tokens=0, decode_batch=0, precompute_rows=0)
+
+
+def block_table(batch, max_blocks, n_pool, seed):
+    """Each request's blocks: distinct pool blocks in a seeded random order."""
+    g = torch.Generator().manual_seed(seed)
+    ids = torch.randperm(n_pool, generator=g)[: batch * max_blocks]
+    return ids.reshape(batch, max_blocks).to(torch.int32)
+
+
+def to_pool(cache, table, blk, n_pool):
+    """Scatter contiguous per-request caches [B, max_blocks*blk, ...] into a pool
+    [n_pool, blk, ...] along ``table``; blocks no request lists hold NaN."""
+    B, S = cache.shape[:2]
+    mb = S // blk
+    pool = torch.full((n_pool, blk) + tuple(cache.shape[2:]), float("nan"), dtype=cache.dtype)
+    pool[table.reshape(-1).long()] = cache.reshape((B * mb, blk) + tuple(cache.shape[2:]))
+    return pool
+
+
+def padded(t, S):
+    """Pad the token dimension of [B, s, ...] to S rows (NaN: never read)."""
+    if t is None or t.shape[1] == S:
+        return t
+    pad = torch.full((t.shape[0], S - t.shape[1]) + tuple(t.shape[2:]), float("nan"), dtype=t.dtype)
+    return torch.cat([t, pad], dim=1)
+
+
+# id, d, r, n_q, n_kv, n_tok, kv_lens, lr, block size, LR layout
+#   LR layout "own": one LR pool shared by every request with its own table;
+#   "planes": a pool per request indexed by the base table (agent planes).
+PAGED_CASES = [
+    ("prefill_d128_r16", 128, 16, 8, 2, 70, [300, 233], "kv", 64, "own"),
+    ("prefill_d64_r8_blk128", 64, 8, 4, 4, 130, [400], "kv", 128, "planes"),
+    ("prefill_r64_blk256", 128, 64, 10, 2, 37, [600, 150], "kv", 256, "own"),
+    ("prefill_qv_r32", 128, 32, 8, 2, 45, [190, 64], "v", 64, "planes"),
+    ("prefill_plain", 128, 16, 8, 2, 50, [300], "none", 128, "own"),
+    ("decode_d128_r16", 128, 16, 8, 2, 1, [1000, 77, 1, 640], "kv", 64, "own"),
+    ("decode_d64_r32_blk128", 64, 32, 8, 4, 1, [333, 129], "kv", 128, "planes"),
+    ("decode_r64", 128, 64, 8, 2, 1, [700, 64], "kv", 64, "own"),
+    ("decode_qv_r8_long", 128, 8, 8, 2, 1, [5000, 2999], "v", 256, "planes"),
+    ("decode_k_only", 64, 8, 4, 2, 1, [90, 300], "k", 64, "own"),
+    ("decode_plain_many", 64, 16, 8, 8, 1, [64, 65, 63, 1, 17, 200, 31, 128], "none", 64, "own"),
+]
+
+
+@pytest.mark.parametrize("case", PAGED_CASES, ids=[c[0] for c in PAGED_CASES])
+def test_paged_attention(case):
+    cid, d, r, n_q, n_kv, n_tok, kv_lens, lr, blk, lr_layout = case
+    print(f"paged attention {cid}", flush=True)
+    B = len(kv_lens)
+    max_blocks = -(-max(kv_lens) // blk)
+    S = max_blocks * blk
+    cfg = mk_cfg(70 + len(cid), n_q, n_kv, d, r)
+    pos = [list(range(k - n_tok, k)) for k in kv_lens]
+    c = attention_case(cfg, batch=B, n_tok=n_tok, kv_len=kv_lens, positions=pos, s_cap=max(kv_lens),
+                       seed_base=11 * len(cid), lr_k=lr in ("kv", "k"), lr_v=lr in ("kv", "v"))
+    for name in ("K_base", "V_base", "L_k", "L_v"):
+        c[name] = padded(c[name], S)
+    dev = {k: (v.cuda() if isinstance(v, torch.Tensor) else v) for k, v in c.items()}
+
+    # Contiguous reference call with the same capacity (same decode split plan).
+    O_c, lse_c = prc.lr_shared_attention(dev["Q"], dev["K_base"], dev["V_base"], dev["L_k"], dev["L_v"],
+                                         dev["Bk_rows"], dev["Bv_rows"], dev["positions"], dev["kv_len"],
+                                         rope_theta=cfg.theta, want_lse=True)
+
+    n_pool = B * max_blocks + 3
+    kv_tbl = block_table(B, max_blocks, n_pool, 1000 + len(cid))
+    K_pool = to_pool(c["K_base"], kv_tbl, blk, n_pool).cuda()
+    V_pool = to_pool(c["V_base"], kv_tbl, blk, n_pool).cuda()
+    lr_tbl = None
+    Lk = Lv = None
+    if lr_layout == "own":
+        n_lr = B * max_blocks + 5
+        lr_tbl = block_table(B, max_blocks, n_lr, 2000 + len(cid))
+        Lk = None if c["L_k"] is None else to_pool(c["L_k"], lr_tbl, blk, n_lr).cuda()
+        Lv = None if c["L_v"] is None else to_pool(c["L_v"], lr_tbl, blk, n_lr).cuda()
+        lr_tbl = lr_tbl.cuda()
+    else:
+        # Request b's LR pool is its own plane, indexed by the base table.
+        def planes(t):
+            if t is None:
+                return None
+            return torch.stack([to_pool(t[b:b + 1], kv_tbl[b:b + 1], blk, n_pool) for b in range(B)]).cuda()
+        Lk, Lv = planes(c["L_k"]), planes(c["L_v"])
+    O_p, lse_p = prc.lr_shared_attention_paged(dev["Q"], K_pool, V_pool, Lk, Lv, dev["Bk_rows"], dev["Bv_rows"],
+                                               dev["positions"], dev["kv_len"], kv_tbl.cuda(),
+                                               lr_block_table=lr_tbl, rope_theta=cfg.theta, want_lse=True)
+    torch.cuda.synchronize()
+    assert torch.equal(O_p, O_c)
+    assert torch.equal(lse_p, lse_c)
+    Oref, lref = oracle_attention(c, cfg.theta)
+    mx, mean = attn_errors(O_p, Oref)
+    assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (mx, mean)
+    assert lse_error(lse_p, lref) <= LSE_ATOL
+
+
+def test_paged_blocks_shared_between_requests():
+    """Agents of one trajectory list the same base blocks (one pool, request
+    stride 0), and a second trajectory shares the first one's prefix blocks;
+    each request keeps its own LR plane."""
+    cfg = mk_cfg(90, 8, 2, 128, 16, theta=5e5)
+    blk, S = 64, 448
+    mb = S // blk
+    base = attention_case(cfg, batch=2, n_tok=1, kv_len=[S, S], positions=[[S - 1], [S - 1]], s_cap=S,
+                          seed_base=901, poison_tail=False)
+    # Trajectory 1 reuses trajectory 0's first 3 blocks (a shared prefix).
+    traj_k = base["K_base"].clone()
+    traj_v = base["V_base"].clone()
+    traj_k[1, : 3 * blk] = traj_k[0, : 3 * blk]
+    traj_v[1, : 3 * blk] = traj_v[0, : 3 * blk]
+    n_pool = 2 * mb + 2
+    t = block_table(2, mb, n_pool, 903)
+    t[1, :3] = t[0, :3]
+    K_pool = to_pool(traj_k, t, blk, n_pool)
+    V_pool = to_pool(traj_v, t, blk, n_pool)
+    # Requests: agents 0, 1 on trajectory 0 and agents 2, 3 on trajectory 1.
+    B = 4
+    traj = [0, 0, 1, 1]
+    kv_lens = [S, 300, S - 1, 100]
+    q = normal_bf16((B, 1, 8, 128), 1.0, 905)
+    Lk = normal_bf16((B, S, 16), 1.0, 906)
+    Lv = normal_bf16((B, S, 16), 1.0, 907)
+    Bk = normal_bf16((B, 2 * 128, 16), 0.05, 908)
+    Bv = normal_bf16((B, 2 * 128, 16), 0.05, 909)
+    tables = torch.stack([t[j] for j in traj])
+    lr_pool_k = torch.stack([to_pool(Lk[b:b + 1], tables[b:b + 1], blk, n_pool) for b in range(B)])
+    lr_pool_v = torch.stack([to_pool(Lv[b:b + 1], tables[b:b + 1], blk, n_pool) for b in range(B)])
+    pos = torch.tensor([[k - 1] for k in kv_lens], dtype=torch.int32)
+    kvl = torch.tensor(kv_lens, dtype=torch.int32)
+    O, lse = prc.lr_shared_attention_paged(q.cuda(), K_pool.cuda(), V_pool.cuda(), lr_pool_k.cuda(),
+                                           lr_pool_v.cuda(), Bk.cuda(), Bv.cuda(), pos.cuda(), kvl.cuda(),
+                                           tables.cuda(), rope_theta=cfg.theta, want_lse=True)
+    torch.cuda.synchronize()
+    Kb = torch.stack([traj_k[j] for j in traj])
+    Vb = torch.stack([traj_v[j] for j in traj])
+    Oref, lref = oracle.lr_shared_attention(f64(q), f64(Kb), f64(Vb), f64(Lk), f64(Lv), b_paper(Bk), b_paper(Bv),
+                                            pos.numpy(), kv_lens, cfg.theta)
+    mx, mean = attn_errors(O, Oref)
+    assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (mx, mean)
+    assert lse_error(lse, lref) <= LSE_ATOL
+
+
+def test_paged_projection_matches_contiguous():
+    """The paged projection writes, bit for bit, the rows the contiguous one
+    writes, at the table's blocks, and nothing else."""
+    T, d_in, n_kv, d, n_proj, N, r, off, theta = 300, 256, 2, 128, 2, 3, 16, 70, 5e5
+    blk, mb, n_pool = 64, 7, 12
+    X = normal_bf16((T, d_in), 1.0, 931)
+    W_rows = normal_bf16((2 * n_kv * d, d_in), 1.0 / math.sqrt(d_in), 932)
+    A_rows = normal_bf16((n_proj * N * r, d_in), 1.0 / math.sqrt(d_in), 933)
+    S = mb * blk
+    K = torch.zeros((S, n_kv, d), dtype=torch.bfloat16, device="cuda")
+    V = torch.zeros_like(K)
+    L = torch.zeros((n_proj, N, S, r), dtype=torch.bfloat16, device="cuda")
+    prc.project_kv_and_lr_cache(X.cuda(), W_rows.cuda(), A_rows.cuda(), n_kv, d, n_proj, N, r, K, V, L,
+                                rope_theta=theta, tok_offset=off)
+    tbl = block_table(1, mb, n_pool, 934)[0]
+    sentinel = -5.0
+    Kp = torch.full((n_pool, blk, n_kv, d), sentinel, dtype=torch.bfloat16, device="cuda")
+    Vp = torch.full_like(Kp, sentinel)
+    Lp = torch.full((n_proj, N, n_pool, blk, r), sentinel, dtype=torch.bfloat16, device="cuda")
+    prc.project_kv_and_lr_cache_paged(X.cuda(), W_rows.cuda(), A_rows.cuda(), n_kv, d, n_proj, N, r, Kp, Vp, Lp,
+                                      tbl.cuda(), rope_theta=theta, tok_offset=off)
+    torch.cuda.synchronize()
+    rows = torch.arange(off, off + T)
+    blocks, within = tbl[rows // blk].long(), rows % blk
+    assert torch.equal(Kp[blocks, within], K[off:off + T])
+    assert torch.equal(Vp[blocks, within], V[off:off + T])
+    assert torch.equal(Lp[:, :, blocks, within], L[:, :, off:off + T])
+    written = torch.zeros((n_pool, blk), dtype=torch.bool)
+    written[blocks, within] = True
+    written = written.cuda()
+    assert (Kp[~written].float() == sentinel).all() and (Vp[~written].float() == sentinel).all()
+    assert (Lp[:, :, ~written].float() == sentinel).all()
+    # LR planes alone (no base projection): the same LR rows, base pools untouched.
+    Lp2 = torch.full_like(Lp, sentinel)
+    prc.project_kv_and_lr_cache_paged(X.cuda(), None, A_rows.cuda(), 0, 0, n_proj, N, r, None, None, Lp2,
+                                      tbl.cuda(), rope_theta=theta, tok_offset=off)
+    torch.cuda.synchronize()
+    ref = oracle.precompute_lr_cache(f64(X), f64(A_rows).T, n_proj, N, r)
+    got = f64(Lp2[:, :, blocks, within])
+    assert np.linalg.norm(got - ref) / np.linalg.norm(ref) <= PRE_REL
+    assert (Lp2[:, :, ~written].float() == sentinel).all()
+
+
+def test_chunked_prefill_then_decode():
+    """A trajectory grows chunk by chunk (ragged, not block aligned): each chunk
+    is projected into the paged pools and then attended over everything written
+    so far by N agents; a last token is appended and decoded.  Every output is
+    compared with the oracle run over the whole trajectory at once (projection
+    and attention in fp64)."""
+    d_in, n_kv, d, n_q, N, r, theta = 256, 2, 128, 8, 3, 16, 5e5
+    chunks = [256, 200, 1, 143]
+    S = sum(chunks) + 1            # + the decoded token
+    blk = 128
+    mb = -(-S // blk)
+    n_pool = mb + 4
+    X = normal_bf16((S, d_in), 1.0, 941)
+    W_rows = normal_bf16((2 * n_kv * d, d_in), 1.0 / math.sqrt(d_in), 942)
+    A_rows = normal_bf16((2 * N * r, d_in), 1.0 / math.sqrt(d_in), 943)
+    Bk = normal_bf16((N, n_kv * d, r), 0.05, 944)
+    Bv = normal_bf16((N, n_kv * d, r), 0.05, 945)
+    Q = normal_bf16((N, S, n_q, d), 1.0, 946)
+    tbl = block_table(1, mb, n_pool, 947)
+    Kp = torch.full((n_pool, blk, n_kv, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+    Vp = torch.full_like(Kp, float("nan"))
+    Lp = torch.full((2, N, n_pool, blk, r), float("nan"), dtype=torch.bfloat16, device="cuda")
+    tables = tbl.expand(N, mb).contiguous().cuda()
+    Xd, Wd, Ad, Bkd, Bvd, Qd = (t.cuda() for t in (X, W_rows, A_rows, Bk, Bv, Q))
+    outs, lses = [], []
+    s0 = 0
+    for c in chunks + [1]:
+        s1 = s0 + c
+        print(f"chunk [{s0}, {s1})", flush=True)
+        prc.project_kv_and_lr_cache_paged(Xd[s0:s1], Wd, Ad, n_kv, d, 2, N, r, Kp, Vp, Lp, tbl[0].cuda(),
+                                          rope_theta=theta, tok_offset=s0)
+        pos = torch.arange(s0, s1, dtype=torch.int32).expand(N, c).contiguous().cuda()
+        kvl = torch.full((N,), s1, dtype=torch.int32, device="cuda")
+        O, lse = prc.lr_shared_attention_paged(Qd[:, s0:s1].contiguous(), Kp, Vp, Lp[0], Lp[1], Bkd, Bvd, pos, kvl,
+                                               tables, rope_theta=theta, want_lse=True)
+        outs.append(O)
+        lses.append(lse)
+        s0 = s1
+    torch.cuda.synchronize()
+    O = torch.cat(outs, dim=1)
+    lse = torch.cat(lses, dim=1)
+    Kr, Vr, Lr = oracle.project_kv_and_lr(f64(X), f64(W_rows[: n_kv * d]).T, f64(W_rows[n_kv * d:]).T,
+                                          f64(A_rows).T, n_kv, 2, N, r, np.arange(S), theta)
+    rep = lambda x: np.broadcast_to(x, (N,) + x.shape)
+    Oref, lref = oracle.lr_shared_attention(f64(Q), rep(Kr), rep(Vr), Lr[0], Lr[1], b_paper(Bk), b_paper(Bv),
+                                            np.broadcast_to(np.arange(S), (N, S)), [S] * N, theta)
+    mx, mean = attn_errors(O, Oref)
+    assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (mx, mean)
+    assert lse_error(lse, lref) <= LSE_ATOL
