@@ -491,6 +491,96 @@ def fused_projection(prc, w, dev, steps, warmup):
         "lr_cost_in_fused_ms": round(t_fused - t_base, 4)}), flush=True)
 
 
+def paged(prc, w, dev, steps, warmup):
+    """The step's decode, prefill and segment projection over paged caches
+    (pools of fixed-size blocks in a random order, reached through block
+    tables), against the same calls over contiguous caches.  One JSON line
+    per stage and block size."""
+    import torch
+    x = make_inputs(w, dev)
+    theta = w["theta"]
+    g = torch.Generator(device="cpu").manual_seed(7000)
+
+    def table(n_req, mb):
+        ids = torch.randperm(n_req * mb, generator=g)
+        return ids.reshape(n_req, mb).to(torch.int32).to(dev)
+
+    def to_pool(cache, tbl, blk):
+        B, S = cache.shape[:2]
+        pool = torch.empty((B * S // blk, blk) + tuple(cache.shape[2:]), dtype=cache.dtype, device=dev)
+        pool[tbl.reshape(-1).long()] = cache.reshape((B * S // blk, blk) + tuple(cache.shape[2:]))
+        return pool
+
+    def timeit(fn):
+        for _ in range(warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    work = algorithmic_work(w)
+    for stage in ("decode", "prefill"):
+        c = x["dec" if stage == "decode" else "pre"]
+        O = torch.empty_like(c["Q"])
+        O2 = torch.empty_like(c["Q"])
+        dims = prc.make_dims(c["Q"], c["K_base"], c["L_k"], c["L_v"], c["Bk_rows"], c["Bv_rows"], theta)
+        ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
+        t_c = timeit(lambda: attn(prc, c, theta, O, ws))
+        S = c["K_base"].shape[1]
+        for blk in (64, 256):
+            if S % blk:
+                continue
+            B, mb = c["K_base"].shape[0], S // blk
+            tk, tl = table(B, mb), table(B, mb)
+            Kp, Vp = to_pool(c["K_base"], tk, blk), to_pool(c["V_base"], tk, blk)
+            Lkp, Lvp = to_pool(c["L_k"], tl, blk), to_pool(c["L_v"], tl, blk)
+
+            def run():
+                prc.lr_shared_attention_paged(c["Q"], Kp, Vp, Lkp, Lvp, c["Bk_rows"], c["Bv_rows"],
+                                              c["positions"], c["kv_len"], tk, lr_block_table=tl,
+                                              rope_theta=theta, O=O2, workspace=ws)
+            t_p = timeit(run)
+            rec = {"bench": "paged", "stage": stage, "block_size": blk, "requests": B, "context": S,
+                   "ms_paged": round(t_p, 4), "ms_contiguous": round(t_c, 4),
+                   "paged_over_contiguous": round(t_p / t_c, 4), "bitwise_equal": bool(torch.equal(O, O2))}
+            if stage == "decode":
+                rec["hbm_frac_paged"] = round(work["decode_bytes"] / (t_p * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
+            else:
+                rec["mfma_frac_paged"] = round(work["prefill_flops"] / (t_p * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
+            print(json.dumps(rec), flush=True)
+            del Kp, Vp, Lkp, Lvp
+
+    # Segment projection (base K/V + all agents' LR rows) into paged pools.
+    T, hid, n_kv, d, r, N, S = w["seg"], w["hidden"], w["n_kv"], w["d"], w["r"], w["N"], w["S"]
+    X = x["X"][0]
+    W_rows = (torch.randn((2 * n_kv * d, hid), generator=torch.Generator(device=dev).manual_seed(7001),
+                          device=dev) / math.sqrt(hid)).to(torch.bfloat16)
+    s_cap = S + T
+    K = torch.empty((s_cap, n_kv, d), dtype=torch.bfloat16, device=dev)
+    V = torch.empty_like(K)
+    L = torch.empty((2, N, s_cap, r), dtype=torch.bfloat16, device=dev)
+    t_c = timeit(lambda: prc.project_kv_and_lr_cache(X, W_rows, x["A_rows"], n_kv, d, 2, N, r, K, V, L,
+                                                     rope_theta=theta, tok_offset=S))
+    for blk in (64, 256):
+        mb = s_cap // blk
+        tbl = table(1, mb)[0]
+        Kp = torch.empty((mb, blk, n_kv, d), dtype=torch.bfloat16, device=dev)
+        Vp = torch.empty_like(Kp)
+        Lp = torch.empty((2, N, mb, blk, r), dtype=torch.bfloat16, device=dev)
+        t_p = timeit(lambda: prc.project_kv_and_lr_cache_paged(X, W_rows, x["A_rows"], n_kv, d, 2, N, r, Kp, Vp,
+                                                               Lp, tbl, rope_theta=theta, tok_offset=S))
+        rows = torch.arange(S, s_cap, device=dev)
+        same = torch.equal(Kp[tbl[rows // blk].long(), rows % blk], K[S:])
+        print(json.dumps({"bench": "paged", "stage": "projection", "block_size": blk, "tokens": T,
+                          "ms_paged": round(t_p, 4), "ms_contiguous": round(t_c, 4),
+                          "paged_over_contiguous": round(t_p / t_c, 4), "bitwise_equal": bool(same)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -511,6 +601,9 @@ def main():
     ap.add_argument("--fused-projection", action="store_true",
                     help="instead of the step: the base K/V projection and the LR precompute of a segment as "
                          "one GEMM, against the two as separate calls")
+    ap.add_argument("--paged", action="store_true",
+                    help="instead of the step: decode, prefill and segment projection over paged (block-table) "
+                         "caches, against the same calls over contiguous caches")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -533,6 +626,9 @@ def main():
         return
     if args.fused_projection:
         fused_projection(prc, w, dev, args.steps, args.warmup)
+        return
+    if args.paged:
+        paged(prc, w, dev, args.steps, args.warmup)
         return
     work = algorithmic_work(w)
     print(f"bench: generating inputs ({w['B']} x {w['S']}-token decode caches)", file=sys.stderr, flush=True)

@@ -122,18 +122,52 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // The angle is formed in fp64 revolutions, reduced to [0, 1) in fp64, and only
 // then rounded to fp32 for the hardware sin/cos (which take revolutions).  The
 // fp32 error stays near 1e-7 at every position below 2^31.
-// First element of token t0's row in one request's cache: contiguous
-// (tbl == nullptr: base + t0 * stride) or paged in blocks of blk tokens, the
-// block read from the request's row of the block table and clamped into the
-// pool's nblk blocks.  t0 is wave-uniform, so the entry is a scalar load.
-__device__ __forceinline__ const uint16_t* cache_row(const uint16_t* base, const int32_t* tbl, int blk, int nblk,
-                                                     int64_t t0, int64_t stride) {
-  if (tbl == nullptr) return base + t0 * stride;
-  const int64_t q = t0 / blk;
-  int32_t e = tbl[q];
-  e = e < 0 ? 0 : (e >= nblk ? nblk - 1 : e);
-  return base + ((int64_t)e * blk + (t0 - q * blk)) * stride;
-}
+// Walks one request's rows of the block tables of paged caches in token
+// order, one tile of `step` tokens at a time (step divides the block size,
+// so no tile straddles two blocks).  A block's table entries are fetched
+// once, with vector loads, when the walk enters the block -- a tile before
+// they are used: scalar loads share their wait counter with LDS traffic, so
+// every LDS wait in between would wait on them.  Entries are clamped into
+// the pools, and table indexes past the row read as 0.  All state is
+// wave-uniform except the fetched entries.
+struct PageWalk {
+  __amdgpu_buffer_rsrc_t kvt, lrt;
+  int blk, kv_nblk, lr_nblk;
+  int q, rem;         // block of the next tile and its first row there
+  int32_t ekv, elr;   // table entries of block q
+
+  __device__ __forceinline__ void fetch() {
+    ekv = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(kvt, q * 4, 0, 0);
+    elr = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(lrt, q * 4, 0, 0);
+  }
+  // Start at token t_first (a multiple of step); t_end bounds the walk.
+  __device__ __forceinline__ void start(const int32_t* kv_tbl, const int32_t* lr_tbl, int max_blk, int blk_,
+                                        int kvn, int lrn, int64_t t_first, int64_t t_end) {
+    kvt = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(kv_tbl), (short)0, max_blk * 4, 0x00020000);
+    lrt = __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(lr_tbl), (short)0, max_blk * 4, 0x00020000);
+    blk = blk_;
+    kv_nblk = kvn;
+    lr_nblk = lrn;
+    q = (int)(t_first / blk_);
+    rem = (int)(t_first - (int64_t)q * blk_);
+    ekv = elr = 0;
+    if (t_first < t_end) fetch();
+  }
+  // Pool rows (base, LR) of the next tile's first token; then step on.
+  __device__ __forceinline__ void next(int step, int64_t t_end, int64_t& kv_row, int64_t& lr_row) {
+    int32_t ek = __builtin_amdgcn_readfirstlane(ekv), el = __builtin_amdgcn_readfirstlane(elr);
+    ek = ek < 0 ? 0 : (ek >= kv_nblk ? kv_nblk - 1 : ek);
+    el = el < 0 ? 0 : (el >= lr_nblk ? lr_nblk - 1 : el);
+    kv_row = (int64_t)ek * blk + rem;
+    lr_row = (int64_t)el * blk + rem;
+    rem += step;
+    if (rem == blk) {
+      rem = 0;
+      ++q;
+      if ((int64_t)q * blk < t_end) fetch();
+    }
+  }
+};
 
 __device__ __forceinline__ void rope_cs(int pos, double w2pi, float& c, float& s) {
   double rev = (double)pos * w2pi;

@@ -120,21 +120,18 @@ __device__ __forceinline__ StageOffsets<D, R> stage_offsets(int64_t row, int lan
 template <int D, int R>
 __device__ __forceinline__ void stage_load(Stage<D, R>& s, const StageOffsets<D, R>& o, const uint16_t* Kb,
                                            const uint16_t* Vb, const uint16_t* Lk, const uint16_t* Lv,
-                                           const int32_t* kvt, const int32_t* lrt, int blk, int kvn, int lrn,
-                                           int64_t row, int64_t t0, int64_t t_end) {
+                                           int64_t kv_row, int64_t lr_row, int64_t row, int64_t t0,
+                                           int64_t t_end) {
   using C = Dec<D, R>;
   // Valid tokens of the sub-block (none past the end: every load reads zeros).
   const int64_t n = t_end - t0 < 0 ? 0 : (t_end - t0 < 16 ? t_end - t0 : 16);
   const int32_t kv_bytes = n > 0 ? (int32_t)((n - 1) * row * 2 + D * 2) : 0;
-  // A sub-block with no valid token reads nothing (and no block table entry:
-  // t0 may lie past the request's last block).
-  const auto rk = make_rsrc(n > 0 ? cache_row(Kb, kvt, blk, kvn, t0, row) : Kb, kv_bytes);
-  const auto rv = make_rsrc(n > 0 ? cache_row(Vb, kvt, blk, kvn, t0, row) : Vb, kv_bytes);
+  // kv_row / lr_row: cache rows of token t0 (t0 itself unless paged).
+  const auto rk = make_rsrc(Kb + kv_row * row, kv_bytes);
+  const auto rv = make_rsrc(Vb + kv_row * row, kv_bytes);
   // Absent LR caches get empty resources (loads read zeros, touch nothing).
-  const auto rlk = make_rsrc(Lk != nullptr && n > 0 ? cache_row(Lk, lrt, blk, lrn, t0, R) : Kb,
-                             Lk != nullptr ? (int32_t)(n * R * 2) : 0);
-  const auto rlv = make_rsrc(Lv != nullptr && n > 0 ? cache_row(Lv, lrt, blk, lrn, t0, R) : Kb,
-                             Lv != nullptr ? (int32_t)(n * R * 2) : 0);
+  const auto rlk = make_rsrc(Lk != nullptr ? Lk + lr_row * R : Kb, Lk != nullptr ? (int32_t)(n * R * 2) : 0);
+  const auto rlv = make_rsrc(Lv != nullptr ? Lv + lr_row * R : Kb, Lv != nullptr ? (int32_t)(n * R * 2) : 0);
 #pragma unroll
   for (int kk = 0; kk < C::NCH; ++kk)
     s.kb[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, o.kb[kk], 0, 0));
@@ -148,7 +145,9 @@ __device__ __forceinline__ void stage_load(Stage<D, R>& s, const StageOffsets<D,
     s.v[iv] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, o.v[iv], 0, 0));
 }
 
-template <int D, int R>
+// PAGED: the caches are pools reached through block tables (a separate
+// instantiation, so the contiguous kernel carries none of the walk's state).
+template <int D, int R, bool PAGED>
 __global__ void __launch_bounds__(dec_waves(R) * 64, dec_waves(R) / 4)
 lrsa_decode_kernel(const AttnArgs a) {
   using C = Dec<D, R>;
@@ -206,8 +205,6 @@ lrsa_decode_kernel(const AttnArgs a) {
   const int64_t row = (int64_t)a.n_kv * D;  // elements between tokens
   // This request's caches (or pools, paged through its rows of the block
   // tables).
-  const int32_t* kvt = a.kv_tbl != nullptr ? a.kv_tbl + (int64_t)b * a.max_blk : nullptr;
-  const int32_t* lrt = a.lr_tbl != nullptr ? a.lr_tbl + (int64_t)b * a.max_blk : nullptr;
   const uint16_t* Kb = a.Kb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Lk = has_lk ? a.Lk + (int64_t)b * a.l_stride : nullptr;
@@ -243,7 +240,17 @@ lrsa_decode_kernel(const AttnArgs a) {
 
   const StageOffsets<D, R> so = stage_offsets<D, R>(row, lane);
   Stage<D, R> st[2];
-  stage_load<D, R>(st[0], so, Kb, Vb, Lk, Lv, kvt, lrt, a.blk, a.kv_nblk, a.lr_nblk, row, t_begin, t_end_w);
+  // Sub-blocks are loaded in token order, so paged caches are walked with them.
+  PageWalk walk;
+  if constexpr (PAGED)
+    walk.start(a.kv_tbl + (int64_t)b * a.max_blk, a.lr_tbl + (int64_t)b * a.max_blk, a.max_blk, a.blk, a.kv_nblk,
+               a.lr_nblk, t_begin, t_end_w);
+  auto load = [&](Stage<D, R>& s, int64_t t) {
+    int64_t kr = t, lr = t;
+    if constexpr (PAGED) walk.next(16, t_end_w, kr, lr);
+    stage_load<D, R>(s, so, Kb, Vb, Lk, Lv, kr, lr, row, t, t_end_w);
+  };
+  load(st[0], t_begin);
 
   __syncthreads();  // base angles of the first tile, zeroed L_v tiles
 
@@ -277,7 +284,7 @@ lrsa_decode_kernel(const AttnArgs a) {
       if (ts >= t_end) break;
       // Issue the next sub-block's loads before consuming this one (past the
       // split end they read zeros and touch no memory).
-      stage_load<D, R>(nxt, so, Kb, Vb, Lk, Lv, kvt, lrt, a.blk, a.kv_nblk, a.lr_nblk, row, ts + 16, t_end_w);
+      load(nxt, ts + 16);
 
       // ---- V and L_v rows into the wave's LDS tile ------------------------
 #pragma unroll
@@ -780,7 +787,11 @@ template <int D, int R>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   using C = Dec<D, R>;
   const int hg = (a.n_kv + C::NW - 1) / C::NW;
-  hipLaunchKernelGGL((lrsa_decode_kernel<D, R>), dim3(a.n_splits, hg, a.batch), dim3(C::NT), 0, st, a);
+  const dim3 grid(a.n_splits, hg, a.batch);
+  if (a.kv_tbl != nullptr)
+    hipLaunchKernelGGL((lrsa_decode_kernel<D, R, true>), grid, dim3(C::NT), 0, st, a);
+  else
+    hipLaunchKernelGGL((lrsa_decode_kernel<D, R, false>), grid, dim3(C::NT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch), dim3(64 * MW), 0, st, a);

@@ -134,7 +134,9 @@ struct Unit {
   u32x4 lv[Pre<D, R>::NLP];       // L_v half blocks (32 tokens x 16 ranks, A layout)
 };
 
-template <int D, int R, bool LK, bool LV>
+// PAGED: the caches are pools reached through block tables (a separate
+// instantiation, so the contiguous kernel carries none of the walk's state).
+template <int D, int R, bool LK, bool LV, bool PAGED>
 __global__ void __launch_bounds__(NTHR)
 lrsa_prefill_kernel(const AttnArgs a) {
   using C = Pre<D, R>;
@@ -189,8 +191,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int64_t row_el = (int64_t)a.n_kv * D;
   // This request's caches (or pools, paged through its rows of the block
   // tables).
-  const int32_t* kvt = a.kv_tbl != nullptr ? a.kv_tbl + (int64_t)b * a.max_blk : nullptr;
-  const int32_t* lrt = a.lr_tbl != nullptr ? a.lr_tbl + (int64_t)b * a.max_blk : nullptr;
+  PageWalk walk;
+  if constexpr (PAGED)
+    walk.start(a.kv_tbl + (int64_t)b * a.max_blk, a.lr_tbl + (int64_t)b * a.max_blk, a.max_blk, a.blk, a.kv_nblk,
+               a.lr_nblk, 0, kv_hi);
   const uint16_t* Kb = a.Kb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Lk = LK ? a.Lk + (int64_t)b * a.l_stride : nullptr;
@@ -278,11 +282,14 @@ lrsa_prefill_kernel(const AttnArgs a) {
     const int r0 = 32 * lrb + 16 * p + (lane >> 5) * 8;
     offlv[p] = r0 < R ? (32 * ltb + (lane & 31)) * R * 2 + r0 * 2 : INT32_MIN;
   }
+  // Tiles are loaded in token order, so paged caches are walked with them.
   auto load_unit = [&](Unit<D, R>& u, int64_t t0) {
     const int rows = (int)(kv_hi - t0 < TKV ? kv_hi - t0 : TKV);  // valid rows of this tile (> 0)
     const int32_t kv_bytes = (rows - 1) * (int32_t)(row_el * 2) + D * 2;
-    const auto rk = make_rsrc(cache_row(Kb, kvt, a.blk, a.kv_nblk, t0, row_el), kv_bytes);
-    const auto rv = make_rsrc(cache_row(Vb, kvt, a.blk, a.kv_nblk, t0, row_el), kv_bytes);
+    int64_t kr = t0, lr = t0;  // cache rows of the tile's first token
+    if constexpr (PAGED) walk.next(TKV, kv_hi, kr, lr);
+    const auto rk = make_rsrc(Kb + kr * row_el, kv_bytes);
+    const auto rv = make_rsrc(Vb + kr * row_el, kv_bytes);
     if constexpr (C::SEG == 8) {
       const u32x4 lo = buf_ld16(rk, offk), hi = buf_ld16(rk, offk + C::HALF * 2);
 #pragma unroll
@@ -299,14 +306,14 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
     }
     if constexpr (LK) {
-      const auto rl = make_rsrc(cache_row(Lk, lrt, a.blk, a.lr_nblk, t0, R), rows * R * 2);
+      const auto rl = make_rsrc(Lk + lr * R, rows * R * 2);
 #pragma unroll
       for (int rc = 0; rc < C::RC; ++rc) u.lk[rc] = rc * 16 + q * 4 < R ? buf_ld8(rl, offlk + rc * 32) : u32x2{0u, 0u};
     }
 #pragma unroll
     for (int hb = 0; hb < C::NHB; ++hb) u.v[hb] = buf_ld16(rv, offv[hb]);
     if constexpr (LV) {
-      const auto rl = make_rsrc(cache_row(Lv, lrt, a.blk, a.lr_nblk, t0, R), rows * R * 2);
+      const auto rl = make_rsrc(Lv + lr * R, rows * R * 2);
 #pragma unroll
       for (int p = 0; p < C::NLP; ++p) u.lv[p] = lv_wave ? buf_ld16(rl, offlv[p]) : u32x4{0u, 0u, 0u, 0u};
     }
@@ -650,7 +657,11 @@ template <int D, int R, bool LK, bool LV>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const int n_rows = a.n_tok * a.group;
   const int tiles = (n_rows + BROWS - 1) / BROWS;
-  hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV>), dim3(tiles, a.n_kv, a.batch), dim3(NTHR), 0, st, a);
+  const dim3 grid(tiles, a.n_kv, a.batch);
+  if (a.kv_tbl != nullptr)
+    hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, true>), grid, dim3(NTHR), 0, st, a);
+  else
+    hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, false>), grid, dim3(NTHR), 0, st, a);
   return hipGetLastError();
 }
 

@@ -167,6 +167,22 @@ __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const Prec
   // k = (l / 32) * 8 + 0..7.
   const int l32 = lane & 31, h = lane >> 5;
   const int ra_row0 = (TB / 2) * (w & 1) + l32, rx_row0 = (TB / 2) * (w >> 1) + l32;
+  // Cache row of each of the lane's tokens: its position tok_offset + t, or
+  // its row in the paged pools.  The table is read here, so that its latency
+  // hides behind the first stage's loads.
+  int64_t srow[QB];
+#pragma unroll
+  for (int bt = 0; bt < QB; ++bt) {
+    const int64_t t = tok0 + (TB / 2) * (w >> 1) + 32 * bt + l32;
+    const int p = (int)(a.tok_offset + t);  // positions stay below 2^31
+    srow[bt] = p;
+    if (a.tbl != nullptr && t < a.T) {
+      const int q = p / a.blk;
+      int32_t e = a.tbl[q];
+      e = e < 0 ? 0 : (e >= a.nblk ? a.nblk - 1 : e);
+      srow[bt] = (int64_t)e * a.blk + (p - q * a.blk);
+    }
+  }
   f32x16 acc[QB][QB];
 #pragma unroll
   for (int bc = 0; bc < QB; ++bc)
@@ -202,14 +218,7 @@ __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const Prec
     const int64_t t = tok0 + (TB / 2) * (w >> 1) + 32 * bt + l32;
     if (t >= a.T) continue;
     const int64_t trow = a.tok_offset + t;  // absolute position of the token
-    // Its cache row: the position itself, or its row in the paged pools.
-    int64_t srow = trow;
-    if (a.tbl != nullptr) {
-      const int64_t q = trow / a.blk;
-      int32_t e = a.tbl[q];
-      e = e < 0 ? 0 : (e >= a.nblk ? a.nblk - 1 : e);
-      srow = (int64_t)e * a.blk + (trow - q * a.blk);
-    }
+    const int64_t row = srow[bt];           // its cache row
 #pragma unroll
     for (int bc = 0; bc < QB; ++bc) {
       const f32x16& r = acc[bc][bt];
@@ -231,7 +240,7 @@ __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const Prec
             lo[i] = x * cs - y * sn;
             hi[i] = y * cs + x * sn;
           }
-          uint16_t* kp = a.Kout + srow * a.nkv + hd * a.head_dim + j0;
+          uint16_t* kp = a.Kout + row * a.nkv + hd * a.head_dim + j0;
           *reinterpret_cast<u32x2*>(kp) = u32x2{pack_bf16(lo[0], lo[1]), pack_bf16(lo[2], lo[3])};
           *reinterpret_cast<u32x2*>(kp + a.head_dim / 2) = u32x2{pack_bf16(hi[0], hi[1]), pack_bf16(hi[2], hi[3])};
         }
@@ -244,12 +253,12 @@ __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const Prec
         o[0] = pack_bf16(r[4 * jg + 0], r[4 * jg + 1]);
         o[1] = pack_bf16(r[4 * jg + 2], r[4 * jg + 3]);
         if (region == 1) {
-          *reinterpret_cast<u32x2*>(a.Vout + srow * a.nkv + (c - a.nkv)) = o;
+          *reinterpret_cast<u32x2*>(a.Vout + row * a.nkv + (c - a.nkv)) = o;
         } else {
           const int lc = c - 2 * a.nkv;
           if (lc >= a.n_cols) continue;
           const int plane = lc / a.rank, jr = lc - plane * a.rank;
-          *reinterpret_cast<u32x2*>(a.L + ((int64_t)plane * a.s_cap + srow) * a.rank + jr) = o;
+          *reinterpret_cast<u32x2*>(a.L + ((int64_t)plane * a.s_cap + row) * a.rank + jr) = o;
         }
       }
     }
