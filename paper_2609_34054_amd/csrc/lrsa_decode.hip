@@ -19,8 +19,9 @@
 // q = l/16):
 //   1. scores S^T = K Q^T on 16x16x32 MFMAs in two parts: the raw bf16
 //      K_base rows (no rounding) plus bf16(RoPE(E)), where E^T = B_k^T L_k^T
-//      comes from 16x16x16 MFMAs whose result layout holds both halves of
-//      every RoPE pair in one lane;
+//      comes from 16x16 MFMAs (16x16x32 over 32-rank chunks for ranks 32 and
+//      64, 16x16x16 below) whose result layout holds both halves of every
+//      RoPE pair in one lane;
 //   2. online softmax per head (lane l%16), exp2 domain;
 //   3. O^T += V^T P^T and (P L_v)^T += L_v^T P^T on 16x16x16 MFMAs.  V and
 //      L_v rows pass through a wave-private LDS tile and come back through
@@ -77,10 +78,10 @@ __device__ __forceinline__ i16x4 lds_read_tr(const uint16_t* p) {
 
 template <int D, int R>
 struct Stage {
-  u32x4 kb[D / 32];               // K_base chunks of token l%16
-  u32x2 lk[RCH(R)];               // L_k row fragment of token l%16
-  u32x4 v[Dec<D, R>::NVL];        // V rows, natural layout
-  u32x2 lv[RCH(R)];               // L_v row fragment of token l%16
+  u32x4 kb[D / 32];                         // K_base chunks of token l%16
+  typename Ex<R>::Frag lk[Ex<R>::NC];       // L_k row fragments of token l%16 (expansion B operand)
+  u32x4 v[Dec<D, R>::NVL];                  // V rows, natural layout
+  u32x2 lv[RCH(R)];                         // L_v row fragment of token l%16
 };
 
 // Buffer resource over `bytes` bytes from `base` (raw, stride 0): loads at
@@ -96,7 +97,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base
 // loads in flight while the current one is consumed.
 template <int D, int R>
 struct StageOffsets {
-  int32_t kb[D / 32], lr[RCH(R)], v[Dec<D, R>::NVL];
+  int32_t kb[D / 32], lk[Ex<R>::NC], lr[RCH(R)], v[Dec<D, R>::NVL];
 };
 
 template <int D, int R>
@@ -111,10 +112,24 @@ __device__ __forceinline__ StageOffsets<D, R> stage_offsets(int64_t row, int lan
     const int r0 = rc * 16 + q * 4;
     o.lr[rc] = r0 < R ? c16 * R * 2 + r0 * 2 : INT32_MIN;  // ranks past r read as zeros
   }
+#pragma unroll
+  for (int c = 0; c < Ex<R>::NC; ++c) {
+    const int r0 = Ex<R>::rank0(c, q);
+    o.lk[c] = r0 < R ? c16 * R * 2 + r0 * 2 : INT32_MIN;
+  }
   const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
 #pragma unroll
   for (int iv = 0; iv < C::NVL; ++iv) o.v[iv] = (vrow + C::RPL * iv) * (int32_t)(row * 2) + vdim * 2;
   return o;
+}
+
+// One expansion fragment of an LR row through a buffer resource.
+template <int R>
+__device__ __forceinline__ typename Ex<R>::Frag lr_frag_load(__amdgpu_buffer_rsrc_t r, int32_t off) {
+  if constexpr (Ex<R>::WIDE)
+    return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  else
+    return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
 
 template <int D, int R>
@@ -136,10 +151,10 @@ __device__ __forceinline__ void stage_load(Stage<D, R>& s, const StageOffsets<D,
   for (int kk = 0; kk < C::NCH; ++kk)
     s.kb[kk] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, o.kb[kk], 0, 0));
 #pragma unroll
-  for (int rc = 0; rc < C::RC; ++rc) {
-    s.lk[rc] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rlk, o.lr[rc], 0, 0));
+  for (int c = 0; c < Ex<R>::NC; ++c) s.lk[c] = lr_frag_load<R>(rlk, o.lk[c]);
+#pragma unroll
+  for (int rc = 0; rc < C::RC; ++rc)
     s.lv[rc] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rlv, o.lr[rc], 0, 0));
-  }
 #pragma unroll
   for (int iv = 0; iv < C::NVL; ++iv)
     s.v[iv] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, o.v[iv], 0, 0));
@@ -219,7 +234,7 @@ lrsa_decode_kernel(const AttnArgs a) {
 #pragma unroll
     for (int kk = 0; kk < C::NCH; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
   }
-  i16x4 bkf[C::NBLK][C::RC];
+  typename Ex<R>::Frag bkf[C::NBLK][Ex<R>::NC];
   load_bt_frags<D, R>(bkf, has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr,
                       has_lk && active, lane);
 
@@ -307,9 +322,9 @@ lrsa_decode_kernel(const AttnArgs a) {
         for (int blk = 0; blk < C::NB; ++blk) {
           f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-          for (int rc = 0; rc < C::RC; ++rc) {
-            elo = mfma16x16x16(bkf[blk][rc], as_i16x4(cur.lk[rc]), elo);
-            ehi = mfma16x16x16(bkf[blk + C::NB][rc], as_i16x4(cur.lk[rc]), ehi);
+          for (int c = 0; c < Ex<R>::NC; ++c) {
+            elo = Ex<R>::mma(bkf[blk][c], cur.lk[c], elo);
+            ehi = Ex<R>::mma(bkf[blk + C::NB][c], cur.lk[c], ehi);
           }
           float rlo[4], rhi[4];
 #pragma unroll
@@ -605,23 +620,29 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
   // This wave's LR rows of a sub-block (rank chunks of token l%16), zero past
   // its end.
   struct LrStage {
-    u32x2 lk[C::RC], lv[C::RC];
+    typename Ex<R>::Frag lk[Ex<R>::NC];
+    u32x2 lv[C::RC];
   };
-  int32_t lroff[C::RC];
+  int32_t lroff[C::RC], lkoff[Ex<R>::NC];
 #pragma unroll
   for (int rc = 0; rc < C::RC; ++rc) {
     const int r0 = rc * 16 + q * 4;
     lroff[rc] = r0 < R ? c16 * R * 2 + r0 * 2 : INT32_MIN;
+  }
+#pragma unroll
+  for (int c = 0; c < Ex<R>::NC; ++c) {
+    const int r0 = Ex<R>::rank0(c, q);
+    lkoff[c] = r0 < R ? c16 * R * 2 + r0 * 2 : INT32_MIN;
   }
   auto lr_load = [&](LrStage& s, int64_t t0) {
     const int64_t n = t_end - t0 < 0 ? 0 : (t_end - t0 < SB ? t_end - t0 : SB);
     const auto rlk = make_rsrc(Lk != nullptr ? Lk + t0 * R : Kb, Lk != nullptr ? (int32_t)(n * R * 2) : 0);
     const auto rlv = make_rsrc(Lv != nullptr ? Lv + t0 * R : Kb, Lv != nullptr ? (int32_t)(n * R * 2) : 0);
 #pragma unroll
-    for (int rc = 0; rc < C::RC; ++rc) {
-      s.lk[rc] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rlk, lroff[rc], 0, 0));
+    for (int c = 0; c < Ex<R>::NC; ++c) s.lk[c] = lr_frag_load<R>(rlk, lkoff[c]);
+#pragma unroll
+    for (int rc = 0; rc < C::RC; ++rc)
       s.lv[rc] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rlv, lroff[rc], 0, 0));
-    }
   };
 
   bf16x8 qf[C::NCH];
@@ -631,7 +652,7 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
 #pragma unroll
     for (int kk = 0; kk < C::NCH; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
   }
-  i16x4 bkf[C::NBLK][C::RC];
+  typename Ex<R>::Frag bkf[C::NBLK][Ex<R>::NC];
   load_bt_frags<D, R>(bkf, has_lk && active ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr,
                       has_lk && active, lane);
 
@@ -701,9 +722,9 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
           for (int blk = 0; blk < C::NB; ++blk) {
             f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int rc = 0; rc < C::RC; ++rc) {
-              elo = mfma16x16x16(bkf[blk][rc], as_i16x4(cur.lk[rc]), elo);
-              ehi = mfma16x16x16(bkf[blk + C::NB][rc], as_i16x4(cur.lk[rc]), ehi);
+            for (int c = 0; c < Ex<R>::NC; ++c) {
+              elo = Ex<R>::mma(bkf[blk][c], cur.lk[c], elo);
+              ehi = Ex<R>::mma(bkf[blk + C::NB][c], cur.lk[c], ehi);
             }
             float rlo[4], rhi[4];
 #pragma unroll

@@ -12,7 +12,7 @@
 // A query row is a (token, q head of the GQA group) pair, so the group's heads
 // share every rebuilt tile.  Every wave both builds and attends:
 //   build   wave w rebuilds 16 tokens (w % 4) x half of the RoPE pair blocks
-//           (w / 4) of the next KV tile: E^T = B_k^T L_k^T on 16x16x16 MFMAs
+//           (w / 4) of the next KV tile: E^T = B_k^T L_k^T on 16x16 MFMAs
 //           (lane l: token l%16, both halves of each pair in the same lane),
 //           RoPE by angle addition (exact per-tile base angle in LDS, exact
 //           per-lane offsets), + base, bf16 into LDS.  It also transposes a
@@ -59,7 +59,8 @@ struct Pre {
   static constexpr int NBW = NB / 2;         // low blocks rebuilt per wave
   static constexpr int SEG = 4 * NBW;        // contiguous dims per lane and half
   static constexpr int QPG = D / 8;          // dims per lane group per half
-  static constexpr int RC = RCH(R);          // 16-wide rank chunks
+  static constexpr int RC = RCH(R);          // 16-wide rank chunks (value side)
+  static constexpr int NC = Ex<R>::NC;       // rank chunks of the key expansion
   static constexpr int RB = (R + 31) / 32;   // 32-row blocks of (P L_v)^T
   static constexpr int NKQ = D / 16;         // 32x32x16 k-chunks over d
   static constexpr int NDB = D / 32;         // 32-dim blocks of O^T
@@ -121,15 +122,12 @@ __device__ __forceinline__ u32x4 buf_ld16(__amdgpu_buffer_rsrc_t r, int32_t off)
 __device__ __forceinline__ u32x2 buf_ld8(__amdgpu_buffer_rsrc_t r, int32_t off) {
   return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
-__device__ __forceinline__ uint32_t buf_ld4(__amdgpu_buffer_rsrc_t r, int32_t off) {
-  return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
-}
 
 // Global data one wave stages for one KV tile.
 template <int D, int R>
 struct Unit {
   Seg<Pre<D, R>::SEG> klo, khi;   // K_base of the lane's rebuild token, both halves
-  u32x2 lk[RCH(R)];               // L_k row of that token (expansion B operand)
+  typename Ex<R>::Frag lk[Ex<R>::NC];  // L_k row of that token (expansion B operand)
   u32x4 v[Pre<D, R>::NHB];        // V_base half blocks (32 tokens x 16 dims, A layout)
   u32x4 lv[Pre<D, R>::NLP];       // L_v half blocks (32 tokens x 16 ranks, A layout)
 };
@@ -149,9 +147,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // [wave][pair of frequencies][lane] (one 16-byte read per pair).
   __shared__ __attribute__((aligned(16))) f32x4 off_cs[LK ? NW : 1][C::SEG / 2][64];
   // B_k^T fragments of this KV head for ranks > 16, [RoPE half ph][block i]
-  // [lane][rank chunk]: each lane's RC fragments are contiguous, so a block's
-  // set comes in RC / 2 16-byte reads.
-  __shared__ __attribute__((aligned(16))) u32x2 bk_lds[LK && !C::BK_REG ? 2 * 2 * C::NBW * 64 * C::RC : 2];
+  // [lane][rank chunk]: each lane's NC 16-byte fragments are contiguous.
+  __shared__ __attribute__((aligned(16))) u32x4 bk_lds[LK && !C::BK_REG ? 2 * 2 * C::NBW * 64 * C::NC : 1];
   __shared__ int s_maxpos;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -163,12 +160,13 @@ lrsa_prefill_kernel(const AttnArgs a) {
   if (tid == 0) s_maxpos = -1;
   if constexpr (LK && !C::BK_REG) {
     const uint16_t* bh = a.Bk + (int64_t)blockIdx.z * a.b_stride + (int64_t)blockIdx.y * D * R;
-    for (int e = tid; e < 2 * 2 * C::NBW * 64 * C::RC; e += NTHR) {
-      const int rc = e % C::RC, l = (e / C::RC) % 64, i = (e / (C::RC * 64)) % (2 * C::NBW);
-      const int phe = e / (C::RC * 64 * 2 * C::NBW);
+    for (int e = tid; e < 2 * 2 * C::NBW * 64 * C::NC; e += NTHR) {
+      const int c = e % C::NC, l = (e / C::NC) % 64, i = (e / (C::NC * 64)) % (2 * C::NBW);
+      const int phe = e / (C::NC * 64 * 2 * C::NBW);
       const int blk = phe * C::NBW + (i % C::NBW) + (i / C::NBW) * C::NB;
-      const int r0 = rc * 16 + (l >> 4) * 4;
-      bk_lds[e] = r0 < R ? *reinterpret_cast<const u32x2*>(bh + blk_dim<D>(blk, l & 15) * R + r0) : u32x2{0u, 0u};
+      // Ranks > 16 use 32-wide chunks: 8 ranks per lane, one 16-byte fragment.
+      const int r0 = Ex<R>::rank0(c, l >> 4);
+      bk_lds[e] = r0 < R ? *reinterpret_cast<const u32x4*>(bh + blk_dim<D>(blk, l & 15) * R + r0) : u32x4{0u, 0u, 0u, 0u};
     }
   }
   int64_t kvl = a.kv_len[b];
@@ -228,34 +226,28 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // B_k^T fragment (16x16x16 A operand) of low block i (i < NBW) or of its
   // RoPE partner (i >= NBW), rank chunk rc: lane = dim row, 4 ranks from q*4.
   const uint16_t* bhead = LK ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr;
-  auto bk_frag_at = [&](const uint16_t* base, int i, int rc) -> u32x2 {
-    const int blk = blk0 + (i % C::NBW) + (i / C::NBW) * C::NB;
-    const int r0 = rc * 16 + q * 4;
-    return *reinterpret_cast<const u32x2*>(base + blk_dim<D>(blk, c16) * R + (r0 < R ? r0 : 0));
-  };
-  u32x2 bkr[C::BK_REG && LK ? 2 * C::NBW : 1][C::RC];
+  using Frag = typename Ex<R>::Frag;
+  Frag bkr[C::BK_REG && LK ? 2 * C::NBW : 1][C::NC];
   if constexpr (C::BK_REG && LK) {
 #pragma unroll
-    for (int i = 0; i < 2 * C::NBW; ++i)
+    for (int i = 0; i < 2 * C::NBW; ++i) {
+      const int blk = blk0 + (i % C::NBW) + (i / C::NBW) * C::NB;
 #pragma unroll
-      for (int rc = 0; rc < C::RC; ++rc) {
-        const u32x2 v = bk_frag_at(bhead, i, rc);
-        bkr[i][rc] = rc * 16 + q * 4 < R ? v : u32x2{0u, 0u};
+      for (int c = 0; c < C::NC; ++c) {
+        const int r0 = Ex<R>::rank0(c, q);
+        bkr[i][c] = Ex<R>::load(bhead + blk_dim<D>(blk, c16) * R + r0, r0 < R);
       }
+    }
   }
-  // The RC fragments of block set i (registers, or 16-byte LDS reads).
-  auto bk_set = [&](int i, u32x2 (&f)[C::RC]) {
+  // The NC fragments of block set i (registers, or 16-byte LDS reads).
+  auto bk_set = [&](int i, Frag (&f)[C::NC]) {
     if constexpr (C::BK_REG) {
 #pragma unroll
-      for (int rc = 0; rc < C::RC; ++rc) f[rc] = bkr[i][rc];
+      for (int c = 0; c < C::NC; ++c) f[c] = bkr[i][c];
     } else {
-      const u32x4* p = reinterpret_cast<const u32x4*>(bk_lds + ((ph * 2 * C::NBW + i) * 64 + lane) * C::RC);
+      const u32x4* p = bk_lds + ((ph * 2 * C::NBW + i) * 64 + lane) * C::NC;
 #pragma unroll
-      for (int j = 0; j < C::RC / 2; ++j) {
-        const u32x4 v = p[j];
-        f[2 * j] = u32x2{v[0], v[1]};
-        f[2 * j + 1] = u32x2{v[2], v[3]};
-      }
+      for (int c = 0; c < C::NC; ++c) f[c] = p[c];
     }
   };
   if constexpr (LK) {
@@ -271,7 +263,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // tile itself is addressed by buffer resources built per tile, whose
   // range check returns zeros for rows at or beyond kv_hi.
   const int32_t offk = delta * (int32_t)(row_el * 2) + lo_dim0 * 2;
-  const int32_t offlk = delta * R * 2 + q * 8;
+  const int32_t offlk = delta * R * 2 + Ex<R>::rank0(0, q) * 2;
   int32_t offv[C::NHB];
 #pragma unroll
   for (int hb = 0; hb < C::NHB; ++hb)
@@ -308,7 +300,12 @@ lrsa_prefill_kernel(const AttnArgs a) {
     if constexpr (LK) {
       const auto rl = make_rsrc(Lk + lr * R, rows * R * 2);
 #pragma unroll
-      for (int rc = 0; rc < C::RC; ++rc) u.lk[rc] = rc * 16 + q * 4 < R ? buf_ld8(rl, offlk + rc * 32) : u32x2{0u, 0u};
+      for (int c = 0; c < C::NC; ++c) {
+        if constexpr (Ex<R>::WIDE)
+          u.lk[c] = buf_ld16(rl, offlk + c * 64);
+        else
+          u.lk[c] = Ex<R>::rank0(c, q) < R ? buf_ld8(rl, offlk) : u32x2{0u, 0u};
+      }
     }
 #pragma unroll
     for (int hb = 0; hb < C::NHB; ++hb) u.v[hb] = buf_ld16(rv, offv[hb]);
@@ -324,13 +321,13 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < C::NBW; ++i) {
         f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
-        u32x2 fl[C::RC], fh[C::RC];
+        Frag fl[C::NC], fh[C::NC];
         bk_set(i, fl);
         bk_set(C::NBW + i, fh);
 #pragma unroll
-        for (int rc = 0; rc < C::RC; ++rc) {
-          elo = mfma16x16x16(as_i16x4(fl[rc]), as_i16x4(u.lk[rc]), elo);
-          ehi = mfma16x16x16(as_i16x4(fh[rc]), as_i16x4(u.lk[rc]), ehi);
+        for (int c = 0; c < C::NC; ++c) {
+          elo = Ex<R>::mma(fl[c], u.lk[c], elo);
+          ehi = Ex<R>::mma(fh[c], u.lk[c], ehi);
         }
         float vlo[4], vhi[4];
         const f32x4 od0 = off_cs[w][2 * i][lane], od1 = off_cs[w][2 * i + 1][lane];

@@ -56,9 +56,9 @@ materialize_kernel(const AttnArgs a) {
   u32x4 x[D / 32];
   load_chunks<D>(x, a.Kb + in_off, ok, lane);
   if (has_lk) {
-    i16x4 bf[D / 16][RCH(R)];
+    typename Ex<R>::Frag bf[D / 16][Ex<R>::NC];
     load_bt_frags<D, R>(bf, a.Bk + boff, true, lane);
-    u32x2 l[RCH(R)];
+    typename Ex<R>::Frag l[Ex<R>::NC];
     load_lr_frag<R>(l, a.Lk + (int64_t)b * a.l_stride + t * R, ok, lane);
     const float2* csr = cs_lds + c16 * CS_ROW + q * QPG;
     float cc[NB][4], ss[NB][4];
@@ -75,9 +75,9 @@ materialize_kernel(const AttnArgs a) {
 
   load_chunks<D>(x, a.Vb + in_off, ok, lane);
   if (has_lv) {
-    i16x4 bf[D / 16][RCH(R)];
+    typename Ex<R>::Frag bf[D / 16][Ex<R>::NC];
     load_bt_frags<D, R>(bf, a.Bv + boff, true, lane);
-    u32x2 l[RCH(R)];
+    typename Ex<R>::Frag l[Ex<R>::NC];
     load_lr_frag<R>(l, a.Lv + (int64_t)b * a.l_stride + t * R, ok, lane);
     add_expansion<D, R>(x, bf, l);
   }

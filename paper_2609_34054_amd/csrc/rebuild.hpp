@@ -11,19 +11,50 @@
 // These dims are kept as D/32 "chunks" of 8 consecutive bf16 (u32x4):
 // chunk kk starts at chunk_dim(kk, q).
 //
-// The rank-r expansion is E^T = B^T L^T on 16x16x16 MFMAs, one per 16-dim
-// block.  Row m of block blk is head dim blk_dim(blk, m), which makes result
-// row 4q+i of block blk land on element (blk&1)*4+i of chunk blk>>1 -- the
-// chunk layout above.  Blocks blk < D/32 cover the low RoPE half and pair
-// with block blk + D/32.
+// The rank-r expansion is E^T = B^T L^T on 16x16 MFMAs, one 16x16 output per
+// 16-dim block.  Row m of block blk is head dim blk_dim(blk, m), which makes
+// result row 4q+i of block blk land on element (blk&1)*4+i of chunk blk>>1 --
+// the chunk layout above.  Blocks blk < D/32 cover the low RoPE half and
+// pair with block blk + D/32.
 #pragma once
+
+#include <type_traits>
 
 #include "common.hpp"
 
 namespace prc {
 
-// Number of 16-wide rank chunks of the expansion (r = 8 pads to 16).
+// Number of 16-wide rank chunks (r = 8 pads to 16).  The value side's
+// P L_v product is laid out in these.
 constexpr int RCH(int r) { return r < 16 ? 1 : r / 16; }
+
+// Rank chunks of the expansion E^T = B^T L^T.  Ranks 32 and 64 use 32-wide
+// chunks on the full-rate 16x16x32 MFMA (lane l holds ranks c*32 + (l/16)*8
+// .. +7, one 16-byte fragment); ranks 8 and 16 one 16-wide chunk on 16x16x16
+// (ranks (l/16)*4 .. +3; rank 8 pads to 16).  Both give the same 16x16 result
+// layout, so only the operand fragments differ.
+template <int R>
+struct Ex {
+  static constexpr bool WIDE = R >= 32;
+  static constexpr int K = WIDE ? 32 : 16;    // ranks per chunk
+  static constexpr int NC = WIDE ? R / 32 : 1;
+  static constexpr int PER = K / 4;           // ranks per lane and chunk
+  typedef typename std::conditional<WIDE, u32x4, u32x2>::type Frag;
+  static __device__ __forceinline__ int rank0(int c, int q) { return c * K + q * PER; }
+  static __device__ __forceinline__ f32x4 mma(Frag a, Frag b, f32x4 acc) {
+    if constexpr (WIDE)
+      return mfma16x16x32(as_bf16x8(a), as_bf16x8(b), acc);
+    else
+      return mfma16x16x16(as_i16x4(a), as_i16x4(b), acc);
+  }
+  // PER consecutive bf16 at p (zeros when !ok).
+  static __device__ __forceinline__ Frag load(const uint16_t* p, bool ok) {
+    if constexpr (WIDE)
+      return ld16(p, ok);
+    else
+      return ld8(p, ok);
+  }
+};
 
 template <int D, int R>
 struct Rb {
@@ -52,31 +83,33 @@ __device__ __forceinline__ int blk_dim(int blk, int m) {
 // B^T fragments (A operand of the expansion) of one KV head.  `bhead` points
 // at the head's first row of an up-projection stored [n_kv*d, r].
 template <int D, int R>
-__device__ __forceinline__ void load_bt_frags(i16x4 (&f)[D / 16][RCH(R)], const uint16_t* bhead,
+__device__ __forceinline__ void load_bt_frags(typename Ex<R>::Frag (&f)[D / 16][Ex<R>::NC], const uint16_t* bhead,
                                               bool ok, int lane) {
+  using E = Ex<R>;
   const int c16 = lane & 15, q = lane >> 4;
 #pragma unroll
   for (int blk = 0; blk < D / 16; ++blk) {
     const int dim = blk_dim<D>(blk, c16);
 #pragma unroll
-    for (int rc = 0; rc < RCH(R); ++rc) {
-      const int r0 = rc * 16 + q * 4;
+    for (int c = 0; c < E::NC; ++c) {
+      const int r0 = E::rank0(c, q);
       const bool v = ok && r0 < R;
-      f[blk][rc] = as_i16x4(ld8(v ? bhead + (int64_t)dim * R + r0 : nullptr, v));
+      f[blk][c] = E::load(v ? bhead + (int64_t)dim * R + r0 : nullptr, v);
     }
   }
 }
 
 // One LR row as the B operand of the expansion (k = rank index).
 template <int R>
-__device__ __forceinline__ void load_lr_frag(u32x2 (&l)[RCH(R)], const uint16_t* lrow, bool ok,
+__device__ __forceinline__ void load_lr_frag(typename Ex<R>::Frag (&l)[Ex<R>::NC], const uint16_t* lrow, bool ok,
                                              int lane) {
+  using E = Ex<R>;
   const int q = lane >> 4;
 #pragma unroll
-  for (int rc = 0; rc < RCH(R); ++rc) {
-    const int r0 = rc * 16 + q * 4;
+  for (int c = 0; c < E::NC; ++c) {
+    const int r0 = E::rank0(c, q);
     const bool v = ok && r0 < R;
-    l[rc] = ld8(v ? lrow + r0 : nullptr, v);
+    l[c] = E::load(v ? lrow + r0 : nullptr, v);
   }
 }
 
@@ -102,13 +135,13 @@ __device__ __forceinline__ float chunk_get(const u32x4& c, int el) {
 
 // x += L B (value side), rounded back to bf16.
 template <int D, int R>
-__device__ __forceinline__ void add_expansion(u32x4 (&x)[D / 32], const i16x4 (&bf)[D / 16][RCH(R)],
-                                              const u32x2 (&l)[RCH(R)]) {
+__device__ __forceinline__ void add_expansion(u32x4 (&x)[D / 32], const typename Ex<R>::Frag (&bf)[D / 16][Ex<R>::NC],
+                                              const typename Ex<R>::Frag (&l)[Ex<R>::NC]) {
 #pragma unroll
   for (int blk = 0; blk < D / 16; ++blk) {
     f32x4 e = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int rc = 0; rc < RCH(R); ++rc) e = mfma16x16x16(bf[blk][rc], as_i16x4(l[rc]), e);
+    for (int c = 0; c < Ex<R>::NC; ++c) e = Ex<R>::mma(bf[blk][c], l[c], e);
     const int kk = blk >> 1, w0 = (blk & 1) * 2;
     float v[4];
 #pragma unroll
@@ -121,17 +154,18 @@ __device__ __forceinline__ void add_expansion(u32x4 (&x)[D / 32], const i16x4 (&
 // x += RoPE(L B) (key side), rounded back to bf16.  c[blk][i], s[blk][i] are
 // cos/sin of the token's angle at frequency q*QPG + blk*4 + i.
 template <int D, int R>
-__device__ __forceinline__ void add_rotated_expansion(u32x4 (&x)[D / 32], const i16x4 (&bf)[D / 16][RCH(R)],
-                                                      const u32x2 (&l)[RCH(R)],
+__device__ __forceinline__ void add_rotated_expansion(u32x4 (&x)[D / 32],
+                                                      const typename Ex<R>::Frag (&bf)[D / 16][Ex<R>::NC],
+                                                      const typename Ex<R>::Frag (&l)[Ex<R>::NC],
                                                       const float (&c)[D / 32][4], const float (&s)[D / 32][4]) {
   constexpr int NB = D / 32;
 #pragma unroll
   for (int blk = 0; blk < NB; ++blk) {
     f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int rc = 0; rc < RCH(R); ++rc) {
-      elo = mfma16x16x16(bf[blk][rc], as_i16x4(l[rc]), elo);
-      ehi = mfma16x16x16(bf[blk + NB][rc], as_i16x4(l[rc]), ehi);
+    for (int rc = 0; rc < Ex<R>::NC; ++rc) {
+      elo = Ex<R>::mma(bf[blk][rc], l[rc], elo);
+      ehi = Ex<R>::mma(bf[blk + NB][rc], l[rc], ehi);
     }
     const int klo = blk >> 1, khi = (blk + NB) >> 1, w0 = (blk & 1) * 2;
     float vlo[4], vhi[4];
