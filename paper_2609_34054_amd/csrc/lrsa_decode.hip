@@ -55,7 +55,10 @@ struct Dec {
   static constexpr int NCH = D / 32;          // 8-dim chunks per lane
   static constexpr int QPG = D / 8;           // dims per lane group per half
   static constexpr int RC = RCH(R);           // 16-wide rank chunks
-  static constexpr int CS_ROW = HALF + 2;     // float2 per table row (padded)
+  // float2 per table row.  A lane reads row l%16 at frequencies from
+  // (l/16)*QPG; with an odd row length (d = 128) the 32 lanes of each
+  // half-wave pass then cover all 64 banks once.
+  static constexpr int CS_ROW = D == 128 ? HALF + 1 : HALF + 2;
   static constexpr int EPT = TK * HALF / NT;  // table entries per thread
   // Row strides of the tiles read with ds_read_b64_tr_b16: the two 16-lane
   // groups serviced together read 8 consecutive rows of 32 bytes, which land
