@@ -149,7 +149,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // B_k^T fragments of this KV head for ranks > 16, [RoPE half ph][block i]
   // [lane][rank chunk]: each lane's NC 16-byte fragments are contiguous.
   __shared__ __attribute__((aligned(16))) u32x4 bk_lds[LK && !C::BK_REG ? 2 * 2 * C::NBW * 64 * C::NC : 1];
-  __shared__ int s_maxpos;
+  __shared__ int s_maxpos, s_minpos;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   // Heaviest row tiles (latest positions, most keys) are dispatched first.
@@ -157,7 +157,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int G = a.group;
   const int n_rows = a.n_tok * G;
 
-  if (tid == 0) s_maxpos = -1;
+  if (tid == 0) {
+    s_maxpos = -1;
+    s_minpos = INT32_MAX;
+  }
   if constexpr (LK && !C::BK_REG) {
     const uint16_t* bh = a.Bk + (int64_t)blockIdx.z * a.b_stride + (int64_t)blockIdx.y * D * R;
     for (int e = tid; e < 2 * 2 * C::NBW * 64 * C::NC; e += NTHR) {
@@ -182,9 +185,17 @@ lrsa_prefill_kernel(const AttnArgs a) {
 
   __syncthreads();
   if (row_ok && last >= 0) atomicMax(&s_maxpos, (int)last);
+  if (row_ok) atomicMin(&s_minpos, (int)(last < 0 ? -1 : last));
   __syncthreads();
   const int64_t kv_hi = (int64_t)s_maxpos + 1;  // keys [0, kv_hi) are needed
   const int n_tiles = (int)((kv_hi + TKV - 1) / TKV);
+  // Tiles [0, n_full) lie wholly at or below every row's last visible key:
+  // no row needs a mask there and every wave attends them.  Rank 64 keeps
+  // the per-half loop for all tiles: the straight-line main loop needs more
+  // registers than it has.
+  constexpr bool kMainLoop = R < 64;
+  const int n_full_raw = s_minpos < 0 ? 0 : (int)(((int64_t)s_minpos + 1) / TKV);
+  const int n_full = !kMainLoop ? 0 : (n_full_raw < n_tiles ? n_full_raw : n_tiles);
 
   const int64_t row_el = (int64_t)a.n_kv * D;
   // This request's caches (or pools, paged through its rows of the block
@@ -276,8 +287,11 @@ lrsa_prefill_kernel(const AttnArgs a) {
   }
   // Tiles are loaded in token order, so paged caches are walked with them.
   auto load_unit = [&](Unit<D, R>& u, int64_t t0) {
-    const int rows = (int)(kv_hi - t0 < TKV ? kv_hi - t0 : TKV);  // valid rows of this tile (> 0)
-    const int32_t kv_bytes = (rows - 1) * (int32_t)(row_el * 2) + D * 2;
+    // Valid rows of this tile; a tile at or past kv_hi gets empty resources
+    // (its loads return zeros).
+    const int64_t left = kv_hi - t0;
+    const int rows = (int)(left < TKV ? (left > 0 ? left : 0) : TKV);
+    const int32_t kv_bytes = rows > 0 ? (rows - 1) * (int32_t)(row_el * 2) + D * 2 : 0;
     int64_t kr = t0, lr = t0;  // cache rows of the tile's first token
     if constexpr (PAGED) walk.next(TKV, kv_hi, kr, lr);
     const auto rk = make_rsrc(Kb + kr * row_el, kv_bytes);
@@ -455,7 +469,93 @@ lrsa_prefill_kernel(const AttnArgs a) {
   }
   __syncthreads();
 
-  for (int tile = 0; tile < n_tiles; ++tile) {
+  // Main loop, tiles that need no mask: the scores of both halves, one
+  // maximum and one (rare) rescale per tile, then a single straight-line
+  // block that holds the exponentials and PV of both halves and the build of
+  // the next tile, so that the compiler can interleave the build's vector
+  // work and transposes with the PV MFMAs.
+  int tile = 0;
+  if constexpr (kMainLoop)
+  for (; tile < n_full; ++tile) {
+    const int buf = tile & 1;
+    const int64_t t0 = (int64_t)tile * TKV;
+    bf16x8 kf[C::NKQ];
+    auto k_frag = [&](int tb, int kk) {
+      return as_bf16x8(*reinterpret_cast<const u32x4*>(k_lds[buf] + (tb * 32 + l32) * C::K_ROW + h32 * 8 + kk * 16));
+    };
+    f32x16 sh[2];
+#pragma unroll
+    for (int kk = 0; kk < C::NKQ; ++kk) kf[kk] = k_frag(0, kk);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) sh[0][j] = sh[1][j] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < C::NKQ; ++kk) {
+      sh[0] = mfma32x32x16(kf[kk], qf[kk], sh[0]);
+      kf[kk] = k_frag(1, kk);
+    }
+#pragma unroll
+    for (int kk = 0; kk < C::NKQ; ++kk) sh[1] = mfma32x32x16(kf[kk], qf[kk], sh[1]);
+    float mx = fmaxf(sh[0][0], sh[0][1]);
+#pragma unroll
+    for (int j = 2; j < 16; ++j) mx = fmaxf(mx, sh[0][j]);
+#pragma unroll
+    for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sh[1][j]);
+    mx = max_xor32(mx) * a.scale_log2;
+    if (__ballot(mx > m_run + kRescaleLog2)) {
+      const float mn = fmaxf(m_run, mx);
+      const float alpha = fast_exp2(m_run - (mn == -INFINITY ? 0.f : mn));
+#pragma unroll
+      for (int db = 0; db < C::NDB; ++db) acc[db] *= alpha;
+#pragma unroll
+      for (int rb = 0; rb < C::RB; ++rb) accl[rb] *= alpha;
+      l_run *= alpha;
+      m_run = mn;
+    }
+    const float ms = (m_run == -INFINITY) ? 0.f : m_run;
+    float ls = 0.f;
+#pragma unroll
+    for (int tb = 0; tb < 2; ++tb) {
+      const uint16_t* vt = v_lds[buf];
+      const uint16_t* lvt = lv_lds[buf];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        bf16x8 vf[C::NDB], lvf[C::RB];
+#pragma unroll
+        for (int db = 0; db < C::NDB; ++db)
+          vf[db] = as_bf16x8(*reinterpret_cast<const u32x4*>(vt + (((2 * tb + hf) * C::NDB + db) * 64 + lane) * 8));
+        if constexpr (LV) {
+#pragma unroll
+          for (int rb = 0; rb < C::RB; ++rb)
+            lvf[rb] = as_bf16x8(*reinterpret_cast<const u32x4*>(lvt + (((2 * tb + hf) * C::RB + rb) * 64 + lane) * 8));
+        }
+        u32x4 pw;  // bf16 P of this 16-token chunk
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          const float p0 = fast_exp2(__builtin_fmaf(sh[tb][hf * 8 + 2 * c], a.scale_log2, -ms));
+          const float p1 = fast_exp2(__builtin_fmaf(sh[tb][hf * 8 + 2 * c + 1], a.scale_log2, -ms));
+          if constexpr (!ones_sum) ls += p0 + p1;
+          pw[c] = pack_bf16(p0, p1);
+        }
+        const bf16x8 pb = as_bf16x8(pw);
+#pragma unroll
+        for (int db = 0; db < C::NDB; ++db) acc[db] = mfma32x32x16(vf[db], pb, acc[db]);
+        if constexpr (LV) {
+#pragma unroll
+          for (int rb = 0; rb < C::RB; ++rb) accl[rb] = mfma32x32x16(lvf[rb], pb, accl[rb]);
+        }
+      }
+    }
+    if constexpr (!ones_sum) l_run += ls;
+    // Build tile + 1 and start the loads of tile + 2 (past the last tile this
+    // writes a buffer no wave reads again and loads nothing).
+    rebuild(u, buf ^ 1);
+    load_unit(u, t0 + 2 * TKV);
+    base_angles(t0 + 2 * TKV, buf);
+    __syncthreads();  // tile + 1 in LDS; tile consumed by every wave
+  }
+
+  // Tiles that cross some row's causal limit.
+  for (; tile < n_tiles; ++tile) {
     const int buf = tile & 1;
     const int64_t t0 = (int64_t)tile * TKV;
     // Build tile + 1 (its data arrived during the previous tile) and start
