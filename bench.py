@@ -40,9 +40,9 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
 
 
 # --------------------------------------------------------------- the workload
-def workload_dims():
+def workload_dims(index=3):
     from workload import CONFIGS
-    cfg = CONFIGS[3]
+    cfg = CONFIGS[index]
     S = cfg.context
     return cfg, dict(
         S=S, seg=cfg.precompute_rows, n_pre=cfg.prefill_tokens, B=cfg.decode_batch,
@@ -581,6 +581,103 @@ def paged(prc, w, dev, steps, warmup):
                           "paged_over_contiguous": round(t_p / t_c, 4), "bitwise_equal": bool(same)}), flush=True)
 
 
+def workload_bench(prc, index, dev, steps, warmup):
+    """Precompute, prefill and decode at the shapes of another workload (the
+    8B-shaped layer at 8k context, or the 14B-shaped one at 64k with rank 64),
+    each against the materialise-then-attend reference; one JSON line.  Every
+    timed call reads a different input set, with enough sets that one pass
+    over them exceeds the 256 MB Infinity Cache, so decode is timed from HBM
+    even where one request's caches would fit in the cache."""
+    import torch
+    cfg, w = workload_dims(index)
+    g = torch.Generator(device=dev).manual_seed(5000 + index)
+
+    def nrm(shape, std=1.0):
+        x = torch.randn(*shape, generator=g, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            x.mul_(std)
+        return x.to(torch.bfloat16)
+
+    S, d, n_q, n_kv, r, B, N = w["S"], w["d"], w["n_q"], w["n_kv"], w["r"], w["B"], w["N"]
+    kv_pre = S + w["n_pre"]
+    work = algorithmic_work(w)
+    bstd = math.sqrt(0.02)
+    mall = 256 << 20
+    n_dec = max(1, -(-2 * mall // work["decode_bytes"]))
+    n_pre = max(1, -(-2 * mall // (kv_pre * n_kv * d * 4)))
+
+    def case(nb, n_tok, kv, pos0):
+        return dict(Q=nrm((nb, n_tok, n_q, d)), K_base=nrm((nb, kv, n_kv, d)), V_base=nrm((nb, kv, n_kv, d)),
+                    L_k=nrm((nb, kv, r)), L_v=nrm((nb, kv, r)), Bk_rows=nrm((nb, n_kv * d, r), bstd),
+                    Bv_rows=nrm((nb, n_kv * d, r), bstd),
+                    positions=(torch.arange(pos0, pos0 + n_tok, dtype=torch.int32, device=dev)[None]
+                               .repeat(nb, 1).contiguous()),
+                    kv_len=torch.full((nb,), kv, dtype=torch.int32, device=dev))
+
+    print(f"bench: workload {index}: {n_dec} decode and {n_pre} prefill input sets", file=sys.stderr, flush=True)
+    dec = [case(B, 1, S, S - 1) for _ in range(n_dec)]
+    pre = [case(1, w["n_pre"], kv_pre, S) for _ in range(n_pre)]
+    X = [nrm((w["seg"], w["hidden"])) for _ in range(4)]
+    A_rows = nrm((2 * N * r, w["hidden"]), 1.0 / math.sqrt(w["hidden"]))
+    L = torch.zeros((2, N, w["seg"], r), dtype=torch.bfloat16, device=dev)
+    O_dec = torch.empty_like(dec[0]["Q"])
+    O_pre = torch.empty_like(pre[0]["Q"])
+    dims = prc.make_dims(dec[0]["Q"], dec[0]["K_base"], dec[0]["L_k"], dec[0]["L_v"], dec[0]["Bk_rows"],
+                         dec[0]["Bv_rows"], w["theta"])
+    ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
+    Kd, Vd = torch.empty_like(dec[0]["K_base"]), torch.empty_like(dec[0]["V_base"])
+    Kp, Vp = torch.empty_like(pre[0]["K_base"]), torch.empty_like(pre[0]["V_base"])
+
+    def plain(c, K, V):
+        return dict(c, K_base=K, V_base=V, L_k=None, L_v=None, Bk_rows=None, Bv_rows=None)
+
+    def materialised(c, K, V, O, wsp):
+        prc.materialize_agent_kv(c["K_base"], c["V_base"], c["L_k"], c["L_v"], c["Bk_rows"], c["Bv_rows"],
+                                 c["kv_len"], rope_theta=w["theta"], K_full=K, V_full=V)
+        attn(prc, plain(c, K, V), w["theta"], O, wsp)
+
+    def timed(fn, n_sets):
+        for i in range(warmup):
+            fn(i % n_sets)
+        torch.cuda.synchronize()
+        ts = []
+        for i in range(steps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn(i % n_sets)
+            e1.record()
+            ts.append((e0, e1))
+        torch.cuda.synchronize()
+        v = sorted(a.elapsed_time(b) for a, b in ts)
+        return v[len(v) // 2]
+
+    t_pc = timed(lambda i: prc.precompute_lr_cache(X[i % 4], A_rows, 2, N, r, L), 4)
+    t_pre = timed(lambda i: attn(prc, pre[i], w["theta"], O_pre, None), n_pre)
+    t_dec = timed(lambda i: attn(prc, dec[i], w["theta"], O_dec, ws), n_dec)
+    t_pre_m = timed(lambda i: materialised(pre[i], Kp, Vp, O_pre, None), n_pre)
+    t_dec_m = timed(lambda i: materialised(dec[i], Kd, Vd, O_dec, ws), n_dec)
+    pre_tf = work["prefill_flops"] / (t_pre * 1e-3) / 1e12
+    dec_gbs = work["decode_bytes"] / (t_dec * 1e-3) / 1e9
+    pc_gbs = work["precompute_bytes"] / (t_pc * 1e-3) / 1e9
+    pc_tf = work["precompute_flops"] / (t_pc * 1e-3) / 1e12
+    print(json.dumps({
+        "bench": "workload", "index": index, "workload": cfg.name,
+        "shape": {"hidden": w["hidden"], "n_q_heads": n_q, "n_kv_heads": n_kv, "head_dim": d, "agents": N,
+                  "rank": r, "context": S, "decode_batch": B, "prefill_tokens": w["n_pre"],
+                  "precompute_rows": w["seg"]},
+        "input_sets": {"decode": n_dec, "prefill": n_pre},
+        "precompute": {"ms": round(t_pc, 4), "gbs": round(pc_gbs, 1), "hbm_frac": round(pc_gbs / HBM_PEAK_GBS, 4),
+                       "tflops": round(pc_tf, 1), "mfma_frac": round(pc_tf / MFMA_BF16_PEAK_TFLOPS, 4)},
+        "prefill": {"ms": round(t_pre, 4), "tflops": round(pre_tf, 1),
+                    "mfma_frac": round(pre_tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                    "materialise_ms": round(t_pre_m, 4), "speedup": round(t_pre_m / t_pre, 3)},
+        "decode": {"ms": round(t_dec, 4), "gbs": round(dec_gbs, 1), "hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4),
+                   "materialise_ms": round(t_dec_m, 4), "speedup": round(t_dec_m / t_dec, 3)},
+        "algorithmic": {"decode_bytes": work["decode_bytes"], "prefill_flops": work["prefill_flops"],
+                        "precompute_bytes": work["precompute_bytes"]},
+    }), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -604,6 +701,9 @@ def main():
     ap.add_argument("--paged", action="store_true",
                     help="instead of the step: decode, prefill and segment projection over paged (block-table) "
                          "caches, against the same calls over contiguous caches")
+    ap.add_argument("--workload", type=int, choices=(2, 4), default=None,
+                    help="instead of the step: precompute, prefill and decode at the 8k-context 8B-shaped (2) or "
+                         "64k-context 14B-shaped rank-64 (4) workload, against materialise-then-attend")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
@@ -629,6 +729,9 @@ def main():
         return
     if args.paged:
         paged(prc, w, dev, args.steps, args.warmup)
+        return
+    if args.workload is not None:
+        workload_bench(prc, args.workload, dev, args.steps, args.warmup)
         return
     work = algorithmic_work(w)
     print(f"bench: generating inputs ({w['B']} x {w['S']}-token decode caches)", file=sys.stderr, flush=True)

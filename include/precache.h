@@ -204,9 +204,12 @@ typedef struct lrsa_dims {
  *   lse        [B, n_tok, n_q] fp32 natural-log log-sum-exp of the scaled scores,
  *              or NULL.  A row that sees no key gets O = 0 and lse = -inf.
  *   workspace  device scratch of at least lr_shared_attention_workspace_size(dims)
- *              bytes (only decode, n_tok == 1, uses it; NULL allowed when the size
- *              is 0).  Contents need no initialisation; calls that share a
- *              workspace must be ordered on one stream.
+ *              bytes (NULL allowed when the size is 0): the split partials of
+ *              decode (n_tok == 1), and of a prefill too small to fill the GPU
+ *              on its own (fewer than 512 units of 256 query rows x KV head x
+ *              request), which is then also split over its KV tiles.
+ *              Contents need no initialisation; calls that share a workspace
+ *              must be ordered on one stream.
  * Arithmetic: bf16 inputs; fp32 accumulation and softmax; rebuilt K tiles are
  * rounded to bf16 before the QK^T contraction; output rounded to bf16.
  */

@@ -325,9 +325,18 @@ PRC_API prc_status project_kv_and_lr_cache_paged(const uint16_t* X, int64_t T, i
 namespace {
 
 size_t workspace_size(const lrsa_dims* dims, bool paged) {
-  if (dims == nullptr || dims->n_tok != 1 || dims->batch < 1 || dims->n_kv_heads < 1 || dims->s_cap < 1)
+  if (dims == nullptr || dims->n_tok < 1 || dims->batch < 1 || dims->n_kv_heads < 1 || dims->s_cap < 1 ||
+      dims->n_q_heads < dims->n_kv_heads)
     return 0;
   const int r = rank_ok(dims->rank) ? dims->rank : 8;
+  if (dims->n_tok > 1) {
+    // Prefill: partials of a split over the KV tiles, when the call is too
+    // small to fill the GPU otherwise.
+    int splits = 1, split_tiles = 0;
+    prc::prefill_plan(dims->n_tok, dims->n_q_heads / dims->n_kv_heads, dims->n_kv_heads, dims->batch, dims->s_cap,
+                      &splits, &split_tiles);
+    return prc::prefill_workspace_bytes(dims->batch, dims->n_tok, dims->n_q_heads, splits, dims->head_dim, r);
+  }
   int n_splits = 0, split_tiles = 0;
   // Paged caches always take the per-request decode kernel.
   const bool shared = !paged && prc::decode_shares_base(dims->batch, dims->kv_req_stride);
@@ -365,6 +374,15 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
     a.ws = static_cast<float*>(workspace);
     snprintf(what, sizeof(what), "%s (decode)", who);
     return launch_status(prc::launch_decode(a, st), what);
+  }
+  prc::prefill_plan(a.n_tok, a.group, a.n_kv, a.batch, a.s_cap, &a.pf_splits, &a.pf_split_tiles);
+  if (a.pf_splits > 1) {
+    const size_t need = prc::prefill_workspace_bytes(a.batch, a.n_tok, a.n_q, a.pf_splits, a.head_dim, a.rank);
+    if (workspace == nullptr || workspace_bytes < need)
+      return fail(PRC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace == nullptr ? 0 : workspace_bytes,
+                  need);
+    if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
+    a.ws = static_cast<float*>(workspace);
   }
   snprintf(what, sizeof(what), "%s (prefill)", who);
   return launch_status(prc::launch_prefill(a, st), what);

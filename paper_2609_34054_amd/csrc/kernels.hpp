@@ -51,6 +51,8 @@ struct AttnArgs {
   int32_t rank;
   int32_t n_splits;     // decode: KV splits per request
   int32_t split_tiles;  // decode: KV tiles per split
+  int32_t pf_splits;    // prefill: KV splits per row tile (1: none)
+  int32_t pf_split_tiles;  // prefill: 64-token KV tiles per split
   float scale_log2;     // softmax scale * log2(e)
   double w2pi[kMaxHalfDim];  // RoPE omega_j / (2 pi), fp64
 };
@@ -65,7 +67,15 @@ void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base,
 size_t decode_workspace_bytes(int batch, int n_q, int n_splits, int head_dim, int rank);
 hipError_t launch_decode(const AttnArgs& a, hipStream_t stream);
 
-// Prefill (several query tokens per request): causal flash attention.
+// Log-sum-exp merge of split partials ws[((b n_tok + i) n_q + h) n_splits
+// + s][4 + d + r] into O (and lse), with the deferred B_v up-projection.
+hipError_t launch_split_merge(const AttnArgs& a, hipStream_t stream);
+
+// Prefill (several query tokens per request): causal flash attention.  A
+// call with too few (row tile, KV head, request) units to fill the GPU is
+// also split over the KV tiles, each split writing partials for the merge.
+void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int* splits, int* split_tiles);
+size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int head_dim, int rank);
 hipError_t launch_prefill(const AttnArgs& a, hipStream_t stream);
 
 // Reference point: write the full per-agent K/V.

@@ -412,8 +412,10 @@ lrsa_decode_kernel(const AttnArgs a) {
   }
 }
 
-// Merge the split partials of one (request, q head): log-sum-exp weights,
-// then the deferred up-projection O += (sum_s w_s P_s L_v) B_v, then 1/l.
+// Merge the split partials of one (request, query token, q head):
+// log-sum-exp weights, then the deferred up-projection
+// O += (sum_s w_s P_s L_v) B_v, then 1/l.  Decode has one query token per
+// request; a split prefill has n_tok.
 // Four waves each fold a quarter of the splits (independent loads in flight),
 // and the four partial sums meet in LDS.
 constexpr int MW = 4;  // waves per merge workgroup
@@ -426,10 +428,12 @@ lrsa_merge_kernel(const AttnArgs a) {
   __shared__ float red_lr[MW][64];
   __shared__ float red_l[MW];
   __shared__ float red_m[MW];
-  const int h = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int h = blockIdx.x, bi = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int b = bi / a.n_tok;  // bi = request * n_tok + query token
   const int g = h / a.group;
   const bool has_lv = a.Lv != nullptr;
-  const float* base = a.ws + ((int64_t)b * a.n_q + h) * (int64_t)a.n_splits * PS;
+  const int64_t orow = (int64_t)bi * a.n_q + h;  // (request, token, head) row of O
+  const float* base = a.ws + orow * (int64_t)a.n_splits * PS;
 
   float M = -INFINITY;
   for (int s = tid; s < a.n_splits; s += 64 * MW) M = fmaxf(M, base[(int64_t)s * PS]);
@@ -492,14 +496,14 @@ lrsa_merge_kernel(const AttnArgs a) {
     }
   }
   const float inv = L > 0.f ? 1.f / L : 0.f;
-  uint16_t* o = a.O + ((int64_t)b * a.n_tok * a.n_q + h) * D;
+  uint16_t* o = a.O + orow * D;
 #pragma unroll
   for (int dd = 0; dd < DPL; ++dd) {
     const uint32_t pk = pack_bf16(acc[dd] * inv, 0.f);
     o[lane + 64 * dd] = (uint16_t)(pk & 0xffffu);
   }
   if (a.lse != nullptr && lane == 0)
-    a.lse[(int64_t)b * a.n_tok * a.n_q + h] = L > 0.f ? (M + __log2f(L)) * kLn2 : -INFINITY;
+    a.lse[orow] = L > 0.f ? (M + __log2f(L)) * kLn2 : -INFINITY;
 }
 
 // ---------------------------------------------------------------------------
@@ -818,7 +822,7 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((lrsa_decode_kernel<D, R, false>), grid, dim3(C::NT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch), dim3(64 * MW), 0, st, a);
+  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch * a.n_tok), dim3(64 * MW), 0, st, a);
   return hipGetLastError();
 }
 
@@ -829,8 +833,25 @@ hipError_t launch_shared_t(const AttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((lrsa_decode_shared_kernel<D, R>), dim3(a.n_splits, a.n_kv, rg), dim3(C::NT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch), dim3(64 * MW), 0, st, a);
+  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch * a.n_tok), dim3(64 * MW), 0, st, a);
   return hipGetLastError();
+}
+
+template <int D, int R>
+hipError_t launch_merge_t(const AttnArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch * a.n_tok), dim3(64 * MW), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_merge_r(const AttnArgs& a, hipStream_t st) {
+  switch (a.rank) {
+    case 8: return launch_merge_t<D, 8>(a, st);
+    case 16: return launch_merge_t<D, 16>(a, st);
+    case 32: return launch_merge_t<D, 32>(a, st);
+    case 64: return launch_merge_t<D, 64>(a, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 template <int D>
@@ -873,6 +894,12 @@ void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base,
 
 size_t decode_workspace_bytes(int batch, int n_q, int n_splits, int head_dim, int rank) {
   return (size_t)batch * n_q * n_splits * (4 + head_dim + rank) * sizeof(float);
+}
+
+hipError_t launch_split_merge(const AttnArgs& a, hipStream_t st) {
+  if (a.head_dim == 64) return launch_merge_r<64>(a, st);
+  if (a.head_dim == 128) return launch_merge_r<128>(a, st);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_decode(const AttnArgs& a, hipStream_t st) {

@@ -153,7 +153,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   // Heaviest row tiles (latest positions, most keys) are dispatched first.
-  const int rtile = gridDim.x - 1 - blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  // Grid: (row tile, KV head x KV split, request).
+  const int nsp = a.pf_splits > 1 ? a.pf_splits : 1;
+  const int rtile = gridDim.x - 1 - blockIdx.x, b = blockIdx.z;
+  const int g = (int)blockIdx.y / nsp, split = (int)blockIdx.y - g * nsp;
   const int G = a.group;
   const int n_rows = a.n_tok * G;
 
@@ -162,7 +165,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
     s_minpos = INT32_MAX;
   }
   if constexpr (LK && !C::BK_REG) {
-    const uint16_t* bh = a.Bk + (int64_t)blockIdx.z * a.b_stride + (int64_t)blockIdx.y * D * R;
+    const uint16_t* bh = a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R;
     for (int e = tid; e < 2 * 2 * C::NBW * 64 * C::NC; e += NTHR) {
       const int c = e % C::NC, l = (e / C::NC) % 64, i = (e / (C::NC * 64)) % (2 * C::NBW);
       const int phe = e / (C::NC * 64 * 2 * C::NBW);
@@ -196,6 +199,9 @@ lrsa_prefill_kernel(const AttnArgs a) {
   constexpr bool kMainLoop = R < 64;
   const int n_full_raw = s_minpos < 0 ? 0 : (int)(((int64_t)s_minpos + 1) / TKV);
   const int n_full = !kMainLoop ? 0 : (n_full_raw < n_tiles ? n_full_raw : n_tiles);
+  // This workgroup's tiles: all of them, or its split's share.
+  const int t_lo = nsp > 1 ? (split * a.pf_split_tiles < n_tiles ? split * a.pf_split_tiles : n_tiles) : 0;
+  const int t_hi = nsp > 1 ? (t_lo + a.pf_split_tiles < n_tiles ? t_lo + a.pf_split_tiles : n_tiles) : n_tiles;
 
   const int64_t row_el = (int64_t)a.n_kv * D;
   // This request's caches (or pools, paged through its rows of the block
@@ -203,7 +209,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
   PageWalk walk;
   if constexpr (PAGED)
     walk.start(a.kv_tbl + (int64_t)b * a.max_blk, a.lr_tbl + (int64_t)b * a.max_blk, a.max_blk, a.blk, a.kv_nblk,
-               a.lr_nblk, 0, kv_hi);
+               a.lr_nblk, (int64_t)t_lo * TKV, kv_hi);
   const uint16_t* Kb = a.Kb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Lk = LK ? a.Lk + (int64_t)b * a.l_stride : nullptr;
@@ -455,17 +461,18 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // workgroup is laid out) take the two jobs in opposite order.
   const bool build_first = ((w >> 2) ^ w) & 1;
 
-  // Prologue: tile 0 into LDS buffer 0, tile 1 in flight.
+  // Prologue: the first tile into its LDS buffer (tile parity), the next in
+  // flight.
   Unit<D, R> u;
-  if (n_tiles > 0) {
-    load_unit(u, 0);
-    base_angles(0, 0);
+  if (t_lo < t_hi) {
+    load_unit(u, (int64_t)t_lo * TKV);
+    base_angles((int64_t)t_lo * TKV, t_lo & 1);
   }
   __syncthreads();
-  if (n_tiles > 0) rebuild(u, 0);
-  if (n_tiles > 1) {
-    load_unit(u, TKV);
-    base_angles(TKV, 1);
+  if (t_lo < t_hi) rebuild(u, t_lo & 1);
+  if (t_lo + 1 < t_hi) {
+    load_unit(u, (int64_t)(t_lo + 1) * TKV);
+    base_angles((int64_t)(t_lo + 1) * TKV, (t_lo + 1) & 1);
   }
   __syncthreads();
 
@@ -474,9 +481,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // block that holds the exponentials and PV of both halves and the build of
   // the next tile, so that the compiler can interleave the build's vector
   // work and transposes with the PV MFMAs.
-  int tile = 0;
+  int tile = t_lo;
+  const int main_end = n_full < t_hi ? n_full : t_hi;
   if constexpr (kMainLoop)
-  for (; tile < n_full; ++tile) {
+  for (; tile < main_end; ++tile) {
     const int buf = tile & 1;
     const int64_t t0 = (int64_t)tile * TKV;
     bf16x8 kf[C::NKQ];
@@ -555,14 +563,14 @@ lrsa_prefill_kernel(const AttnArgs a) {
   }
 
   // Tiles that cross some row's causal limit.
-  for (; tile < n_tiles; ++tile) {
+  for (; tile < t_hi; ++tile) {
     const int buf = tile & 1;
     const int64_t t0 = (int64_t)tile * TKV;
     // Build tile + 1 (its data arrived during the previous tile) and start
     // the loads of tile + 2.
     auto build = [&]() {
-      if (tile + 1 < n_tiles) rebuild(u, buf ^ 1);
-      if (tile + 2 < n_tiles) load_unit(u, t0 + 2 * TKV);
+      if (tile + 1 < t_hi) rebuild(u, buf ^ 1);
+      if (tile + 2 < t_hi) load_unit(u, t0 + 2 * TKV);
     };
     if (build_first) build();
     if (t0 <= (int64_t)wave_last) {
@@ -692,8 +700,48 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
     }
     if (!build_first) build();
-    if (tile + 2 < n_tiles) base_angles(t0 + 2 * TKV, buf);
+    if (tile + 2 < t_hi) base_angles(t0 + 2 * TKV, buf);
     __syncthreads();  // tile + 1 in LDS; tile consumed by every wave
+  }
+
+  // Row sum: from the ones row of (P L_v)^T (row R: register 4 (R/8) + R%4 of
+  // block 0 in lanes (R%8)/4*32 .. +31), else from the per-lane partial sums.
+  float l_tot;
+  if constexpr (ones_sum) {
+    constexpr int jr = 4 * ((R % 32) / 8) + (R % 4);
+    l_tot = __shfl(accl[0][jr], l32 + 32 * ((R % 8) / 4), 64);
+  } else {
+    l_tot = sum_xor32(l_run);
+  }
+  if (nsp > 1) {
+    // ---- split epilogue: this split's partial (m, l, O^T, (P L_v)^T) for
+    // the merge, which applies B_v and 1/l.
+    if (!row_ok) return;
+    constexpr int PS = 4 + D + R;
+    const int64_t orow = ((int64_t)b * a.n_tok + qi) * a.n_q + (int64_t)g * G + hh;
+    float* wsp = a.ws + (orow * nsp + split) * PS;
+    if (h32 == 0) {
+      wsp[0] = m_run;
+      wsp[1] = l_tot;
+    }
+#pragma unroll
+    for (int db = 0; db < C::NDB; ++db)
+#pragma unroll
+      for (int jg = 0; jg < 4; ++jg)
+        *reinterpret_cast<f32x4*>(wsp + 4 + db * 32 + jg * 8 + h32 * 4) =
+            f32x4{acc[db][jg * 4], acc[db][jg * 4 + 1], acc[db][jg * 4 + 2], acc[db][jg * 4 + 3]};
+    if constexpr (LV) {
+#pragma unroll
+      for (int rb = 0; rb < C::RB; ++rb)
+#pragma unroll
+        for (int jg = 0; jg < 4; ++jg) {
+          const int rk = rb * 32 + jg * 8 + h32 * 4;
+          if (rk < R)
+            *reinterpret_cast<f32x4*>(wsp + 4 + D + rk) =
+                f32x4{accl[rb][jg * 4], accl[rb][jg * 4 + 1], accl[rb][jg * 4 + 2], accl[rb][jg * 4 + 3]};
+        }
+    }
+    return;
   }
 
   // ---- epilogue: O^T += B_v^T (P L_v)^T, then O = acc / l, lse -------------
@@ -723,15 +771,6 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
     }
   }
-  // Row sum: from the ones row of (P L_v)^T (row R: register 4 (R/8) + R%4 of
-  // block 0 in lanes (R%8)/4*32 .. +31), else from the per-lane partial sums.
-  float l_tot;
-  if constexpr (ones_sum) {
-    constexpr int jr = 4 * ((R % 32) / 8) + (R % 4);
-    l_tot = __shfl(accl[0][jr], l32 + 32 * ((R % 8) / 4), 64);
-  } else {
-    l_tot = sum_xor32(l_run);
-  }
   if (!row_ok) return;
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   uint16_t* op = a.O + (((int64_t)b * a.n_tok + qi) * a.n_q + (int64_t)g * G + hh) * D;
@@ -754,12 +793,17 @@ template <int D, int R, bool LK, bool LV>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const int n_rows = a.n_tok * a.group;
   const int tiles = (n_rows + BROWS - 1) / BROWS;
-  const dim3 grid(tiles, a.n_kv, a.batch);
+  const int nsp = a.pf_splits > 1 ? a.pf_splits : 1;
+  const dim3 grid(tiles, a.n_kv * nsp, a.batch);
   if (a.kv_tbl != nullptr)
     hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, true>), grid, dim3(NTHR), 0, st, a);
   else
     hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, false>), grid, dim3(NTHR), 0, st, a);
-  return hipGetLastError();
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || nsp == 1) return e;
+  AttnArgs m = a;
+  m.n_splits = nsp;
+  return launch_split_merge(m, st);
 }
 
 template <int D, int R>
@@ -783,6 +827,30 @@ hipError_t launch_r(const AttnArgs& a, hipStream_t st) {
 }
 
 }  // namespace
+
+void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int* splits, int* split_tiles) {
+  // Units of work without a split: (row tile, KV head, request).  A call with
+  // fewer than two rounds of one workgroup per CU splits the KV tiles so that
+  // there are about four, each split at least 8 tiles long.
+  const int64_t rows = (int64_t)n_tok * group;
+  const int64_t units = ((rows + BROWS - 1) / BROWS) * n_kv * (batch > 0 ? batch : 1);
+  const int64_t tiles = (s_cap + TKV - 1) / TKV;
+  *splits = 1;
+  *split_tiles = (int)(tiles > 0 ? tiles : 1);
+  if (units >= 512) return;
+  int64_t ns = (1024 + units - 1) / units;
+  if (ns > 8) ns = 8;
+  if (ns > tiles / 8) ns = tiles / 8;
+  if (ns < 2) return;
+  const int64_t st = (tiles + ns - 1) / ns;
+  *splits = (int)((tiles + st - 1) / st);
+  *split_tiles = (int)st;
+}
+
+size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int head_dim, int rank) {
+  if (splits <= 1) return 0;
+  return (size_t)batch * n_tok * n_q * splits * (4 + head_dim + rank) * sizeof(float);
+}
 
 hipError_t launch_prefill(const AttnArgs& a, hipStream_t st) {
   if (a.head_dim == 64) return launch_r<64>(a, st);

@@ -237,7 +237,10 @@ def test_decode_workspace_query_and_check():
     d = _dims(n_tok=1)
     need = L.lr_shared_attention_workspace_size(ctypes.byref(d))
     assert need > 0
-    assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=8))) == 0
+    # Prefill needs no workspace when one pass per KV head already fills the
+    # chip (4096 queries, 8 KV heads) or the context is a handful of tiles.
+    assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=4096, batch=1, s_cap=36864))) == 0
+    assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=8, s_cap=256))) == 0
     assert _attn(d, ws=None) == EWS
     assert _attn(d, ws=A16, ws_bytes=need - 1) == EWS
     assert _attn(d, ws=A16 + 4, ws_bytes=need) == EALIGN
@@ -245,6 +248,21 @@ def test_decode_workspace_query_and_check():
     # contexts.
     big = L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=1, batch=16, s_cap=32768)))
     assert big >= 16 * 32 * (4 + 128 + 16) * 4
+
+
+def test_split_prefill_workspace_query_and_check():
+    # A small prefill over a long context splits its KV range: the call then
+    # needs one fp32 partial (max, sum, d + r accumulators) per query row,
+    # head and split, and refuses a missing or short workspace.
+    L = prc.lib()
+    d = _dims(n_tok=8, batch=2, s_cap=8192, kv_req_stride=8192 * 8 * 128, l_req_stride=8192 * 16)
+    need = L.lr_shared_attention_workspace_size(ctypes.byref(d))
+    rows = 2 * 8 * 32
+    assert need > 0 and need % (rows * (4 + 128 + 16) * 4) == 0
+    assert 2 <= need // (rows * (4 + 128 + 16) * 4) <= 8
+    assert _attn(d, ws=None) == EWS
+    assert _attn(d, ws=A16, ws_bytes=need - 1) == EWS
+    assert _attn(d, ws=A16 + 4, ws_bytes=need) == EALIGN
 
 
 # ------------------------------------------------------------ paged attention

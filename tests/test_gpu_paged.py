@@ -60,6 +60,11 @@ PAGED_CASES = [
     ("prefill_r64_blk256", 128, 64, 10, 2, 37, [600, 150], "kv", 256, "own"),
     ("prefill_qv_r32", 128, 32, 8, 2, 45, [190, 64], "v", 64, "planes"),
     ("prefill_plain", 128, 16, 8, 2, 50, [300], "none", 128, "own"),
+    # Split KV ranges (small prefill over 16+ tiles); with 128-token blocks
+    # the second split starts in the middle of a block.
+    ("split_prefill_d128_r16", 128, 16, 8, 2, 40, [1500, 300], "kv", 64, "own"),
+    ("split_prefill_r64_blk256", 128, 64, 10, 2, 20, [2000, 700], "kv", 256, "planes"),
+    ("split_prefill_qv_r32_blk128", 128, 32, 8, 2, 16, [1100], "v", 128, "own"),
     ("decode_d128_r16", 128, 16, 8, 2, 1, [1000, 77, 1, 640], "kv", 64, "own"),
     ("decode_d64_r32_blk128", 64, 32, 8, 4, 1, [333, 129], "kv", 128, "planes"),
     ("decode_r64", 128, 64, 8, 2, 1, [700, 64], "kv", 64, "own"),

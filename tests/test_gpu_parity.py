@@ -170,6 +170,18 @@ ATTN_CASES = [
     ("mid_positions_prefill", 128, 16, 8, 2, 12, [300], 304, "kv", 1.0, "mid"),
     ("mid_positions_decode", 128, 16, 8, 2, 1, [300, 500], 512, "kv", 1.0, "mid"),
     ("many_requests_decode", 64, 16, 8, 8, 1, [64, 65, 63, 1, 17, 200, 31, 128], 256, "kv", 1.0, "end"),
+    # Prefill calls too small to fill the chip split their KV tiles (16+
+    # tiles of 64 keys): partials per split, then the merge.  Shorter
+    # requests of a ragged batch leave whole splits empty, and mid positions
+    # leave the last splits past every row's causal limit.
+    ("split_prefill_ragged", 128, 16, 8, 2, 40, [1500, 300, 64], 1536, "kv", 1.0, "end"),
+    ("split_r64_prefill", 128, 64, 10, 2, 20, [2000], 2048, "kv", 1.0, "end"),
+    ("split_r32_prefill", 128, 32, 16, 2, 9, [1100, 1031], 1152, "kv", 1.0, "end"),
+    ("split_d64_r8_prefill", 64, 8, 4, 4, 16, [1200], 1216, "kv", 1.0, "end"),
+    ("split_qv_prefill", 128, 16, 8, 2, 24, [1300], 1344, "v", 1.0, "end"),
+    ("split_k_only_d64_r32_prefill", 64, 32, 8, 2, 17, [1025], 1088, "k", 1.0, "end"),
+    ("split_plain_prefill", 128, 16, 8, 2, 30, [1800], 1856, "none", 1.0, "end"),
+    ("split_mid_positions_prefill", 128, 16, 8, 2, 12, [3000], 3008, "kv", 1.0, "mid"),
 ]
 
 
