@@ -154,13 +154,45 @@ def run_fused(prc, x, w, steps, warmup):
         step(i, evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    stage = {"precompute": 0.0, "prefill": 0.0, "decode": 0.0}
-    for e in evs:
-        stage["precompute"] += e[0].elapsed_time(e[1])
-        stage["prefill"] += e[1].elapsed_time(e[2])
-        stage["decode"] += e[2].elapsed_time(e[3])
+    per = stage_times(evs)
     total = sum(evs[i][0].elapsed_time(evs[i][3]) for i in range(steps))
-    return {k: v / steps for k, v in stage.items()}, total / steps, wall / steps * 1e3
+    return {k: sum(v) / steps for k, v in per.items()}, total / steps, wall / steps * 1e3, per
+
+
+def stage_times(evs):
+    """Per-step times (ms) of the three stages from four events per step."""
+    per = {"precompute": [], "prefill": [], "decode": []}
+    for e in evs:
+        per["precompute"].append(e[0].elapsed_time(e[1]))
+        per["prefill"].append(e[1].elapsed_time(e[2]))
+        per["decode"].append(e[2].elapsed_time(e[3]))
+    return per
+
+
+def percentiles(v):
+    import numpy as np
+    p10, p50, p90 = np.percentile(np.asarray(v, dtype=np.float64), [10, 50, 90])
+    return {"p10": round(float(p10), 4), "median": round(float(p50), 4), "p90": round(float(p90), 4)}
+
+
+def copy_ceiling(dev, gib=1.0, reps=10):
+    """HBM rate of a plain device copy (read + write of `gib` GiB each), the
+    measured ceiling beside the 8 TB/s spec peak."""
+    import torch
+    n = int(gib * (1 << 30)) // 4
+    a = torch.empty(n, dtype=torch.float32, device=dev).fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(reps):
+        b.copy_(a)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / reps
+    del a, b
+    return {"kind": f"device copy of {gib:g} GiB (read + write)", "gbs": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}
 
 
 def run_materialized(prc, x, w, steps, warmup):
@@ -200,12 +232,7 @@ def run_materialized(prc, x, w, steps, warmup):
     for i in range(steps):
         step(i, evs[i])
     torch.cuda.synchronize()
-    stage = {"precompute": 0.0, "prefill": 0.0, "decode": 0.0}
-    for e in evs:
-        stage["precompute"] += e[0].elapsed_time(e[1])
-        stage["prefill"] += e[1].elapsed_time(e[2])
-        stage["decode"] += e[2].elapsed_time(e[3])
-    return {k: v / steps for k, v in stage.items()}
+    return {k: sum(v) / steps for k, v in stage_times(evs).items()}
 
 
 # ------------------------------------------------------------- CPU baseline
@@ -581,6 +608,184 @@ def paged(prc, w, dev, steps, warmup):
                           "paged_over_contiguous": round(t_p / t_c, 4), "bitwise_equal": bool(same)}), flush=True)
 
 
+def stack_bench(prc, dev):
+    """The 32-layer stack over 16 turns (8B-shaped layers, 8 agents, rank 16
+    on k and v): turn k (k = 1..16, T = 4096 k, agent k mod 8) precomputes
+    every layer's LR rows of the newest 4096-token segment [T - 4096, T),
+    prefills 256 tokens at [T, T + 256) (a 256-row precompute, then
+    attention), and runs 128 decode steps, each appending one LR row per
+    layer with a 1-row precompute and attending over [0, pos].  Each layer
+    has its own base cache, LR planes, A and B; the base rows are synthetic.
+
+    The 128 x 32 decode steps of a turn are launch-bound at short contexts, so
+    each turn's decode loop is captured once into a HIP graph (before the
+    timed region) and replayed; precompute and prefill launch directly.  The
+    reference materialises each layer's agent K/V once per turn (after
+    computing that turn's LR rows in one pass), then runs the same schedule
+    with plain attention.  One JSON line."""
+    import torch
+    cfg, w = workload_dims(5)
+    ex = cfg.extra
+    n_layers, turns, turn, n_pre, n_dec = cfg.layers, ex["turns"], ex["turn_tokens"], cfg.prefill_tokens, \
+        ex["decode_steps"]
+    hid, n_q, n_kv, d, r, N, theta = w["hidden"], w["n_q"], w["n_kv"], w["d"], w["r"], w["N"], w["theta"]
+    S_cap = turns * turn + n_pre + n_dec
+    g = torch.Generator(device=dev).manual_seed(5005)
+
+    def nrm(shape, std=1.0):
+        x = torch.randn(*shape, generator=g, device=dev, dtype=torch.float32)
+        if std != 1.0:
+            x.mul_(std)
+        return x.to(torch.bfloat16)
+
+    print(f"bench: stack: {n_layers} layers x {S_cap} tokens of base cache", file=sys.stderr, flush=True)
+    bstd = math.sqrt(0.02)
+    K = [nrm((1, S_cap, n_kv, d)) for _ in range(n_layers)]
+    V = [nrm((1, S_cap, n_kv, d)) for _ in range(n_layers)]
+    Lp = [torch.zeros((2, N, S_cap, r), dtype=torch.bfloat16, device=dev) for _ in range(n_layers)]
+    A = [nrm((2 * N * r, hid), 1.0 / math.sqrt(hid)) for _ in range(n_layers)]
+    Bk = [nrm((N, n_kv * d, r), bstd) for _ in range(n_layers)]
+    Bv = [nrm((N, n_kv * d, r), bstd) for _ in range(n_layers)]
+    X_seg = [nrm((turn, hid)) for _ in range(4)]
+    X_pre = [nrm((n_pre, hid)) for _ in range(2)]
+    X_dec = nrm((n_dec, hid))
+    Q_pre = nrm((1, n_pre, n_q, d))
+    Q_dec = nrm((n_dec, 1, n_q, d))
+    O_pre = torch.empty_like(Q_pre)
+    O_dec = torch.empty((1, 1, n_q, d), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(64 << 20, dtype=torch.uint8, device=dev)
+    Kf = [torch.empty_like(K[0]) for _ in range(n_layers)]
+    Vf = [torch.empty_like(V[0]) for _ in range(n_layers)]
+
+    def i32(v):
+        return torch.tensor(v, dtype=torch.int32, device=dev)
+
+    T_of = {k: turn * k for k in range(1, turns + 1)}
+    cap = {k: T_of[k] + n_pre + n_dec for k in T_of}
+    pos_pre = {k: i32([list(range(T_of[k], T_of[k] + n_pre))]) for k in T_of}
+    kvl_pre = {k: i32([T_of[k] + n_pre]) for k in T_of}
+    pos_dec = {k: i32([[T_of[k] + n_pre + j] for j in range(n_dec)]) for k in T_of}
+    kvl_dec = {k: i32([T_of[k] + n_pre + j + 1 for j in range(n_dec)]) for k in T_of}
+    kvl_cap = {k: i32([cap[k]]) for k in T_of}
+
+    def views(k, l, fused):
+        s, a = cap[k], k % N
+        if fused:
+            return (K[l][:, :s], V[l][:, :s], Lp[l][0, a, :s][None], Lp[l][1, a, :s][None], Bk[l][a:a + 1],
+                    Bv[l][a:a + 1])
+        return Kf[l][:, :s], Vf[l][:, :s], None, None, None, None
+
+    def segment(k):
+        for l in range(n_layers):
+            prc.precompute_lr_cache(X_seg[(l + k) % 4], A[l], 2, N, r, Lp[l], tok_offset=T_of[k] - turn)
+
+    def prefill(k, fused):
+        for l in range(n_layers):
+            if fused:
+                prc.precompute_lr_cache(X_pre[(l + k) % 2], A[l], 2, N, r, Lp[l], tok_offset=T_of[k])
+            Kv, Vv, Lk, Lv, B_k, B_v = views(k, l, fused)
+            prc.lr_shared_attention(Q_pre, Kv, Vv, Lk, Lv, B_k, B_v, pos_pre[k], kvl_pre[k], rope_theta=theta,
+                                    O=O_pre, workspace=ws)
+
+    def decode(k, fused):
+        for j in range(n_dec):
+            for l in range(n_layers):
+                if fused:
+                    prc.precompute_lr_cache(X_dec[j:j + 1], A[l], 2, N, r, Lp[l], tok_offset=T_of[k] + n_pre + j)
+                Kv, Vv, Lk, Lv, B_k, B_v = views(k, l, fused)
+                prc.lr_shared_attention(Q_dec[j:j + 1], Kv, Vv, Lk, Lv, B_k, B_v, pos_dec[k][j:j + 1],
+                                        kvl_dec[k][j:j + 1], rope_theta=theta, O=O_dec, workspace=ws)
+
+    def materialise(k):
+        # The reference computes the turn's LR rows in one pass, then writes
+        # each layer's agent K/V over [0, cap).
+        for l in range(n_layers):
+            prc.precompute_lr_cache(X_pre[(l + k) % 2], A[l], 2, N, r, Lp[l], tok_offset=T_of[k])
+            prc.precompute_lr_cache(X_dec, A[l], 2, N, r, Lp[l], tok_offset=T_of[k] + n_pre)
+            Kv, Vv, Lk, Lv, B_k, B_v = views(k, l, True)
+            prc.materialize_agent_kv(Kv, Vv, Lk, Lv, B_k, B_v, kvl_cap[k], rope_theta=theta,
+                                     K_full=Kf[l][:, :cap[k]], V_full=Vf[l][:, :cap[k]])
+
+    def capture(fused):
+        graphs = {}
+        for k in T_of:
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                decode(k, fused)
+            graphs[k] = gr
+            print(f"bench: stack: captured decode of turn {k} ({'LR-shared' if fused else 'materialised'})",
+                  file=sys.stderr, flush=True)
+        return graphs
+
+    def run(fused, graphs):
+        ev = {ph: [] for ph in ("segment", "materialise", "prefill", "decode")}
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for k in T_of:
+            for ph, fn in (("segment", lambda: segment(k)),
+                           ("materialise", (lambda: None) if fused else (lambda: materialise(k))),
+                           ("prefill", lambda: prefill(k, fused)),
+                           ("decode", lambda: graphs[k].replay())):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fn()
+                e1.record()
+                ev[ph].append((e0, e1))
+        t1.record()
+        torch.cuda.synchronize()
+        out = {ph: round(sum(a.elapsed_time(b) for a, b in v), 3) for ph, v in ev.items()}
+        out["total"] = round(t0.elapsed_time(t1), 3)
+        return out
+
+    # Warm-up outside capture (first calls load kernels), then capture.
+    segment(1)
+    prefill(1, True)
+    decode(1, True)
+    materialise(1)
+    prefill(1, False)
+    decode(1, False)
+    torch.cuda.synchronize()
+    g_fused = capture(True)
+    # A replay reproduces the eager result (last turn's last step).
+    g_fused[turns].replay()
+    torch.cuda.synchronize()
+    o_graph = O_dec.clone()
+    decode(turns, True)
+    torch.cuda.synchronize()
+    same = torch.equal(o_graph, O_dec)
+    print("bench: stack: timing the LR-shared run", file=sys.stderr, flush=True)
+    fused = run(True, g_fused)
+    del g_fused
+    g_mat = capture(False)
+    print("bench: stack: timing the materialised run", file=sys.stderr, flush=True)
+    mat = run(False, g_mat)
+    del g_mat
+
+    dec_bytes = 0
+    for k in T_of:
+        for j in range(n_dec):
+            kv = T_of[k] + n_pre + j + 1
+            dec_bytes += n_layers * (kv * n_kv * d * 4 + kv * r * 4 + 2 * n_q * d * 2 + 2 * n_kv * d * r * 2)
+    print(json.dumps({
+        "bench": "workload", "index": 5, "workload": cfg.name,
+        "shape": {"layers": n_layers, "hidden": hid, "n_q_heads": n_q, "n_kv_heads": n_kv, "head_dim": d,
+                  "agents": N, "rank": r, "turns": turns, "turn_tokens": turn, "prefill_tokens": n_pre,
+                  "decode_steps": n_dec, "s_cap": S_cap},
+        "lr_shared_ms": fused, "materialised_ms": mat,
+        "speedup_total": round(mat["total"] / fused["total"], 3),
+        "speedup_decode": round((mat["decode"] + mat["materialise"]) / fused["decode"], 3),
+        "decode_algorithmic_bytes": dec_bytes,
+        "decode_gbs": round(dec_bytes / (fused["decode"] * 1e-3) / 1e9, 1),
+        "decode_hbm_frac": round(dec_bytes / (fused["decode"] * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+        "graph_replay_equals_eager": bool(same),
+        "resident_gb": {"base_cache": round(2 * n_layers * S_cap * n_kv * d * 2 / 1e9, 2),
+                        "lr_planes": round(n_layers * 2 * N * S_cap * r * 2 / 1e9, 2),
+                        "materialised_copy": round(2 * n_layers * S_cap * n_kv * d * 2 / 1e9, 2)},
+    }), flush=True)
+
+
 def workload_bench(prc, index, dev, steps, warmup):
     """Precompute, prefill and decode at the shapes of another workload (the
     8B-shaped layer at 8k context, or the 14B-shaped one at 64k with rank 64),
@@ -681,7 +886,7 @@ def workload_bench(prc, index, dev, steps, warmup):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-materialize", action="store_true")
@@ -701,7 +906,7 @@ def main():
     ap.add_argument("--paged", action="store_true",
                     help="instead of the step: decode, prefill and segment projection over paged (block-table) "
                          "caches, against the same calls over contiguous caches")
-    ap.add_argument("--workload", type=int, choices=(2, 4), default=None,
+    ap.add_argument("--workload", type=int, choices=(2, 4, 5), default=None,
                     help="instead of the step: precompute, prefill and decode at the 8k-context 8B-shaped (2) or "
                          "64k-context 14B-shaped rank-64 (4) workload, against materialise-then-attend")
     args = ap.parse_args()
@@ -730,6 +935,9 @@ def main():
     if args.paged:
         paged(prc, w, dev, args.steps, args.warmup)
         return
+    if args.workload == 5:
+        stack_bench(prc, dev)
+        return
     if args.workload is not None:
         workload_bench(prc, args.workload, dev, args.steps, args.warmup)
         return
@@ -741,7 +949,7 @@ def main():
         pmc_pass(prc, x, w, dev)
         return
     print("bench: timing fused path", file=sys.stderr, flush=True)
-    stage, ms_step, wall_ms = run_fused(prc, x, w, args.steps, args.warmup)
+    stage, ms_step, wall_ms, per_step = run_fused(prc, x, w, args.steps, args.warmup)
 
     dec_gbs = work["decode_bytes"] / (stage["decode"] * 1e-3) / 1e9
     pre_tf = work["prefill_flops"] / (stage["prefill"] * 1e-3) / 1e12
@@ -792,6 +1000,7 @@ def main():
         "roofline": dict(rooflines[dominant], stage=dominant),
         "rooflines": rooflines,
         "host_ms_per_step": round(wall_ms, 4),
+        "stage_ms_percentiles": {k: percentiles(v) for k, v in per_step.items()},
     }
     if not args.no_materialize:
         print("bench: timing materialise-then-attend reference", file=sys.stderr, flush=True)
@@ -804,6 +1013,9 @@ def main():
         }
     del x
     torch.cuda.empty_cache()
+    ceil = copy_ceiling(dev)
+    ceil["decode_frac"] = round(dec_gbs / ceil["gbs"], 4)
+    out["measured_hbm_ceiling"] = ceil
     if not args.no_cpu_baseline:
         print("bench: timing the fp64 oracle on a host sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)

@@ -416,93 +416,95 @@ lrsa_decode_kernel(const AttnArgs a) {
 // log-sum-exp weights, then the deferred up-projection
 // O += (sum_s w_s P_s L_v) B_v, then 1/l.  Decode has one query token per
 // request; a split prefill has n_tok.
-// Four waves each fold a quarter of the splits (independent loads in flight),
-// and the four partial sums meet in LDS.
-constexpr int MW = 4;  // waves per merge workgroup
-
-template <int D, int R>
+// A row's partials are n_splits x (d + r) fp32 beside their maxima and sums.
+// Thread t owns float4 column t % NV of those d + r accumulators for the
+// splits congruent to t / NV modulo the number of such groups, so a
+// workgroup keeps one independent 16-byte load per thread and split group
+// in flight; the groups' sums then meet in LDS.  Rows with many splits
+// (small decode batches) take 16-wave workgroups, rows with few 4-wave ones.
+template <int D, int R, int MW>
 __global__ void __launch_bounds__(64 * MW)
 lrsa_merge_kernel(const AttnArgs a) {
-  constexpr int PS = 4 + D + R, DPL = D / 64;
-  __shared__ float red_acc[MW][D];
-  __shared__ float red_lr[MW][64];
-  __shared__ float red_l[MW];
-  __shared__ float red_m[MW];
+  constexpr int PS = 4 + D + R, NT = 64 * MW;
+  constexpr int NV = (D + R) / 4;  // float4 columns of the accumulators
+  constexpr int NG = NT / NV;      // split groups
+  __shared__ float red[NG][D + R];
+  __shared__ float red_w[MW][2];
+  __shared__ float fin[D + R];
   const int h = blockIdx.x, bi = blockIdx.y, tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int b = bi / a.n_tok;  // bi = request * n_tok + query token
   const int g = h / a.group;
   const bool has_lv = a.Lv != nullptr;
+  const int ns = a.n_splits;
   const int64_t orow = (int64_t)bi * a.n_q + h;  // (request, token, head) row of O
-  const float* base = a.ws + orow * (int64_t)a.n_splits * PS;
+  const float* base = a.ws + orow * (int64_t)ns * PS;
 
+  // Global maximum over the splits.
   float M = -INFINITY;
-  for (int s = tid; s < a.n_splits; s += 64 * MW) M = fmaxf(M, base[(int64_t)s * PS]);
+  for (int s = tid; s < ns; s += NT) M = fmaxf(M, base[(int64_t)s * PS]);
 #pragma unroll
   for (int x = 1; x < 64; x <<= 1) M = fmaxf(M, shfl_xor(M, x));
-  if (lane == 0) red_m[w] = M;
+  if (lane == 0) red_w[w][0] = M;
   __syncthreads();
 #pragma unroll
-  for (int i = 0; i < MW; ++i) M = fmaxf(M, red_m[i]);
+  for (int i = 0; i < MW; ++i) M = fmaxf(M, red_w[i][0]);
   const float Ms = (M == -INFINITY) ? 0.f : M;
 
-  float L = 0.f, accl = 0.f, acc[DPL];
-#pragma unroll
-  for (int dd = 0; dd < DPL; ++dd) acc[dd] = 0.f;
-#pragma unroll 4
-  for (int s = w; s < a.n_splits; s += MW) {
+  // Row sum L = sum_s w_s l_s.
+  float L = 0.f;
+  for (int s = tid; s < ns; s += NT) {
     const float* p = base + (int64_t)s * PS;
-    const float wgt = fast_exp2(p[0] - Ms);
-    L += wgt * p[1];
-#pragma unroll
-    for (int dd = 0; dd < DPL; ++dd) acc[dd] += wgt * p[4 + lane + 64 * dd];
-    if (has_lv && lane < R) accl += wgt * p[4 + D + lane];
+    L += fast_exp2(p[0] - Ms) * p[1];
   }
 #pragma unroll
-  for (int dd = 0; dd < DPL; ++dd) red_acc[w][lane + 64 * dd] = acc[dd];
-  red_lr[w][lane] = accl;
-  if (lane == 0) red_l[w] = L;
+  for (int x = 1; x < 64; x <<= 1) L += shfl_xor(L, x);
+
+  // Weighted accumulators (d of P V, r of P L_v), one float4 column per thread.
+  const int grp = tid / NV, v = tid - grp * NV;
+  const int nv_used = has_lv ? NV : D / 4;
+  if (grp < NG && v < nv_used) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+    for (int s = grp; s < ns; s += NG) {
+      const float* p = base + (int64_t)s * PS;
+      const float wgt = fast_exp2(p[0] - Ms);
+      const f32x4 x = *reinterpret_cast<const f32x4*>(p + 4 + 4 * v);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) acc[c] += wgt * x[c];
+    }
+    *reinterpret_cast<f32x4*>(&red[grp][4 * v]) = acc;
+  }
+  if (lane == 0) red_w[w][1] = L;
   __syncthreads();
-  if (w != 0) return;
-#pragma unroll
-  for (int dd = 0; dd < DPL; ++dd) {
-    acc[dd] = 0.f;
-#pragma unroll
-    for (int i = 0; i < MW; ++i) acc[dd] += red_acc[i][lane + 64 * dd];
+  for (int c = tid; c < D + R; c += NT) {
+    float t = 0.f;
+    if (c < D || has_lv)
+      for (int i = 0; i < NG; ++i) t += red[i][c];
+    fin[c] = t;
   }
   L = 0.f;
 #pragma unroll
-  for (int i = 0; i < MW; ++i) L += red_l[i];
-  if (has_lv) {
-    // The four waves' P L_v sums, added in lane order into red_lr[0].
-    float t = 0.f;
-#pragma unroll
-    for (int i = 0; i < MW; ++i) t += red_lr[i][lane];
-    __builtin_amdgcn_wave_barrier();
-    red_lr[0][lane] = t;
-    __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int dd = 0; dd < DPL; ++dd) {
-      const int dim = lane + 64 * dd;
+  for (int i = 0; i < MW; ++i) L += red_w[i][1];
+  __syncthreads();
+
+  // O = (acc + (sum_s w_s P_s L_v) B_v) / L, one head dim per thread.
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  uint16_t* o = a.O + orow * D;
+  for (int dim = tid; dim < D; dim += NT) {
+    float sum = fin[dim];
+    if (has_lv) {
       const uint16_t* bv = a.Bv + (int64_t)b * a.b_stride + ((int64_t)g * D + dim) * R;
-      float sum = 0.f;
 #pragma unroll
       for (int j = 0; j < R; j += 8) {
         const u32x4 u = *reinterpret_cast<const u32x4*>(bv + j);
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          sum += red_lr[0][j + 2 * c] * bf_lo(u[c]) + red_lr[0][j + 2 * c + 1] * bf_hi(u[c]);
+        for (int c = 0; c < 4; ++c) sum += fin[D + j + 2 * c] * bf_lo(u[c]) + fin[D + j + 2 * c + 1] * bf_hi(u[c]);
       }
-      acc[dd] += sum;
     }
+    const uint32_t pk = pack_bf16(sum * inv, 0.f);
+    o[dim] = (uint16_t)(pk & 0xffffu);
   }
-  const float inv = L > 0.f ? 1.f / L : 0.f;
-  uint16_t* o = a.O + orow * D;
-#pragma unroll
-  for (int dd = 0; dd < DPL; ++dd) {
-    const uint32_t pk = pack_bf16(acc[dd] * inv, 0.f);
-    o[lane + 64 * dd] = (uint16_t)(pk & 0xffffu);
-  }
-  if (a.lse != nullptr && lane == 0)
+  if (a.lse != nullptr && tid == 0)
     a.lse[orow] = L > 0.f ? (M + __log2f(L)) * kLn2 : -INFINITY;
 }
 
@@ -812,6 +814,16 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
 }
 
 template <int D, int R>
+hipError_t launch_merge_t(const AttnArgs& a, hipStream_t st) {
+  const dim3 grid(a.n_q, a.batch * a.n_tok);
+  if (a.n_splits > 64)
+    hipLaunchKernelGGL((lrsa_merge_kernel<D, R, 16>), grid, dim3(64 * 16), 0, st, a);
+  else
+    hipLaunchKernelGGL((lrsa_merge_kernel<D, R, 4>), grid, dim3(64 * 4), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int D, int R>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   using C = Dec<D, R>;
   const int hg = (a.n_kv + C::NW - 1) / C::NW;
@@ -822,8 +834,7 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((lrsa_decode_kernel<D, R, false>), grid, dim3(C::NT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch * a.n_tok), dim3(64 * MW), 0, st, a);
-  return hipGetLastError();
+  return launch_merge_t<D, R>(a, st);
 }
 
 template <int D, int R>
@@ -833,14 +844,7 @@ hipError_t launch_shared_t(const AttnArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((lrsa_decode_shared_kernel<D, R>), dim3(a.n_splits, a.n_kv, rg), dim3(C::NT), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch * a.n_tok), dim3(64 * MW), 0, st, a);
-  return hipGetLastError();
-}
-
-template <int D, int R>
-hipError_t launch_merge_t(const AttnArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((lrsa_merge_kernel<D, R>), dim3(a.n_q, a.batch * a.n_tok), dim3(64 * MW), 0, st, a);
-  return hipGetLastError();
+  return launch_merge_t<D, R>(a, st);
 }
 
 template <int D>

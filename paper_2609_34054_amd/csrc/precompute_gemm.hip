@@ -275,9 +275,53 @@ hipError_t launch_tb(const PrecomputeArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// A handful of rows (the LR rows of newly decoded tokens) is a matrix-vector
+// product: one wave per output column streams that column's row of A_rows
+// (contiguous along d_in, 16 bytes per lane and step) against the T <= GV_T
+// rows of X, which every wave reads from L2, then reduces over its lanes.
+// This spreads A over n_cols workgroups instead of the few tiles the GEMM
+// would have.
+constexpr int GV_T = 4;
+
+__global__ void __launch_bounds__(64) precompute_gemv_kernel(const PrecomputeArgs a) {
+  const int lane = threadIdx.x;
+  const int c = blockIdx.x;  // output column: plane c / r, rank c % r
+  const uint16_t* arow = a.A + (int64_t)c * a.d_in;
+  const int T = (int)a.T;
+  float acc[GV_T] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int64_t k = (int64_t)lane * 8; k < a.d_in; k += 512) {
+    const u32x4 av = *reinterpret_cast<const u32x4*>(arow + k);
+#pragma unroll
+    for (int t = 0; t < GV_T; ++t) {
+      if (t < T) {
+        const u32x4 xv = *reinterpret_cast<const u32x4*>(a.X + t * a.ld_x + k);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[t] += bf_lo(av[e]) * bf_lo(xv[e]) + bf_hi(av[e]) * bf_hi(xv[e]);
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < GV_T; ++t)
+#pragma unroll
+    for (int x = 1; x < 64; x <<= 1) acc[t] += shfl_xor(acc[t], x);
+  if (lane < T) {
+    float v = acc[0];
+#pragma unroll
+    for (int t = 1; t < GV_T; ++t)
+      if (lane == t) v = acc[t];
+    const int64_t plane = c / a.rank, j = c - plane * a.rank;
+    a.L[(plane * a.s_cap + a.tok_offset + lane) * a.rank + j] = (uint16_t)(pack_bf16(v, 0.f) & 0xffffu);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t st) {
+  if (a.nkv == 0 && a.tbl == nullptr && a.T <= GV_T) {
+    hipLaunchKernelGGL(precompute_gemv_kernel, dim3(a.n_cols), dim3(64), 0, st, a);
+    return hipGetLastError();
+  }
   // 128-wide tiles halve the bytes loaded per MFMA but need enough of them to
   // fill the 256 CUs; the K/V boundary must fall on a tile edge.
   const int64_t wide = (int64_t)((2 * a.nkv + a.n_cols + 127) / 128) * ((a.T + 127) / 128);

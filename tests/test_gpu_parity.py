@@ -30,6 +30,11 @@ PRE_CASES = [
     ("r32_single_proj", 130, 512, 1, 5, 32, 3, 200),
     ("r64", 64, 128, 2, 1, 64, 0, 64),
     ("one_row", 1, 4096, 2, 8, 16, 31, 32),
+    # 1-4 rows take the matrix-vector kernel (one wave per output column).
+    ("gemv_t2_r8", 2, 4096, 2, 3, 8, 7, 9),
+    ("gemv_t3_ragged_d_in", 3, 264, 2, 2, 16, 5, 100),
+    ("gemv_t4_r64", 4, 520, 1, 3, 64, 0, 4),
+    ("gemm_t5", 5, 520, 2, 2, 32, 1, 6),
     ("c2_chunk", 512, 4096, 2, 4, 16, 8192, 8704),
     ("c3_segment", 4096, 4096, 2, 8, 16, 32768, 36864),
     ("c4_chunk", 2048, 5120, 2, 6, 64, 0, 2048),
@@ -395,3 +400,115 @@ def test_tiny_workload_full_chain():
                                                  pos.numpy(), kvl.numpy(), cfg.theta)
             mx, mean = attn_errors(O, Oref)
             assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (n_tok, a, mx, mean)
+
+
+def test_multi_turn_stack_chain():
+    """The 32-layer multi-turn schedule at small scale (2 layers, 3 turns of
+    256 tokens, 32-token prefills, 3 decode steps): per turn, a segment
+    precompute per layer, a prefill whose LR rows come from a 32-row
+    precompute, and decode steps that each append one LR row (1-row
+    precompute) before attending.  Every attention output is checked against
+    the oracle run on its own fp64 LR rows of the same hidden states; the
+    last turn's decode loop, captured in a HIP graph, is replayed three times
+    with eager work in between and must equal the eager outputs bitwise."""
+    n_layers, turns, turn, n_pre, n_dec = 2, 3, 256, 32, 3
+    hid, n_q, n_kv, d, r, N, theta = 256, 8, 2, 128, 16, 3, 5e5
+    S_cap = turns * turn + n_pre + n_dec
+    seed = iter(range(9100, 9999))
+
+    def rnd(shape, std=1.0):
+        return normal_bf16(shape, std, next(seed))
+
+    K = [rnd((1, S_cap, n_kv, d)) for _ in range(n_layers)]
+    V = [rnd((1, S_cap, n_kv, d)) for _ in range(n_layers)]
+    A = [rnd((2 * N * r, hid), 1.0 / math.sqrt(hid)) for _ in range(n_layers)]
+    Bk = [rnd((N, n_kv * d, r), math.sqrt(0.02)) for _ in range(n_layers)]
+    Bv = [rnd((N, n_kv * d, r), math.sqrt(0.02)) for _ in range(n_layers)]
+    X_seg = [rnd((turn, hid)) for _ in range(turns)]
+    X_pre = [rnd((n_pre, hid)) for _ in range(turns)]
+    X_dec = [rnd((n_dec, hid)) for _ in range(turns)]
+    Q_pre = rnd((1, n_pre, n_q, d))
+    Q_dec = rnd((n_dec, 1, n_q, d))
+    g = {k: [t.cuda() for t in v] for k, v in dict(K=K, V=V, A=A, Bk=Bk, Bv=Bv).items()}
+    Lp = [torch.zeros((2, N, S_cap, r), dtype=torch.bfloat16, device="cuda") for _ in range(n_layers)]
+    L_or = [np.zeros((2, N, S_cap, r)) for _ in range(n_layers)]
+    Xg = {k: [t.cuda() for t in v] for k, v in dict(seg=X_seg, pre=X_pre, dec=X_dec).items()}
+    Qg_pre, Qg_dec = Q_pre.cuda(), Q_dec.cuda()
+
+    def append(l, X, Xc, off):
+        prc.precompute_lr_cache(Xc, g["A"][l], 2, N, r, Lp[l], tok_offset=off)
+        L_or[l][:, :, off:off + X.shape[0]] = oracle.precompute_lr_cache(f64(X), f64(A[l]).T, 2, N, r)
+
+    def attend(k, l, Qc, Qh, pos, kvl, O):
+        s, a = turn * (k + 1) + n_pre + n_dec, (k + 1) % N
+        prc.lr_shared_attention(Qc, g["K"][l][:, :s], g["V"][l][:, :s], Lp[l][0, a, :s][None],
+                                Lp[l][1, a, :s][None], g["Bk"][l][a:a + 1], g["Bv"][l][a:a + 1],
+                                pos.cuda(), kvl.cuda(), rope_theta=theta, O=O)
+        ref, _ = oracle.lr_shared_attention(f64(Qh), f64(K[l][:, :s]), f64(V[l][:, :s]), L_or[l][0, a, :s][None],
+                                            L_or[l][1, a, :s][None], b_paper(Bk[l][a:a + 1]),
+                                            b_paper(Bv[l][a:a + 1]), pos.numpy(), kvl.numpy(), theta)
+        return ref
+
+    checks = []
+    for k in range(turns):
+        T = turn * (k + 1)
+        for l in range(n_layers):
+            append(l, X_seg[k], Xg["seg"][k], T - turn)
+        for l in range(n_layers):
+            append(l, X_pre[k], Xg["pre"][k], T)
+            O = torch.empty((1, n_pre, n_q, d), dtype=torch.bfloat16, device="cuda")
+            pos = torch.arange(T, T + n_pre, dtype=torch.int32)[None]
+            ref = attend(k, l, Qg_pre, Q_pre, pos, torch.tensor([T + n_pre], dtype=torch.int32), O)
+            checks.append((("prefill", k, l), O, ref))
+        for j in range(n_dec):
+            p = T + n_pre + j
+            for l in range(n_layers):
+                append(l, X_dec[k][j:j + 1], Xg["dec"][k][j:j + 1], p)
+                O = torch.empty((1, 1, n_q, d), dtype=torch.bfloat16, device="cuda")
+                ref = attend(k, l, Qg_dec[j:j + 1], Q_dec[j:j + 1], torch.tensor([[p]], dtype=torch.int32),
+                             torch.tensor([p + 1], dtype=torch.int32), O)
+                checks.append((("decode", k, j, l), O, ref))
+    torch.cuda.synchronize()
+    for what, O, ref in checks:
+        mx, mean = attn_errors(O, ref)
+        assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (what, mx, mean)
+
+    # The last turn's decode loop as a HIP graph: device-resident positions,
+    # preallocated outputs and workspace, nothing allocated inside.
+    k = turns - 1
+    T = turn * turns
+    s, a = T + n_pre + n_dec, turns % N
+    pos_d = torch.tensor([[T + n_pre + j] for j in range(n_dec)], dtype=torch.int32, device="cuda")
+    kvl_d = pos_d[:, 0] + 1
+    O_all = torch.empty((n_dec, n_layers, 1, 1, n_q, d), dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(1 << 20, dtype=torch.uint8, device="cuda")
+
+    def loop():
+        for j in range(n_dec):
+            for l in range(n_layers):
+                prc.precompute_lr_cache(Xg["dec"][k][j:j + 1], g["A"][l], 2, N, r, Lp[l], tok_offset=T + n_pre + j)
+                prc.lr_shared_attention(Qg_dec[j:j + 1], g["K"][l][:, :s], g["V"][l][:, :s],
+                                        Lp[l][0, a, :s][None], Lp[l][1, a, :s][None], g["Bk"][l][a:a + 1],
+                                        g["Bv"][l][a:a + 1], pos_d[j:j + 1], kvl_d[j:j + 1], rope_theta=theta,
+                                        O=O_all[j, l], workspace=ws)
+
+    loop()
+    torch.cuda.synchronize()
+    eager = O_all.clone()
+    for (what, O, _) in checks:
+        if what[0] == "decode" and what[1] == k:
+            assert torch.equal(O, eager[what[2], what[3]]), what
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        loop()
+    for rep in range(3):
+        O_all.zero_()
+        # Eager work between replays: a prefill over the same caches.
+        prc.lr_shared_attention(Qg_pre, g["K"][0][:, :s], g["V"][0][:, :s], Lp[0][0, a, :s][None],
+                                Lp[0][1, a, :s][None], g["Bk"][0][a:a + 1], g["Bv"][0][a:a + 1],
+                                torch.arange(T, T + n_pre, dtype=torch.int32, device="cuda")[None],
+                                torch.tensor([T + n_pre], dtype=torch.int32, device="cuda"), rope_theta=theta)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(O_all, eager), rep
