@@ -276,21 +276,25 @@ hipError_t launch_tb(const PrecomputeArgs& a, hipStream_t st) {
 }
 
 // A handful of rows (the LR rows of newly decoded tokens) is a matrix-vector
-// product: one wave per output column streams that column's row of A_rows
-// (contiguous along d_in, 16 bytes per lane and step) against the T <= GV_T
-// rows of X, which every wave reads from L2, then reduces over its lanes.
-// This spreads A over n_cols workgroups instead of the few tiles the GEMM
-// would have.
+// product: one workgroup per output column streams that column's row of
+// A_rows (contiguous along d_in; 4 waves x 64 lanes x 16 bytes = 4096
+// elements per step, so a 4096-wide row is one load per lane) against the
+// T <= GV_T rows of X, which every workgroup reads from L2, then reduces over
+// lanes and waves.  This spreads A over n_cols workgroups instead of the few
+// tiles the GEMM would have, and keeps a whole row's loads in flight at once
+// (the rows of A are usually cold in the decode loop).
 constexpr int GV_T = 4;
+constexpr int GV_W = 4;  // waves per column
 
-__global__ void __launch_bounds__(64) precompute_gemv_kernel(const PrecomputeArgs a) {
-  const int lane = threadIdx.x;
+__global__ void __launch_bounds__(64 * GV_W) precompute_gemv_kernel(const PrecomputeArgs a) {
+  __shared__ float red[GV_W][GV_T];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int c = blockIdx.x;  // output column: plane c / r, rank c % r
   const uint16_t* arow = a.A + (int64_t)c * a.d_in;
   const int T = (int)a.T;
   float acc[GV_T] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int64_t k = (int64_t)lane * 8; k < a.d_in; k += 512) {
+#pragma unroll 2
+  for (int64_t k = (int64_t)tid * 8; k < a.d_in; k += 64 * GV_W * 8) {
     const u32x4 av = *reinterpret_cast<const u32x4*>(arow + k);
 #pragma unroll
     for (int t = 0; t < GV_T; ++t) {
@@ -302,16 +306,18 @@ __global__ void __launch_bounds__(64) precompute_gemv_kernel(const PrecomputeArg
     }
   }
 #pragma unroll
-  for (int t = 0; t < GV_T; ++t)
+  for (int t = 0; t < GV_T; ++t) {
 #pragma unroll
     for (int x = 1; x < 64; x <<= 1) acc[t] += shfl_xor(acc[t], x);
-  if (lane < T) {
-    float v = acc[0];
+    if (lane == 0) red[w][t] = acc[t];
+  }
+  __syncthreads();
+  if (tid < T) {
+    float v = 0.f;
 #pragma unroll
-    for (int t = 1; t < GV_T; ++t)
-      if (lane == t) v = acc[t];
+    for (int i = 0; i < GV_W; ++i) v += red[i][tid];
     const int64_t plane = c / a.rank, j = c - plane * a.rank;
-    a.L[(plane * a.s_cap + a.tok_offset + lane) * a.rank + j] = (uint16_t)(pack_bf16(v, 0.f) & 0xffffu);
+    a.L[(plane * a.s_cap + a.tok_offset + tid) * a.rank + j] = (uint16_t)(pack_bf16(v, 0.f) & 0xffffu);
   }
 }
 
@@ -319,7 +325,7 @@ __global__ void __launch_bounds__(64) precompute_gemv_kernel(const PrecomputeArg
 
 hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t st) {
   if (a.nkv == 0 && a.tbl == nullptr && a.T <= GV_T) {
-    hipLaunchKernelGGL(precompute_gemv_kernel, dim3(a.n_cols), dim3(64), 0, st, a);
+    hipLaunchKernelGGL(precompute_gemv_kernel, dim3(a.n_cols), dim3(64 * GV_W), 0, st, a);
     return hipGetLastError();
   }
   // 128-wide tiles halve the bytes loaded per MFMA but need enough of them to
