@@ -813,8 +813,84 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
   }
 }
 
+// The same merge for rows with at most 16 splits (split prefill, longer
+// decode splits): one wave per row and four rows per workgroup.  Lane s < ns
+// reads split s's maximum and sum; lane v < (d + r)/4 owns float4 column v of
+// the accumulators and folds every split into it (all loads of the row in
+// flight at once); the row's (d + r) sums then pass through LDS for the
+// B_v product.
+constexpr int MR_ROWS = 4;
+
+template <int D, int R>
+__global__ void __launch_bounds__(64 * MR_ROWS) lrsa_merge_rows_kernel(const AttnArgs a, int64_t n_rows) {
+  constexpr int PS = 4 + D + R, NV = (D + R) / 4;
+  static_assert(NV <= 64, "one lane per float4 column");
+  __shared__ __attribute__((aligned(16))) float fin[MR_ROWS][D + R];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t orow = (int64_t)blockIdx.x * MR_ROWS + w;  // (request, token, head) row of O
+  if (orow >= n_rows) return;
+  const int ns = a.n_splits;
+  const int h = (int)(orow % a.n_q);
+  const int b = (int)(orow / a.n_q / a.n_tok);
+  const int g = h / a.group;
+  const bool has_lv = a.Lv != nullptr;
+  const float* base = a.ws + orow * (int64_t)ns * PS;
+
+  const float m_s = lane < ns ? base[(int64_t)lane * PS] : -INFINITY;
+  const float l_s = lane < ns ? base[(int64_t)lane * PS + 1] : 0.f;
+  float M = m_s;
+#pragma unroll
+  for (int x = 1; x < 64; x <<= 1) M = fmaxf(M, shfl_xor(M, x));
+  const float Ms = (M == -INFINITY) ? 0.f : M;
+  const float w_s = lane < ns ? fast_exp2(m_s - Ms) : 0.f;
+  float L = w_s * l_s;
+#pragma unroll
+  for (int x = 1; x < 64; x <<= 1) L += shfl_xor(L, x);
+
+  const int nv_used = has_lv ? NV : D / 4;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  const int v = lane < nv_used ? lane : 0;
+#pragma unroll 4
+  for (int s = 0; s < ns; ++s) {
+    const float wgt = __shfl(w_s, s, 64);
+    const f32x4 x = *reinterpret_cast<const f32x4*>(base + (int64_t)s * PS + 4 + 4 * v);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[c] += wgt * x[c];
+  }
+  if (lane < nv_used) *reinterpret_cast<f32x4*>(&fin[w][4 * lane]) = acc;
+  __builtin_amdgcn_wave_barrier();
+
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  uint16_t* o = a.O + orow * D;
+#pragma unroll
+  for (int dd = 0; dd < D / 64; ++dd) {
+    const int dim = lane + 64 * dd;
+    float sum = fin[w][dim];
+    if (has_lv) {
+      const uint16_t* bv = a.Bv + (int64_t)b * a.b_stride + ((int64_t)g * D + dim) * R;
+#pragma unroll
+      for (int j = 0; j < R; j += 8) {
+        const u32x4 u = *reinterpret_cast<const u32x4*>(bv + j);
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          sum += fin[w][D + j + 2 * c] * bf_lo(u[c]) + fin[w][D + j + 2 * c + 1] * bf_hi(u[c]);
+      }
+    }
+    const uint32_t pk = pack_bf16(sum * inv, 0.f);
+    o[dim] = (uint16_t)(pk & 0xffffu);
+  }
+  if (a.lse != nullptr && lane == 0)
+    a.lse[orow] = L > 0.f ? (M + __log2f(L)) * kLn2 : -INFINITY;
+}
+
 template <int D, int R>
 hipError_t launch_merge_t(const AttnArgs& a, hipStream_t st) {
+  if (a.n_splits <= 16) {
+    const int64_t n_rows = (int64_t)a.batch * a.n_tok * a.n_q;
+    hipLaunchKernelGGL((lrsa_merge_rows_kernel<D, R>), dim3((unsigned)((n_rows + MR_ROWS - 1) / MR_ROWS)),
+                       dim3(64 * MR_ROWS), 0, st, a, n_rows);
+    return hipGetLastError();
+  }
   const dim3 grid(a.n_q, a.batch * a.n_tok);
   if (a.n_splits > 64)
     hipLaunchKernelGGL((lrsa_merge_kernel<D, R, 16>), grid, dim3(64 * 16), 0, st, a);

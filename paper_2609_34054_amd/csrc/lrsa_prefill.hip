@@ -829,20 +829,29 @@ hipError_t launch_r(const AttnArgs& a, hipStream_t st) {
 }  // namespace
 
 void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int* splits, int* split_tiles) {
-  // Units of work without a split: (row tile, KV head, request).  A call with
-  // fewer than two rounds of one workgroup per CU splits the KV tiles so that
-  // there are about four, each split at least 8 tiles long.
+  // Units of work without a split: (row tile, KV head, request), one
+  // workgroup per CU at a time.  Splitting the KV tiles ns ways gives
+  // units * ns workgroups of 1/ns the work, so the time per CU goes as
+  // ceil(units * ns / CUs) / ns.  Take the ns in 1..8 (splits at least 8
+  // tiles long) that minimises it, the smallest on ties: every split adds
+  // partials to write and merge.
+  constexpr int64_t kCUs = 256;
   const int64_t rows = (int64_t)n_tok * group;
   const int64_t units = ((rows + BROWS - 1) / BROWS) * n_kv * (batch > 0 ? batch : 1);
   const int64_t tiles = (s_cap + TKV - 1) / TKV;
+  int64_t best = 1;
+  double best_cost = (double)((units + kCUs - 1) / kCUs);
+  for (int64_t ns = 2; ns <= 8 && ns <= tiles / 8; ++ns) {
+    const double cost = (double)((units * ns + kCUs - 1) / kCUs) / (double)ns;
+    if (cost < best_cost - 1e-9) {
+      best = ns;
+      best_cost = cost;
+    }
+  }
   *splits = 1;
   *split_tiles = (int)(tiles > 0 ? tiles : 1);
-  if (units >= 512) return;
-  int64_t ns = (1024 + units - 1) / units;
-  if (ns > 8) ns = 8;
-  if (ns > tiles / 8) ns = tiles / 8;
-  if (ns < 2) return;
-  const int64_t st = (tiles + ns - 1) / ns;
+  if (best < 2) return;
+  const int64_t st = (tiles + best - 1) / best;
   *splits = (int)((tiles + st - 1) / st);
   *split_tiles = (int)st;
 }
