@@ -130,6 +130,9 @@ struct Unit {
   typename Ex<R>::Frag lk[Ex<R>::NC];  // L_k row of that token (expansion B operand)
   u32x4 v[Pre<D, R>::NHB];        // V_base half blocks (32 tokens x 16 dims, A layout)
   u32x4 lv[Pre<D, R>::NLP];       // L_v half blocks (32 tokens x 16 ranks, A layout)
+  // Ranks >= 32: L_v of the V half blocks' 32 tokens, all ranks in 16-rank
+  // chunks (A layout), for V = V_base + L_v B_v rebuilt on chip.
+  u32x4 lvv[R >= 32 ? R / 16 : 1];
 };
 
 // PAGED: the caches are pools reached through block tables (a separate
@@ -138,10 +141,18 @@ template <int D, int R, bool LK, bool LV, bool PAGED>
 __global__ void __launch_bounds__(NTHR)
 lrsa_prefill_kernel(const AttnArgs a) {
   using C = Pre<D, R>;
-  constexpr bool ones_sum = LV && R < 32;
+  // Value side: ranks below 32 keep associativity, P V_base + (P L_v) B_v,
+  // with the softmax row sums in a spare row of (P L_v)^T.  From rank 32 on
+  // the tile's V = V_base + L_v B_v is rebuilt on chip instead: per 64-token
+  // tile a workgroup then spends 2 * 64 * d * r flop on the expansion rather
+  // than 2 * 256 * 64 * r on P L_v, and needs no (P L_v)^T accumulator.
+  constexpr bool VREB = LV && R >= 32;
+  constexpr bool LVA = LV && !VREB;
+  constexpr int NRB = LVA ? Pre<D, R>::RB : 1;
+  constexpr bool ones_sum = LVA && R < 32;
   __shared__ __attribute__((aligned(16))) uint16_t k_lds[2][TKV * C::K_ROW];
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][TKV * D];  // V^T fragments
-  __shared__ __attribute__((aligned(16))) uint16_t lv_lds[LV ? 2 : 1][LV ? TKV * 32 * C::RB : 8];  // L_v^T fragments
+  __shared__ __attribute__((aligned(16))) uint16_t lv_lds[LVA ? 2 : 1][LVA ? TKV * 32 * C::RB : 8];  // L_v^T fragments
   __shared__ __attribute__((aligned(16))) float2 base_cs[2][C::HALF];
   // cos/sin of each build lane's in-tile offset at its SEG frequencies,
   // [wave][pair of frequencies][lane] (one 16-byte read per pair).
@@ -193,10 +204,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int64_t kv_hi = (int64_t)s_maxpos + 1;  // keys [0, kv_hi) are needed
   const int n_tiles = (int)((kv_hi + TKV - 1) / TKV);
   // Tiles [0, n_full) lie wholly at or below every row's last visible key:
-  // no row needs a mask there and every wave attends them.  Rank 64 keeps
-  // the per-half loop for all tiles: the straight-line main loop needs more
-  // registers than it has.
-  constexpr bool kMainLoop = R < 64;
+  // no row needs a mask there and every wave attends them.  Rank 64 with key
+  // LR keeps the per-half loop for all tiles: with it the straight-line main
+  // loop needs more registers than there are (16 spilled against 4).
+  constexpr bool kMainLoop = R < 64 || (VREB && !LK);
   const int n_full_raw = s_minpos < 0 ? 0 : (int)(((int64_t)s_minpos + 1) / TKV);
   const int n_full = !kMainLoop ? 0 : (n_full_raw < n_tiles ? n_full_raw : n_tiles);
   // This workgroup's tiles: all of them, or its split's share.
@@ -239,7 +250,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
     }
   // L_v half blocks of this wave (waves < 2 RB): tokens 32 ltb.., ranks 32 lrb..
   const int ltb = w & 1, lrb = w >> 1;
-  const bool lv_wave = LV && w < 2 * C::RB;
+  const bool lv_wave = LVA && w < 2 * C::RB;
   // B_k^T fragment (16x16x16 A operand) of low block i (i < NBW) or of its
   // RoPE partner (i >= NBW), rank chunk rc: lane = dim row, 4 ranks from q*4.
   const uint16_t* bhead = LK ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr;
@@ -291,6 +302,21 @@ lrsa_prefill_kernel(const AttnArgs a) {
     const int r0 = 32 * lrb + 16 * p + (lane >> 5) * 8;
     offlv[p] = r0 < R ? (32 * ltb + (lane & 31)) * R * 2 + r0 * 2 : INT32_MIN;
   }
+  // Ranks >= 32: L_v of the V block's tokens (A operand: lane = token l%32,
+  // ranks 16 kc + (l/32)*8 ..) and B_v of its 32 dims (B operand: lane =
+  // dim column l%32, same ranks), so that the expansion lands in the layout
+  // of the V transpose.
+  int32_t offlvv[VREB ? R / 16 : 1];
+  u32x4 bvf[VREB ? R / 16 : 1];
+  if constexpr (VREB) {
+    const uint16_t* bvp =
+        a.Bv + (int64_t)b * a.b_stride + ((int64_t)g * D + 32 * vdb + (lane & 31)) * R + (lane >> 5) * 8;
+#pragma unroll
+    for (int kc = 0; kc < R / 16; ++kc) {
+      offlvv[kc] = (32 * vtb + (lane & 31)) * R * 2 + (16 * kc + (lane >> 5) * 8) * 2;
+      bvf[kc] = ld16(bvp + 16 * kc, true);
+    }
+  }
   // Tiles are loaded in token order, so paged caches are walked with them.
   auto load_unit = [&](Unit<D, R>& u, int64_t t0) {
     // Valid rows of this tile; a tile at or past kv_hi gets empty resources
@@ -329,10 +355,15 @@ lrsa_prefill_kernel(const AttnArgs a) {
     }
 #pragma unroll
     for (int hb = 0; hb < C::NHB; ++hb) u.v[hb] = buf_ld16(rv, offv[hb]);
-    if constexpr (LV) {
+    if constexpr (LVA) {
       const auto rl = make_rsrc(Lv + lr * R, rows * R * 2);
 #pragma unroll
       for (int p = 0; p < C::NLP; ++p) u.lv[p] = lv_wave ? buf_ld16(rl, offlv[p]) : u32x4{0u, 0u, 0u, 0u};
+    }
+    if constexpr (VREB) {
+      const auto rl = make_rsrc(Lv + lr * R, rows * R * 2);
+#pragma unroll
+      for (int kc = 0; kc < R / 16; ++kc) u.lvv[kc] = buf_ld16(rl, offlvv[kc]);
     }
   };
   auto rebuild = [&](const Unit<D, R>& u, int buf) {
@@ -371,10 +402,15 @@ lrsa_prefill_kernel(const AttnArgs a) {
     st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + C::HALF + lo_dim0, hi);
     {
       // Transpose the V half blocks on the MFMA and store them as fragments
-      // (2 vtb, vdb) and (2 vtb + 1, vdb).
+      // (2 vtb, vdb) and (2 vtb + 1, vdb); from rank 32 on the transpose
+      // accumulates onto L_v B_v of the same tokens and dims.
       f32x16 t;
 #pragma unroll
       for (int j = 0; j < 16; ++j) t[j] = 0.f;
+      if constexpr (VREB) {
+#pragma unroll
+        for (int kc = 0; kc < R / 16; ++kc) t = mfma32x32x16(as_bf16x8(u.lvv[kc]), as_bf16x8(bvf[kc]), t);
+      }
 #pragma unroll
       for (int hb = 0; hb < C::NHB; ++hb) t = mfma32x32x16(as_bf16x8(u.v[hb]), as_bf16x8(vid[vp0 + hb]), t);
       // With one half block per wave (d = 64) the wave owns only its 16 dims
@@ -389,7 +425,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
         }
       }
     }
-    if (lv_wave) {
+    if (LVA && lv_wave) {
       // L_v^T fragments (2 ltb + hf, lrb).  With rank < 32, rank row `rank`
       // holds ones: the (P L_v)^T product then carries the softmax row sums in
       // its spare row for free.
@@ -445,13 +481,13 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // flight and would wait for all of those at the first score MFMA.
   __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
   f32x16 acc[C::NDB];   // O^T: lane col = row l%32
-  f32x16 accl[C::RB];   // (P L_v)^T
+  f32x16 accl[NRB];     // (P L_v)^T
 #pragma unroll
   for (int db = 0; db < C::NDB; ++db)
 #pragma unroll
     for (int j = 0; j < 16; ++j) acc[db][j] = 0.f;
 #pragma unroll
-  for (int rb = 0; rb < C::RB; ++rb)
+  for (int rb = 0; rb < NRB; ++rb)
 #pragma unroll
     for (int j = 0; j < 16; ++j) accl[rb][j] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
@@ -515,7 +551,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
       for (int db = 0; db < C::NDB; ++db) acc[db] *= alpha;
 #pragma unroll
-      for (int rb = 0; rb < C::RB; ++rb) accl[rb] *= alpha;
+      for (int rb = 0; rb < NRB; ++rb) accl[rb] *= alpha;
       l_run *= alpha;
       m_run = mn;
     }
@@ -527,11 +563,11 @@ lrsa_prefill_kernel(const AttnArgs a) {
       const uint16_t* lvt = lv_lds[buf];
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        bf16x8 vf[C::NDB], lvf[C::RB];
+        bf16x8 vf[C::NDB], lvf[NRB];
 #pragma unroll
         for (int db = 0; db < C::NDB; ++db)
           vf[db] = as_bf16x8(*reinterpret_cast<const u32x4*>(vt + (((2 * tb + hf) * C::NDB + db) * 64 + lane) * 8));
-        if constexpr (LV) {
+        if constexpr (LVA) {
 #pragma unroll
           for (int rb = 0; rb < C::RB; ++rb)
             lvf[rb] = as_bf16x8(*reinterpret_cast<const u32x4*>(lvt + (((2 * tb + hf) * C::RB + rb) * 64 + lane) * 8));
@@ -547,7 +583,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
         const bf16x8 pb = as_bf16x8(pw);
 #pragma unroll
         for (int db = 0; db < C::NDB; ++db) acc[db] = mfma32x32x16(vf[db], pb, acc[db]);
-        if constexpr (LV) {
+        if constexpr (LVA) {
 #pragma unroll
           for (int rb = 0; rb < C::RB; ++rb) accl[rb] = mfma32x32x16(lvf[rb], pb, accl[rb]);
         }
@@ -622,7 +658,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
           for (int db = 0; db < C::NDB; ++db) acc[db] *= alpha;
 #pragma unroll
-          for (int rb = 0; rb < C::RB; ++rb) accl[rb] *= alpha;
+          for (int rb = 0; rb < NRB; ++rb) accl[rb] *= alpha;
           l_run *= alpha;
           m_run = mn;
         }
@@ -630,13 +666,13 @@ lrsa_prefill_kernel(const AttnArgs a) {
         // PV A fragments of this half.
         const uint16_t* vt = v_lds[buf];
         const uint16_t* lvt = lv_lds[buf];
-        bf16x8 vf[2][C::NDB], lvf[2][C::RB];
+        bf16x8 vf[2][C::NDB], lvf[2][NRB];
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
 #pragma unroll
           for (int db = 0; db < C::NDB; ++db)
             vf[hf][db] = as_bf16x8(*reinterpret_cast<const u32x4*>(vt + (((2 * tb + hf) * C::NDB + db) * 64 + lane) * 8));
-          if constexpr (LV) {
+          if constexpr (LVA) {
 #pragma unroll
             for (int rb = 0; rb < C::RB; ++rb)
               lvf[hf][rb] = as_bf16x8(*reinterpret_cast<const u32x4*>(lvt + (((2 * tb + hf) * C::RB + rb) * 64 + lane) * 8));
@@ -670,7 +706,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
           const bf16x8 pb = as_bf16x8(pw[hf]);
 #pragma unroll
           for (int db = 0; db < C::NDB; ++db) acc[db] = mfma32x32x16(vf[hf][db], pb, acc[db]);
-          if constexpr (LV) {
+          if constexpr (LVA) {
 #pragma unroll
             for (int rb = 0; rb < C::RB; ++rb) accl[rb] = mfma32x32x16(lvf[hf][rb], pb, accl[rb]);
           }
@@ -730,7 +766,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
       for (int jg = 0; jg < 4; ++jg)
         *reinterpret_cast<f32x4*>(wsp + 4 + db * 32 + jg * 8 + h32 * 4) =
             f32x4{acc[db][jg * 4], acc[db][jg * 4 + 1], acc[db][jg * 4 + 2], acc[db][jg * 4 + 3]};
-    if constexpr (LV) {
+    if constexpr (LVA) {
 #pragma unroll
       for (int rb = 0; rb < C::RB; ++rb)
 #pragma unroll
@@ -745,7 +781,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
   }
 
   // ---- epilogue: O^T += B_v^T (P L_v)^T, then O = acc / l, lse -------------
-  if constexpr (LV) {
+  if constexpr (LVA) {
     // (P L_v)^T registers of rank chunk jc (16 ranks) are the B operand in
     // the same k order as P; split into bf16 hi + lo to keep fp32 accuracy.
 #pragma unroll
@@ -803,6 +839,9 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   if (e != hipSuccess || nsp == 1) return e;
   AttnArgs m = a;
   m.n_splits = nsp;
+  // From rank 32 on B_v is already inside the rebuilt V: the partials carry
+  // no (P L_v) part for the merge to expand.
+  if (LV && R >= 32) m.Lv = nullptr;
   return launch_split_merge(m, st);
 }
 
