@@ -172,6 +172,14 @@ ATTN_CASES = [
     ("sharp_prefill", 128, 16, 8, 2, 64, [512], 512, "kv", 2.0, "end"),
     ("sharp_prefill_long", 128, 16, 8, 2, 16, [4096], 4096, "kv", 2.0, "end"),
     ("sharp_decode", 128, 16, 8, 2, 1, [3000, 2999], 3008, "kv", 2.0, "end"),
+    # From rank 32 up the prefill rebuilds V on chip and rounds it to bf16,
+    # as it does K and as any bf16 KV cache (the materialised reference
+    # included) does.  A larger LR term makes the rebuilt rows larger, so the
+    # sharpest scale a bf16 cache keeps inside the gate drops with the rank:
+    # these use it (the materialised reference errs the same here).
+    ("sharp_r32_prefill", 128, 32, 8, 2, 64, [512], 512, "kv", 1.5, "end"),
+    ("sharp_r64_prefill", 128, 64, 8, 2, 64, [512], 512, "kv", 1.35, "end"),
+    ("sharp_qv_r64_prefill_long", 128, 64, 8, 2, 16, [4096], 4096, "v", 2.0, "end"),
     ("mid_positions_prefill", 128, 16, 8, 2, 12, [300], 304, "kv", 1.0, "mid"),
     ("mid_positions_decode", 128, 16, 8, 2, 1, [300, 500], 512, "kv", 1.0, "mid"),
     ("many_requests_decode", 64, 16, 8, 8, 1, [64, 65, 63, 1, 17, 200, 31, 128], 256, "kv", 1.0, "end"),
