@@ -175,9 +175,10 @@ def percentiles(v):
     return {"p10": round(float(p10), 4), "median": round(float(p50), 4), "p90": round(float(p90), 4)}
 
 
-def copy_ceiling(dev, gib=1.0, reps=10):
-    """HBM rate of a plain device copy (read + write of `gib` GiB each), the
-    measured ceiling beside the 8 TB/s spec peak."""
+def torch_copy_rate(dev, gib=1.0, reps=10):
+    """HBM rate of torch's device copy (read + write of `gib` GiB each), for
+    context beside the 8 TB/s spec peak; torch's own kernels, not a ceiling
+    (the decode kernel reads faster than this copy moves data)."""
     import torch
     n = int(gib * (1 << 30)) // 4
     a = torch.empty(n, dtype=torch.float32, device=dev).fill_(1.0)
@@ -192,7 +193,7 @@ def copy_ceiling(dev, gib=1.0, reps=10):
     torch.cuda.synchronize()
     ms = ev[0].elapsed_time(ev[1]) / reps
     del a, b
-    return {"kind": f"device copy of {gib:g} GiB (read + write)", "gbs": round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)}
+    return round(2 * n * 4 / (ms * 1e-3) / 1e9, 1)
 
 
 def run_materialized(prc, x, w, steps, warmup):
@@ -1013,9 +1014,7 @@ def main():
         }
     del x
     torch.cuda.empty_cache()
-    ceil = copy_ceiling(dev)
-    ceil["decode_frac"] = round(dec_gbs / ceil["gbs"], 4)
-    out["measured_hbm_ceiling"] = ceil
+    out["torch_copy_gbs"] = torch_copy_rate(dev)
     if not args.no_cpu_baseline:
         print("bench: timing the fp64 oracle on a host sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
