@@ -350,3 +350,32 @@ def test_python_wrappers_refuse_wrong_dtypes():
     X = torch.zeros(4, 8, dtype=torch.float32)
     with pytest.raises(TypeError):
         prc.precompute_lr_cache(X, X, 1, 1, 8, torch.zeros(1, 1, 4, 8))
+
+
+@pytest.mark.parametrize("n_tok,n_q,s_cap,splits", [
+    (512, 32, 8704, 4),      # 64 units: one round of 4 splits beats two of 8
+    (256, 32, 65920, 8),     # 32 units
+    (2048, 40, 67584, 4),    # 320 units: 1280 workgroups, five full rounds
+    (4096, 32, 36864, 1),    # 512 units: two full rounds already
+    (16, 32, 256, 1),        # 4 tiles: too short to split
+])
+def test_prefill_split_count(n_tok, n_q, s_cap, splits):
+    """The prefill split count minimises ceil(units * ns / 256) / ns over
+    ns in 1..8 (splits at least 8 tiles), smallest on ties; the workspace
+    query reports one fp32 partial per row and split."""
+    d = _dims(batch=1, n_tok=n_tok, n_q_heads=n_q, n_kv_heads=8, s_cap=s_cap, kv_req_stride=0, l_req_stride=0,
+              b_req_stride=0)
+    need = prc.lib().lr_shared_attention_workspace_size(ctypes.byref(d))
+    assert need == (0 if splits == 1 else n_tok * n_q * splits * (4 + 128 + 16) * 4)
+
+
+@pytest.mark.parametrize("batch,s_cap,splits", [
+    (16, 32768, 32),   # two rounds of 512 workgroups, 32-tile splits
+    (1, 36864, 231),   # two rounds would cut splits to 3 tiles: one round
+    (1, 66048, 230),
+    (1, 4480, 140),    # one 32-token tile per split
+])
+def test_decode_split_count(batch, s_cap, splits):
+    d = _dims(batch=batch, n_tok=1, s_cap=s_cap, kv_req_stride=s_cap * 8 * 128, l_req_stride=s_cap * 16)
+    need = prc.lib().lr_shared_attention_workspace_size(ctypes.byref(d))
+    assert need == batch * 32 * splits * (4 + 128 + 16) * 4
