@@ -275,57 +275,104 @@ hipError_t launch_tb(const PrecomputeArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-// A handful of rows (the LR rows of newly decoded tokens) is a matrix-vector
-// product: one workgroup per output column streams that column's row of
-// A_rows (contiguous along d_in; 4 waves x 64 lanes x 16 bytes = 4096
-// elements per step, so a 4096-wide row is one load per lane) against the
-// T <= GV_T rows of X, which every workgroup reads from L2, then reduces over
-// lanes and waves.  This spreads A over n_cols workgroups instead of the few
-// tiles the GEMM would have, and keeps a whole row's loads in flight at once
-// (the rows of A are usually cold in the decode loop).
+// A handful of rows (the K/V and LR rows of newly decoded tokens) is a
+// matrix-vector product: one workgroup per output column streams that
+// column's row of W_rows or A_rows (contiguous along d_in; 4 waves x 64 lanes
+// x 16 bytes = 4096 elements per step, so a 4096-wide row is one load per
+// lane) against the T <= GV_T rows of X, which every workgroup reads from L2,
+// then reduces over lanes and waves.  Key workgroups take the two rows of one
+// RoPE pair (dims j and j + d/2 of a head) and rotate them at the token's
+// position.  This spreads the weights over thousands of workgroups instead
+// of the few tiles the GEMM would have, and keeps a whole row's loads in
+// flight at once (the rows are usually cold in the decode loop).
 constexpr int GV_T = 4;
 constexpr int GV_W = 4;  // waves per column
 
-__global__ void __launch_bounds__(64 * GV_W) precompute_gemv_kernel(const PrecomputeArgs a) {
-  __shared__ float red[GV_W][GV_T];
+__global__ void __launch_bounds__(64 * GV_W) project_gemv_kernel(const PrecomputeArgs a) {
+  __shared__ float red[GV_W][2][GV_T];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int c = blockIdx.x;  // output column: plane c / r, rank c % r
-  const uint16_t* arow = a.A + (int64_t)c * a.d_in;
+  const int u = blockIdx.x;
+  const int n_pair = a.nkv / 2;  // key RoPE pairs (nkv = n_kv * head_dim, 0 without K/V)
+  const int half = a.head_dim / 2;
+  // Region of this workgroup: 0 keys (a pair of rows), 1 values, 2 LR.
+  int region, hd = 0, j = 0, c = 0;
+  const uint16_t* r0;
+  const uint16_t* r1 = nullptr;
+  if (u < n_pair) {
+    region = 0;
+    hd = u / half;
+    j = u - hd * half;
+    r0 = a.W + (int64_t)(hd * a.head_dim + j) * a.d_in;
+    r1 = r0 + (int64_t)half * a.d_in;
+  } else if (u < n_pair + a.nkv) {
+    region = 1;
+    c = u - n_pair;
+    r0 = a.W + (int64_t)(a.nkv + c) * a.d_in;
+  } else {
+    region = 2;
+    c = u - n_pair - a.nkv;
+    r0 = a.A + (int64_t)c * a.d_in;
+  }
   const int T = (int)a.T;
-  float acc[GV_T] = {0.f, 0.f, 0.f, 0.f};
+  float acc0[GV_T] = {0.f, 0.f, 0.f, 0.f}, acc1[GV_T] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll 2
   for (int64_t k = (int64_t)tid * 8; k < a.d_in; k += 64 * GV_W * 8) {
-    const u32x4 av = *reinterpret_cast<const u32x4*>(arow + k);
+    const u32x4 av = *reinterpret_cast<const u32x4*>(r0 + k);
+    u32x4 bv = {0u, 0u, 0u, 0u};
+    if (r1 != nullptr) bv = *reinterpret_cast<const u32x4*>(r1 + k);
 #pragma unroll
     for (int t = 0; t < GV_T; ++t) {
       if (t < T) {
         const u32x4 xv = *reinterpret_cast<const u32x4*>(a.X + t * a.ld_x + k);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc[t] += bf_lo(av[e]) * bf_lo(xv[e]) + bf_hi(av[e]) * bf_hi(xv[e]);
+        for (int e = 0; e < 4; ++e) {
+          acc0[t] += bf_lo(av[e]) * bf_lo(xv[e]) + bf_hi(av[e]) * bf_hi(xv[e]);
+          acc1[t] += bf_lo(bv[e]) * bf_lo(xv[e]) + bf_hi(bv[e]) * bf_hi(xv[e]);
+        }
       }
     }
   }
 #pragma unroll
   for (int t = 0; t < GV_T; ++t) {
 #pragma unroll
-    for (int x = 1; x < 64; x <<= 1) acc[t] += shfl_xor(acc[t], x);
-    if (lane == 0) red[w][t] = acc[t];
+    for (int x = 1; x < 64; x <<= 1) {
+      acc0[t] += shfl_xor(acc0[t], x);
+      acc1[t] += shfl_xor(acc1[t], x);
+    }
+    if (lane == 0) {
+      red[w][0][t] = acc0[t];
+      red[w][1][t] = acc1[t];
+    }
   }
   __syncthreads();
   if (tid < T) {
-    float v = 0.f;
+    float x = 0.f, y = 0.f;
 #pragma unroll
-    for (int i = 0; i < GV_W; ++i) v += red[i][tid];
-    const int64_t plane = c / a.rank, j = c - plane * a.rank;
-    a.L[(plane * a.s_cap + a.tok_offset + tid) * a.rank + j] = (uint16_t)(pack_bf16(v, 0.f) & 0xffffu);
+    for (int i = 0; i < GV_W; ++i) {
+      x += red[i][0][tid];
+      y += red[i][1][tid];
+    }
+    const int64_t row = a.tok_offset + tid;  // absolute position and cache row
+    if (region == 0) {
+      float cs, sn;
+      rope_cs((int)row, a.w2pi[j], cs, sn);
+      uint16_t* kp = a.Kout + row * a.nkv + hd * a.head_dim + j;
+      kp[0] = (uint16_t)(pack_bf16(x * cs - y * sn, 0.f) & 0xffffu);
+      kp[half] = (uint16_t)(pack_bf16(y * cs + x * sn, 0.f) & 0xffffu);
+    } else if (region == 1) {
+      a.Vout[row * a.nkv + c] = (uint16_t)(pack_bf16(x, 0.f) & 0xffffu);
+    } else {
+      const int64_t plane = c / a.rank, jr = c - plane * a.rank;
+      a.L[(plane * a.s_cap + row) * a.rank + jr] = (uint16_t)(pack_bf16(x, 0.f) & 0xffffu);
+    }
   }
 }
 
 }  // namespace
 
 hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t st) {
-  if (a.nkv == 0 && a.tbl == nullptr && a.T <= GV_T) {
-    hipLaunchKernelGGL(precompute_gemv_kernel, dim3(a.n_cols), dim3(64 * GV_W), 0, st, a);
+  if (a.tbl == nullptr && a.T <= GV_T) {
+    hipLaunchKernelGGL(project_gemv_kernel, dim3(a.nkv / 2 + a.nkv + a.n_cols), dim3(64 * GV_W), 0, st, a);
     return hipGetLastError();
   }
   // 128-wide tiles halve the bytes loaded per MFMA but need enough of them to

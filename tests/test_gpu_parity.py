@@ -78,6 +78,9 @@ PROJ_CASES = [
     ("d128_ragged", 100, 256, 2, 128, 2, 3, 8, 5, 128, 5e5),
     ("d64_large_positions", 70, 264, 4, 64, 2, 2, 16, 10000, 10100, 1e4),
     ("single_token_append", 1, 512, 2, 128, 2, 4, 16, 333, 400, 5e5),
+    # 1-4 rows take the matrix-vector kernel (keys rotated per RoPE pair).
+    ("gemv_t3_d64_far_positions", 3, 264, 4, 64, 2, 2, 16, 60000, 60010, 1e4),
+    ("gemv_t4_d128_r64", 4, 4096, 8, 128, 2, 3, 64, 65532, 65536, 5e5),
     ("r64_one_proj", 130, 320, 1, 128, 1, 3, 64, 0, 130, 5e5),
     # Enough 128-wide tiles (16 x 17) for the wide-tile kernel; ragged tokens.
     ("wide_tiles", 2000, 256, 8, 128, 2, 2, 16, 3, 2003, 5e5),
