@@ -28,6 +28,7 @@ import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -316,10 +317,15 @@ def pmc_pass(prc, x, w, dev):
 
 
 def source_digest(*names):
+    """Digest of the kernel sources' code: comments and white space are
+    dropped, so a comment edit does not orphan the counters taken on it."""
     h = hashlib.sha256()
     for n in names:
-        with open(os.path.join(ROOT, "paper_2609_34054_amd", "csrc", n), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2609_34054_amd", "csrc", n), encoding="utf-8") as f:
+            src = f.read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        src = re.sub(r"//[^\n]*", "", src)
+        h.update(re.sub(r"\s+", "", src).encode())
     return h.hexdigest()[:16]
 
 

@@ -4,9 +4,12 @@
 // cache plus the current agent's LR cache (Sec. 3.1, reuse step).
 //   keys:   each KV tile is rebuilt in LDS, K = K_base + RoPE(L_k B_k), with
 //           the rank-r expansion before RoPE (App. D.2);
-//   values: associativity (App. D.2), O = P V_base + (P L_v) B_v: V_base and
-//           L_v go to LDS unchanged in value, P L_v is accumulated beside
-//           P V_base and B_v is applied once in the epilogue.
+//   values: ranks 8 and 16 use associativity (App. D.2),
+//           O = P V_base + (P L_v) B_v: V_base and L_v go to LDS unchanged in
+//           value, P L_v is accumulated beside P V_base and B_v is applied
+//           once in the epilogue.  Ranks 32 and 64 rebuild V = V_base + L_v B_v
+//           in the tile (bf16, like K): with 256 query rows per workgroup that
+//           is half the flops of P L_v and needs no (P L_v)^T accumulator.
 //
 // Work split: one workgroup of 8 waves per (request, KV head, 256 query rows).
 // A query row is a (token, q head of the GQA group) pair, so the group's heads
@@ -18,21 +21,26 @@
 //           per-lane offsets), + base, bf16 into LDS.  It also transposes a
 //           32-token block of V_base (and, for the first waves, of L_v) on
 //           the MFMA against a shifted identity, which writes them to LDS
-//           directly in the PV A-fragment layout.  Its global loads for the
-//           tile after next are in flight meanwhile;
+//           directly in the PV A-fragment layout; from rank 32 the transpose
+//           accumulates onto L_v B_v of the same block.  Its global loads for
+//           the tile after next are in flight meanwhile;
 //   attend  over 32 query rows (lanes l and l^32 share row l%32), in two
 //           halves of 32 tokens:
 //     scores  S^T = K Q^T on 32x32x16 MFMAs, so softmax statistics are per
 //             lane; causal mask only on halves that cross it;
 //     softmax online, exp2 domain, lazily rescaled;
-//     PV      O^T += V^T P^T and (P L_v)^T += L_v^T P^T on 32x32x16 MFMAs,
+//     PV      O^T += V^T P^T (and, below rank 32, (P L_v)^T += L_v^T P^T) on
+//             32x32x16 MFMAs,
 //             one conflict-free 16-byte LDS read per A fragment; P is
 //             already in the B operand layout.
 // LDS instructions, not bytes, bound the tile rate here (each costs the CU
 // about 4 cycles whatever its width), hence the fragment layouts above and
-// the register-resident identities and small-rank B_k fragments.  The two
-// waves that share a SIMD run the two jobs in opposite order.  LDS is
-// double-buffered with one barrier per tile.
+// the register-resident identities and small-rank B_k fragments.  Tiles
+// below every row's causal limit run a straight-line main loop (scores, then
+// one block of exponentials, PV and the next tile's build); tiles that cross
+// a limit run a per-half loop in which the two waves sharing a SIMD take
+// build and attend in opposite order.  LDS is double-buffered with one
+// barrier per tile.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
