@@ -318,16 +318,18 @@ __global__ void __launch_bounds__(64 * GV_W) project_gemv_kernel(const Precomput
 #pragma unroll 2
   for (int64_t k = (int64_t)tid * 8; k < a.d_in; k += 64 * GV_W * 8) {
     const u32x4 av = *reinterpret_cast<const u32x4*>(r0 + k);
+    const bool pair = region == 0;  // uniform over the workgroup
     u32x4 bv = {0u, 0u, 0u, 0u};
-    if (r1 != nullptr) bv = *reinterpret_cast<const u32x4*>(r1 + k);
+    if (pair) bv = *reinterpret_cast<const u32x4*>(r1 + k);
 #pragma unroll
     for (int t = 0; t < GV_T; ++t) {
       if (t < T) {
         const u32x4 xv = *reinterpret_cast<const u32x4*>(a.X + t * a.ld_x + k);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          acc0[t] += bf_lo(av[e]) * bf_lo(xv[e]) + bf_hi(av[e]) * bf_hi(xv[e]);
-          acc1[t] += bf_lo(bv[e]) * bf_lo(xv[e]) + bf_hi(bv[e]) * bf_hi(xv[e]);
+        for (int e = 0; e < 4; ++e) acc0[t] += bf_lo(av[e]) * bf_lo(xv[e]) + bf_hi(av[e]) * bf_hi(xv[e]);
+        if (pair) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc1[t] += bf_lo(bv[e]) * bf_lo(xv[e]) + bf_hi(bv[e]) * bf_hi(xv[e]);
         }
       }
     }
