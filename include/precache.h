@@ -20,7 +20,9 @@
  *   - Every call first validates its arguments on the host, before any HIP
  *     call is made.  A failed check returns a non-zero prc_status and launches
  *     nothing; prc_last_error() then gives a thread-local message naming the
- *     argument.  HIP launch failures return PRC_ELAUNCH.
+ *     argument.  A call that passes every check and has work to do then
+ *     requires the current HIP device to be a gfx950 (PRC_EDEVICE otherwise,
+ *     nothing launched).  HIP launch failures return PRC_ELAUNCH.
  *   - Row-major layouts throughout; "[a, b, c]" lists dimensions from
  *     outermost to innermost; the innermost dimension is contiguous.
  *   - All bf16 pointers must be 16-byte aligned, and every row stride given
@@ -82,8 +84,8 @@ const char* prc_version(void);
  *            nothing else is touched.
  * Arithmetic: bf16 inputs, fp32 accumulation, round-to-nearest-even to bf16.
  * Requires d_in % 8 == 0, ld_x % 8 == 0, d_in <= ld_x < 2^24 (PRC_EUNSUPPORTED
- * otherwise), r in {8, 16, 32, 64}, 0 <= tok_offset and tok_offset + T <= s_cap.
- * T == 0 is a no-op.
+ * otherwise), r in {8, 16, 32, 64}, 1 <= s_cap < 2^31, 0 <= tok_offset and
+ * tok_offset + T <= s_cap.  T == 0 is a no-op.
  */
 prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
                                const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
@@ -205,9 +207,10 @@ typedef struct lrsa_dims {
  *              or NULL.  A row that sees no key gets O = 0 and lse = -inf.
  *   workspace  device scratch of at least lr_shared_attention_workspace_size(dims)
  *              bytes (NULL allowed when the size is 0): the split partials of
- *              decode (n_tok == 1), and of a prefill too small to fill the GPU
- *              on its own (fewer than 512 units of 256 query rows x KV head x
- *              request), which is then also split over its KV tiles.
+ *              decode (n_tok == 1), and of a prefill whose units of work (256
+ *              query rows x KV head x request) fill the device's CUs so
+ *              unevenly that splitting the KV tiles 2-8 ways shortens the
+ *              modelled time (rounds of one unit per CU) by at least 10%.
  *              Contents need no initialisation; calls that share a workspace
  *              must be ordered on one stream.
  * Arithmetic: bf16 inputs; fp32 accumulation and softmax; rebuilt K tiles are

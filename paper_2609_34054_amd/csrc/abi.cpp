@@ -10,6 +10,8 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstring>
+#include <mutex>
 #include <string>
 
 #include "kernels.hpp"
@@ -37,6 +39,55 @@ prc_status ok() {
 
 bool aligned(const void* p, size_t n) { return (reinterpret_cast<uintptr_t>(p) % n) == 0; }
 bool rank_ok(int64_t r) { return r == 8 || r == 16 || r == 32 || r == 64; }
+
+// The current device, probed once per device: the kernels are built for
+// gfx950 only, and the split plans size themselves to its compute units.
+struct DeviceInfo {
+  bool probed = false;
+  bool gfx950 = false;
+  int cus = 0;
+};
+constexpr int kMaxDevices = 64;
+DeviceInfo g_dev[kMaxDevices];
+std::mutex g_dev_mu;
+// Plans made where no device is visible (a workspace query on a host without
+// a GPU) assume the 256 CUs of an MI355X.
+constexpr int kDefaultCUs = 256;
+
+const DeviceInfo* current_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lk(g_dev_mu);
+  DeviceInfo& d = g_dev[dev];
+  if (!d.probed) {
+    hipDeviceProp_t p;
+    if (hipGetDeviceProperties(&p, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    d.gfx950 = std::strncmp(p.gcnArchName, "gfx950", 6) == 0;
+    d.cus = p.multiProcessorCount;
+    d.probed = true;
+  }
+  return &d;
+}
+
+int plan_cus() {
+  const DeviceInfo* d = current_device();
+  return d != nullptr && d->cus > 0 ? d->cus : kDefaultCUs;
+}
+
+// Checked right before a launch, after every argument check.
+prc_status device_ready(int* cus) {
+  const DeviceInfo* d = current_device();
+  if (d == nullptr) return fail(PRC_EDEVICE, "no HIP device is current");
+  if (!d->gfx950) return fail(PRC_EDEVICE, "the current device is not a gfx950 (MI355X)");
+  *cus = d->cus > 0 ? d->cus : kDefaultCUs;
+  return PRC_OK;
+}
 
 prc_status launch_status(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(PRC_ELAUNCH, "%s: HIP launch failed: %s", what, hipGetErrorString(e));
@@ -197,7 +248,8 @@ PRC_API prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_i
   if (!rank_ok(rank)) return fail(PRC_EUNSUPPORTED, "rank=%d (built: 8, 16, 32, 64)", rank);
   const int64_t n_cols = (int64_t)n_proj * n_agents * rank;
   if (n_cols > 65535LL * 64) return fail(PRC_EINVAL, "n_proj*n_agents*rank=%lld too large", (long long)n_cols);
-  if (s_cap < 1) return fail(PRC_EINVAL, "s_cap=%lld must be positive", (long long)s_cap);
+  if (s_cap < 1 || s_cap > INT32_MAX)
+    return fail(PRC_EINVAL, "s_cap=%lld must be in [1, 2^31)", (long long)s_cap);
   if (tok_offset < 0 || tok_offset + T > s_cap)
     return fail(PRC_ESHAPE, "rows [%lld, %lld) fall outside s_cap=%lld", (long long)tok_offset,
                 (long long)(tok_offset + T), (long long)s_cap);
@@ -217,6 +269,8 @@ PRC_API prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_i
   a.tok_offset = tok_offset;
   a.n_cols = (int32_t)n_cols;
   a.rank = rank;
+  int cus = 0;
+  if (prc_status ds = device_ready(&cus)) return ds;
   return launch_status(prc::launch_precompute(a, static_cast<hipStream_t>(stream)), "precompute_lr_cache");
 }
 
@@ -288,6 +342,8 @@ prc_status project_impl(const char* who, const uint16_t* X, int64_t T, int64_t d
   if (with_base)
     for (int j = 0; j < head_dim / 2; ++j)
       a.w2pi[j] = std::pow(rope_theta, -2.0 * j / (double)head_dim) / (2.0 * M_PI);
+  int cus = 0;
+  if (prc_status ds = device_ready(&cus)) return ds;
   return launch_status(prc::launch_precompute(a, stream), who);
 }
 
@@ -334,13 +390,13 @@ size_t workspace_size(const lrsa_dims* dims, bool paged) {
     // small to fill the GPU otherwise.
     int splits = 1, split_tiles = 0;
     prc::prefill_plan(dims->n_tok, dims->n_q_heads / dims->n_kv_heads, dims->n_kv_heads, dims->batch, dims->s_cap,
-                      &splits, &split_tiles);
+                      plan_cus(), &splits, &split_tiles);
     return prc::prefill_workspace_bytes(dims->batch, dims->n_tok, dims->n_q_heads, splits, dims->head_dim, r);
   }
   int n_splits = 0, split_tiles = 0;
   // Paged caches always take the per-request decode kernel.
   const bool shared = !paged && prc::decode_shares_base(dims->batch, dims->kv_req_stride);
-  prc::decode_plan(dims->s_cap, dims->batch, dims->n_kv_heads, r, shared, &n_splits, &split_tiles);
+  prc::decode_plan(dims->s_cap, dims->batch, dims->n_kv_heads, r, shared, plan_cus(), &n_splits, &split_tiles);
   return prc::decode_workspace_bytes(dims->batch, dims->n_q_heads, n_splits, dims->head_dim, r);
 }
 
@@ -369,13 +425,17 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
       return fail(PRC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace == nullptr ? 0 : workspace_bytes,
                   need);
     if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
+    int cus = 0;
+    if (prc_status ds = device_ready(&cus)) return ds;
     prc::decode_plan(a.s_cap, a.batch, a.n_kv, a.rank,
-                     pg == nullptr && prc::decode_shares_base(a.batch, a.kv_stride), &a.n_splits, &a.split_tiles);
+                     pg == nullptr && prc::decode_shares_base(a.batch, a.kv_stride), cus, &a.n_splits,
+                     &a.split_tiles);
     a.ws = static_cast<float*>(workspace);
     snprintf(what, sizeof(what), "%s (decode)", who);
     return launch_status(prc::launch_decode(a, st), what);
   }
-  prc::prefill_plan(a.n_tok, a.group, a.n_kv, a.batch, a.s_cap, &a.pf_splits, &a.pf_split_tiles);
+  const int plan_cu = plan_cus();
+  prc::prefill_plan(a.n_tok, a.group, a.n_kv, a.batch, a.s_cap, plan_cu, &a.pf_splits, &a.pf_split_tiles);
   if (a.pf_splits > 1) {
     const size_t need = prc::prefill_workspace_bytes(a.batch, a.n_tok, a.n_q, a.pf_splits, a.head_dim, a.rank);
     if (workspace == nullptr || workspace_bytes < need)
@@ -384,6 +444,8 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
     if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
     a.ws = static_cast<float*>(workspace);
   }
+  int cus = 0;
+  if (prc_status ds = device_ready(&cus)) return ds;
   snprintf(what, sizeof(what), "%s (prefill)", who);
   return launch_status(prc::launch_prefill(a, st), what);
 }
@@ -422,22 +484,37 @@ PRC_API prc_status materialize_agent_kv(const lrsa_dims* dims, const uint16_t* K
   if (s != PRC_OK || c.empty) return s;
   if (K_full == nullptr || V_full == nullptr) return fail(PRC_EINVAL, "K_full/V_full is NULL");
   if (!aligned(K_full, 16) || !aligned(V_full, 16)) return fail(PRC_EALIGN, "K_full/V_full not 16-byte aligned");
-  // Outputs must not overlap any input (each is [B, s_cap, n_kv, d]).
-  const uintptr_t bytes = (uintptr_t)dims->batch * dims->s_cap * dims->n_kv_heads * dims->head_dim * 2;
-  const uint16_t* ins[] = {K_base, V_base, L_k, L_v, B_k, B_v};
-  for (const uint16_t* o : {static_cast<const uint16_t*>(K_full), static_cast<const uint16_t*>(V_full)}) {
-    const uintptr_t o0 = reinterpret_cast<uintptr_t>(o), o1 = o0 + bytes;
-    for (const uint16_t* in : ins) {
-      if (in == nullptr) continue;
-      const uintptr_t i0 = reinterpret_cast<uintptr_t>(in);
-      if (i0 >= o0 && i0 < o1) return fail(PRC_EINVAL, "K_full/V_full overlap an input");
-    }
+  // Outputs must not overlap any input.  Each output spans batch * s_cap
+  // rows; each input its requests' extents (a request stride of 0 means one
+  // buffer for all).
+  const int64_t nkvd = (int64_t)dims->n_kv_heads * dims->head_dim;
+  const int64_t r = c.a.rank;
+  const int64_t nb = dims->batch;
+  auto extent = [&](int64_t stride, int64_t per_req) -> uintptr_t {
+    const int64_t reqs = stride == 0 ? 1 : nb;
+    return (uintptr_t)(((reqs - 1) * stride + per_req) * 2);
+  };
+  const uintptr_t out_bytes = (uintptr_t)nb * dims->s_cap * nkvd * 2;
+  struct Span {
+    const void* p;
+    uintptr_t bytes;
+  } ins[] = {{K_base, extent(dims->kv_req_stride, dims->s_cap * nkvd)},
+             {V_base, extent(dims->kv_req_stride, dims->s_cap * nkvd)},
+             {L_k, extent(dims->l_req_stride, dims->s_cap * r)},
+             {L_v, extent(dims->l_req_stride, dims->s_cap * r)},
+             {B_k, extent(dims->b_req_stride, nkvd * r)},
+             {B_v, extent(dims->b_req_stride, nkvd * r)}};
+  auto overlap = [](uintptr_t a0, uintptr_t an, uintptr_t b0, uintptr_t bn) { return a0 < b0 + bn && b0 < a0 + an; };
+  for (const void* o : {static_cast<const void*>(K_full), static_cast<const void*>(V_full)}) {
+    const uintptr_t o0 = reinterpret_cast<uintptr_t>(o);
+    for (const Span& in : ins)
+      if (in.p != nullptr && overlap(o0, out_bytes, reinterpret_cast<uintptr_t>(in.p), in.bytes))
+        return fail(PRC_EINVAL, "K_full/V_full overlap an input");
   }
-  {
-    const uintptr_t k0 = reinterpret_cast<uintptr_t>(K_full), v0 = reinterpret_cast<uintptr_t>(V_full);
-    if ((k0 >= v0 && k0 < v0 + bytes) || (v0 >= k0 && v0 < k0 + bytes))
-      return fail(PRC_EINVAL, "K_full and V_full overlap");
-  }
+  if (overlap(reinterpret_cast<uintptr_t>(K_full), out_bytes, reinterpret_cast<uintptr_t>(V_full), out_bytes))
+    return fail(PRC_EINVAL, "K_full and V_full overlap");
+  int cus = 0;
+  if (prc_status ds = device_ready(&cus)) return ds;
   c.a.Kout = K_full;
   c.a.Vout = V_full;
   return launch_status(prc::launch_materialize(c.a, static_cast<hipStream_t>(stream)), "materialize_agent_kv");

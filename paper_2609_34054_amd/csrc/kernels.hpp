@@ -62,7 +62,8 @@ int decode_tile_tokens();
 // A decode batch whose requests all read one base cache (request stride 0)
 // runs the shared-base kernel: each base tile is read once for all of them.
 bool decode_shares_base(int batch, int64_t kv_req_stride);
-void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base, int* n_splits,
+// `cus`: compute units of the device the call runs on.
+void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base, int cus, int* n_splits,
                  int* split_tiles);
 size_t decode_workspace_bytes(int batch, int n_q, int n_splits, int head_dim, int rank);
 hipError_t launch_decode(const AttnArgs& a, hipStream_t stream);
@@ -74,7 +75,8 @@ hipError_t launch_split_merge(const AttnArgs& a, hipStream_t stream);
 // Prefill (several query tokens per request): causal flash attention.  A
 // call with too few (row tile, KV head, request) units to fill the GPU is
 // also split over the KV tiles, each split writing partials for the merge.
-void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int* splits, int* split_tiles);
+void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int cus, int* splits,
+                  int* split_tiles);
 size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int head_dim, int rank);
 hipError_t launch_prefill(const AttnArgs& a, hipStream_t stream);
 

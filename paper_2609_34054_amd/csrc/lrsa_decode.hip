@@ -951,7 +951,7 @@ int decode_tile_tokens() { return TK; }
 
 bool decode_shares_base(int batch, int64_t kv_req_stride) { return batch > 1 && kv_req_stride == 0; }
 
-void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base, int* n_splits,
+void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base, int cus, int* n_splits,
                  int* split_tiles) {
   const int64_t tiles = (s_cap + TK - 1) / TK;
   const int nw = dec_waves(rank);
@@ -961,7 +961,7 @@ void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base,
   const int64_t groups = shared_base ? (int64_t)n_kv * ((nb + nw - 1) / nw) : nb * ((n_kv + nw - 1) / nw);
   // Splits for a target of `rounds` 8-wave workgroups per CU.
   auto plan = [&](int64_t rounds, int64_t* ns_out, int64_t* st_out) {
-    const int64_t target_wgs = rounds * 256 * 8 / nw;
+    const int64_t target_wgs = rounds * (cus > 0 ? cus : 1) * 8 / nw;
     int64_t ns = (target_wgs + groups - 1) / groups;
     if (ns < 1) ns = 1;
     if (ns > tiles) ns = tiles > 0 ? tiles : 1;

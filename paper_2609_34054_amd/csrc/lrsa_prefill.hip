@@ -45,10 +45,6 @@
 #include "kernels.hpp"
 #include "rebuild.hpp"
 
-#ifndef SGB
-#define SGB 0
-#endif
-
 namespace prc {
 namespace {
 
@@ -719,28 +715,6 @@ lrsa_prefill_kernel(const AttnArgs a) {
             for (int rb = 0; rb < C::RB; ++rb) accl[rb] = mfma32x32x16(lvf[hf][rb], pb, accl[rb]);
           }
         }
-#if SGB
-        // Issue order of the block: LDS reads first, then (first half only)
-        // one score MFMA per 5 vector instructions, then the PV MFMAs of
-        // chunk 0 interleaved with the rest of the vector work.
-        constexpr int NPV = C::NDB + (LV ? C::RB : 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2 * NPV + (LV ? 2 * C::RB : 0), 0);
-        if (tb == 0) {
-#pragma unroll
-          for (int i = 0; i < C::NKQ; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x402, 3, 0);
-          }
-        } else {
-          __builtin_amdgcn_sched_group_barrier(0x402, 20, 0);
-        }
-#pragma unroll
-        for (int i = 0; i < NPV; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(0x402, 4, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x008, NPV, 0);
-#endif
       }
     }
     if (!build_first) build();
@@ -847,6 +821,9 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   if (e != hipSuccess || nsp == 1) return e;
   AttnArgs m = a;
   m.n_splits = nsp;
+  // The partials are laid out for the rank this kernel was built with (a
+  // call without LR runs the rank-8 build whatever dims.rank says).
+  m.rank = R;
   // From rank 32 on B_v is already inside the rebuilt V: the partials carry
   // no (P L_v) part for the merge to expand.
   if (LV && R >= 32) m.Lv = nullptr;
@@ -875,21 +852,24 @@ hipError_t launch_r(const AttnArgs& a, hipStream_t st) {
 
 }  // namespace
 
-void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int* splits, int* split_tiles) {
+void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int cus, int* splits,
+                  int* split_tiles) {
   // Units of work without a split: (row tile, KV head, request), one
   // workgroup per CU at a time.  Splitting the KV tiles ns ways gives
   // units * ns workgroups of 1/ns the work, so the time per CU goes as
   // ceil(units * ns / CUs) / ns.  Take the ns in 1..8 (splits at least 8
-  // tiles long) that minimises it, the smallest on ties: every split adds
-  // partials to write and merge.
-  constexpr int64_t kCUs = 256;
+  // tiles long) that minimises it, the smallest on ties, and split only when
+  // that model gains at least a tenth over one pass: every split adds fp32
+  // partials to write and merge, which a gain of a few per cent does not pay.
+  const int64_t n_cu = cus > 0 ? cus : 1;
   const int64_t rows = (int64_t)n_tok * group;
   const int64_t units = ((rows + BROWS - 1) / BROWS) * n_kv * (batch > 0 ? batch : 1);
   const int64_t tiles = (s_cap + TKV - 1) / TKV;
+  const double one_pass = (double)((units + n_cu - 1) / n_cu);
   int64_t best = 1;
-  double best_cost = (double)((units + kCUs - 1) / kCUs);
+  double best_cost = one_pass;
   for (int64_t ns = 2; ns <= 8 && ns <= tiles / 8; ++ns) {
-    const double cost = (double)((units * ns + kCUs - 1) / kCUs) / (double)ns;
+    const double cost = (double)((units * ns + n_cu - 1) / n_cu) / (double)ns;
     if (cost < best_cost - 1e-9) {
       best = ns;
       best_cost = cost;
@@ -897,7 +877,7 @@ void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int*
   }
   *splits = 1;
   *split_tiles = (int)(tiles > 0 ? tiles : 1);
-  if (best < 2) return;
+  if (best < 2 || best_cost > 0.9 * one_pass) return;
   const int64_t st = (tiles + best - 1) / best;
   *splits = (int)((tiles + st - 1) / st);
   *split_tiles = (int)st;

@@ -90,32 +90,42 @@ def _tiny(seed, d=8, n_q=4, n_kv=2, S=24, r=4, hidden=16, n_agents=3):
 # ---------------------------------------------------------------------------
 # Pins
 # ---------------------------------------------------------------------------
-def pin_merged_weights(orc, seed=1, d=8, theta=500.0, S=24, n_new=5):
-    """(a) Eq. 1: base cache + LR cache == attention with merged weights W + A B."""
+def pin_merged_weights(orc, seed=1, d=8, theta=500.0, S=24, n_new=5, t0=0):
+    """(a) Eq. 1: base cache + LR cache == attention with merged weights W + A B.
+
+    With ``t0 > 0`` the trajectory is preceded by t0 all-zero hidden states, so
+    its S tokens sit at absolute positions t0 .. t0 + S - 1 (a zero state has
+    zero keys, values and LR rows, in both routes alike)."""
     c = _tiny(seed, d=d, S=S)
     n_q, n_kv, r, N = c["n_q"], c["n_kv"], c["r"], c["N"]
-    X = c["X"]
+    X = np.concatenate([np.zeros((t0, c["hidden"])), c["X"]])
+    n = t0 + S
     group = n_q // n_kv
-    pos = np.arange(S - n_new, S)
+    pos = np.arange(n - n_new, n)
     scale = 1.0 / math.sqrt(d)
+
+    def keys(Wk):
+        K = np.zeros((n, n_kv, d))
+        for t in range(t0, n):
+            K[t] = np.stack([loop_rope((X[t] @ Wk)[g * d:(g + 1) * d], t, theta) for g in range(n_kv)])
+        return K
+
     # Oracle route: precompute every agent's LR caches from X (Sec. 3.1), base
     # caches from the frozen weights, then LR-shared attention.
     A_stack = np.concatenate([c["Ak"][a] for a in range(N)] + [c["Av"][a] for a in range(N)], axis=1)
     L = orc.precompute_lr_cache(X, A_stack, 2, N, r)
-    Kb = np.stack([np.stack([loop_rope((X[t] @ c["Wk"])[g * d:(g + 1) * d], t, theta)
-                             for g in range(n_kv)]) for t in range(S)])
-    Vb = (X @ c["Wv"]).reshape(S, n_kv, d)
+    Kb = keys(c["Wk"])
+    Vb = (X @ c["Wv"]).reshape(n, n_kv, d)
     Q = np.stack([np.stack([loop_rope((X[p] @ c["Wq"])[h * d:(h + 1) * d], p, theta)
                             for h in range(n_q)]) for p in pos])
     for a in range(N):
         O, _ = orc.lr_shared_attention(Q[None], Kb[None], Vb[None], L[0, a][None], L[1, a][None],
-                                       c["Bk"][a][None], c["Bv"][a][None], pos[None], [S], theta)
+                                       c["Bk"][a][None], c["Bv"][a][None], pos[None], [n], theta)
         # Merged route: the adapted projections of Eq. 1, written out.
         Wk_a = c["Wk"] + c["Ak"][a] @ c["Bk"][a]
         Wv_a = c["Wv"] + c["Av"][a] @ c["Bv"][a]
-        Kf = np.stack([np.stack([loop_rope((X[t] @ Wk_a)[g * d:(g + 1) * d], t, theta)
-                                 for g in range(n_kv)]) for t in range(S)])
-        Vf = (X @ Wv_a).reshape(S, n_kv, d)
+        Kf = keys(Wk_a)
+        Vf = (X @ Wv_a).reshape(n, n_kv, d)
         ref = loop_attention(Q, Kf, Vf, pos, group, scale)
         err = np.abs(O[0] - ref).max()
         assert err <= RTOL_EXACT * max(1.0, np.abs(ref).max()), f"agent {a}: merged-weights mismatch {err}"

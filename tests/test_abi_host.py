@@ -59,6 +59,7 @@ def _pc(X=A16, T=64, d_in=256, ld_x=256, A=A16, n_proj=2, N=3, r=8, L=A16, s_cap
     (dict(r=12), EUNSUP),
     (dict(r=128), EUNSUP),
     (dict(s_cap=0), EINVAL),
+    (dict(s_cap=1 << 31), EINVAL),
     (dict(off=100), ESHAPE),
     (dict(off=-1), ESHAPE),
     (dict(X=None), EINVAL),
@@ -74,6 +75,22 @@ def test_precompute_rejects(kw, code):
 
 def test_precompute_empty_segment_is_a_noop():
     assert _pc(T=0, X=None, A=None, L=None) == 0
+
+
+EDEVICE = 7
+
+
+def test_valid_calls_need_a_gfx950_device():
+    # Every argument check passes; the device check comes last, before any
+    # launch, and this host has no GPU.
+    assert _pc() == EDEVICE
+    assert "device" in prc.lib().prc_last_error().decode()
+    assert _pj() == EDEVICE
+    d = _dims(n_tok=1)
+    need = prc.lib().lr_shared_attention_workspace_size(ctypes.byref(d))
+    assert _attn(d, ws=A16, ws_bytes=need) == EDEVICE
+    assert _attn(_dims(n_tok=64, s_cap=256)) == EDEVICE
+    assert _mat(_dims()) == EDEVICE
 
 
 # -------------------------------------------------------- fused projection
@@ -341,6 +358,10 @@ def test_materialize_rejects():
     assert _mat(d, Vf=0x4000000 + 8) == EALIGN
     assert _mat(d, Kf=A16) == EINVAL          # output overlaps K_base
     assert _mat(d, Vf=0x4000000 + 16) == EINVAL  # K_full and V_full overlap
+    # An output that starts inside an input's extent (K_base spans 2 requests
+    # of 1024 x 8 x 128 elements from A16) overlaps it too.
+    assert _mat(d, Kf=A16 + (1 << 20)) == EINVAL
+    assert _mat(d, Kf=A16 + 2 * 1024 * 8 * 128 * 2 + (16 << 20)) == EDEVICE
     assert _mat(_dims(head_dim=80)) == EUNSUP
     assert _mat(_dims(batch=0), K=None, V=None, kvl=None) == 0
 
@@ -358,11 +379,14 @@ def test_python_wrappers_refuse_wrong_dtypes():
     (2048, 40, 67584, 4),    # 320 units: 1280 workgroups, five full rounds
     (4096, 32, 36864, 1),    # 512 units: two full rounds already
     (16, 32, 256, 1),        # 4 tiles: too short to split
+    (16128, 32, 65536, 1),   # 2016 units: 8 splits would gain 1.6%, below the 10% bar
+    (4104, 32, 36864, 8),    # 520 units: a third round for 8 units; 8 splits gain 29%
 ])
 def test_prefill_split_count(n_tok, n_q, s_cap, splits):
     """The prefill split count minimises ceil(units * ns / 256) / ns over
-    ns in 1..8 (splits at least 8 tiles), smallest on ties; the workspace
-    query reports one fp32 partial per row and split."""
+    ns in 1..8 (splits at least 8 tiles), smallest on ties, and splits only
+    when that gains at least 10% over one pass; the workspace query reports
+    one fp32 partial per row and split."""
     d = _dims(batch=1, n_tok=n_tok, n_q_heads=n_q, n_kv_heads=8, s_cap=s_cap, kv_req_stride=0, l_req_stride=0,
               b_req_stride=0)
     need = prc.lib().lr_shared_attention_workspace_size(ctypes.byref(d))

@@ -523,3 +523,32 @@ def test_multi_turn_stack_chain():
         graph.replay()
         torch.cuda.synchronize()
         assert torch.equal(O_all, eager), rep
+
+
+@pytest.mark.parametrize("rank", [16, 32, 64])
+def test_split_prefill_without_lr_ignores_dims_rank(rank):
+    """A plain call (no LR cache) whose dims still carry a built rank: the
+    header says the rank is then ignored, so the split prefill's partials and
+    their merge must agree on the layout whatever dims.rank says."""
+    import ctypes
+    from paper_2609_34054_amd.binding import lib, make_dims
+    print(f"plain split prefill with dims.rank={rank}", flush=True)
+    cfg, c = _case("split_plain_prefill", 128, 16, 8, 2, 30, [1800], 1856, "none", 1.0, "end")
+    g = to_dev(c)
+    dims = make_dims(g["Q"], g["K_base"], None, None, None, None, cfg.theta)
+    dims.rank = rank
+    need = lib().lr_shared_attention_workspace_size(ctypes.byref(dims))
+    assert need > 0  # the call splits its KV tiles
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    O = torch.empty_like(g["Q"])
+    lse = torch.empty(g["Q"].shape[:3], dtype=torch.float32, device="cuda")
+    p = lambda t: ctypes.c_void_p(t.data_ptr())
+    st = lib().lr_shared_attention(ctypes.byref(dims), p(g["Q"]), p(g["K_base"]), p(g["V_base"]), None, None,
+                                   None, None, p(g["positions"]), p(g["kv_len"]), p(O), p(lse), p(ws), need,
+                                   ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert st == 0, lib().prc_last_error()
+    torch.cuda.synchronize()
+    Oref, lref = oracle_attention(c, cfg.theta)
+    mx, mean = attn_errors(O, Oref)
+    assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (mx, mean)
+    assert lse_error(lse, lref) <= LSE_ATOL
