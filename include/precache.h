@@ -228,6 +228,30 @@ prc_status lr_shared_attention(const lrsa_dims* dims, const uint16_t* Q,
  * dims is invalid; validation errors are reported by the call itself). */
 size_t lr_shared_attention_workspace_size(const lrsa_dims* dims);
 
+/*
+ * lr_shared_attention_noalloc -- lr_shared_attention for callers that cannot
+ * allocate device memory or hand in a workspace: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, output, arithmetic and errors as lr_shared_attention, minus the
+ * workspace: the split partials go to a static device array of
+ * PRC_NOALLOC_WORKSPACE_BYTES that the library holds on each device it runs
+ * on until the process ends (its device address is fetched on the first call
+ * made with that device current).  The call allocates nothing.
+ *   - A call whose partials (lr_shared_attention_workspace_size(dims)) exceed
+ *     PRC_NOALLOC_WORKSPACE_BYTES returns PRC_EWORKSPACE and launches nothing.
+ *   - Every call on one device shares that device's array.  No part of it
+ *     needs to start at zero (each split writes all of its partial before the
+ *     merge reads it), but calls that overlap on one device, on different
+ *     streams or from different threads, race on it: order them on one stream.
+ */
+#define PRC_NOALLOC_WORKSPACE_BYTES (32u << 20)
+prc_status lr_shared_attention_noalloc(const lrsa_dims* dims, const uint16_t* Q,
+                                       const uint16_t* K_base, const uint16_t* V_base,
+                                       const uint16_t* L_k, const uint16_t* L_v,
+                                       const uint16_t* B_k, const uint16_t* B_v,
+                                       const int32_t* positions, const int32_t* kv_len,
+                                       uint16_t* O, float* lse, void* stream);
+
 /* Block tables of a paged lr_shared_attention_paged call. */
 typedef struct lrsa_paging {
   const int32_t* kv_block_table; /* [B, max_blocks] int32, DEVICE memory: row b

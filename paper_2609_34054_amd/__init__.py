@@ -11,6 +11,7 @@ from .binding import (  # noqa: F401
     PrecacheError,
     lib,
     lr_shared_attention,
+    lr_shared_attention_noalloc,
     lr_shared_attention_paged,
     make_dims,
     materialize_agent_kv,

@@ -22,7 +22,8 @@ STATUS_NAMES = {0: "PRC_OK", 1: "PRC_EINVAL", 2: "PRC_ESHAPE", 3: "PRC_EALIGN",
 
 EXPORTS = ("precompute_lr_cache", "project_kv_and_lr_cache", "project_kv_and_lr_cache_paged",
            "lr_shared_attention", "lr_shared_attention_workspace_size", "lr_shared_attention_paged",
-           "lr_shared_attention_paged_workspace_size", "materialize_agent_kv", "prc_last_error",
+           "lr_shared_attention_paged_workspace_size", "lr_shared_attention_noalloc", "materialize_agent_kv",
+           "prc_last_error",
            "prc_status_string", "prc_version")
 
 
@@ -82,6 +83,9 @@ def lib() -> ctypes.CDLL:
         L.lr_shared_attention.argtypes = [ctypes.POINTER(LrsaDims), vp, vp, vp, vp, vp, vp, vp, vp, vp,
                                           vp, vp, vp, ctypes.c_size_t, vp]
         L.lr_shared_attention.restype = ctypes.c_int
+        L.lr_shared_attention_noalloc.argtypes = [ctypes.POINTER(LrsaDims), vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                                  vp, vp, vp]
+        L.lr_shared_attention_noalloc.restype = ctypes.c_int
         L.lr_shared_attention_workspace_size.argtypes = [ctypes.POINTER(LrsaDims)]
         L.lr_shared_attention_workspace_size.restype = ctypes.c_size_t
         L.lr_shared_attention_paged.argtypes = [ctypes.POINTER(LrsaDims), ctypes.POINTER(LrsaPaging), vp, vp, vp,
@@ -296,6 +300,28 @@ def lr_shared_attention(Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len
                                    _ptr(L_v), _ptr(B_k), _ptr(B_v), _ptr(positions), _ptr(kv_len), _ptr(O),
                                    _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream))
     _check("lr_shared_attention", st)
+    return O, lse
+
+
+def lr_shared_attention_noalloc(Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len, *,
+                                rope_theta: float, softmax_scale: float = 0.0, O, lse=None, stream=None):
+    """:func:`lr_shared_attention` through the entry point that allocates nothing:
+    the caller preallocates ``O`` (and ``lse``); split partials go to the
+    library's static per-device workspace."""
+    for name, t, nd in (("Q", Q, 4), ("K_base", K_base, 4), ("V_base", V_base, 4), ("L_k", L_k, 3),
+                        ("L_v", L_v, 3), ("B_k", B_k, 3), ("B_v", B_v, 3), ("O", O, 4)):
+        _bf16(name, t, nd)
+    if K_base.shape != V_base.shape or K_base.stride() != V_base.stride():
+        raise ValueError("K_base and V_base must share shape and strides")
+    if tuple(O.shape) != tuple(Q.shape) or not O.is_contiguous():
+        raise ValueError("O must be a contiguous tensor shaped like Q")
+    if positions.dtype != torch.int32 or kv_len.dtype != torch.int32:
+        raise TypeError("positions and kv_len must be int32")
+    dims = make_dims(Q, K_base, L_k, L_v, B_k, B_v, rope_theta, softmax_scale)
+    st = lib().lr_shared_attention_noalloc(ctypes.byref(dims), _ptr(Q), _ptr(K_base), _ptr(V_base), _ptr(L_k),
+                                           _ptr(L_v), _ptr(B_k), _ptr(B_v), _ptr(positions), _ptr(kv_len),
+                                           _ptr(O), _ptr(lse), _stream(stream))
+    _check("lr_shared_attention_noalloc", st)
     return O, lse
 
 

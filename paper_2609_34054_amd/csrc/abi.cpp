@@ -452,7 +452,62 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
 
 }  // namespace
 
+namespace {
+
+// Split partials of lr_shared_attention_noalloc: one array per device, held
+// until the process ends.  Host code never passes `scratch` itself to a
+// kernel or a copy (in host code its name is only a stand-in); it uses the
+// device address fetched once per device below.
+constexpr size_t kStaticWsBytes = (size_t)PRC_NOALLOC_WORKSPACE_BYTES;
+static __device__ __align__(256) float scratch[kStaticWsBytes / sizeof(float)];
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of this device's `scratch`, fetched on the first call made
+// with the device current.
+prc_status static_workspace(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return fail(PRC_EDEVICE, "no HIP device is current");
+  }
+  std::lock_guard<std::mutex> lk(g_dev_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr) {
+      (void)hipGetLastError();
+      return fail(PRC_EDEVICE, "static workspace unavailable on device %d: %s", dev, hipGetErrorString(e));
+    }
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return PRC_OK;
+}
+
+}  // namespace
+
 PRC_API size_t lr_shared_attention_workspace_size(const lrsa_dims* dims) { return workspace_size(dims, false); }
+
+PRC_API prc_status lr_shared_attention_noalloc(const lrsa_dims* dims, const uint16_t* Q, const uint16_t* K_base,
+                                               const uint16_t* V_base, const uint16_t* L_k, const uint16_t* L_v,
+                                               const uint16_t* B_k, const uint16_t* B_v, const int32_t* positions,
+                                               const int32_t* kv_len, uint16_t* O, float* lse, void* stream) {
+  Checked c;
+  prc_status s = check_attention(dims, Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len, true, nullptr, &c);
+  if (s != PRC_OK || c.empty) return s;
+  const size_t need = workspace_size(dims, false);
+  if (need > kStaticWsBytes)
+    return fail(PRC_EWORKSPACE, "the call needs %zu bytes of split partials, above the %zu-byte static workspace",
+                need, kStaticWsBytes);
+  void* ws = nullptr;
+  if (need > 0) {
+    int cus = 0;
+    if (prc_status ds = device_ready(&cus)) return ds;
+    if (prc_status ss = static_workspace(&ws)) return ss;
+  }
+  return attention_impl("lr_shared_attention_noalloc", dims, nullptr, Q, K_base, V_base, L_k, L_v, B_k, B_v,
+                        positions, kv_len, O, lse, ws, need > 0 ? kStaticWsBytes : 0, stream);
+}
 
 PRC_API size_t lr_shared_attention_paged_workspace_size(const lrsa_dims* dims) { return workspace_size(dims, true); }
 

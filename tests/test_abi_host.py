@@ -403,3 +403,19 @@ def test_decode_split_count(batch, s_cap, splits):
     d = _dims(batch=batch, n_tok=1, s_cap=s_cap, kv_req_stride=s_cap * 8 * 128, l_req_stride=s_cap * 16)
     need = prc.lib().lr_shared_attention_workspace_size(ctypes.byref(d))
     assert need == batch * 32 * splits * (4 + 128 + 16) * 4
+
+
+def test_noalloc_checks_size_before_the_device():
+    # The call with no workspace argument rejects a call whose split partials
+    # exceed its static buffer on the host, before any device call.
+    L = prc.lib()
+    d = _dims(n_tok=1, batch=4096, kv_req_stride=0, l_req_stride=0, b_req_stride=0)
+    assert L.lr_shared_attention_workspace_size(ctypes.byref(d)) > 32 << 20
+    args = [ctypes.byref(d), A16, A16, A16, A16, A16, A16, A16, A16, A16, A16, None, None]
+    assert L.lr_shared_attention_noalloc(*args) == EWS
+    assert "static workspace" in L.prc_last_error().decode()
+    # Argument checks come first, as for lr_shared_attention.
+    bad = _dims(n_tok=1, head_dim=96)
+    assert L.lr_shared_attention_noalloc(ctypes.byref(bad), *args[1:]) == EUNSUP
+    ok = _dims(n_tok=1)
+    assert L.lr_shared_attention_noalloc(ctypes.byref(ok), *args[1:]) == 7  # no gfx950 device here
