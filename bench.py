@@ -97,13 +97,13 @@ def make_inputs(w, dev, seed=3000):
     x = {}
     # Precompute: 4 rotating segment buffers so every step reads X from HBM.
     x["X"] = [nrm((w["seg"], w["hidden"])) for _ in range(4)]
-    x["A_rows"] = nrm((2 * N * r, w["hidden"]), 1.0 / math.sqrt(w["hidden"]))
+    x["A_stack"] = nrm((w["hidden"], 2 * N * r), 1.0 / math.sqrt(w["hidden"]))
     x["L_planes"] = torch.zeros((2, N, kv_pre, r), dtype=torch.bfloat16, device=dev)
     # Prefill: one request (agent 0) over the shared trajectory.
     x["pre"] = dict(
         Q=nrm((1, w["n_pre"], n_q, d)), K_base=nrm((1, kv_pre, n_kv, d)), V_base=nrm((1, kv_pre, n_kv, d)),
         L_k=nrm((1, kv_pre, r)), L_v=nrm((1, kv_pre, r)),
-        Bk_rows=nrm((1, n_kv * d, r), bstd), Bv_rows=nrm((1, n_kv * d, r), bstd),
+        B_k=nrm((1, r, n_kv * d), bstd), B_v=nrm((1, r, n_kv * d), bstd),
         positions=torch.arange(S, kv_pre, dtype=torch.int32, device=dev)[None],
         kv_len=torch.tensor([kv_pre], dtype=torch.int32, device=dev))
     # Decode: 16 requests, each its own base cache, LR plane (agent b mod N)
@@ -111,7 +111,7 @@ def make_inputs(w, dev, seed=3000):
     x["dec"] = dict(
         Q=nrm((B, 1, n_q, d)), K_base=nrm((B, S, n_kv, d)), V_base=nrm((B, S, n_kv, d)),
         L_k=nrm((B, S, r)), L_v=nrm((B, S, r)),
-        Bk_rows=nrm((B, n_kv * d, r), bstd), Bv_rows=nrm((B, n_kv * d, r), bstd),
+        B_k=nrm((B, r, n_kv * d), bstd), B_v=nrm((B, r, n_kv * d), bstd),
         positions=torch.full((B, 1), S - 1, dtype=torch.int32, device=dev),
         kv_len=torch.full((B,), S, dtype=torch.int32, device=dev))
     return x
@@ -119,8 +119,8 @@ def make_inputs(w, dev, seed=3000):
 
 # ------------------------------------------------------------ GPU timing loop
 def attn(prc, c, theta, O, ws):
-    return prc.lr_shared_attention(c["Q"], c["K_base"], c["V_base"], c["L_k"], c["L_v"], c["Bk_rows"],
-                                   c["Bv_rows"], c["positions"], c["kv_len"], rope_theta=theta, O=O,
+    return prc.lr_shared_attention(c["Q"], c["K_base"], c["V_base"], c["L_k"], c["L_v"], c["B_k"],
+                                   c["B_v"], c["positions"], c["kv_len"], rope_theta=theta, O=O,
                                    workspace=ws)
 
 
@@ -129,14 +129,14 @@ def run_fused(prc, x, w, steps, warmup):
     theta = w["theta"]
     O_pre = torch.empty_like(x["pre"]["Q"])
     O_dec = torch.empty_like(x["dec"]["Q"])
-    dims = prc.make_dims(x["dec"]["Q"], x["dec"]["K_base"], x["dec"]["L_k"], x["dec"]["L_v"], x["dec"]["Bk_rows"],
-                         x["dec"]["Bv_rows"], theta)
+    dims = prc.make_dims(x["dec"]["Q"], x["dec"]["K_base"], x["dec"]["L_k"], x["dec"]["L_v"], x["dec"]["B_k"],
+                         x["dec"]["B_v"], theta)
     ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=O_dec.device)
 
     def step(i, ev=None):
         if ev is not None:
             ev[0].record()
-        prc.precompute_lr_cache(x["X"][i % 4], x["A_rows"], 2, w["N"], w["r"], x["L_planes"], tok_offset=w["S"])
+        prc.precompute_lr_cache(x["X"][i % 4], x["A_stack"], 2, w["N"], w["r"], x["L_planes"], tok_offset=w["S"])
         if ev is not None:
             ev[1].record()
         attn(prc, x["pre"], theta, O_pre, None)
@@ -205,24 +205,24 @@ def run_materialized(prc, x, w, steps, warmup):
     Kp = torch.empty_like(p["K_base"]); Vp = torch.empty_like(p["V_base"])
     Kd = torch.empty_like(dcs["K_base"]); Vd = torch.empty_like(dcs["V_base"])
     O_pre = torch.empty_like(p["Q"]); O_dec = torch.empty_like(dcs["Q"])
-    plain_pre = dict(p, K_base=Kp, V_base=Vp, L_k=None, L_v=None, Bk_rows=None, Bv_rows=None)
-    plain_dec = dict(dcs, K_base=Kd, V_base=Vd, L_k=None, L_v=None, Bk_rows=None, Bv_rows=None)
+    plain_pre = dict(p, K_base=Kp, V_base=Vp, L_k=None, L_v=None, B_k=None, B_v=None)
+    plain_dec = dict(dcs, K_base=Kd, V_base=Vd, L_k=None, L_v=None, B_k=None, B_v=None)
     dims = prc.make_dims(dcs["Q"], Kd, None, None, None, None, theta)
     ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=O_dec.device)
 
     def step(i, ev=None):
         if ev is not None:
             ev[0].record()
-        prc.precompute_lr_cache(x["X"][i % 4], x["A_rows"], 2, w["N"], w["r"], x["L_planes"], tok_offset=w["S"])
+        prc.precompute_lr_cache(x["X"][i % 4], x["A_stack"], 2, w["N"], w["r"], x["L_planes"], tok_offset=w["S"])
         if ev is not None:
             ev[1].record()
-        prc.materialize_agent_kv(p["K_base"], p["V_base"], p["L_k"], p["L_v"], p["Bk_rows"], p["Bv_rows"],
+        prc.materialize_agent_kv(p["K_base"], p["V_base"], p["L_k"], p["L_v"], p["B_k"], p["B_v"],
                                  p["kv_len"], rope_theta=theta, K_full=Kp, V_full=Vp)
         attn(prc, plain_pre, theta, O_pre, None)
         if ev is not None:
             ev[2].record()
-        prc.materialize_agent_kv(dcs["K_base"], dcs["V_base"], dcs["L_k"], dcs["L_v"], dcs["Bk_rows"],
-                                 dcs["Bv_rows"], dcs["kv_len"], rope_theta=theta, K_full=Kd, V_full=Vd)
+        prc.materialize_agent_kv(dcs["K_base"], dcs["V_base"], dcs["L_k"], dcs["L_v"], dcs["B_k"],
+                                 dcs["B_v"], dcs["kv_len"], rope_theta=theta, K_full=Kd, V_full=Vd)
         attn(prc, plain_dec, theta, O_dec, ws)
         if ev is not None:
             ev[3].record()
@@ -257,7 +257,6 @@ def cpu_baseline(w, budget_s=20.0):
     except Exception:  # pragma: no cover
         threads = 1
     f64 = lambda t: None if t is None else t.double().numpy()
-    tr = lambda t: None if t is None else np.swapaxes(f64(t), -1, -2)
     S, work = w["S"], algorithmic_work(w)
     dec_t, dec_n = 0.0, 0
     while dec_t < budget_s / 2 and dec_n < w["B"]:
@@ -265,7 +264,7 @@ def cpu_baseline(w, budget_s=20.0):
                            seed_base=50_000 + dec_n, poison_tail=False)
         t0 = time.perf_counter()
         oracle.lr_shared_attention(f64(c["Q"]), f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]),
-                                   f64(c["L_v"]), tr(c["Bk_rows"]), tr(c["Bv_rows"]), c["positions"].numpy(),
+                                   f64(c["L_v"]), f64(c["B_k"]), f64(c["B_v"]), c["positions"].numpy(),
                                    c["kv_len"].numpy(), cfg.theta)
         dec_t += time.perf_counter() - t0
         dec_n += 1
@@ -277,7 +276,7 @@ def cpu_baseline(w, budget_s=20.0):
                        poison_tail=False)
     t0 = time.perf_counter()
     oracle.lr_shared_attention(f64(c["Q"]), f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]), f64(c["L_v"]),
-                               tr(c["Bk_rows"]), tr(c["Bv_rows"]), c["positions"].numpy(), c["kv_len"].numpy(),
+                               f64(c["B_k"]), f64(c["B_v"]), c["positions"].numpy(), c["kv_len"].numpy(),
                                cfg.theta)
     pre_t = time.perf_counter() - t0
     pre_flops = 4 * w["n_q"] * w["d"] * sum(p + 1 for p in pos)
@@ -307,7 +306,7 @@ def pmc_pass(prc, x, w, dev):
     theta = w["theta"]
     O_pre = torch.empty_like(x["pre"]["Q"])
     O_dec = torch.empty_like(x["dec"]["Q"])
-    prc.precompute_lr_cache(x["X"][0], x["A_rows"], 2, w["N"], w["r"], x["L_planes"], tok_offset=w["S"])
+    prc.precompute_lr_cache(x["X"][0], x["A_stack"], 2, w["N"], w["r"], x["L_planes"], tok_offset=w["S"])
     torch.cuda.synchronize()
     attn(prc, x["pre"], theta, O_pre, None)
     torch.cuda.synchronize()
@@ -389,13 +388,13 @@ def rank_sweep(prc, w, dev, steps, warmup):
             c = dict(base[st])
             c["L_k"] = nrm((nb, ntok, r)) if lk else None
             c["L_v"] = nrm((nb, ntok, r)) if lv else None
-            c["Bk_rows"] = nrm((nb, n_kv * d, r), bstd) if lk else None
-            c["Bv_rows"] = nrm((nb, n_kv * d, r), bstd) if lv else None
+            c["B_k"] = nrm((nb, r, n_kv * d), bstd) if lk else None
+            c["B_v"] = nrm((nb, r, n_kv * d), bstd) if lv else None
             cases[st] = c
         O_pre = torch.empty_like(cases["pre"]["Q"])
         O_dec = torch.empty_like(cases["dec"]["Q"])
         cd = cases["dec"]
-        dims = prc.make_dims(cd["Q"], cd["K_base"], cd["L_k"], cd["L_v"], cd["Bk_rows"], cd["Bv_rows"], w["theta"])
+        dims = prc.make_dims(cd["Q"], cd["K_base"], cd["L_k"], cd["L_v"], cd["B_k"], cd["B_v"], w["theta"])
         ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
         t_pre = timed(lambda: attn(prc, cases["pre"], w["theta"], O_pre, None))
         t_dec = timed(lambda: attn(prc, cases["dec"], w["theta"], O_dec, ws))
@@ -430,15 +429,15 @@ def shared_base_decode(prc, w, dev, steps, warmup):
     S, d, n_q, n_kv, r, N = w["S"], w["d"], w["n_q"], w["n_kv"], w["r"], w["N"]
     bstd = math.sqrt(0.02)
     c = dict(Q=nrm((N, 1, n_q, d)), K_base=nrm((1, S, n_kv, d)), V_base=nrm((1, S, n_kv, d)),
-             L_k=nrm((N, S, r)), L_v=nrm((N, S, r)), Bk_rows=nrm((N, n_kv * d, r), bstd),
-             Bv_rows=nrm((N, n_kv * d, r), bstd),
+             L_k=nrm((N, S, r)), L_v=nrm((N, S, r)), B_k=nrm((N, r, n_kv * d), bstd),
+             B_v=nrm((N, r, n_kv * d), bstd),
              positions=torch.full((N, 1), S - 1, dtype=torch.int32, device=dev),
              kv_len=torch.full((N,), S, dtype=torch.int32, device=dev))
     O = torch.empty_like(c["Q"])
 
     def timed(case):
-        dims = prc.make_dims(case["Q"], case["K_base"], case["L_k"], case["L_v"], case["Bk_rows"],
-                             case["Bv_rows"], w["theta"])
+        dims = prc.make_dims(case["Q"], case["K_base"], case["L_k"], case["L_v"], case["B_k"],
+                             case["B_v"], w["theta"])
         ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
         for _ in range(warmup):
             attn(prc, case, w["theta"], O, ws)
@@ -486,8 +485,8 @@ def fused_projection(prc, w, dev, steps, warmup):
     S, T, hid, n_kv, d, r, N = w["S"], w["seg"], w["hidden"], w["n_kv"], w["d"], w["r"], w["N"]
     s_cap = S + T
     X = nrm((T, hid))
-    W_rows = nrm((2 * n_kv * d, hid), 1.0 / math.sqrt(hid))
-    A_rows = nrm((2 * N * r, hid), 1.0 / math.sqrt(hid))
+    W = nrm((hid, 2 * n_kv * d), 1.0 / math.sqrt(hid))
+    A_stack = nrm((hid, 2 * N * r), 1.0 / math.sqrt(hid))
     K = torch.empty((s_cap, n_kv, d), dtype=torch.bfloat16, device=dev)
     V = torch.empty_like(K)
     L = torch.empty((2, N, s_cap, r), dtype=torch.bfloat16, device=dev)
@@ -505,11 +504,11 @@ def fused_projection(prc, w, dev, steps, warmup):
         return e0.elapsed_time(e1) / steps
 
     th = w["theta"]
-    t_fused = timed(lambda: prc.project_kv_and_lr_cache(X, W_rows, A_rows, n_kv, d, 2, N, r, K, V, L,
+    t_fused = timed(lambda: prc.project_kv_and_lr_cache(X, W, A_stack, n_kv, d, 2, N, r, K, V, L,
                                                         rope_theta=th, tok_offset=S))
-    t_base = timed(lambda: prc.project_kv_and_lr_cache(X, W_rows, None, n_kv, d, 2, 0, r, K, V, None,
+    t_base = timed(lambda: prc.project_kv_and_lr_cache(X, W, None, n_kv, d, 2, 0, r, K, V, None,
                                                        rope_theta=th, tok_offset=S))
-    t_pre = timed(lambda: prc.precompute_lr_cache(X, A_rows, 2, N, r, L, tok_offset=S))
+    t_pre = timed(lambda: prc.precompute_lr_cache(X, A_stack, 2, N, r, L, tok_offset=S))
     cols = 2 * n_kv * d + 2 * N * r
     flops = 2 * T * hid * cols
     byts = (T * hid + cols * hid + T * cols) * 2
@@ -562,7 +561,7 @@ def paged(prc, w, dev, steps, warmup):
         c = x["dec" if stage == "decode" else "pre"]
         O = torch.empty_like(c["Q"])
         O2 = torch.empty_like(c["Q"])
-        dims = prc.make_dims(c["Q"], c["K_base"], c["L_k"], c["L_v"], c["Bk_rows"], c["Bv_rows"], theta)
+        dims = prc.make_dims(c["Q"], c["K_base"], c["L_k"], c["L_v"], c["B_k"], c["B_v"], theta)
         ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
         t_c = timeit(lambda: attn(prc, c, theta, O, ws))
         S = c["K_base"].shape[1]
@@ -575,7 +574,7 @@ def paged(prc, w, dev, steps, warmup):
             Lkp, Lvp = to_pool(c["L_k"], tl, blk), to_pool(c["L_v"], tl, blk)
 
             def run():
-                prc.lr_shared_attention_paged(c["Q"], Kp, Vp, Lkp, Lvp, c["Bk_rows"], c["Bv_rows"],
+                prc.lr_shared_attention_paged(c["Q"], Kp, Vp, Lkp, Lvp, c["B_k"], c["B_v"],
                                               c["positions"], c["kv_len"], tk, lr_block_table=tl,
                                               rope_theta=theta, O=O2, workspace=ws)
             t_p = timeit(run)
@@ -592,13 +591,13 @@ def paged(prc, w, dev, steps, warmup):
     # Segment projection (base K/V + all agents' LR rows) into paged pools.
     T, hid, n_kv, d, r, N, S = w["seg"], w["hidden"], w["n_kv"], w["d"], w["r"], w["N"], w["S"]
     X = x["X"][0]
-    W_rows = (torch.randn((2 * n_kv * d, hid), generator=torch.Generator(device=dev).manual_seed(7001),
-                          device=dev) / math.sqrt(hid)).to(torch.bfloat16)
+    W = (torch.randn((hid, 2 * n_kv * d), generator=torch.Generator(device=dev).manual_seed(7001),
+                     device=dev) / math.sqrt(hid)).to(torch.bfloat16)
     s_cap = S + T
     K = torch.empty((s_cap, n_kv, d), dtype=torch.bfloat16, device=dev)
     V = torch.empty_like(K)
     L = torch.empty((2, N, s_cap, r), dtype=torch.bfloat16, device=dev)
-    t_c = timeit(lambda: prc.project_kv_and_lr_cache(X, W_rows, x["A_rows"], n_kv, d, 2, N, r, K, V, L,
+    t_c = timeit(lambda: prc.project_kv_and_lr_cache(X, W, x["A_stack"], n_kv, d, 2, N, r, K, V, L,
                                                      rope_theta=theta, tok_offset=S))
     for blk in (64, 256):
         mb = s_cap // blk
@@ -606,7 +605,7 @@ def paged(prc, w, dev, steps, warmup):
         Kp = torch.empty((mb, blk, n_kv, d), dtype=torch.bfloat16, device=dev)
         Vp = torch.empty_like(Kp)
         Lp = torch.empty((2, N, mb, blk, r), dtype=torch.bfloat16, device=dev)
-        t_p = timeit(lambda: prc.project_kv_and_lr_cache_paged(X, W_rows, x["A_rows"], n_kv, d, 2, N, r, Kp, Vp,
+        t_p = timeit(lambda: prc.project_kv_and_lr_cache_paged(X, W, x["A_stack"], n_kv, d, 2, N, r, Kp, Vp,
                                                                Lp, tbl, rope_theta=theta, tok_offset=S))
         rows = torch.arange(S, s_cap, device=dev)
         same = torch.equal(Kp[tbl[rows // blk].long(), rows % blk], K[S:])
@@ -651,8 +650,8 @@ def stack_bench(prc, dev):
     V = [nrm((1, S_cap, n_kv, d)) for _ in range(n_layers)]
     Lp = [torch.zeros((2, N, S_cap, r), dtype=torch.bfloat16, device=dev) for _ in range(n_layers)]
     A = [nrm((2 * N * r, hid), 1.0 / math.sqrt(hid)) for _ in range(n_layers)]
-    Bk = [nrm((N, n_kv * d, r), bstd) for _ in range(n_layers)]
-    Bv = [nrm((N, n_kv * d, r), bstd) for _ in range(n_layers)]
+    Bk = [nrm((N, r, n_kv * d), bstd) for _ in range(n_layers)]
+    Bv = [nrm((N, r, n_kv * d), bstd) for _ in range(n_layers)]
     X_seg = [nrm((turn, hid)) for _ in range(4)]
     X_pre = [nrm((n_pre, hid)) for _ in range(2)]
     X_dec = nrm((n_dec, hid))
@@ -820,8 +819,8 @@ def workload_bench(prc, index, dev, steps, warmup):
 
     def case(nb, n_tok, kv, pos0):
         return dict(Q=nrm((nb, n_tok, n_q, d)), K_base=nrm((nb, kv, n_kv, d)), V_base=nrm((nb, kv, n_kv, d)),
-                    L_k=nrm((nb, kv, r)), L_v=nrm((nb, kv, r)), Bk_rows=nrm((nb, n_kv * d, r), bstd),
-                    Bv_rows=nrm((nb, n_kv * d, r), bstd),
+                    L_k=nrm((nb, kv, r)), L_v=nrm((nb, kv, r)), B_k=nrm((nb, r, n_kv * d), bstd),
+                    B_v=nrm((nb, r, n_kv * d), bstd),
                     positions=(torch.arange(pos0, pos0 + n_tok, dtype=torch.int32, device=dev)[None]
                                .repeat(nb, 1).contiguous()),
                     kv_len=torch.full((nb,), kv, dtype=torch.int32, device=dev))
@@ -830,21 +829,21 @@ def workload_bench(prc, index, dev, steps, warmup):
     dec = [case(B, 1, S, S - 1) for _ in range(n_dec)]
     pre = [case(1, w["n_pre"], kv_pre, S) for _ in range(n_pre)]
     X = [nrm((w["seg"], w["hidden"])) for _ in range(4)]
-    A_rows = nrm((2 * N * r, w["hidden"]), 1.0 / math.sqrt(w["hidden"]))
+    A_stack = nrm((w["hidden"], 2 * N * r), 1.0 / math.sqrt(w["hidden"]))
     L = torch.zeros((2, N, w["seg"], r), dtype=torch.bfloat16, device=dev)
     O_dec = torch.empty_like(dec[0]["Q"])
     O_pre = torch.empty_like(pre[0]["Q"])
-    dims = prc.make_dims(dec[0]["Q"], dec[0]["K_base"], dec[0]["L_k"], dec[0]["L_v"], dec[0]["Bk_rows"],
-                         dec[0]["Bv_rows"], w["theta"])
+    dims = prc.make_dims(dec[0]["Q"], dec[0]["K_base"], dec[0]["L_k"], dec[0]["L_v"], dec[0]["B_k"],
+                         dec[0]["B_v"], w["theta"])
     ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
     Kd, Vd = torch.empty_like(dec[0]["K_base"]), torch.empty_like(dec[0]["V_base"])
     Kp, Vp = torch.empty_like(pre[0]["K_base"]), torch.empty_like(pre[0]["V_base"])
 
     def plain(c, K, V):
-        return dict(c, K_base=K, V_base=V, L_k=None, L_v=None, Bk_rows=None, Bv_rows=None)
+        return dict(c, K_base=K, V_base=V, L_k=None, L_v=None, B_k=None, B_v=None)
 
     def materialised(c, K, V, O, wsp):
-        prc.materialize_agent_kv(c["K_base"], c["V_base"], c["L_k"], c["L_v"], c["Bk_rows"], c["Bv_rows"],
+        prc.materialize_agent_kv(c["K_base"], c["V_base"], c["L_k"], c["L_v"], c["B_k"], c["B_v"],
                                  c["kv_len"], rope_theta=w["theta"], K_full=K, V_full=V)
         attn(prc, plain(c, K, V), w["theta"], O, wsp)
 
@@ -863,7 +862,7 @@ def workload_bench(prc, index, dev, steps, warmup):
         v = sorted(a.elapsed_time(b) for a, b in ts)
         return v[len(v) // 2]
 
-    t_pc = timed(lambda i: prc.precompute_lr_cache(X[i % 4], A_rows, 2, N, r, L), 4)
+    t_pc = timed(lambda i: prc.precompute_lr_cache(X[i % 4], A_stack, 2, N, r, L), 4)
     t_pre = timed(lambda i: attn(prc, pre[i], w["theta"], O_pre, None), n_pre)
     t_dec = timed(lambda i: attn(prc, dec[i], w["theta"], O_dec, ws), n_dec)
     t_pre_m = timed(lambda i: materialised(pre[i], Kp, Vp, O_pre, None), n_pre)

@@ -32,11 +32,13 @@
  *     by the host.  Kernels clamp kv_len[b] into [0, s_cap], so no access ever
  *     leaves the caller's buffers.
  *
- * Orientation of the LoRA weights.  The paper writes Y = X (W0 + A B) with
- * A in R^{d_in x r} and B in R^{r x d_out}.  This ABI stores both factors
- * transposed, as PEFT stores them: down-projections as rows (A^T) and
- * up-projections as [d_out, r] (B^T).  Both MFMA operands are then contiguous
- * along the contracted dimension.
+ * Orientation of the weights.  Every weight matrix is passed in the
+ * orientation of Eq. 1 (Sec. 2.1), Y = X (W0 + A B) with row vectors: frozen
+ * projections W [d_in, d_out], down-projections A [d_in, r] (stacked side by
+ * side for all agents: A_stack [d_in, n_proj*N*r]) and up-projections
+ * B [r, d_out], all row-major.  A caller holding PEFT-style transposed
+ * storage ([d_out, d_in], [r, d_in], [d_out, r]) transposes it once, when the
+ * adapters are loaded.
  */
 #ifndef PRECACHE_H
 #define PRECACHE_H
@@ -70,25 +72,28 @@ const char* prc_version(void);
  * precompute_lr_cache -- the LR-cache precompute of Sec. 3.1 (Fig. 1 A1-A3).
  *
  * For a newly processed segment of T hidden states, apply EVERY agent's LoRA
- * down-projection, for every adapted projection, in one batched GEMM:
- *     L[p][a][tok_offset + t][j] = sum_k X[t][k] * A_rows[(p*N + a)*r + j][k]
+ * down-projection, for every adapted projection, in one batched GEMM
+ * X . [A_1 | ... | A_N]:
+ *     L[p][a][tok_offset + t][j] = sum_k X[t][k] * A_stack[k][(p*N + a)*r + j]
  * This is X A_k of Sec. 2.2 for all agents k at once.
  *
  *   X        [T, d_in] bf16, row stride ld_x (elements, >= d_in).  These are
  *            the hidden states that feed k_proj/v_proj.
- *   A_rows   [n_proj*N*r, d_in] bf16, contiguous.  Row (p*N + a)*r + j is
- *            column j of agent a's down-projection A for projection p
- *            (p = 0: k_proj, p = 1: v_proj when n_proj = 2).
+ *   A_stack  [d_in, n_proj*N*r] bf16, contiguous.  Columns
+ *            [(p*N + a)*r, (p*N + a + 1)*r) hold agent a's down-projection
+ *            A [d_in, r] for projection p (p = 0: k_proj, p = 1: v_proj when
+ *            n_proj = 2).
  *   L_out    [n_proj, N, s_cap, r] bf16, contiguous.  Rows
  *            [tok_offset, tok_offset + T) of every plane are overwritten;
  *            nothing else is touched.
  * Arithmetic: bf16 inputs, fp32 accumulation, round-to-nearest-even to bf16.
- * Requires d_in % 8 == 0, ld_x % 8 == 0, d_in <= ld_x < 2^24 (PRC_EUNSUPPORTED
- * otherwise), r in {8, 16, 32, 64}, 1 <= s_cap < 2^31, 0 <= tok_offset and
- * tok_offset + T <= s_cap.  T == 0 is a no-op.
+ * Requires d_in % 8 == 0, ld_x % 8 == 0, d_in <= ld_x < 2^23 and
+ * (d_in + 128) * n_proj*N*r < 2^30 (PRC_EUNSUPPORTED otherwise), r in
+ * {8, 16, 32, 64}, 1 <= s_cap < 2^31, 0 <= tok_offset and tok_offset + T <=
+ * s_cap.  T == 0 is a no-op.
  */
 prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
-                               const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                               const uint16_t* A_stack, int32_t n_proj, int32_t n_agents,
                                int32_t rank, uint16_t* L_out, int64_t s_cap,
                                int64_t tok_offset, void* stream);
 
@@ -99,28 +104,28 @@ prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64
  * over the segment's hidden states, so X is read once for all of it:
  *     K_base[tok_offset + t][h][:] = RoPE(X[t] . W_k[:, h*d:(h+1)*d], tok_offset + t)
  *     V_base[tok_offset + t][h][:] = X[t] . W_v[:, h*d:(h+1)*d]
- *     L[p][a][tok_offset + t][j]  = X[t] . A_rows[(p*N + a)*r + j]
+ *     L[p][a][tok_offset + t][j]  = X[t] . A_stack[:, (p*N + a)*r + j]
  * RoPE is the rotate-half form with omega_j = rope_theta^(-2j/d), each token
  * at its absolute position tok_offset + t (KV token t sits at position t).
  *
  *   X        [T, d_in] bf16, row stride ld_x, as for precompute_lr_cache.
- *   W_rows   [2*n_kv*d, d_in] bf16, contiguous: row h*d + j is column h*d + j
- *            of W_k (key projection), row n_kv*d + h*d + j that of W_v.
- *   A_rows   as for precompute_lr_cache.
+ *   W        [d_in, 2*n_kv*d] bf16, contiguous: [W_k | W_v], the key
+ *            projection's n_kv*d columns, then the value projection's.
+ *   A_stack  as for precompute_lr_cache.
  *   K_base, V_base  [s_cap, n_kv, d] bf16, contiguous (one request's base
  *            cache); rows [tok_offset, tok_offset + T) are overwritten.
  *   L_out    [n_proj, N, s_cap, r] bf16, contiguous; the same rows of every
  *            plane are overwritten.  Nothing else is touched.
- *   n_proj * n_agents == 0 computes the base cache alone; A_rows and L_out
+ *   n_proj * n_agents == 0 computes the base cache alone; A_stack and L_out
  *            may then be NULL and rank is ignored.
  * Arithmetic: bf16 inputs, fp32 accumulation, RoPE in fp32 with angles
  * reduced in fp64, round-to-nearest-even to bf16.  Requires d in {64, 128},
- * the precompute_lr_cache limits, 2*n_kv*d*d_in < 2^29 and s_cap < 2^31
- * (PRC_EUNSUPPORTED / PRC_EINVAL otherwise).  T == 0 is a no-op.
+ * the precompute_lr_cache limits, 2*n_kv*d*(d_in + 128) < 2^29 and
+ * s_cap < 2^31 (PRC_EUNSUPPORTED / PRC_EINVAL otherwise).  T == 0 is a no-op.
  */
 prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
-                                   const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
-                                   const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                   const uint16_t* W, int32_t n_kv_heads, int32_t head_dim,
+                                   const uint16_t* A_stack, int32_t n_proj, int32_t n_agents,
                                    int32_t rank, double rope_theta, uint16_t* K_base,
                                    uint16_t* V_base, uint16_t* L_out, int64_t s_cap,
                                    int64_t tok_offset, void* stream);
@@ -142,7 +147,7 @@ prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, i
  *   L_pool   [n_proj, N, n_blocks, block_size, r] bf16, contiguous: each
  *            agent's LR plane is a pool indexed by the same block ids as the
  *            base pools.
- *   n_kv_heads == 0 writes the LR planes alone (W_rows, K_pool, V_pool may be
+ *   n_kv_heads == 0 writes the LR planes alone (W, K_pool, V_pool may be
  *            NULL; head_dim and rope_theta are ignored); n_proj * n_agents == 0
  *            the base pools alone.
  * Requires block_size a positive multiple of 64, max_blocks and n_blocks >= 1,
@@ -152,8 +157,8 @@ prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, i
  * touched.
  */
 prc_status project_kv_and_lr_cache_paged(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
-                                         const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
-                                         const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                         const uint16_t* W, int32_t n_kv_heads, int32_t head_dim,
+                                         const uint16_t* A_stack, int32_t n_proj, int32_t n_agents,
                                          int32_t rank, double rope_theta, uint16_t* K_pool,
                                          uint16_t* V_pool, uint16_t* L_pool, const int32_t* block_table,
                                          int32_t block_size, int32_t max_blocks, int32_t n_blocks,
@@ -182,8 +187,8 @@ typedef struct lrsa_dims {
  * its own LR cache (Sec. 3.1, reuse step; value-side reordering of App. D.2).
  *
  * For request b, query token i and query head h (KV head g = h / (n_q/n_kv)):
- *     K[t] = K_base[t][g] + RoPE(L_k[t] . B_k[g*d:(g+1)*d], t)
- *     V[t] = V_base[t][g] + L_v[t] . B_v[g*d:(g+1)*d]
+ *     K[t] = K_base[t][g] + RoPE(L_k[t] . B_k[:, g*d:(g+1)*d], t)
+ *     V[t] = V_base[t][g] + L_v[t] . B_v[:, g*d:(g+1)*d]
  *     O[b][i][h] = softmax_t( scale * Q[b][i][h] . K[t] ) . V[t]
  * over the keys t with t < kv_len[b] and t <= positions[b][i].  KV token t sits
  * at absolute position t.  RoPE is rotate-half: element j pairs with j + d/2,
@@ -197,8 +202,9 @@ typedef struct lrsa_dims {
  *   L_k, L_v   [B, s_cap, r] bf16 (request stride l_req_stride): each request's
  *              agent plane of the LR cache.  NULL = that projection is not
  *              adapted.  The QV setting of the paper passes L_k = NULL.
- *   B_k, B_v   [B, n_kv*d, r] bf16 (request stride b_req_stride): each request's
- *              agent up-projection, stored transposed (B^T).  Must be NULL
+ *   B_k, B_v   [B, r, n_kv*d] bf16 (request stride b_req_stride): each request's
+ *              agent up-projection B of Eq. 1 (row j: rank j, all KV heads'
+ *              columns; head g owns columns [g*d, (g+1)*d)).  Must be NULL
  *              exactly when the matching L is NULL.
  *   positions  [B, n_tok] int32, absolute query positions.
  *   kv_len     [B] int32, number of valid cache rows per request (device memory).
@@ -304,13 +310,15 @@ size_t lr_shared_attention_paged_workspace_size(const lrsa_dims* dims);
  * materialize_agent_kv -- the reference point: write out each request's full
  * per-agent K/V (the keys and values NonShared/BaseShared agents would hold,
  * Sec. 3.1) so that a plain attention call (L_k = L_v = NULL) can consume them.
- *     K_full[b][t][g] = K_base[b][t][g] + RoPE(L_k[b][t] . B_k[g], t)
- *     V_full[b][t][g] = V_base[b][t][g] + L_v[b][t] . B_v[g]
+ *     K_full[b][t][g] = K_base[b][t][g] + RoPE(L_k[b][t] . B_k[b][:, g*d:(g+1)*d], t)
+ *     V_full[b][t][g] = V_base[b][t][g] + L_v[b][t] . B_v[b][:, g*d:(g+1)*d]
  * for t < kv_len[b].  Rows t >= kv_len[b] of K_full/V_full are not written.
  *   K_full, V_full  [B, s_cap, n_kv, d] bf16, contiguous (request stride
  *                   s_cap*n_kv*d), and must not alias the inputs.
- * Other arguments as in lr_shared_attention (n_tok, softmax_scale ignored).
- * A NULL L_k (or L_v) copies K_base (or V_base) unchanged.
+ * Other arguments (B_k, B_v as [B, r, n_kv*d]) as in lr_shared_attention
+ * (n_tok, softmax_scale ignored).  No output byte may lie in any input's
+ * extent (PRC_EINVAL).  A NULL L_k (or L_v) copies K_base (or V_base)
+ * unchanged.
  */
 prc_status materialize_agent_kv(const lrsa_dims* dims, const uint16_t* K_base,
                                 const uint16_t* V_base, const uint16_t* L_k,

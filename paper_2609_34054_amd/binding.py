@@ -138,44 +138,46 @@ def _req_stride(t, batch):
     return t.stride(0)
 
 
-def precompute_lr_cache(X, A_rows, n_proj: int, n_agents: int, rank: int, L_out, tok_offset: int = 0,
+def precompute_lr_cache(X, A_stack, n_proj: int, n_agents: int, rank: int, L_out, tok_offset: int = 0,
                         stream=None):
-    """``L_out[p][a][tok_offset + t] = X[t] @ A_rows[(p*N+a)*r:(p*N+a+1)*r].T`` (Sec. 3.1).
+    """``L_out[p][a][tok_offset + t] = X[t] @ A_stack[:, (p*N+a)*r:(p*N+a+1)*r]`` (Sec. 3.1).
 
-    ``X [T, d_in]`` bf16 (row stride may exceed d_in), ``A_rows [n_proj*N*r, d_in]``,
+    ``X [T, d_in]`` bf16 (row stride may exceed d_in), ``A_stack [d_in, n_proj*N*r]``,
     ``L_out [n_proj, N, s_cap, r]`` bf16 contiguous.
     """
     _bf16("X", X, 2)
-    _bf16("A_rows", A_rows, 2)
+    _bf16("A_stack", A_stack, 2)
     _bf16("L_out", L_out, 4)
-    if not A_rows.is_contiguous() or not L_out.is_contiguous():
-        raise ValueError("A_rows and L_out must be contiguous")
+    if not A_stack.is_contiguous() or not L_out.is_contiguous():
+        raise ValueError("A_stack and L_out must be contiguous")
+    if tuple(A_stack.shape) != (X.shape[1], n_proj * n_agents * rank):
+        raise ValueError(f"A_stack shape {tuple(A_stack.shape)} is not ({X.shape[1]}, {n_proj * n_agents * rank})")
     if tuple(L_out.shape[:2]) != (n_proj, n_agents) or L_out.shape[3] != rank:
         raise ValueError(f"L_out shape {tuple(L_out.shape)} does not match ({n_proj}, {n_agents}, s_cap, {rank})")
     T, d_in = X.shape
-    st = lib().precompute_lr_cache(_ptr(X), T, d_in, X.stride(0), _ptr(A_rows), n_proj, n_agents, rank,
+    st = lib().precompute_lr_cache(_ptr(X), T, d_in, X.stride(0), _ptr(A_stack), n_proj, n_agents, rank,
                                    _ptr(L_out), L_out.shape[2], tok_offset, _stream(stream))
     _check("precompute_lr_cache", st)
     return L_out
 
 
-def project_kv_and_lr_cache(X, W_rows, A_rows, n_kv_heads: int, head_dim: int, n_proj: int, n_agents: int,
+def project_kv_and_lr_cache(X, W, A_stack, n_kv_heads: int, head_dim: int, n_proj: int, n_agents: int,
                             rank: int, K_base, V_base, L_out, *, rope_theta: float, tok_offset: int = 0,
                             stream=None):
     """Base K/V (RoPE on keys) and every agent's LR rows of one segment in one GEMM
     over ``X`` (Sec. 2.2 base cache, Sec. 3.1 precompute).
 
-    ``X [T, d_in]`` bf16; ``W_rows [2*n_kv*d, d_in]`` (W_k^T rows, then W_v^T);
-    ``A_rows [n_proj*N*r, d_in]``; ``K_base, V_base [s_cap, n_kv, d]`` and
+    ``X [T, d_in]`` bf16; ``W [d_in, 2*n_kv*d]`` (``[W_k | W_v]``);
+    ``A_stack [d_in, n_proj*N*r]``; ``K_base, V_base [s_cap, n_kv, d]`` and
     ``L_out [n_proj, N, s_cap, r]`` bf16 contiguous, rows ``tok_offset ..`` written.
     """
     _bf16("X", X, 2)
-    _bf16("W_rows", W_rows, 2)
-    _bf16("A_rows", A_rows, 2)
+    _bf16("W", W, 2)
+    _bf16("A_stack", A_stack, 2)
     _bf16("K_base", K_base, 3)
     _bf16("V_base", V_base, 3)
     _bf16("L_out", L_out, 4)
-    for name, t in (("W_rows", W_rows), ("A_rows", A_rows), ("K_base", K_base), ("V_base", V_base),
+    for name, t in (("W", W), ("A_stack", A_stack), ("K_base", K_base), ("V_base", V_base),
                     ("L_out", L_out)):
         if t is not None and not t.is_contiguous():
             raise ValueError(f"{name} must be contiguous")
@@ -186,14 +188,16 @@ def project_kv_and_lr_cache(X, W_rows, A_rows, n_kv_heads: int, head_dim: int, n
     if n_proj * n_agents and tuple(L_out.shape) != (n_proj, n_agents, s_cap, rank):
         raise ValueError(f"L_out shape {tuple(L_out.shape)} does not match ({n_proj}, {n_agents}, {s_cap}, {rank})")
     T, d_in = X.shape
-    st = lib().project_kv_and_lr_cache(_ptr(X), T, d_in, X.stride(0), _ptr(W_rows), n_kv_heads, head_dim,
-                                       _ptr(A_rows), n_proj, n_agents, rank, float(rope_theta), _ptr(K_base),
+    if tuple(W.shape) != (d_in, 2 * n_kv_heads * head_dim):
+        raise ValueError(f"W shape {tuple(W.shape)} is not ({d_in}, {2 * n_kv_heads * head_dim})")
+    st = lib().project_kv_and_lr_cache(_ptr(X), T, d_in, X.stride(0), _ptr(W), n_kv_heads, head_dim,
+                                       _ptr(A_stack), n_proj, n_agents, rank, float(rope_theta), _ptr(K_base),
                                        _ptr(V_base), _ptr(L_out), s_cap, tok_offset, _stream(stream))
     _check("project_kv_and_lr_cache", st)
     return K_base, V_base, L_out
 
 
-def project_kv_and_lr_cache_paged(X, W_rows, A_rows, n_kv_heads: int, head_dim: int, n_proj: int,
+def project_kv_and_lr_cache_paged(X, W, A_stack, n_kv_heads: int, head_dim: int, n_proj: int,
                                   n_agents: int, rank: int, K_pool, V_pool, L_pool, block_table, *,
                                   rope_theta: float, tok_offset: int = 0, stream=None):
     """:func:`project_kv_and_lr_cache` writing into paged pools: token ``p`` goes to
@@ -204,12 +208,12 @@ def project_kv_and_lr_cache_paged(X, W_rows, A_rows, n_kv_heads: int, head_dim: 
     ``block_table [max_blocks]`` int32, contiguous.
     """
     _bf16("X", X, 2)
-    _bf16("W_rows", W_rows, 2)
-    _bf16("A_rows", A_rows, 2)
+    _bf16("W", W, 2)
+    _bf16("A_stack", A_stack, 2)
     _bf16("K_pool", K_pool, 4)
     _bf16("V_pool", V_pool, 4)
     _bf16("L_pool", L_pool, 5)
-    for name, t in (("W_rows", W_rows), ("A_rows", A_rows), ("K_pool", K_pool), ("V_pool", V_pool),
+    for name, t in (("W", W), ("A_stack", A_stack), ("K_pool", K_pool), ("V_pool", V_pool),
                     ("L_pool", L_pool), ("block_table", block_table)):
         if t is not None and not t.is_contiguous():
             raise ValueError(f"{name} must be contiguous")
@@ -224,8 +228,8 @@ def project_kv_and_lr_cache_paged(X, W_rows, A_rows, n_kv_heads: int, head_dim: 
         raise ValueError(f"L_pool shape {tuple(L_pool.shape)} does not match "
                          f"({n_proj}, {n_agents}, {n_blocks}, {blk}, {rank})")
     T, d_in = X.shape
-    st = lib().project_kv_and_lr_cache_paged(_ptr(X), T, d_in, X.stride(0), _ptr(W_rows), n_kv_heads, head_dim,
-                                             _ptr(A_rows), n_proj, n_agents, rank, float(rope_theta),
+    st = lib().project_kv_and_lr_cache_paged(_ptr(X), T, d_in, X.stride(0), _ptr(W), n_kv_heads, head_dim,
+                                             _ptr(A_stack), n_proj, n_agents, rank, float(rope_theta),
                                              _ptr(K_pool), _ptr(V_pool), _ptr(L_pool), _ptr(block_table), blk,
                                              block_table.shape[0], n_blocks, tok_offset, _stream(stream))
     _check("project_kv_and_lr_cache_paged", st)
@@ -247,8 +251,8 @@ def make_dims(Q, K_base, L_k, L_v, B_k, B_v, rope_theta: float, softmax_scale: f
     rank = lr.shape[-1] if lr is not None else 0
     if lr is not None and lr.shape[-2] != s_cap:
         raise ValueError(f"LR cache holds {lr.shape[-2]} rows, the base cache {s_cap}")
-    if bt is not None and (bt.shape[-2] != n_kv * d or bt.shape[-1] != rank):
-        raise ValueError(f"up-projection shape {tuple(bt.shape)} is not (.., {n_kv * d}, {rank})")
+    if bt is not None and (bt.shape[-2] != rank or bt.shape[-1] != n_kv * d):
+        raise ValueError(f"up-projection shape {tuple(bt.shape)} is not (.., {rank}, {n_kv * d})")
     return LrsaDims(batch=batch, n_tok=n_tok, n_q_heads=n_q, n_kv_heads=n_kv, head_dim=d, rank=rank,
                     s_cap=s_cap, kv_req_stride=_req_stride(K_base, batch),
                     l_req_stride=_req_stride(lr, batch), b_req_stride=_req_stride(bt, batch),
@@ -265,8 +269,8 @@ def lr_shared_attention(Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len
     """Attention over the shared base cache plus one agent's LR cache (Sec. 3.1).
 
     Shapes: ``Q [B, n_tok, n_q, d]``; ``K_base, V_base [B|1, s_cap, n_kv, d]``;
-    ``L_k, L_v [B|1, s_cap, r]`` or None; ``B_k, B_v [B|1, n_kv*d, r]`` or None
-    (stored transposed); ``positions [B, n_tok]`` and ``kv_len [B]`` int32.
+    ``L_k, L_v [B|1, s_cap, r]`` or None; ``B_k, B_v [B|1, r, n_kv*d]`` or None
+    (Eq. 1 orientation); ``positions [B, n_tok]`` and ``kv_len [B]`` int32.
     Returns ``(O, lse)`` (``lse`` None unless requested).
     """
     for name, t, nd in (("Q", Q, 4), ("K_base", K_base, 4), ("V_base", V_base, 4), ("L_k", L_k, 3),
@@ -365,7 +369,7 @@ def lr_shared_attention_paged(Q, K_pool, V_pool, L_k, L_v, B_k, B_v, positions, 
     ``K_pool, V_pool [n_kv_blocks, blk, n_kv, d]`` (one pool) or
     ``[B, n_kv_blocks, blk, n_kv, d]`` (a pool per request); ``L_k, L_v
     [n_lr_blocks, blk, r]`` or ``[B, n_lr_blocks, blk, r]`` or None;
-    ``B_k, B_v [B|1, n_kv*d, r]``; ``kv_block_table`` (and ``lr_block_table``,
+    ``B_k, B_v [B|1, r, n_kv*d]``; ``kv_block_table`` (and ``lr_block_table``,
     default: the same) ``[B, max_blocks]`` int32.
     """
     for name, t in (("K_pool", K_pool), ("V_pool", V_pool), ("L_k", L_k), ("L_v", L_v)):
@@ -392,8 +396,8 @@ def lr_shared_attention_paged(Q, K_pool, V_pool, L_k, L_v, B_k, B_v, positions, 
     n_lr_blocks = lr.shape[-3] if lr is not None else 0
     if lr is not None and lr.shape[-2] != blk:
         raise ValueError(f"LR pool blocks hold {lr.shape[-2]} tokens, base pool blocks {blk}")
-    if bt is not None and (bt.shape[-2] != n_kv * d or bt.shape[-1] != rank):
-        raise ValueError(f"up-projection shape {tuple(bt.shape)} is not (.., {n_kv * d}, {rank})")
+    if bt is not None and (bt.shape[-2] != rank or bt.shape[-1] != n_kv * d):
+        raise ValueError(f"up-projection shape {tuple(bt.shape)} is not (.., {rank}, {n_kv * d})")
     for name, t in (("kv_block_table", kv_block_table), ("lr_block_table", lr_block_table)):
         if t is None:
             continue

@@ -235,19 +235,22 @@ PRC_API const char* prc_status_string(prc_status s) {
 PRC_API const char* prc_version(void) { return "0.1.0"; }
 
 PRC_API prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
-                                       const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                       const uint16_t* A_stack, int32_t n_proj, int32_t n_agents,
                                        int32_t rank, uint16_t* L_out, int64_t s_cap, int64_t tok_offset,
                                        void* stream) {
   if (T < 0) return fail(PRC_EINVAL, "T=%lld is negative", (long long)T);
   if (d_in < 1 || d_in % 8) return fail(PRC_EUNSUPPORTED, "d_in=%lld must be a positive multiple of 8", (long long)d_in);
   if (ld_x < d_in) return fail(PRC_ESHAPE, "ld_x=%lld < d_in=%lld", (long long)ld_x, (long long)d_in);
   if (ld_x % 8) return fail(PRC_EALIGN, "ld_x=%lld is not a multiple of 8 elements", (long long)ld_x);
-  // Tiles of 64 rows are addressed with 32-bit byte offsets.
-  if (ld_x >= (1LL << 24)) return fail(PRC_EUNSUPPORTED, "ld_x=%lld must be below 2^24", (long long)ld_x);
+  // Tiles of up to 128 rows are addressed with 32-bit byte offsets.
+  if (ld_x >= (1LL << 23)) return fail(PRC_EUNSUPPORTED, "ld_x=%lld must be below 2^23", (long long)ld_x);
   if (n_proj < 1 || n_agents < 1) return fail(PRC_EINVAL, "n_proj=%d, n_agents=%d must be positive", n_proj, n_agents);
   if (!rank_ok(rank)) return fail(PRC_EUNSUPPORTED, "rank=%d (built: 8, 16, 32, 64)", rank);
   const int64_t n_cols = (int64_t)n_proj * n_agents * rank;
   if (n_cols > 65535LL * 64) return fail(PRC_EINVAL, "n_proj*n_agents*rank=%lld too large", (long long)n_cols);
+  // A_stack is addressed with 32-bit byte offsets (a stage reads up to 128 k rows past d_in).
+  if ((d_in + 128) * n_cols * 2 >= (1LL << 31))
+    return fail(PRC_EUNSUPPORTED, "d_in*n_cols=%lld weights are too many", (long long)(d_in * n_cols));
   if (s_cap < 1 || s_cap > INT32_MAX)
     return fail(PRC_EINVAL, "s_cap=%lld must be in [1, 2^31)", (long long)s_cap);
   if (tok_offset < 0 || tok_offset + T > s_cap)
@@ -255,12 +258,12 @@ PRC_API prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_i
                 (long long)(tok_offset + T), (long long)s_cap);
   if (T == 0) return ok();
   if (T > (int64_t)INT32_MAX * 64) return fail(PRC_EINVAL, "T too large");
-  if (X == nullptr || A_rows == nullptr || L_out == nullptr) return fail(PRC_EINVAL, "X/A_rows/L_out is NULL");
-  if (!aligned(X, 16) || !aligned(A_rows, 16) || !aligned(L_out, 16))
-    return fail(PRC_EALIGN, "X/A_rows/L_out must be 16-byte aligned");
+  if (X == nullptr || A_stack == nullptr || L_out == nullptr) return fail(PRC_EINVAL, "X/A_stack/L_out is NULL");
+  if (!aligned(X, 16) || !aligned(A_stack, 16) || !aligned(L_out, 16))
+    return fail(PRC_EALIGN, "X/A_stack/L_out must be 16-byte aligned");
   prc::PrecomputeArgs a{};
   a.X = X;
-  a.A = A_rows;
+  a.A = A_stack;
   a.L = L_out;
   a.T = T;
   a.d_in = d_in;
@@ -280,7 +283,7 @@ namespace {
 // the caches are pools of n_blocks blocks of blk tokens and
 // s_cap is the trajectory's logical capacity max_blocks * blk.
 prc_status project_impl(const char* who, const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
-                        const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim, const uint16_t* A_rows,
+                        const uint16_t* W, int32_t n_kv_heads, int32_t head_dim, const uint16_t* A_stack,
                         int32_t n_proj, int32_t n_agents, int32_t rank, double rope_theta, uint16_t* K_base,
                         uint16_t* V_base, uint16_t* L_out, int64_t s_cap, int64_t tok_offset, bool paged,
                         const int32_t* tbl, int32_t blk, int32_t n_blocks, hipStream_t stream) {
@@ -288,7 +291,7 @@ prc_status project_impl(const char* who, const uint16_t* X, int64_t T, int64_t d
   if (d_in < 1 || d_in % 8) return fail(PRC_EUNSUPPORTED, "d_in=%lld must be a positive multiple of 8", (long long)d_in);
   if (ld_x < d_in) return fail(PRC_ESHAPE, "ld_x=%lld < d_in=%lld", (long long)ld_x, (long long)d_in);
   if (ld_x % 8) return fail(PRC_EALIGN, "ld_x=%lld is not a multiple of 8 elements", (long long)ld_x);
-  if (ld_x >= (1LL << 24)) return fail(PRC_EUNSUPPORTED, "ld_x=%lld must be below 2^24", (long long)ld_x);
+  if (ld_x >= (1LL << 23)) return fail(PRC_EUNSUPPORTED, "ld_x=%lld must be below 2^23", (long long)ld_x);
   // Paged calls may leave out the base projection (n_kv_heads == 0).
   const bool with_base = n_kv_heads != 0 || !paged;
   if (with_base && head_dim != 64 && head_dim != 128)
@@ -296,8 +299,9 @@ prc_status project_impl(const char* who, const uint16_t* X, int64_t T, int64_t d
   if (n_kv_heads < 0 || (!paged && n_kv_heads < 1))
     return fail(PRC_EINVAL, "n_kv_heads=%d must be positive", n_kv_heads);
   const int64_t nkv = with_base ? (int64_t)n_kv_heads * head_dim : 0;
-  // Weight rows are addressed with 32-bit byte offsets.
-  if (2 * nkv * d_in * 2 >= (1LL << 31))
+  // The weights are addressed with 32-bit byte offsets (a stage reads up to
+  // 128 k rows past d_in).
+  if (2 * nkv * (d_in + 128) * 2 >= (1LL << 31))
     return fail(PRC_EUNSUPPORTED, "2*n_kv*head_dim*d_in=%lld weights are too many", (long long)(2 * nkv * d_in));
   // n_proj * n_agents == 0: the base projection alone (no LR planes).
   if (n_proj < 0 || n_agents < 0) return fail(PRC_EINVAL, "n_proj=%d, n_agents=%d must not be negative", n_proj, n_agents);
@@ -306,25 +310,27 @@ prc_status project_impl(const char* who, const uint16_t* X, int64_t T, int64_t d
   if (with_lr && !rank_ok(rank)) return fail(PRC_EUNSUPPORTED, "rank=%d (built: 8, 16, 32, 64)", rank);
   const int64_t n_cols = with_lr ? (int64_t)n_proj * n_agents * rank : 0;
   if (2 * nkv + n_cols > 65535LL * 64) return fail(PRC_EINVAL, "too many output columns");
+  if ((d_in + 128) * n_cols * 2 >= (1LL << 31))
+    return fail(PRC_EUNSUPPORTED, "d_in*n_cols=%lld weights are too many", (long long)(d_in * n_cols));
   if (with_base && !(rope_theta > 0.0)) return fail(PRC_EINVAL, "rope_theta must be positive");
   if (s_cap < 1 || s_cap > INT32_MAX) return fail(PRC_EINVAL, "s_cap=%lld must be in [1, 2^31)", (long long)s_cap);
   if (tok_offset < 0 || tok_offset + T > s_cap)
     return fail(PRC_ESHAPE, "rows [%lld, %lld) fall outside s_cap=%lld", (long long)tok_offset,
                 (long long)(tok_offset + T), (long long)s_cap);
   if (T == 0) return ok();
-  if (X == nullptr || (with_base && (W_rows == nullptr || K_base == nullptr || V_base == nullptr)) ||
-      (with_lr && (A_rows == nullptr || L_out == nullptr)))
-    return fail(PRC_EINVAL, "X/W_rows/A_rows/K_base/V_base/L_out is NULL");
-  if (!aligned(X, 16) || (with_base && (!aligned(W_rows, 16) || !aligned(K_base, 16) || !aligned(V_base, 16))) ||
-      (with_lr && (!aligned(A_rows, 16) || !aligned(L_out, 16))))
-    return fail(PRC_EALIGN, "X/W_rows/A_rows/K_base/V_base/L_out must be 16-byte aligned");
+  if (X == nullptr || (with_base && (W == nullptr || K_base == nullptr || V_base == nullptr)) ||
+      (with_lr && (A_stack == nullptr || L_out == nullptr)))
+    return fail(PRC_EINVAL, "X/W/A_stack/K_base/V_base/L_out is NULL");
+  if (!aligned(X, 16) || (with_base && (!aligned(W, 16) || !aligned(K_base, 16) || !aligned(V_base, 16))) ||
+      (with_lr && (!aligned(A_stack, 16) || !aligned(L_out, 16))))
+    return fail(PRC_EALIGN, "X/W/A_stack/K_base/V_base/L_out must be 16-byte aligned");
   if (paged && tbl == nullptr) return fail(PRC_EINVAL, "block_table is NULL");
   if (paged && !aligned(tbl, 4)) return fail(PRC_EALIGN, "block_table is not 4-byte aligned");
   prc::PrecomputeArgs a{};
   a.X = X;
-  a.A = A_rows;
+  a.A = A_stack;
   a.L = L_out;
-  a.W = W_rows;
+  a.W = W;
   a.Kout = K_base;
   a.Vout = V_base;
   a.T = T;
@@ -350,18 +356,18 @@ prc_status project_impl(const char* who, const uint16_t* X, int64_t T, int64_t d
 }  // namespace
 
 PRC_API prc_status project_kv_and_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
-                                           const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
-                                           const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                           const uint16_t* W, int32_t n_kv_heads, int32_t head_dim,
+                                           const uint16_t* A_stack, int32_t n_proj, int32_t n_agents,
                                            int32_t rank, double rope_theta, uint16_t* K_base, uint16_t* V_base,
                                            uint16_t* L_out, int64_t s_cap, int64_t tok_offset, void* stream) {
-  return project_impl("project_kv_and_lr_cache", X, T, d_in, ld_x, W_rows, n_kv_heads, head_dim, A_rows, n_proj,
+  return project_impl("project_kv_and_lr_cache", X, T, d_in, ld_x, W, n_kv_heads, head_dim, A_stack, n_proj,
                       n_agents, rank, rope_theta, K_base, V_base, L_out, s_cap, tok_offset, false, nullptr, 0, 0,
                       static_cast<hipStream_t>(stream));
 }
 
 PRC_API prc_status project_kv_and_lr_cache_paged(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
-                                                 const uint16_t* W_rows, int32_t n_kv_heads, int32_t head_dim,
-                                                 const uint16_t* A_rows, int32_t n_proj, int32_t n_agents,
+                                                 const uint16_t* W, int32_t n_kv_heads, int32_t head_dim,
+                                                 const uint16_t* A_stack, int32_t n_proj, int32_t n_agents,
                                                  int32_t rank, double rope_theta, uint16_t* K_pool,
                                                  uint16_t* V_pool, uint16_t* L_pool, const int32_t* block_table,
                                                  int32_t block_size, int32_t max_blocks, int32_t n_blocks,
@@ -372,7 +378,7 @@ PRC_API prc_status project_kv_and_lr_cache_paged(const uint16_t* X, int64_t T, i
     return fail(PRC_EINVAL, "max_blocks=%d, n_blocks=%d must be positive", max_blocks, n_blocks);
   if ((int64_t)max_blocks * block_size > INT32_MAX || (int64_t)n_blocks * block_size > INT32_MAX)
     return fail(PRC_EINVAL, "max_blocks or n_blocks times block_size reaches 2^31 tokens");
-  return project_impl("project_kv_and_lr_cache_paged", X, T, d_in, ld_x, W_rows, n_kv_heads, head_dim, A_rows,
+  return project_impl("project_kv_and_lr_cache_paged", X, T, d_in, ld_x, W, n_kv_heads, head_dim, A_stack,
                       n_proj, n_agents, rank, rope_theta, K_pool, V_pool, L_pool,
                       (int64_t)max_blocks * block_size, tok_offset, true, block_table, block_size,
                       n_blocks, static_cast<hipStream_t>(stream));

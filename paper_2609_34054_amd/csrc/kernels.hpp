@@ -90,9 +90,9 @@ hipError_t launch_materialize(const AttnArgs& a, hipStream_t stream);
 // the LR precompute alone.
 struct PrecomputeArgs {
   const uint16_t* X;
-  const uint16_t* A;    // [n_cols, d_in]
+  const uint16_t* A;    // [d_in, n_cols] (A_stack, Eq. 1 orientation)
   uint16_t* L;          // [n_cols / r][s_cap][r]
-  const uint16_t* W;    // [2 nkv, d_in]: W_k^T rows, then W_v^T rows (nkv > 0)
+  const uint16_t* W;    // [d_in, 2 nkv]: W_k columns, then W_v columns (nkv > 0)
   uint16_t* Kout;       // [s_cap, nkv] (tokens x (head, dim))
   uint16_t* Vout;
   int64_t T;

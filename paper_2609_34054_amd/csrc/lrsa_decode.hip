@@ -238,8 +238,8 @@ lrsa_decode_kernel(const AttnArgs a) {
     for (int kk = 0; kk < C::NCH; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
   }
   typename Ex<R>::Frag bkf[C::NBLK][Ex<R>::NC];
-  load_bt_frags<D, R>(bkf, has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr,
-                      has_lk && active, lane);
+  load_bt_frags<D, R>(bkf, has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr,
+                      (int64_t)a.n_kv * D, has_lk && active, lane);
 
   float m_run = -INFINITY, l_part = 0.f;
   f32x4 acc[C::NBLK];   // O^T: dims blk*16 + 4q + i, head l%16
@@ -493,13 +493,11 @@ lrsa_merge_kernel(const AttnArgs a) {
   for (int dim = tid; dim < D; dim += NT) {
     float sum = fin[dim];
     if (has_lv) {
-      const uint16_t* bv = a.Bv + (int64_t)b * a.b_stride + ((int64_t)g * D + dim) * R;
-#pragma unroll
-      for (int j = 0; j < R; j += 8) {
-        const u32x4 u = *reinterpret_cast<const u32x4*>(bv + j);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) sum += fin[D + j + 2 * c] * bf_lo(u[c]) + fin[D + j + 2 * c + 1] * bf_hi(u[c]);
-      }
+      // B_v [r, n_kv*d]: rank j of this head dim, coalesced over the threads.
+      const int64_t ldb = (int64_t)a.n_kv * D;
+      const uint16_t* bv = a.Bv + (int64_t)b * a.b_stride + (int64_t)g * D + dim;
+#pragma unroll 8
+      for (int j = 0; j < R; ++j) sum += fin[D + j] * __uint_as_float((uint32_t)bv[j * ldb] << 16);
     }
     const uint32_t pk = pack_bf16(sum * inv, 0.f);
     o[dim] = (uint16_t)(pk & 0xffffu);
@@ -662,8 +660,8 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
     for (int kk = 0; kk < C::NCH; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
   }
   typename Ex<R>::Frag bkf[C::NBLK][Ex<R>::NC];
-  load_bt_frags<D, R>(bkf, has_lk && active ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr,
-                      has_lk && active, lane);
+  load_bt_frags<D, R>(bkf, has_lk && active ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr,
+                      (int64_t)a.n_kv * D, has_lk && active, lane);
 
   float m_run = -INFINITY, l_part = 0.f;
   f32x4 acc[C::NBLK];
@@ -867,14 +865,10 @@ __global__ void __launch_bounds__(64 * MR_ROWS) lrsa_merge_rows_kernel(const Att
     const int dim = lane + 64 * dd;
     float sum = fin[w][dim];
     if (has_lv) {
-      const uint16_t* bv = a.Bv + (int64_t)b * a.b_stride + ((int64_t)g * D + dim) * R;
-#pragma unroll
-      for (int j = 0; j < R; j += 8) {
-        const u32x4 u = *reinterpret_cast<const u32x4*>(bv + j);
-#pragma unroll
-        for (int c = 0; c < 4; ++c)
-          sum += fin[w][D + j + 2 * c] * bf_lo(u[c]) + fin[w][D + j + 2 * c + 1] * bf_hi(u[c]);
-      }
+      const int64_t ldb = (int64_t)a.n_kv * D;
+      const uint16_t* bv = a.Bv + (int64_t)b * a.b_stride + (int64_t)g * D + dim;
+#pragma unroll 8
+      for (int j = 0; j < R; ++j) sum += fin[w][D + j] * __uint_as_float((uint32_t)bv[j * ldb] << 16);
     }
     const uint32_t pk = pack_bf16(sum * inv, 0.f);
     o[dim] = (uint16_t)(pk & 0xffffu);

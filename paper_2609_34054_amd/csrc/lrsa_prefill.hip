@@ -180,14 +180,16 @@ lrsa_prefill_kernel(const AttnArgs a) {
     s_minpos = INT32_MAX;
   }
   if constexpr (LK && !C::BK_REG) {
-    const uint16_t* bh = a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R;
+    // B_k [r, n_kv*d] (Eq. 1 orientation): rank j of head dim c at bh[j*ldb + c].
+    const uint16_t* bh = a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D;
+    const int64_t ldb = (int64_t)a.n_kv * D;
     for (int e = tid; e < 2 * 2 * C::NBW * 64 * C::NC; e += NTHR) {
       const int c = e % C::NC, l = (e / C::NC) % 64, i = (e / (C::NC * 64)) % (2 * C::NBW);
       const int phe = e / (C::NC * 64 * 2 * C::NBW);
       const int blk = phe * C::NBW + (i % C::NBW) + (i / C::NBW) * C::NB;
       // Ranks > 16 use 32-wide chunks: 8 ranks per lane, one 16-byte fragment.
       const int r0 = Ex<R>::rank0(c, l >> 4);
-      bk_lds[e] = r0 < R ? *reinterpret_cast<const u32x4*>(bh + blk_dim<D>(blk, l & 15) * R + r0) : u32x4{0u, 0u, 0u, 0u};
+      bk_lds[e] = Ex<R>::gather(bh + (int64_t)(r0 < R ? r0 : 0) * ldb + blk_dim<D>(blk, l & 15), ldb, r0 < R);
     }
   }
   int64_t kvl = a.kv_len[b];
@@ -257,7 +259,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const bool lv_wave = LVA && w < 2 * C::RB;
   // B_k^T fragment (16x16x16 A operand) of low block i (i < NBW) or of its
   // RoPE partner (i >= NBW), rank chunk rc: lane = dim row, 4 ranks from q*4.
-  const uint16_t* bhead = LK ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D * R : nullptr;
+  const uint16_t* bhead = LK ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr;
+  const int64_t ldb = (int64_t)a.n_kv * D;  // row stride of the [r, n_kv*d] up-projections
   using Frag = typename Ex<R>::Frag;
   Frag bkr[C::BK_REG && LK ? 2 * C::NBW : 1][C::NC];
   if constexpr (C::BK_REG && LK) {
@@ -267,7 +270,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
       for (int c = 0; c < C::NC; ++c) {
         const int r0 = Ex<R>::rank0(c, q);
-        bkr[i][c] = Ex<R>::load(bhead + blk_dim<D>(blk, c16) * R + r0, r0 < R);
+        bkr[i][c] = Ex<R>::gather(bhead + (int64_t)(r0 < R ? r0 : 0) * ldb + blk_dim<D>(blk, c16), ldb, r0 < R);
       }
     }
   }
@@ -313,12 +316,11 @@ lrsa_prefill_kernel(const AttnArgs a) {
   int32_t offlvv[VREB ? R / 16 : 1];
   u32x4 bvf[VREB ? R / 16 : 1];
   if constexpr (VREB) {
-    const uint16_t* bvp =
-        a.Bv + (int64_t)b * a.b_stride + ((int64_t)g * D + 32 * vdb + (lane & 31)) * R + (lane >> 5) * 8;
+    const uint16_t* bvp = a.Bv + (int64_t)b * a.b_stride + (int64_t)g * D + 32 * vdb + (lane & 31);
 #pragma unroll
     for (int kc = 0; kc < R / 16; ++kc) {
       offlvv[kc] = (32 * vtb + (lane & 31)) * R * 2 + (16 * kc + (lane >> 5) * 8) * 2;
-      bvf[kc] = ld16(bvp + 16 * kc, true);
+      bvf[kc] = Ex<R>::gather(bvp + (int64_t)(16 * kc + (lane >> 5) * 8) * ldb, ldb, true);
     }
   }
   // Tiles are loaded in token order, so paged caches are walked with them.
@@ -780,9 +782,9 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
       for (int db = 0; db < C::NDB; ++db) {
         const int dim = db * 32 + l32;
-        const uint16_t* bv = a.Bv + (int64_t)b * a.b_stride + ((int64_t)g * D + dim) * R;
-        const u32x2 b0 = ld8(bv + r0, r0 < R);
-        const u32x2 b1 = ld8(bv + r0 + 8, r0 + 8 < R);
+        const uint16_t* bv = a.Bv + (int64_t)b * a.b_stride + (int64_t)g * D + dim;
+        const u32x2 b0 = Ex<R>::gather(bv + (int64_t)(r0 < R ? r0 : 0) * ldb, ldb, r0 < R);
+        const u32x2 b1 = Ex<R>::gather(bv + (int64_t)(r0 + 8 < R ? r0 + 8 : 0) * ldb, ldb, r0 + 8 < R);
         const u32x4 bw = {b0[0], b0[1], b1[0], b1[1]};
         acc[db] = mfma32x32x16(as_bf16x8(bw), as_bf16x8(hi), acc[db]);
         acc[db] = mfma32x32x16(as_bf16x8(bw), as_bf16x8(lo), acc[db]);

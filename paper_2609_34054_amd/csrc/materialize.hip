@@ -7,10 +7,11 @@
 // lr_shared_attention call with no LR cache) is the "materialise, then
 // attend" path that the fused kernels avoid.
 //
-// One workgroup per (16 tokens, group of up to 8 KV heads, request); one wave
-// per KV head.  The 16 x d/2 RoPE table of the tile is built once in LDS and
-// shared by the waves; the rebuild itself is the same on-chip code the
-// attention kernels use.
+// One workgroup per (64 tokens, group of up to 8 KV heads, request); one wave
+// per KV head, which loads its head's up-projection fragments once and then
+// rebuilds the 64 tokens 16 at a time.  The 64 x d/2 RoPE table of the tile is
+// built once in LDS and shared by the waves; the rebuild itself is the same
+// on-chip code the attention kernels use.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
@@ -18,7 +19,8 @@
 namespace prc {
 namespace {
 
-constexpr int MT = 16;    // tokens per workgroup
+constexpr int MT = 64;    // tokens per workgroup
+constexpr int SBT = 16;   // tokens per rebuild step of a wave
 constexpr int MAXW = 8;   // KV heads per workgroup
 
 template <int D, int R>
@@ -47,41 +49,44 @@ materialize_kernel(const AttnArgs a) {
   __syncthreads();
   if (g >= a.n_kv) return;
 
-  const int64_t t = t0 + c16;
-  const bool ok = t < kvl;
-  const int64_t in_off = (int64_t)b * a.kv_stride + (t * a.n_kv + g) * D;
-  const int64_t out_off = ((int64_t)b * a.s_cap * a.n_kv + t * a.n_kv + g) * D;
-  const int64_t boff = (int64_t)b * a.b_stride + (int64_t)g * D * R;
+  // Up-projections [r, n_kv*d] (Eq. 1 orientation): this head's columns.
+  const int64_t boff = (int64_t)b * a.b_stride + (int64_t)g * D, ldb = (int64_t)a.n_kv * D;
+  typename Ex<R>::Frag bk[D / 16][Ex<R>::NC], bv[D / 16][Ex<R>::NC];
+  if (has_lk) load_bt_frags<D, R>(bk, a.Bk + boff, ldb, true, lane);
+  if (has_lv) load_bt_frags<D, R>(bv, a.Bv + boff, ldb, true, lane);
 
-  u32x4 x[D / 32];
-  load_chunks<D>(x, a.Kb + in_off, ok, lane);
-  if (has_lk) {
-    typename Ex<R>::Frag bf[D / 16][Ex<R>::NC];
-    load_bt_frags<D, R>(bf, a.Bk + boff, true, lane);
-    typename Ex<R>::Frag l[Ex<R>::NC];
-    load_lr_frag<R>(l, a.Lk + (int64_t)b * a.l_stride + t * R, ok, lane);
-    const float2* csr = cs_lds + c16 * CS_ROW + q * QPG;
-    float cc[NB][4], ss[NB][4];
+  for (int sb = 0; sb < MT / SBT; ++sb) {
+    const int64_t t = t0 + sb * SBT + c16;
+    if (t0 + sb * SBT >= kvl) break;  // uniform over the wave
+    const bool ok = t < kvl;
+    const int64_t in_off = (int64_t)b * a.kv_stride + (t * a.n_kv + g) * D;
+    const int64_t out_off = ((int64_t)b * a.s_cap * a.n_kv + t * a.n_kv + g) * D;
+    u32x4 x[D / 32];
+    load_chunks<D>(x, a.Kb + in_off, ok, lane);
+    if (has_lk) {
+      typename Ex<R>::Frag l[Ex<R>::NC];
+      load_lr_frag<R>(l, a.Lk + (int64_t)b * a.l_stride + t * R, ok, lane);
+      const float2* csr = cs_lds + (sb * SBT + c16) * CS_ROW + q * QPG;
+      float cc[NB][4], ss[NB][4];
 #pragma unroll
-    for (int blk = 0; blk < NB; ++blk)
+      for (int blk = 0; blk < NB; ++blk)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        cc[blk][i] = csr[blk * 4 + i].x;
-        ss[blk][i] = csr[blk * 4 + i].y;
-      }
-    add_rotated_expansion<D, R>(x, bf, l, cc, ss);
-  }
-  if (ok) store_chunks<D>(a.Kout + out_off, x, lane);
+        for (int i = 0; i < 4; ++i) {
+          cc[blk][i] = csr[blk * 4 + i].x;
+          ss[blk][i] = csr[blk * 4 + i].y;
+        }
+      add_rotated_expansion<D, R>(x, bk, l, cc, ss);
+    }
+    if (ok) store_chunks<D>(a.Kout + out_off, x, lane);
 
-  load_chunks<D>(x, a.Vb + in_off, ok, lane);
-  if (has_lv) {
-    typename Ex<R>::Frag bf[D / 16][Ex<R>::NC];
-    load_bt_frags<D, R>(bf, a.Bv + boff, true, lane);
-    typename Ex<R>::Frag l[Ex<R>::NC];
-    load_lr_frag<R>(l, a.Lv + (int64_t)b * a.l_stride + t * R, ok, lane);
-    add_expansion<D, R>(x, bf, l);
+    load_chunks<D>(x, a.Vb + in_off, ok, lane);
+    if (has_lv) {
+      typename Ex<R>::Frag l[Ex<R>::NC];
+      load_lr_frag<R>(l, a.Lv + (int64_t)b * a.l_stride + t * R, ok, lane);
+      add_expansion<D, R>(x, bv, l);
+    }
+    if (ok) store_chunks<D>(a.Vout + out_off, x, lane);
   }
-  if (ok) store_chunks<D>(a.Vout + out_off, x, lane);
 }
 
 template <int D, int R>

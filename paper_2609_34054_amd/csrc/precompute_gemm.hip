@@ -3,27 +3,32 @@
 //
 // When a segment of T hidden states is first processed, every agent's LoRA
 // down-projection is applied to it at once:
-//     L[p][a][tok_offset + t][j] = sum_k X[t][k] * A_rows[(p*N + a)*r + j][k]
+//     L[p][a][tok_offset + t][j] = sum_k X[t][k] * A_stack[k][(p*N + a)*r + j]
 // i.e. one GEMM  X[T x d_in] . A_stack[d_in x n_cols]  whose n_cols = n_proj*N*r
 // output columns are scattered into per-agent planes [s_cap][r].  With the
 // base projection joined (Sec. 2.2 base cache), the same GEMM also produces
 // K_base = RoPE(X W_k) and V_base = X W_v: X is read once for all of it.
+// The weights come in the orientation of Eq. 1, [d_in, d_out] row-major.
 //
-// The kernel computes the transposed product C^T = rows . X^T, so both
-// operands are rows contiguous along d_in.  Workgroup tile: TB columns x TB
-// tokens (TB = 64 for the narrow LR-only GEMM, 128 for the wide joined one),
-// 4 compute waves, each owning a TB/2 x TB/2 quarter on 32x32x16 MFMAs, and
-// 8 loader waves (the per-CU load rate from L2 needs about 8 issuing waves).
-// The operand tiles are staged in LDS, 32 KB per stage, in a ring of NST
-// stages filled by direct global->LDS buffer loads: every load instruction
-// brings whole 128- or 256-byte rows, so the texture path sees full cache
-// lines and no VGPRs are spent on staging.  Inside a stage each row's 16-byte
-// chunks are XOR-swizzled by the row index so that the MFMA fragment reads are
-// free of bank conflicts.  Rows past the matrix and k past d_in read as zeros
-// (buffer range check / out-of-range offsets).  The result layout gives each
-// lane 4 consecutive output columns of one token: one 8-byte store.
-// Block order is XCD-aware: the column tiles that share rows of X run on the
-// same XCD, so X is fetched into each L2 once.
+// The kernel computes the transposed product C^T = W^T X^T.  X tiles are
+// staged in LDS k-contiguous, so each lane's B fragment (8 consecutive k of
+// one token) is one 16-byte read.  Weight tiles are staged as they lie in
+// memory, k rows of output columns, and the A fragments (8 consecutive k of
+// one column) come out of the transposing LDS read ds_read_b64_tr_b16 (two
+// per fragment).  A workgroup owns TB columns x TB tokens and has 4 compute
+// waves, each accumulating a 64 x 64 block on 32x32x16 MFMAs (four 16-byte
+// fragment reads per four MFMAs), and 8 loader waves filling a 4-stage ring of
+// 32 KB stages with direct global->LDS buffer loads.  For the narrow LR-only
+// GEMM (TB = 64) the four compute waves split every stage's k steps between
+// them and sum their 64 x 64 partials through LDS at the end, in a fixed
+// order; for the wide joined GEMM (TB = 128) each owns a quarter of the tile.
+// Inside a stage, 16-byte chunks are XOR-swizzled by row so that both kinds
+// of fragment read are free of bank conflicts; with direct-to-LDS loads the
+// swizzle is applied by choosing which global chunk each lane fetches.
+// Tokens past T, k past d_in and LR columns past n_cols read as zeros.  The
+// result layout gives each lane 4 consecutive output columns of one token: one
+// 8-byte store.  Block order is XCD-aware: the column tiles that share rows of
+// X run on the same XCD, so X is fetched into each L2 once.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -38,16 +43,25 @@ constexpr int NXCD = 8;         // XCDs of an MI355X
 
 template <int TB>
 struct Tile {
+  static constexpr bool SPLITK = TB == 64;        // compute waves split k (narrow GEMM)
   static constexpr int KST = TB == 64 ? 128 : 64;  // k per stage: 2 x TB x KST x 2 B = 32 KB
-  static constexpr int CPW = KST / 8;              // 16-byte chunks per row and stage
-  static constexpr int RPI = 64 / CPW;             // rows per load instruction (1 KB)
-  static constexpr int RPW = TB / NPW;             // rows of each tile per loader wave
-  static constexpr int NI = RPW / RPI;             // load instructions per tile, wave and stage
-  static constexpr int QB = TB / 64;               // 32x32 blocks per compute wave and dimension
-  // Physical 16-byte chunk of logical chunk c in row r of a stage tile: the
-  // 16 rows read together by one fragment load hit distinct banks (a 256-byte
-  // row spans all 64 banks; two 128-byte rows share them).
-  static __device__ __forceinline__ int swz(int r, int c) { return CPW == 16 ? c ^ (r & 15) : c ^ ((r >> 1) & 7); }
+  // X tile: TB token rows of KST k (XCPR 16-byte chunks per row).
+  static constexpr int XCPR = KST / 8;
+  static constexpr int XRPI = 64 / XCPR;           // rows per load instruction (1 KB)
+  static constexpr int XRPW = TB / NPW;            // rows per loader wave
+  static constexpr int NIX = XRPW / XRPI;          // X load instructions per wave and stage
+  // Weight tile: KST k rows of TB columns (WCPR chunks per row).
+  static constexpr int WCPR = TB / 8;
+  static constexpr int WRPI = 64 / WCPR;
+  static constexpr int WRPW = KST / NPW;
+  static constexpr int NIW = WRPW / WRPI;
+  // Physical chunk of logical chunk c in row r.  X rows: the 16 rows one
+  // fragment read touches hit distinct banks.  Weight rows: the 4 k rows x 64
+  // bytes a half-wave of transposing reads touches hit distinct banks.
+  static __device__ __forceinline__ int swx(int r, int c) { return XCPR == 16 ? c ^ (r & 15) : c ^ ((r >> 1) & 7); }
+  static __device__ __forceinline__ int sww(int r, int c) {
+    return WCPR == 8 ? c ^ (((r >> 1) & 1) << 2) : c ^ ((r & 3) << 2);
+  }
 };
 
 // s_waitcnt vmcnt(n) for a wave-uniform n in {0, 4, ..., 24}, other
@@ -67,12 +81,33 @@ __device__ __forceinline__ void wait_vmcnt_le(int n) {
   }
 }
 
+// Transposing LDS read of 4 bf16 per lane: lane j of each 16-lane group
+// points at 4 consecutive bf16; lane i receives element i%4 of lanes i/4,
+// i/4+4, i/4+8, i/4+12 of its group.
+__device__ __forceinline__ u32x2 lds_read_tr(const uint16_t* p) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((v4s __attribute__((address_space(3)))*)(p));
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// First W column (within the [d_in, 2 nkv] key/value weights) of the 8
+// output columns starting at key column vc (a multiple of 8).  Key tiles
+// permute the columns of each head so that every RoPE pair (dims j and
+// j + d/2) lands in one lane of the result: local column e of a head (32-column
+// block e / 32) holds dim (e / 32) * 16 + e % 16 + (e % 32 >= 16 ? d / 2 : 0).
+__device__ __forceinline__ int key_wcol(int vc, int head_dim) {
+  const int hd = vc / head_dim, e = vc - hd * head_dim;
+  return hd * head_dim + (e / 32) * 16 + (e % 16) + ((e % 32) / 16) * (head_dim / 2);
+}
+
 template <int TB>
 __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const PrecomputeArgs a, int n_ct, int n_tt) {
   using C = Tile<TB>;
-  constexpr int KST = C::KST, CPW = C::CPW, RPI = C::RPI, RPW = C::RPW, NI = C::NI, QB = C::QB;
-  static_assert(2 * NI * AHEAD <= 24 && (2 * NI) % 4 == 0 && NI >= 1, "vmcnt cases");
-  // [stage][weight tile, X tile][TB rows x KST]
+  constexpr int KST = C::KST;
+  static_assert(2 * (C::NIX + C::NIW) * AHEAD <= 24 && (C::NIX + C::NIW) % 2 == 0 && C::NIX >= 1 && C::NIW >= 1,
+                "vmcnt cases");
+  static_assert(NST * 2 * TB * KST * 2 >= NCW * 4 * 16 * 64 * 4, "ring holds the split-k partials");
+  // [stage][X tile, weight tile][TB x KST]
   __shared__ __attribute__((aligned(1024))) uint16_t tiles[NST][2][TB * KST];
   // Waves 0..NCW-1 compute, the others fill the LDS ring, so loading and
   // computing overlap.
@@ -91,37 +126,35 @@ __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const Prec
   // keys, values, then LR columns.
   const int region = col0 < a.nkv ? 0 : (col0 < 2 * a.nkv ? 1 : 2);
   const int lcol0 = col0 - 2 * a.nkv;  // first LR column of an LR tile
-  const int cols = region < 2 ? TB : (a.n_cols - lcol0 < TB ? a.n_cols - lcol0 : TB);  // valid weight rows
+  const int cols = region < 2 ? TB : (a.n_cols - lcol0 < TB ? a.n_cols - lcol0 : TB);  // valid columns
   const int toks = (int)(a.T - tok0 < TB ? a.T - tok0 : (int64_t)TB);  // valid rows of the X tile
-
-  // Buffer resources over the valid rows of each operand tile (k included).
-  // Key and value tiles read rows of W: a value tile rows col0 - nkv ..; a
-  // key tile reorders the rows of its head so that every RoPE pair (dims j,
-  // j + d/2) lands in one lane of the result: local column e of a head
-  // (32-column block e / 32) holds dim (e / 32) * 16 + e % 16 + (e % 32 >= 16 ? d / 2 : 0).
-  const i32x4 ra = region == 2
-      ? buffer_rsrc(a.A + (int64_t)lcol0 * a.d_in, (int32_t)((cols - 1) * a.d_in * 2 + a.d_in * 2))
-      : buffer_rsrc(a.W, (int32_t)(2 * a.nkv * a.d_in * 2));
-  auto weight_row = [&](int row) -> int {  // row of the resource for local tile row `row`
-    if (region == 2) return row;
-    if (region == 1) return col0 + row;
-    const int vc = col0 + row, hd = vc / a.head_dim, e = vc - hd * a.head_dim;
-    return hd * a.head_dim + (e / 32) * 16 + (e % 16) + ((e % 32) / 16) * (a.head_dim / 2);
-  };
+  const int64_t ldw = region < 2 ? 2 * (int64_t)a.nkv : (int64_t)a.n_cols;  // weight row stride (elements)
+  const i32x4 rw = buffer_rsrc(region < 2 ? a.W : a.A, (int32_t)(a.d_in * ldw * 2));
   const i32x4 rx = buffer_rsrc(a.X + tok0 * a.ld_x, (int32_t)((toks - 1) * a.ld_x * 2 + a.d_in * 2));
 
-  // Loader: each loader wave fills RPW of the TB rows of both tiles per
-  // stage, NI instructions per tile, each writing 1 KB (RPI rows) at
-  // consecutive lane positions.  Lane i of instruction j holds physical chunk
-  // i % CPW of row RPW w + RPI j + i / CPW, i.e. logical chunk swz(row, i % CPW).
-  int32_t offa[NI], offx[NI], kch[NI];
+  // Loader: each instruction writes 1 KB (whole rows) at consecutive LDS
+  // positions.  Lane i of an X instruction holds physical chunk i % XCPR of
+  // token row XRPW w + XRPI j + i / XCPR, i.e. logical chunk swx(row, i % XCPR);
+  // lane i of a weight instruction physical chunk i % WCPR of k row
+  // WRPW w + WRPI j + i / WCPR.
+  int32_t offx[C::NIX], kch[C::NIX], offw[C::NIW], krow[C::NIW];
 #pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    const int row = RPW * w + RPI * j + lane / CPW;
-    const int c = C::swz(row, lane % CPW);
+  for (int j = 0; j < C::NIX; ++j) {
+    const int row = C::XRPW * w + C::XRPI * j + lane / C::XCPR;
+    const int c = C::swx(row, lane % C::XCPR);
     kch[j] = c * 8;  // first k of this lane's chunk within a stage
-    offa[j] = weight_row(row) * (int32_t)(a.d_in * 2) + c * 16;
     offx[j] = row * (int32_t)(a.ld_x * 2) + c * 16;
+  }
+#pragma unroll
+  for (int j = 0; j < C::NIW; ++j) {
+    const int row = C::WRPW * w + C::WRPI * j + lane / C::WCPR;
+    const int c = C::sww(row, lane % C::WCPR);
+    int wcol;
+    if (region == 0) wcol = key_wcol(col0 + 8 * c, a.head_dim);
+    else if (region == 1) wcol = col0 + 8 * c;  // W_v columns follow W_k's
+    else wcol = lcol0 + 8 * c;
+    krow[j] = row;
+    offw[j] = 8 * c < cols ? row * (int32_t)(ldw * 2) + wcol * 2 : INT32_MIN;  // LR columns past n_cols: zeros
   }
   const int nstage = (int)((a.d_in + KST - 1) / KST);
   // Each token tile walks the k stages from its own starting point (the
@@ -135,15 +168,21 @@ __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const Prec
     const int ks = s + rot < nstage ? s + rot : s + rot - nstage;
     const int32_t k0 = ks * KST;
 #pragma unroll
-    for (int j = 0; j < NI; ++j) {
+    for (int j = 0; j < C::NIX; ++j) {
       // Chunks wholly past d_in (d_in is a multiple of 8) read as zeros.
-      const bool kok = k0 + kch[j] < a.d_in;
-      const int32_t oa = kok ? offa[j] : INT32_MIN, ox = kok ? offx[j] : INT32_MIN;
-      lds_dma16(ra, &tiles[sl][0][(RPW * w + RPI * j) * KST], oa, k0 * 2);
-      lds_dma16(rx, &tiles[sl][1][(RPW * w + RPI * j) * KST], ox, k0 * 2);
+      const int32_t ox = k0 + kch[j] < a.d_in ? offx[j] : INT32_MIN;
+      lds_dma16(rx, &tiles[sl][0][(C::XRPW * w + C::XRPI * j) * KST], ox, k0 * 2);
+    }
+#pragma unroll
+    for (int j = 0; j < C::NIW; ++j) {
+      // k rows past d_in read as zeros; the whole offset is range-checked.
+      const int32_t ow =
+          (k0 + krow[j] < a.d_in && offw[j] != INT32_MIN) ? offw[j] + k0 * (int32_t)(ldw * 2) : INT32_MIN;
+      lds_dma16(rw, &tiles[sl][1][(C::WRPW * w + C::WRPI * j) * TB], ow, 0);
     }
   };
 
+  f32x16 acc[2][2];
   if (producer) {
     // Stage s + AHEAD goes into the slot of stage s - 2, which the compute
     // waves finished before the previous barrier, so it is issued before
@@ -154,78 +193,111 @@ __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const Prec
     for (int s = 0; s < nstage; ++s) {
       if (s + AHEAD < nstage) issue(s + AHEAD);
       // Stage s has landed once at most the loads of the stages after it (up
-      // to AHEAD of them, 2 NI instructions each) are still in flight.
+      // to AHEAD of them, NIX + NIW instructions each) are still in flight.
       const int ahead = nstage - 1 - s < AHEAD ? nstage - 1 - s : AHEAD;
-      wait_vmcnt_le(2 * NI * ahead);
+      wait_vmcnt_le((C::NIX + C::NIW) * ahead);
       __syncthreads();  // stage s visible to all waves
     }
-    return;
-  }
-
-  // Compute: wave w owns columns (TB/2)(w & 1) .. and tokens (TB/2)(w >> 1) ..,
-  // QB x QB blocks of 32 x 32.  32x32x16 fragments: lane l holds row l % 32,
-  // k = (l / 32) * 8 + 0..7.
-  const int l32 = lane & 31, h = lane >> 5;
-  const int ra_row0 = (TB / 2) * (w & 1) + l32, rx_row0 = (TB / 2) * (w >> 1) + l32;
-  // Cache row of each of the lane's tokens: its position tok_offset + t, or
-  // its row in the paged pools.  The table is read here, so that its latency
-  // hides behind the first stage's loads.
-  int64_t srow[QB];
+  } else {
+    // Compute: a 64 x 64 block of columns cw0 .. and tokens tw0 ..
+    // (split k: the whole tile, k steps kk with kk % 4 == w).
+    const int l32 = lane & 31, h = lane >> 5, grp = lane >> 4, i16 = lane & 15;
+    const int cw0 = C::SPLITK ? 0 : 64 * (w & 1), tw0 = C::SPLITK ? 0 : 64 * (w >> 1);
 #pragma unroll
-  for (int bt = 0; bt < QB; ++bt) {
-    const int64_t t = tok0 + (TB / 2) * (w >> 1) + 32 * bt + l32;
-    const int p = (int)(a.tok_offset + t);  // positions stay below 2^31
-    srow[bt] = p;
-    if (a.tbl != nullptr && t < a.T) {
-      const int q = p / a.blk;
-      int32_t e = a.tbl[q];
-      e = e < 0 ? 0 : (e >= a.nblk ? a.nblk - 1 : e);
-      srow[bt] = (int64_t)e * a.blk + (p - q * a.blk);
-    }
-  }
-  f32x16 acc[QB][QB];
+    for (int bc = 0; bc < 2; ++bc)
 #pragma unroll
-  for (int bc = 0; bc < QB; ++bc)
+      for (int bt = 0; bt < 2; ++bt)
 #pragma unroll
-    for (int bt = 0; bt < QB; ++bt)
+        for (int j = 0; j < 16; ++j) acc[bc][bt][j] = 0.f;
+    // Transposing-read address of this lane within a k16 step: k row
+    // 8 (grp / 2) + i16 / 4 (+4 for the second read), columns
+    // (grp % 2) * 16 + 4 (i16 % 4) .. + 3 of each 32-column block.
+    const int tr_k = 8 * (grp >> 1) + (i16 >> 2);
+    const int tr_c = (grp & 1) * 16 + 4 * (i16 & 3);
+    auto wfrag = [&](const uint16_t* tw, int kr, int col) {
+      const int ch = col >> 3;
+      return tw + kr * TB + C::sww(kr, ch) * 8 + (col & 7);
+    };
+    constexpr int KK = KST / 16;
+    for (int s = 0; s < nstage; ++s) {
+      __syncthreads();  // stage s visible to all waves; stage s - 1 consumed by all
+      const uint16_t* tx = tiles[s % NST][0];
+      const uint16_t* tw = tiles[s % NST][1];
 #pragma unroll
-      for (int j = 0; j < 16; ++j) acc[bc][bt][j] = 0.f;
-  for (int s = 0; s < nstage; ++s) {
-    __syncthreads();  // stage s visible to all waves; stage s - 1 consumed by all
-    const uint16_t* ta = tiles[s % NST][0];
-    const uint16_t* tx = tiles[s % NST][1];
+      for (int ki = 0; ki < (C::SPLITK ? KK / NCW : KK); ++ki) {
+        const int kk = C::SPLITK ? ki * NCW + w : ki;
+        bf16x8 fa[2], fx[2];
 #pragma unroll
-    for (int kk = 0; kk < KST / 16; ++kk) {
-      const int c = 2 * kk + h;  // logical chunk of this lane's 8 k
-      bf16x8 fa[QB], fx[QB];
+        for (int b = 0; b < 2; ++b) {
+          const int kr = 16 * kk + tr_k, col = cw0 + 32 * b + tr_c;
+          const u32x2 lo = lds_read_tr(wfrag(tw, kr, col)), hi = lds_read_tr(wfrag(tw, kr + 4, col));
+          fa[b] = as_bf16x8(u32x4{lo[0], lo[1], hi[0], hi[1]});
+          const int xr = tw0 + 32 * b + l32, c = 2 * kk + h;
+          fx[b] = as_bf16x8(*reinterpret_cast<const u32x4*>(tx + xr * KST + C::swx(xr, c) * 8));
+        }
 #pragma unroll
-      for (int b = 0; b < QB; ++b) {
-        const int ar = ra_row0 + 32 * b, xr = rx_row0 + 32 * b;
-        fa[b] = as_bf16x8(*reinterpret_cast<const u32x4*>(ta + ar * KST + C::swz(ar, c) * 8));
-        fx[b] = as_bf16x8(*reinterpret_cast<const u32x4*>(tx + xr * KST + C::swz(xr, c) * 8));
+        for (int bc = 0; bc < 2; ++bc)
+#pragma unroll
+          for (int bt = 0; bt < 2; ++bt) acc[bc][bt] = mfma32x32x16(fa[bc], fx[bt], acc[bc][bt]);
       }
-#pragma unroll
-      for (int bc = 0; bc < QB; ++bc)
-#pragma unroll
-        for (int bt = 0; bt < QB; ++bt) acc[bc][bt] = mfma32x32x16(fa[bc], fx[bt], acc[bc][bt]);
     }
   }
 
-  // acc[bc][bt][j]: column (TB/2)(w & 1) + 32 bc + (j / 4) * 8 + h * 4 + j % 4,
-  // token (TB/2)(w >> 1) + 32 bt + l32.
+  // Which 32 x 32 blocks this wave writes: split k sums the four waves'
+  // partials through LDS (the ring is free once every wave is past the last
+  // stage) in a fixed order, and wave w writes block (w & 1, w >> 1).
+  if constexpr (C::SPLITK) {
+    float* part = reinterpret_cast<float*>(&tiles[0][0][0]);  // [wave][bc][bt][16][64]
+    __syncthreads();  // every wave is past the last stage
+    if (!producer) {
 #pragma unroll
-  for (int bt = 0; bt < QB; ++bt) {
-    const int64_t t = tok0 + (TB / 2) * (w >> 1) + 32 * bt + l32;
+      for (int bc = 0; bc < 2; ++bc)
+#pragma unroll
+        for (int bt = 0; bt < 2; ++bt)
+#pragma unroll
+          for (int j = 0; j < 16; ++j) part[(((w * 2 + bc) * 2 + bt) * 16 + j) * 64 + lane] = acc[bc][bt][j];
+    }
+    __syncthreads();
+    if (producer) return;
+    const int bc = w & 1, bt = w >> 1;
+    f32x16 sum;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      float v = 0.f;
+#pragma unroll
+      for (int ww = 0; ww < NCW; ++ww) v += part[(((ww * 2 + bc) * 2 + bt) * 16 + j) * 64 + lane];
+      sum[j] = v;
+    }
+    acc[0][0] = sum;
+  } else {
+    if (producer) return;
+  }
+
+  // acc[bc][bt][j]: column cw + 32 bc + (j / 4) * 8 + h * 4 + j % 4, token
+  // tw + 32 bt + l32 (split k: the one block acc[0][0] at (32 (w & 1), 32 (w >> 1))).
+  const int l32 = lane & 31, h = lane >> 5;
+  const int cw = C::SPLITK ? 32 * (w & 1) : 64 * (w & 1), tw = C::SPLITK ? 32 * (w >> 1) : 64 * (w >> 1);
+  constexpr int NBLK = C::SPLITK ? 1 : 2;
+#pragma unroll
+  for (int bt = 0; bt < NBLK; ++bt) {
+    const int64_t t = tok0 + tw + 32 * bt + l32;
     if (t >= a.T) continue;
     const int64_t trow = a.tok_offset + t;  // absolute position of the token
-    const int64_t row = srow[bt];           // its cache row
+    // Cache row of the token: its position, or its row in the paged pools.
+    int64_t row = trow;
+    if (a.tbl != nullptr) {
+      const int q = (int)(trow / a.blk);
+      int32_t e = a.tbl[q];
+      e = e < 0 ? 0 : (e >= a.nblk ? a.nblk - 1 : e);
+      row = (int64_t)e * a.blk + (trow - (int64_t)q * a.blk);
+    }
 #pragma unroll
-    for (int bc = 0; bc < QB; ++bc) {
+    for (int bc = 0; bc < NBLK; ++bc) {
       const f32x16& r = acc[bc][bt];
-      const int cb = col0 + (TB / 2) * (w & 1) + 32 * bc;  // first column of this 32-column block
+      const int cb = col0 + cw + 32 * bc;  // first column of this 32-column block
       if (region == 0) {
         // Keys: registers j and j + 8 hold dims j0 + i and j0 + i + d/2 of one
-        // head (the row order above); rotate-half RoPE at position trow.
+        // head (the column order above); rotate-half RoPE at position trow.
 #pragma unroll
         for (int jg = 0; jg < 2; ++jg) {
           const int vc = cb + jg * 8 + h * 4;
@@ -276,97 +348,130 @@ hipError_t launch_tb(const PrecomputeArgs& a, hipStream_t st) {
 }
 
 // A handful of rows (the K/V and LR rows of newly decoded tokens) is a
-// matrix-vector product: one workgroup per output column streams that
-// column's row of W_rows or A_rows (contiguous along d_in; 4 waves x 64 lanes
-// x 16 bytes = 4096 elements per step, so a 4096-wide row is one load per
-// lane) against the T <= GV_T rows of X, which every workgroup reads from L2,
-// then reduces over lanes and waves.  Key workgroups take the two rows of one
-// RoPE pair (dims j and j + d/2 of a head) and rotate them at the token's
-// position.  This spreads the weights over thousands of workgroups instead
-// of the few tiles the GEMM would have, and keeps a whole row's loads in
-// flight at once (the rows are usually cold in the decode loop).
+// matrix-vector product.  One workgroup per 8 output columns (a key
+// workgroup: 8 dims of a head and their RoPE partners d/2 further on), so the
+// weights are spread over hundreds of workgroups.  Thread t takes the k rows
+// 8t .. 8t + 7 (+ 2048 per round): one 16-byte load of each of the T <= GV_T
+// rows of X, and one 16-byte load (8 columns) of each weight row.  The
+// partial sums are reduced over the lanes by shuffles and over the waves in
+// LDS.
 constexpr int GV_T = 4;
-constexpr int GV_W = 4;  // waves per column
+constexpr int GV_W = 4;  // waves per workgroup
 
 __global__ void __launch_bounds__(64 * GV_W) project_gemv_kernel(const PrecomputeArgs a) {
-  __shared__ float red[GV_W][2][GV_T];
+  __shared__ float red[GV_W][2][GV_T][8];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int u = blockIdx.x;
-  const int n_pair = a.nkv / 2;  // key RoPE pairs (nkv = n_kv * head_dim, 0 without K/V)
   const int half = a.head_dim / 2;
-  // Region of this workgroup: 0 keys (a pair of rows), 1 values, 2 LR.
-  int region, hd = 0, j = 0, c = 0;
-  const uint16_t* r0;
-  const uint16_t* r1 = nullptr;
+  const int n_pair = a.nkv / 16;  // key workgroups (8 pair columns each)
+  const int n_val = a.nkv / 8;
+  // Region of this workgroup: 0 keys (dims j0 .. j0+7 and their partners), 1
+  // values, 2 LR.
+  int region, c0;
+  const uint16_t* w0;
+  const uint16_t* w1 = nullptr;
+  int64_t ldw;
   if (u < n_pair) {
     region = 0;
-    hd = u / half;
-    j = u - hd * half;
-    r0 = a.W + (int64_t)(hd * a.head_dim + j) * a.d_in;
-    r1 = r0 + (int64_t)half * a.d_in;
-  } else if (u < n_pair + a.nkv) {
+    const int hd = (u * 8) / half, j0 = u * 8 - hd * half;
+    c0 = hd * a.head_dim + j0;  // first dim (column of W_k) of the low half
+    ldw = 2 * (int64_t)a.nkv;
+    w0 = a.W + c0;
+    w1 = w0 + half;
+  } else if (u < n_pair + n_val) {
     region = 1;
-    c = u - n_pair;
-    r0 = a.W + (int64_t)(a.nkv + c) * a.d_in;
+    c0 = (u - n_pair) * 8;
+    ldw = 2 * (int64_t)a.nkv;
+    w0 = a.W + a.nkv + c0;
   } else {
     region = 2;
-    c = u - n_pair - a.nkv;
-    r0 = a.A + (int64_t)c * a.d_in;
+    c0 = (u - n_pair - n_val) * 8;
+    ldw = a.n_cols;
+    w0 = a.A + c0;
   }
   const int T = (int)a.T;
-  float acc0[GV_T] = {0.f, 0.f, 0.f, 0.f}, acc1[GV_T] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 2
-  for (int64_t k = (int64_t)tid * 8; k < a.d_in; k += 64 * GV_W * 8) {
-    const u32x4 av = *reinterpret_cast<const u32x4*>(r0 + k);
-    const bool pair = region == 0;  // uniform over the workgroup
-    u32x4 bv = {0u, 0u, 0u, 0u};
-    if (pair) bv = *reinterpret_cast<const u32x4*>(r1 + k);
+  float acc0[GV_T][8], acc1[GV_T][8];
+#pragma unroll
+  for (int t = 0; t < GV_T; ++t)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc0[t][e] = acc1[t][e] = 0.f;
+  for (int64_t k0 = (int64_t)tid * 8; k0 < a.d_in; k0 += 64 * GV_W * 8) {
+    float x[GV_T][8];
 #pragma unroll
     for (int t = 0; t < GV_T; ++t) {
-      if (t < T) {
-        const u32x4 xv = *reinterpret_cast<const u32x4*>(a.X + t * a.ld_x + k);
+      const u32x4 xv = ld16(a.X + t * a.ld_x + k0, t < T);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) acc0[t] += bf_lo(av[e]) * bf_lo(xv[e]) + bf_hi(av[e]) * bf_hi(xv[e]);
-        if (pair) {
+      for (int e = 0; e < 4; ++e) {
+        x[t][2 * e] = bf_lo(xv[e]);
+        x[t][2 * e + 1] = bf_hi(xv[e]);
+      }
+    }
 #pragma unroll
-          for (int e = 0; e < 4; ++e) acc1[t] += bf_lo(bv[e]) * bf_lo(xv[e]) + bf_hi(bv[e]) * bf_hi(xv[e]);
+    for (int i = 0; i < 8; ++i) {
+      const int64_t k = k0 + i;  // d_in is a multiple of 8: k < d_in
+      const u32x4 wv = *reinterpret_cast<const u32x4*>(w0 + k * ldw);
+      float wf[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        wf[2 * e] = bf_lo(wv[e]);
+        wf[2 * e + 1] = bf_hi(wv[e]);
+      }
+#pragma unroll
+      for (int t = 0; t < GV_T; ++t)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc0[t][e] += x[t][i] * wf[e];
+      if (region == 0) {  // uniform over the workgroup
+        const u32x4 wv1 = *reinterpret_cast<const u32x4*>(w1 + k * ldw);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          wf[2 * e] = bf_lo(wv1[e]);
+          wf[2 * e + 1] = bf_hi(wv1[e]);
         }
+#pragma unroll
+        for (int t = 0; t < GV_T; ++t)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc1[t][e] += x[t][i] * wf[e];
       }
     }
   }
 #pragma unroll
-  for (int t = 0; t < GV_T; ++t) {
+  for (int t = 0; t < GV_T; ++t)
 #pragma unroll
-    for (int x = 1; x < 64; x <<= 1) {
-      acc0[t] += shfl_xor(acc0[t], x);
-      acc1[t] += shfl_xor(acc1[t], x);
+    for (int e = 0; e < 8; ++e) {
+      float v0 = acc0[t][e], v1 = acc1[t][e];
+#pragma unroll
+      for (int x = 1; x < 64; x <<= 1) {
+        v0 += shfl_xor(v0, x);
+        if (region == 0) v1 += shfl_xor(v1, x);
+      }
+      if (lane == 0) {
+        red[w][0][t][e] = v0;
+        red[w][1][t][e] = v1;
+      }
     }
-    if (lane == 0) {
-      red[w][0][t] = acc0[t];
-      red[w][1][t] = acc1[t];
-    }
-  }
   __syncthreads();
-  if (tid < T) {
-    float x = 0.f, y = 0.f;
+  if (tid >= T * 8) return;
+  const int t = tid / 8, e = tid % 8;
+  float x = 0.f, y = 0.f;
 #pragma unroll
-    for (int i = 0; i < GV_W; ++i) {
-      x += red[i][0][tid];
-      y += red[i][1][tid];
-    }
-    const int64_t row = a.tok_offset + tid;  // absolute position and cache row
-    if (region == 0) {
-      float cs, sn;
-      rope_cs((int)row, a.w2pi[j], cs, sn);
-      uint16_t* kp = a.Kout + row * a.nkv + hd * a.head_dim + j;
-      kp[0] = (uint16_t)(pack_bf16(x * cs - y * sn, 0.f) & 0xffffu);
-      kp[half] = (uint16_t)(pack_bf16(y * cs + x * sn, 0.f) & 0xffffu);
-    } else if (region == 1) {
-      a.Vout[row * a.nkv + c] = (uint16_t)(pack_bf16(x, 0.f) & 0xffffu);
-    } else {
-      const int64_t plane = c / a.rank, jr = c - plane * a.rank;
-      a.L[(plane * a.s_cap + row) * a.rank + jr] = (uint16_t)(pack_bf16(x, 0.f) & 0xffffu);
-    }
+  for (int i = 0; i < GV_W; ++i) {
+    x += red[i][0][t][e];
+    y += red[i][1][t][e];
+  }
+  const int64_t row = a.tok_offset + t;  // absolute position and cache row
+  if (region == 0) {
+    const int hd = c0 / a.head_dim, j = c0 - hd * a.head_dim + e;
+    float cs, sn;
+    rope_cs((int)row, a.w2pi[j], cs, sn);
+    uint16_t* kp = a.Kout + row * a.nkv + hd * a.head_dim + j;
+    kp[0] = (uint16_t)(pack_bf16(x * cs - y * sn, 0.f) & 0xffffu);
+    kp[half] = (uint16_t)(pack_bf16(y * cs + x * sn, 0.f) & 0xffffu);
+  } else if (region == 1) {
+    a.Vout[row * a.nkv + c0 + e] = (uint16_t)(pack_bf16(x, 0.f) & 0xffffu);
+  } else {
+    const int c = c0 + e;
+    const int64_t plane = c / a.rank, jr = c - plane * a.rank;
+    a.L[(plane * a.s_cap + row) * a.rank + jr] = (uint16_t)(pack_bf16(x, 0.f) & 0xffffu);
   }
 }
 
@@ -374,11 +479,11 @@ __global__ void __launch_bounds__(64 * GV_W) project_gemv_kernel(const Precomput
 
 hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t st) {
   if (a.tbl == nullptr && a.T <= GV_T) {
-    hipLaunchKernelGGL(project_gemv_kernel, dim3(a.nkv / 2 + a.nkv + a.n_cols), dim3(64 * GV_W), 0, st, a);
+    hipLaunchKernelGGL(project_gemv_kernel, dim3(a.nkv / 16 + a.nkv / 8 + a.n_cols / 8), dim3(64 * GV_W), 0, st, a);
     return hipGetLastError();
   }
   // 128-wide tiles halve the bytes loaded per MFMA but need enough of them to
-  // fill the 256 CUs; the K/V boundary must fall on a tile edge.
+  // fill the CUs; the K/V boundary must fall on a tile edge.
   const int64_t wide = (int64_t)((2 * a.nkv + a.n_cols + 127) / 128) * ((a.T + 127) / 128);
   if (a.nkv % 128 == 0 && wide >= 256) return launch_tb<128>(a, st);
   return launch_tb<64>(a, st);

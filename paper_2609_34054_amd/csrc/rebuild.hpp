@@ -54,6 +54,15 @@ struct Ex {
     else
       return ld8(p, ok);
   }
+  // PER bf16 at p, p + ld, p + 2 ld, ... (consecutive ranks of one column of
+  // an up-projection stored rank-major, [r, ld]); zeros when !ok.
+  static __device__ __forceinline__ Frag gather(const uint16_t* p, int64_t ld, bool ok) {
+    Frag f;
+#pragma unroll
+    for (int i = 0; i < PER / 2; ++i)
+      f[i] = ok ? (uint32_t)p[2 * i * ld] | ((uint32_t)p[(2 * i + 1) * ld] << 16) : 0u;
+    return f;
+  }
 };
 
 template <int D, int R>
@@ -80,11 +89,13 @@ __device__ __forceinline__ int blk_dim(int blk, int m) {
   return (blk / NB) * HALF + (m >> 2) * QPG + (blk % NB) * 4 + (m & 3);
 }
 
-// B^T fragments (A operand of the expansion) of one KV head.  `bhead` points
-// at the head's first row of an up-projection stored [n_kv*d, r].
+// B^T fragments (A operand of the expansion) of one KV head.  The
+// up-projection is stored as in Eq. 1, B [r, n_kv*d] (row j = rank j), with
+// row stride ldb = n_kv*d; `bhead` points at the head's first column of rank
+// 0, B[0][g*d].  A lane gathers its PER ranks of one column.
 template <int D, int R>
 __device__ __forceinline__ void load_bt_frags(typename Ex<R>::Frag (&f)[D / 16][Ex<R>::NC], const uint16_t* bhead,
-                                              bool ok, int lane) {
+                                              int64_t ldb, bool ok, int lane) {
   using E = Ex<R>;
   const int c16 = lane & 15, q = lane >> 4;
 #pragma unroll
@@ -94,7 +105,7 @@ __device__ __forceinline__ void load_bt_frags(typename Ex<R>::Frag (&f)[D / 16][
     for (int c = 0; c < E::NC; ++c) {
       const int r0 = E::rank0(c, q);
       const bool v = ok && r0 < R;
-      f[blk][c] = E::load(v ? bhead + (int64_t)dim * R + r0 : nullptr, v);
+      f[blk][c] = E::gather(v ? bhead + (int64_t)r0 * ldb + dim : nullptr, ldb, v);
     }
   }
 }

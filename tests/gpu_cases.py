@@ -22,18 +22,13 @@ def f64(t):
     return None if t is None else t.detach().double().cpu().numpy()
 
 
-def b_paper(t):
-    """ABI up-projection [.., n_kv*d, r] -> the paper's B [.., r, n_kv*d]."""
-    return None if t is None else np.swapaxes(f64(t), -1, -2)
-
-
 def to_dev(case, dev="cuda"):
     return {k: (v.to(dev) if isinstance(v, torch.Tensor) else v) for k, v in case.items()}
 
 
 def gpu_attention(g, theta, **kw):
-    O, lse = prc.lr_shared_attention(g["Q"], g["K_base"], g["V_base"], g["L_k"], g["L_v"], g["Bk_rows"],
-                                     g["Bv_rows"], g["positions"], g["kv_len"], rope_theta=theta,
+    O, lse = prc.lr_shared_attention(g["Q"], g["K_base"], g["V_base"], g["L_k"], g["L_v"], g["B_k"],
+                                     g["B_v"], g["positions"], g["kv_len"], rope_theta=theta,
                                      want_lse=True, **kw)
     torch.cuda.synchronize()
     return O, lse
@@ -55,7 +50,7 @@ def oracle_attention(c, theta, reqs=None, toks=None, zero_b=False):
 
     Q = f64(pick("Q"))[:, toks]
     pos = c["positions"].numpy()[reqs][:, toks]
-    Bk, Bv = b_paper(pick("Bk_rows")), b_paper(pick("Bv_rows"))
+    Bk, Bv = f64(pick("B_k")), f64(pick("B_v"))
     if zero_b:
         Bk = None if Bk is None else np.zeros_like(Bk)
         Bv = None if Bv is None else np.zeros_like(Bv)

@@ -7,7 +7,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_cases import ATOL_MAX, ATOL_MEAN, LSE_ATOL, attn_errors, b_paper, f64, gpu_attention, lse_error
+from gpu_cases import ATOL_MAX, ATOL_MEAN, LSE_ATOL, attn_errors, f64, gpu_attention, lse_error
 from workload import CONFIGS, attention_case
 
 pytestmark = pytest.mark.gpu
@@ -39,7 +39,7 @@ def check_sampled(cfg, g, O, lse, n_tok, kv_len, pos_of, s_cap, tag, reqs, toks)
         Q = f64(c["Q"])[:, toks]
         pos = c["positions"].numpy()[:, toks]
         Oref, lref = oracle.lr_shared_attention(Q, f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]),
-                                                f64(c["L_v"]), b_paper(c["Bk_rows"]), b_paper(c["Bv_rows"]),
+                                                f64(c["L_v"]), f64(c["B_k"]), f64(c["B_v"]),
                                                 pos, [kv_len], cfg.theta)
         mx, mean = attn_errors(O[b:b + 1, toks], Oref)
         print(f"  request {b}: max abs {mx:.2e}, mean abs {mean:.2e}", flush=True)

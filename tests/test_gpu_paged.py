@@ -13,7 +13,7 @@ import torch
 
 import oracle
 import paper_2609_34054_amd as prc
-from gpu_cases import ATOL_MAX, ATOL_MEAN, LSE_ATOL, PRE_REL, attn_errors, b_paper, f64, lse_error, \
+from gpu_cases import ATOL_MAX, ATOL_MEAN, LSE_ATOL, PRE_REL, attn_errors, f64, lse_error, \
     oracle_attention
 from workload import Config, attention_case
 from workload.gen import normal_bf16
@@ -91,7 +91,7 @@ def test_paged_attention(case):
 
     # Contiguous reference call with the same capacity (same decode split plan).
     O_c, lse_c = prc.lr_shared_attention(dev["Q"], dev["K_base"], dev["V_base"], dev["L_k"], dev["L_v"],
-                                         dev["Bk_rows"], dev["Bv_rows"], dev["positions"], dev["kv_len"],
+                                         dev["B_k"], dev["B_v"], dev["positions"], dev["kv_len"],
                                          rope_theta=cfg.theta, want_lse=True)
 
     n_pool = B * max_blocks + 3
@@ -113,7 +113,7 @@ def test_paged_attention(case):
                 return None
             return torch.stack([to_pool(t[b:b + 1], kv_tbl[b:b + 1], blk, n_pool) for b in range(B)]).cuda()
         Lk, Lv = planes(c["L_k"]), planes(c["L_v"])
-    O_p, lse_p = prc.lr_shared_attention_paged(dev["Q"], K_pool, V_pool, Lk, Lv, dev["Bk_rows"], dev["Bv_rows"],
+    O_p, lse_p = prc.lr_shared_attention_paged(dev["Q"], K_pool, V_pool, Lk, Lv, dev["B_k"], dev["B_v"],
                                                dev["positions"], dev["kv_len"], kv_tbl.cuda(),
                                                lr_block_table=lr_tbl, rope_theta=cfg.theta, want_lse=True)
     torch.cuda.synchronize()
@@ -151,8 +151,8 @@ def test_paged_blocks_shared_between_requests():
     q = normal_bf16((B, 1, 8, 128), 1.0, 905)
     Lk = normal_bf16((B, S, 16), 1.0, 906)
     Lv = normal_bf16((B, S, 16), 1.0, 907)
-    Bk = normal_bf16((B, 2 * 128, 16), 0.05, 908)
-    Bv = normal_bf16((B, 2 * 128, 16), 0.05, 909)
+    Bk = normal_bf16((B, 16, 2 * 128), 0.05, 908)
+    Bv = normal_bf16((B, 16, 2 * 128), 0.05, 909)
     tables = torch.stack([t[j] for j in traj])
     lr_pool_k = torch.stack([to_pool(Lk[b:b + 1], tables[b:b + 1], blk, n_pool) for b in range(B)])
     lr_pool_v = torch.stack([to_pool(Lv[b:b + 1], tables[b:b + 1], blk, n_pool) for b in range(B)])
@@ -164,7 +164,7 @@ def test_paged_blocks_shared_between_requests():
     torch.cuda.synchronize()
     Kb = torch.stack([traj_k[j] for j in traj])
     Vb = torch.stack([traj_v[j] for j in traj])
-    Oref, lref = oracle.lr_shared_attention(f64(q), f64(Kb), f64(Vb), f64(Lk), f64(Lv), b_paper(Bk), b_paper(Bv),
+    Oref, lref = oracle.lr_shared_attention(f64(q), f64(Kb), f64(Vb), f64(Lk), f64(Lv), f64(Bk), f64(Bv),
                                             pos.numpy(), kv_lens, cfg.theta)
     mx, mean = attn_errors(O, Oref)
     assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (mx, mean)
@@ -177,20 +177,20 @@ def test_paged_projection_matches_contiguous():
     T, d_in, n_kv, d, n_proj, N, r, off, theta = 300, 256, 2, 128, 2, 3, 16, 70, 5e5
     blk, mb, n_pool = 64, 7, 12
     X = normal_bf16((T, d_in), 1.0, 931)
-    W_rows = normal_bf16((2 * n_kv * d, d_in), 1.0 / math.sqrt(d_in), 932)
-    A_rows = normal_bf16((n_proj * N * r, d_in), 1.0 / math.sqrt(d_in), 933)
+    W = normal_bf16((d_in, 2 * n_kv * d), 1.0 / math.sqrt(d_in), 932)
+    A_stack = normal_bf16((d_in, n_proj * N * r), 1.0 / math.sqrt(d_in), 933)
     S = mb * blk
     K = torch.zeros((S, n_kv, d), dtype=torch.bfloat16, device="cuda")
     V = torch.zeros_like(K)
     L = torch.zeros((n_proj, N, S, r), dtype=torch.bfloat16, device="cuda")
-    prc.project_kv_and_lr_cache(X.cuda(), W_rows.cuda(), A_rows.cuda(), n_kv, d, n_proj, N, r, K, V, L,
+    prc.project_kv_and_lr_cache(X.cuda(), W.cuda(), A_stack.cuda(), n_kv, d, n_proj, N, r, K, V, L,
                                 rope_theta=theta, tok_offset=off)
     tbl = block_table(1, mb, n_pool, 934)[0]
     sentinel = -5.0
     Kp = torch.full((n_pool, blk, n_kv, d), sentinel, dtype=torch.bfloat16, device="cuda")
     Vp = torch.full_like(Kp, sentinel)
     Lp = torch.full((n_proj, N, n_pool, blk, r), sentinel, dtype=torch.bfloat16, device="cuda")
-    prc.project_kv_and_lr_cache_paged(X.cuda(), W_rows.cuda(), A_rows.cuda(), n_kv, d, n_proj, N, r, Kp, Vp, Lp,
+    prc.project_kv_and_lr_cache_paged(X.cuda(), W.cuda(), A_stack.cuda(), n_kv, d, n_proj, N, r, Kp, Vp, Lp,
                                       tbl.cuda(), rope_theta=theta, tok_offset=off)
     torch.cuda.synchronize()
     rows = torch.arange(off, off + T)
@@ -205,10 +205,10 @@ def test_paged_projection_matches_contiguous():
     assert (Lp[:, :, ~written].float() == sentinel).all()
     # LR planes alone (no base projection): the same LR rows, base pools untouched.
     Lp2 = torch.full_like(Lp, sentinel)
-    prc.project_kv_and_lr_cache_paged(X.cuda(), None, A_rows.cuda(), 0, 0, n_proj, N, r, None, None, Lp2,
+    prc.project_kv_and_lr_cache_paged(X.cuda(), None, A_stack.cuda(), 0, 0, n_proj, N, r, None, None, Lp2,
                                       tbl.cuda(), rope_theta=theta, tok_offset=off)
     torch.cuda.synchronize()
-    ref = oracle.precompute_lr_cache(f64(X), f64(A_rows).T, n_proj, N, r)
+    ref = oracle.precompute_lr_cache(f64(X), f64(A_stack), n_proj, N, r)
     got = f64(Lp2[:, :, blocks, within])
     assert np.linalg.norm(got - ref) / np.linalg.norm(ref) <= PRE_REL
     assert (Lp2[:, :, ~written].float() == sentinel).all()
@@ -227,17 +227,17 @@ def test_chunked_prefill_then_decode():
     mb = -(-S // blk)
     n_pool = mb + 4
     X = normal_bf16((S, d_in), 1.0, 941)
-    W_rows = normal_bf16((2 * n_kv * d, d_in), 1.0 / math.sqrt(d_in), 942)
-    A_rows = normal_bf16((2 * N * r, d_in), 1.0 / math.sqrt(d_in), 943)
-    Bk = normal_bf16((N, n_kv * d, r), 0.05, 944)
-    Bv = normal_bf16((N, n_kv * d, r), 0.05, 945)
+    W = normal_bf16((d_in, 2 * n_kv * d), 1.0 / math.sqrt(d_in), 942)
+    A_stack = normal_bf16((d_in, 2 * N * r), 1.0 / math.sqrt(d_in), 943)
+    Bk = normal_bf16((N, r, n_kv * d), 0.05, 944)
+    Bv = normal_bf16((N, r, n_kv * d), 0.05, 945)
     Q = normal_bf16((N, S, n_q, d), 1.0, 946)
     tbl = block_table(1, mb, n_pool, 947)
     Kp = torch.full((n_pool, blk, n_kv, d), float("nan"), dtype=torch.bfloat16, device="cuda")
     Vp = torch.full_like(Kp, float("nan"))
     Lp = torch.full((2, N, n_pool, blk, r), float("nan"), dtype=torch.bfloat16, device="cuda")
     tables = tbl.expand(N, mb).contiguous().cuda()
-    Xd, Wd, Ad, Bkd, Bvd, Qd = (t.cuda() for t in (X, W_rows, A_rows, Bk, Bv, Q))
+    Xd, Wd, Ad, Bkd, Bvd, Qd = (t.cuda() for t in (X, W, A_stack, Bk, Bv, Q))
     outs, lses = [], []
     s0 = 0
     for c in chunks + [1]:
@@ -255,10 +255,10 @@ def test_chunked_prefill_then_decode():
     torch.cuda.synchronize()
     O = torch.cat(outs, dim=1)
     lse = torch.cat(lses, dim=1)
-    Kr, Vr, Lr = oracle.project_kv_and_lr(f64(X), f64(W_rows[: n_kv * d]).T, f64(W_rows[n_kv * d:]).T,
-                                          f64(A_rows).T, n_kv, 2, N, r, np.arange(S), theta)
+    Kr, Vr, Lr = oracle.project_kv_and_lr(f64(X), f64(W[:, : n_kv * d]), f64(W[:, n_kv * d:]),
+                                          f64(A_stack), n_kv, 2, N, r, np.arange(S), theta)
     rep = lambda x: np.broadcast_to(x, (N,) + x.shape)
-    Oref, lref = oracle.lr_shared_attention(f64(Q), rep(Kr), rep(Vr), Lr[0], Lr[1], b_paper(Bk), b_paper(Bv),
+    Oref, lref = oracle.lr_shared_attention(f64(Q), rep(Kr), rep(Vr), Lr[0], Lr[1], f64(Bk), f64(Bv),
                                             np.broadcast_to(np.arange(S), (N, S)), [S] * N, theta)
     mx, mean = attn_errors(O, Oref)
     assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (mx, mean)

@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import paper_2609_34054_amd as prc
-from gpu_cases import (ATOL_MAX, ATOL_MEAN, LR_SENS, LSE_ATOL, PRE_REL, attn_errors, b_paper, f64,
+from gpu_cases import (ATOL_MAX, ATOL_MEAN, LR_SENS, LSE_ATOL, PRE_REL, attn_errors, f64,
                        gpu_attention, lse_error, oracle_attention, to_dev)
 from workload import CONFIGS, Config, attention_case, precompute_case
 from workload.gen import normal_bf16
@@ -49,9 +49,9 @@ def test_precompute(cid, T, d_in, n_proj, N, r, off, s_cap):
     pc = precompute_case(cfg, T, seed_base=T)
     sentinel = 3.0
     L = torch.full((n_proj, N, s_cap, r), sentinel, dtype=torch.bfloat16, device="cuda")
-    prc.precompute_lr_cache(pc["X"].cuda(), pc["A_rows"].cuda(), n_proj, N, r, L, tok_offset=off)
+    prc.precompute_lr_cache(pc["X"].cuda(), pc["A_stack"].cuda(), n_proj, N, r, L, tok_offset=off)
     torch.cuda.synchronize()
-    ref = oracle.precompute_lr_cache(f64(pc["X"]), f64(pc["A_rows"]).T, n_proj, N, r)
+    ref = oracle.precompute_lr_cache(f64(pc["X"]), f64(pc["A_stack"]), n_proj, N, r)
     got = f64(L)
     rel = np.linalg.norm(got[:, :, off:off + T] - ref) / np.linalg.norm(ref)
     assert rel <= PRE_REL, rel
@@ -66,9 +66,9 @@ def test_precompute_strided_rows():
     wide = torch.zeros(100, 384, dtype=torch.bfloat16)
     wide[:, :256] = pc["X"]
     L = torch.zeros((2, 2, 100, 16), dtype=torch.bfloat16, device="cuda")
-    prc.precompute_lr_cache(wide.cuda()[:, :256], pc["A_rows"].cuda(), 2, 2, 16, L)
+    prc.precompute_lr_cache(wide.cuda()[:, :256], pc["A_stack"].cuda(), 2, 2, 16, L)
     torch.cuda.synchronize()
-    ref = oracle.precompute_lr_cache(f64(pc["X"]), f64(pc["A_rows"]).T, 2, 2, 16)
+    ref = oracle.precompute_lr_cache(f64(pc["X"]), f64(pc["A_stack"]), 2, 2, 16)
     assert np.linalg.norm(f64(L) - ref) / np.linalg.norm(ref) <= PRE_REL
 
 
@@ -93,17 +93,17 @@ def test_project_kv_and_lr(case):
     print(f"projection {cid}", flush=True)
     g = 900 + len(cid)
     X = normal_bf16((T, d_in), 1.0, g + 1)
-    W_rows = normal_bf16((2 * n_kv * d, d_in), 1.0 / math.sqrt(d_in), g + 2)
-    A_rows = normal_bf16((n_proj * N * r, d_in), 1.0 / math.sqrt(d_in), g + 3)
+    W = normal_bf16((d_in, 2 * n_kv * d), 1.0 / math.sqrt(d_in), g + 2)
+    A_stack = normal_bf16((d_in, n_proj * N * r), 1.0 / math.sqrt(d_in), g + 3)
     sentinel = -7.0
     K = torch.full((s_cap, n_kv, d), sentinel, dtype=torch.bfloat16, device="cuda")
     V = torch.full_like(K, sentinel)
     L = torch.full((n_proj, N, s_cap, r), sentinel, dtype=torch.bfloat16, device="cuda")
-    prc.project_kv_and_lr_cache(X.cuda(), W_rows.cuda(), A_rows.cuda(), n_kv, d, n_proj, N, r, K, V, L,
+    prc.project_kv_and_lr_cache(X.cuda(), W.cuda(), A_stack.cuda(), n_kv, d, n_proj, N, r, K, V, L,
                                 rope_theta=theta, tok_offset=off)
     torch.cuda.synchronize()
-    Wk, Wv = f64(W_rows[: n_kv * d]).T, f64(W_rows[n_kv * d:]).T
-    Kr, Vr, Lr = oracle.project_kv_and_lr(f64(X), Wk, Wv, f64(A_rows).T, n_kv, n_proj, N, r,
+    Wk, Wv = f64(W[:, : n_kv * d]), f64(W[:, n_kv * d:])
+    Kr, Vr, Lr = oracle.project_kv_and_lr(f64(X), Wk, Wv, f64(A_stack), n_kv, n_proj, N, r,
                                           np.arange(off, off + T), theta)
     for name, got, ref in (("K", f64(K)[off:off + T], Kr), ("V", f64(V)[off:off + T], Vr),
                            ("L", f64(L)[:, :, off:off + T], Lr)):
@@ -117,26 +117,29 @@ def test_project_kv_and_lr(case):
         assert (out == sentinel).all()
     out = torch.cat([L[:, :, :off], L[:, :, off + T:]], dim=2).float()
     assert (out == sentinel).all()
-    # The LR part agrees with the precompute alone to the last bf16 place (the
-    # two may tile the GEMM differently, so the fp32 sums may differ in order).
+    # The LR part agrees with the precompute alone to about the last bf16
+    # place: the two may tile the GEMM differently (the narrow one splits k
+    # over its waves), so their fp32 sums differ in order, which moves values
+    # near zero (cancellations) by a little more than their own ulp.
     L2 = torch.full_like(L, sentinel)
-    prc.precompute_lr_cache(X.cuda(), A_rows.cuda(), n_proj, N, r, L2, tok_offset=off)
+    prc.precompute_lr_cache(X.cuda(), A_stack.cuda(), n_proj, N, r, L2, tok_offset=off)
     torch.cuda.synchronize()
-    assert ((L.float() - L2.float()).abs() <= 2 ** -7 * L2.float().abs()).all()
+    a, b = L.float(), L2.float()
+    assert ((a - b).abs() <= 2 ** -7 * b.abs() + 1e-3 * b.abs().max()).all()
 
 
 def test_project_base_only():
     """n_agents = 0: the base projection alone (no LR buffers)."""
     T, d_in, n_kv, d, off, s_cap, theta = 65, 128, 2, 64, 7, 80, 5e5
     X = normal_bf16((T, d_in), 1.0, 951)
-    W_rows = normal_bf16((2 * n_kv * d, d_in), 1.0 / math.sqrt(d_in), 952)
+    W = normal_bf16((d_in, 2 * n_kv * d), 1.0 / math.sqrt(d_in), 952)
     K = torch.zeros((s_cap, n_kv, d), dtype=torch.bfloat16, device="cuda")
     V = torch.zeros_like(K)
-    prc.project_kv_and_lr_cache(X.cuda(), W_rows.cuda(), None, n_kv, d, 2, 0, 16, K, V, None, rope_theta=theta,
+    prc.project_kv_and_lr_cache(X.cuda(), W.cuda(), None, n_kv, d, 2, 0, 16, K, V, None, rope_theta=theta,
                                 tok_offset=off)
     torch.cuda.synchronize()
     A0 = np.zeros((d_in, 0))
-    Kr, Vr, _ = oracle.project_kv_and_lr(f64(X), f64(W_rows[: n_kv * d]).T, f64(W_rows[n_kv * d:]).T, A0, n_kv,
+    Kr, Vr, _ = oracle.project_kv_and_lr(f64(X), f64(W[:, : n_kv * d]), f64(W[:, n_kv * d:]), A0, n_kv,
                                          2, 0, 16, np.arange(off, off + T), theta)
     for got, ref in ((f64(K)[off:off + T], Kr), (f64(V)[off:off + T], Vr)):
         assert np.linalg.norm(got - ref) / np.linalg.norm(ref) <= PRE_REL
@@ -169,20 +172,8 @@ ATTN_CASES = [
     ("k_only_decode", 64, 8, 4, 2, 1, [90], 96, "k", 1.0, "end"),
     ("plain_prefill", 128, 16, 8, 2, 50, [300], 304, "none", 1.0, "end"),
     ("plain_decode", 128, 16, 8, 2, 1, [2000, 1], 2000, "none", 1.0, "end"),
-    # Sharper softmax (q std 2): the sharpest setting at which bf16 storage of
-    # the agent's rebuilt keys -- what any bf16 KV cache, the materialised
-    # reference included, holds -- stays inside the gate with margin.
-    ("sharp_prefill", 128, 16, 8, 2, 64, [512], 512, "kv", 2.0, "end"),
-    ("sharp_prefill_long", 128, 16, 8, 2, 16, [4096], 4096, "kv", 2.0, "end"),
-    ("sharp_decode", 128, 16, 8, 2, 1, [3000, 2999], 3008, "kv", 2.0, "end"),
-    # From rank 32 up the prefill rebuilds V on chip and rounds it to bf16,
-    # as it does K and as any bf16 KV cache (the materialised reference
-    # included) does.  A larger LR term makes the rebuilt rows larger, so the
-    # sharpest scale a bf16 cache keeps inside the gate drops with the rank:
-    # these use it (the materialised reference errs the same here).
-    ("sharp_r32_prefill", 128, 32, 8, 2, 64, [512], 512, "kv", 1.5, "end"),
-    ("sharp_r64_prefill", 128, 64, 8, 2, 64, [512], 512, "kv", 1.35, "end"),
-    ("sharp_qv_r64_prefill_long", 128, 64, 8, 2, 16, [4096], 4096, "v", 2.0, "end"),
+    # Sharp data (O(1) outputs decided by a few planted keys at split and tile
+    # boundaries) is covered by the planted-key set in test_gpu_sharp.py.
     ("mid_positions_prefill", 128, 16, 8, 2, 12, [300], 304, "kv", 1.0, "mid"),
     ("mid_positions_decode", 128, 16, 8, 2, 1, [300, 500], 512, "kv", 1.0, "mid"),
     ("many_requests_decode", 64, 16, 8, 8, 1, [64, 65, 63, 1, 17, 200, 31, 128], 256, "kv", 1.0, "end"),
@@ -228,7 +219,8 @@ def test_attention(case):
     assert lse_error(lse, lref) <= LSE_ATOL
 
 
-@pytest.mark.parametrize("cid", ["c1_prefill", "g4_r16_decode_ragged", "g5_r64_prefill", "sharp_decode"])
+@pytest.mark.parametrize("cid", ["c1_prefill", "g4_r16_decode_ragged", "g5_r64_prefill", "g4_r16_decode_long",
+                                 "split_prefill_ragged", "split_r64_prefill", "split_qv_prefill"])
 def test_lr_sensitivity(cid):
     """The LR term's contribution, O - O(B=0), is reproduced (a kernel that drops
     or mis-rotates the LR term fails this even when O itself is small)."""
@@ -237,8 +229,9 @@ def test_lr_sensitivity(cid):
     g = to_dev(c)
     O, _ = gpu_attention(g, cfg.theta)
     z = dict(g)
-    z["Bk_rows"] = torch.zeros_like(g["Bk_rows"])
-    z["Bv_rows"] = torch.zeros_like(g["Bv_rows"])
+    for k in ("B_k", "B_v"):
+        if z[k] is not None:
+            z[k] = torch.zeros_like(z[k])
     O0, _ = gpu_attention(z, cfg.theta)
     Oref, _ = oracle_attention(c, cfg.theta)
     O0ref, _ = oracle_attention(c, cfg.theta, zero_b=True)
@@ -251,8 +244,8 @@ def test_absent_lr_equals_zero_up_projection():
     cfg, c = _case("qv_decode", 128, 16, 8, 2, 1, [512, 300], 512, "kv", 1.0, "end")
     g = to_dev(c)
     for n_tok in (1,):
-        zk = dict(g, Bk_rows=torch.zeros_like(g["Bk_rows"]))
-        nk = dict(g, L_k=None, Bk_rows=None)
+        zk = dict(g, B_k=torch.zeros_like(g["B_k"]))
+        nk = dict(g, L_k=None, B_k=None)
         Oz, lz = gpu_attention(zk, cfg.theta)
         On, ln = gpu_attention(nk, cfg.theta)
         assert torch.equal(Oz, On) and torch.equal(lz, ln)
@@ -287,14 +280,14 @@ def test_shared_buffers_across_requests():
     Q = normal_bf16((B, 1, 8, 128), 1.0, 4242).cuda()
     pos = torch.tensor([[399], [250], [10]], dtype=torch.int32, device="cuda")
     kvl = torch.tensor([400, 251, 11], dtype=torch.int32, device="cuda")
-    O, _ = prc.lr_shared_attention(Q, g["K_base"], g["V_base"], g["L_k"], g["L_v"], g["Bk_rows"], g["Bv_rows"],
+    O, _ = prc.lr_shared_attention(Q, g["K_base"], g["V_base"], g["L_k"], g["L_v"], g["B_k"], g["B_v"],
                                    pos, kvl, rope_theta=cfg.theta)
     torch.cuda.synchronize()
     for b in range(B):
         n = int(kvl[b])
         Oref, _ = oracle.lr_shared_attention(f64(Q[b:b + 1]), f64(c["K_base"])[:, :n], f64(c["V_base"])[:, :n],
-                                             f64(c["L_k"])[:, :n], f64(c["L_v"])[:, :n], b_paper(c["Bk_rows"]),
-                                             b_paper(c["Bv_rows"]), pos[b:b + 1].cpu().numpy(), [n], cfg.theta)
+                                             f64(c["L_k"])[:, :n], f64(c["L_v"])[:, :n], f64(c["B_k"]),
+                                             f64(c["B_v"]), pos[b:b + 1].cpu().numpy(), [n], cfg.theta)
         mx, mean = attn_errors(O[b:b + 1], Oref)
         assert mx <= ATOL_MAX and mean <= ATOL_MEAN
 
@@ -346,7 +339,7 @@ def test_custom_softmax_scale():
     O, _ = gpu_attention(to_dev(c), cfg.theta, softmax_scale=0.05)
     Q = f64(c["Q"])
     Ks, Vs = oracle.materialize_agent_kv(f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]), f64(c["L_v"]),
-                                         b_paper(c["Bk_rows"]), b_paper(c["Bv_rows"]), [100], cfg.theta)
+                                         f64(c["B_k"]), f64(c["B_v"]), [100], cfg.theta)
     Oref, _ = oracle.attention(Q[0], Ks[0], Vs[0], c["positions"].numpy()[0], 100, scale=0.05)
     mx, mean = attn_errors(O[0], Oref)
     assert mx <= ATOL_MAX and mean <= ATOL_MEAN
@@ -358,11 +351,11 @@ def test_materialize(cid):
     case = next(c for c in ATTN_CASES if c[0] == cid)
     cfg, c = _case(*case)
     g = to_dev(c)
-    Kf, Vf = prc.materialize_agent_kv(g["K_base"], g["V_base"], g["L_k"], g["L_v"], g["Bk_rows"], g["Bv_rows"],
+    Kf, Vf = prc.materialize_agent_kv(g["K_base"], g["V_base"], g["L_k"], g["L_v"], g["B_k"], g["B_v"],
                                       g["kv_len"], rope_theta=cfg.theta)
     torch.cuda.synchronize()
     Ks, Vs = oracle.materialize_agent_kv(f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]), f64(c["L_v"]),
-                                         b_paper(c["Bk_rows"]), b_paper(c["Bv_rows"]), c["kv_len"].numpy(),
+                                         f64(c["B_k"]), f64(c["B_v"]), c["kv_len"].numpy(),
                                          cfg.theta)
     for b, n in enumerate(c["kv_len"].tolist()):
         for got, ref in ((f64(Kf)[b, :n], Ks[b]), (f64(Vf)[b, :n], Vs[b])):
@@ -395,19 +388,19 @@ def test_tiny_workload_full_chain():
     bf = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(torch.bfloat16)
     Kb_t, Vb_t, Q_t = bf(Kb)[None], bf(Vb)[None], bf(Q_all)
     L = torch.zeros((2, N, S, r), dtype=torch.bfloat16, device="cuda")
-    prc.precompute_lr_cache(lc["X"].cuda(), lc["A_rows"].cuda(), 2, N, r, L)
-    L_or = oracle.precompute_lr_cache(X, f64(lc["A_rows"]).T, 2, N, r)
+    prc.precompute_lr_cache(lc["X"].cuda(), lc["A_stack"].cuda(), 2, N, r, L)
+    L_or = oracle.precompute_lr_cache(X, f64(lc["A_stack"]), 2, N, r)
     for n_tok in (cfg.prefill_tokens, 1):
         q_t = Q_t[S - n_tok:][None]
         pos = torch.arange(S - n_tok, S, dtype=torch.int32)[None]
         kvl = torch.tensor([S], dtype=torch.int32)
         for a in range(N):
             O, _ = prc.lr_shared_attention(q_t.cuda(), Kb_t.cuda(), Vb_t.cuda(), L[0, a][None], L[1, a][None],
-                                           lc["Bk_rows"][a][None].cuda(), lc["Bv_rows"][a][None].cuda(),
+                                           lc["B_k"][a][None].cuda(), lc["B_v"][a][None].cuda(),
                                            pos.cuda(), kvl.cuda(), rope_theta=cfg.theta)
             torch.cuda.synchronize()
             Oref, _ = oracle.lr_shared_attention(f64(q_t), f64(Kb_t), f64(Vb_t), L_or[0, a][None], L_or[1, a][None],
-                                                 b_paper(lc["Bk_rows"][a][None]), b_paper(lc["Bv_rows"][a][None]),
+                                                 f64(lc["B_k"][a][None]), f64(lc["B_v"][a][None]),
                                                  pos.numpy(), kvl.numpy(), cfg.theta)
             mx, mean = attn_errors(O, Oref)
             assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (n_tok, a, mx, mean)
@@ -432,9 +425,9 @@ def test_multi_turn_stack_chain():
 
     K = [rnd((1, S_cap, n_kv, d)) for _ in range(n_layers)]
     V = [rnd((1, S_cap, n_kv, d)) for _ in range(n_layers)]
-    A = [rnd((2 * N * r, hid), 1.0 / math.sqrt(hid)) for _ in range(n_layers)]
-    Bk = [rnd((N, n_kv * d, r), math.sqrt(0.02)) for _ in range(n_layers)]
-    Bv = [rnd((N, n_kv * d, r), math.sqrt(0.02)) for _ in range(n_layers)]
+    A = [rnd((hid, 2 * N * r), 1.0 / math.sqrt(hid)) for _ in range(n_layers)]
+    Bk = [rnd((N, r, n_kv * d), math.sqrt(0.02)) for _ in range(n_layers)]
+    Bv = [rnd((N, r, n_kv * d), math.sqrt(0.02)) for _ in range(n_layers)]
     X_seg = [rnd((turn, hid)) for _ in range(turns)]
     X_pre = [rnd((n_pre, hid)) for _ in range(turns)]
     X_dec = [rnd((n_dec, hid)) for _ in range(turns)]
@@ -448,7 +441,7 @@ def test_multi_turn_stack_chain():
 
     def append(l, X, Xc, off):
         prc.precompute_lr_cache(Xc, g["A"][l], 2, N, r, Lp[l], tok_offset=off)
-        L_or[l][:, :, off:off + X.shape[0]] = oracle.precompute_lr_cache(f64(X), f64(A[l]).T, 2, N, r)
+        L_or[l][:, :, off:off + X.shape[0]] = oracle.precompute_lr_cache(f64(X), f64(A[l]), 2, N, r)
 
     def attend(k, l, Qc, Qh, pos, kvl, O):
         s, a = turn * (k + 1) + n_pre + n_dec, (k + 1) % N
@@ -456,8 +449,8 @@ def test_multi_turn_stack_chain():
                                 Lp[l][1, a, :s][None], g["Bk"][l][a:a + 1], g["Bv"][l][a:a + 1],
                                 pos.cuda(), kvl.cuda(), rope_theta=theta, O=O)
         ref, _ = oracle.lr_shared_attention(f64(Qh), f64(K[l][:, :s]), f64(V[l][:, :s]), L_or[l][0, a, :s][None],
-                                            L_or[l][1, a, :s][None], b_paper(Bk[l][a:a + 1]),
-                                            b_paper(Bv[l][a:a + 1]), pos.numpy(), kvl.numpy(), theta)
+                                            L_or[l][1, a, :s][None], f64(Bk[l][a:a + 1]),
+                                            f64(Bv[l][a:a + 1]), pos.numpy(), kvl.numpy(), theta)
         return ref
 
     checks = []

@@ -32,8 +32,8 @@ def test_tiny_workload_runs_and_is_finite():
     case = attention_case(cfg, batch=1, n_tok=cfg.prefill_tokens, kv_len=[S], positions=pos,
                           s_cap=S + 8)
     f = lambda t: None if t is None else t.double().numpy()
-    Bk = f(case["Bk_rows"]).transpose(0, 2, 1)
-    Bv = f(case["Bv_rows"]).transpose(0, 2, 1)
+    Bk = f(case["B_k"])
+    Bv = f(case["B_v"])
     O, lse = oracle.lr_shared_attention(f(case["Q"]), f(case["K_base"]), f(case["V_base"]),
                                         f(case["L_k"]), f(case["L_v"]), Bk, Bv,
                                         case["positions"].numpy(), case["kv_len"].numpy(), cfg.theta)

@@ -29,7 +29,7 @@ def _run(noalloc, dims, g):
     lse = torch.full(g["Q"].shape[:3], float("nan"), dtype=torch.float32, device="cuda")
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     args = [ctypes.byref(dims), _p(g["Q"]), _p(g["K_base"]), _p(g["V_base"]), _p(g["L_k"]), _p(g["L_v"]),
-            _p(g["Bk_rows"]), _p(g["Bv_rows"]), _p(g["positions"]), _p(g["kv_len"]), _p(O), _p(lse)]
+            _p(g["B_k"]), _p(g["B_v"]), _p(g["positions"]), _p(g["kv_len"]), _p(O), _p(lse)]
     if noalloc:
         st = lib().lr_shared_attention_noalloc(*args, stream)
     else:
@@ -59,7 +59,7 @@ def test_noalloc_matches_workspace_call(pair):
         c = attention_case(cfg, batch=len(kv_lens), n_tok=n_tok, kv_len=kv_lens, positions=pos, s_cap=s_cap,
                            seed_base=31 * len(cid))
         g = to_dev(c)
-        dims = make_dims(g["Q"], g["K_base"], g["L_k"], g["L_v"], g["Bk_rows"], g["Bv_rows"], cfg.theta)
+        dims = make_dims(g["Q"], g["K_base"], g["L_k"], g["L_v"], g["B_k"], g["B_v"], cfg.theta)
         assert lib().lr_shared_attention_workspace_size(ctypes.byref(dims)) > 0  # partials are used
         O_ws, lse_ws = _run(False, dims, g)
         O_na, lse_na = _run(True, dims, g)
@@ -74,12 +74,12 @@ def test_noalloc_refuses_calls_beyond_its_workspace():
     cfg = _cfg(90, 32, 8, 128, 16)
     c = attention_case(cfg, batch=1, n_tok=1, kv_len=[64], positions=[[63]], s_cap=64, poison_tail=False)
     g = to_dev(c)
-    dims = make_dims(g["Q"], g["K_base"], g["L_k"], g["L_v"], g["Bk_rows"], g["Bv_rows"], cfg.theta)
+    dims = make_dims(g["Q"], g["K_base"], g["L_k"], g["L_v"], g["B_k"], g["B_v"], cfg.theta)
     dims.batch = 4096  # 4096 requests at the same (shared) buffers need far more partials
     dims.kv_req_stride = dims.l_req_stride = dims.b_req_stride = 0
     assert lib().lr_shared_attention_workspace_size(ctypes.byref(dims)) > 32 << 20
     O = torch.empty(1, dtype=torch.bfloat16, device="cuda")
     st = lib().lr_shared_attention_noalloc(ctypes.byref(dims), _p(g["Q"]), _p(g["K_base"]), _p(g["V_base"]),
-                                           _p(g["L_k"]), _p(g["L_v"]), _p(g["Bk_rows"]), _p(g["Bv_rows"]),
+                                           _p(g["L_k"]), _p(g["L_v"]), _p(g["B_k"]), _p(g["B_v"]),
                                            _p(g["positions"]), _p(g["kv_len"]), _p(O), None, None)
     assert st == 5, st  # PRC_EWORKSPACE, nothing launched
