@@ -326,6 +326,19 @@ prc_status materialize_agent_kv(const lrsa_dims* dims, const uint16_t* K_base,
                                 const uint16_t* B_v, const int32_t* kv_len,
                                 uint16_t* K_full, uint16_t* V_full, void* stream);
 
+/*
+ * prc_stream_read -- measurement helper, not part of the hot path: reads
+ * `bytes` bytes of device memory at `src` with 16-byte loads from `grid`
+ * workgroups of 256 threads (grid-stride) and writes one XOR word per
+ * workgroup to `sink` [grid] uint32 (device memory), so the reads cannot be
+ * elided.  Timing it over a buffer far larger than the 256 MB Infinity Cache
+ * gives the device's achievable HBM read rate, the measured ceiling the
+ * bandwidth-bound kernels are compared with.  Requires bytes a positive
+ * multiple of 16 (at most 2^40), src 16-byte and sink 4-byte aligned,
+ * 1 <= grid <= 2^20.
+ */
+prc_status prc_stream_read(const void* src, size_t bytes, uint32_t* sink, int32_t grid, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,6 +18,7 @@ from .binding import (  # noqa: F401
     precompute_lr_cache,
     project_kv_and_lr_cache,
     project_kv_and_lr_cache_paged,
+    stream_read,
     workspace_size,
 )
 

@@ -23,7 +23,7 @@ STATUS_NAMES = {0: "PRC_OK", 1: "PRC_EINVAL", 2: "PRC_ESHAPE", 3: "PRC_EALIGN",
 EXPORTS = ("precompute_lr_cache", "project_kv_and_lr_cache", "project_kv_and_lr_cache_paged",
            "lr_shared_attention", "lr_shared_attention_workspace_size", "lr_shared_attention_paged",
            "lr_shared_attention_paged_workspace_size", "lr_shared_attention_noalloc", "materialize_agent_kv",
-           "prc_last_error",
+           "prc_stream_read", "prc_last_error",
            "prc_status_string", "prc_version")
 
 
@@ -95,6 +95,8 @@ def lib() -> ctypes.CDLL:
         L.lr_shared_attention_paged_workspace_size.restype = ctypes.c_size_t
         L.materialize_agent_kv.argtypes = [ctypes.POINTER(LrsaDims), vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
         L.materialize_agent_kv.restype = ctypes.c_int
+        L.prc_stream_read.argtypes = [vp, ctypes.c_size_t, vp, i32, vp]
+        L.prc_stream_read.restype = ctypes.c_int
         L.prc_last_error.restype = ctypes.c_char_p
         L.prc_status_string.argtypes = [ctypes.c_int]
         L.prc_status_string.restype = ctypes.c_char_p
@@ -433,3 +435,13 @@ def lr_shared_attention_paged(Q, K_pool, V_pool, L_k, L_v, B_k, B_v, positions, 
                                          ws_bytes, _stream(stream))
     _check("lr_shared_attention_paged", st)
     return O, lse
+
+
+def stream_read(src, sink, grid: int, stream=None):
+    """Measurement helper: stream all of ``src`` (a device tensor) through
+    ``prc_stream_read``; ``sink`` is a uint32/int32 device tensor of ``grid``
+    elements."""
+    nbytes = src.numel() * src.element_size()
+    if sink.numel() < grid or sink.element_size() != 4:
+        raise ValueError("sink must hold grid 4-byte words")
+    _check("prc_stream_read", lib().prc_stream_read(_ptr(src), nbytes, _ptr(sink), grid, _stream(stream)))

@@ -25,6 +25,7 @@ SOURCES = [
     "lrsa_decode.hip",
     "lrsa_prefill.hip",
     "materialize.hip",
+    "stream_read.hip",
 ]
 
 ARCH = "gfx950"

@@ -580,3 +580,14 @@ PRC_API prc_status materialize_agent_kv(const lrsa_dims* dims, const uint16_t* K
   c.a.Vout = V_full;
   return launch_status(prc::launch_materialize(c.a, static_cast<hipStream_t>(stream)), "materialize_agent_kv");
 }
+
+PRC_API prc_status prc_stream_read(const void* src, size_t bytes, uint32_t* sink, int32_t grid, void* stream) {
+  if (src == nullptr || sink == nullptr) return fail(PRC_EINVAL, "src/sink is NULL");
+  if (bytes == 0 || bytes % 16 || bytes > ((size_t)1 << 40)) return fail(PRC_EINVAL, "bytes=%zu must be a positive multiple of 16", bytes);
+  if (!aligned(src, 16) || !aligned(sink, 4)) return fail(PRC_EALIGN, "src must be 16-byte and sink 4-byte aligned");
+  if (grid < 1 || grid > (1 << 20)) return fail(PRC_EINVAL, "grid=%d outside [1, 2^20]", grid);
+  int cus = 0;
+  if (prc_status ds = device_ready(&cus)) return ds;
+  return launch_status(prc::launch_stream_read(src, (int64_t)bytes, sink, grid, static_cast<hipStream_t>(stream)),
+                       "prc_stream_read");
+}

@@ -114,4 +114,8 @@ struct PrecomputeArgs {
 };
 hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t stream);
 
+// Measurement helper: stream `bytes` (a multiple of 16) from src with `grid`
+// workgroups, one XOR word per workgroup to sink.
+hipError_t launch_stream_read(const void* src, int64_t bytes, uint32_t* sink, int grid, hipStream_t stream);
+
 }  // namespace prc

@@ -238,8 +238,8 @@ lrsa_decode_kernel(const AttnArgs a) {
     for (int kk = 0; kk < C::NCH; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
   }
   typename Ex<R>::Frag bkf[C::NBLK][Ex<R>::NC];
-  load_bt_frags<D, R>(bkf, has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr,
-                      (int64_t)a.n_kv * D, has_lk && active, lane);
+  load_bt_frags_staged<D, R>(bkf, has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr,
+                             (int64_t)a.n_kv * D, has_lk && active, lane, v_lds[w]);
 
   float m_run = -INFINITY, l_part = 0.f;
   f32x4 acc[C::NBLK];   // O^T: dims blk*16 + 4q + i, head l%16
@@ -660,8 +660,9 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
     for (int kk = 0; kk < C::NCH; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
   }
   typename Ex<R>::Frag bkf[C::NBLK][Ex<R>::NC];
-  load_bt_frags<D, R>(bkf, has_lk && active ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr,
-                      (int64_t)a.n_kv * D, has_lk && active, lane);
+  // Staged through this wave's share of the (not yet used) V tiles.
+  load_bt_frags_staged<D, R>(bkf, has_lk && active ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr,
+                             (int64_t)a.n_kv * D, has_lk && active, lane, &v_lds[0][0] + w * 16 * C::V_ROW);
 
   float m_run = -INFINITY, l_part = 0.f;
   f32x4 acc[C::NBLK];

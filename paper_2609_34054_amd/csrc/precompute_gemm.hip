@@ -100,13 +100,69 @@ __device__ __forceinline__ int key_wcol(int vc, int head_dim) {
   return hd * head_dim + (e / 32) * 16 + (e % 16) + ((e % 32) / 16) * (head_dim / 2);
 }
 
+// Writes one 32 x 32 block of C^T in the 32x32x16 result layout: r[j] is
+// output column cb + (j / 4) * 8 + h * 4 + j % 4 of token t (h = lane / 32).
+// Keys are rotated at the token's position as they are written; every token
+// goes to its cache row (its position, or its row in the paged pools).
+__device__ __forceinline__ void store_block(const PrecomputeArgs& a, const f32x16& r, int region, int cb, int64_t t,
+                                            int h) {
+  if (t >= a.T) return;
+  const int64_t trow = a.tok_offset + t;  // absolute position of the token
+  int64_t row = trow;
+  if (a.tbl != nullptr) {
+    const int q = (int)(trow / a.blk);
+    int32_t e = a.tbl[q];
+    e = e < 0 ? 0 : (e >= a.nblk ? a.nblk - 1 : e);
+    row = (int64_t)e * a.blk + (trow - (int64_t)q * a.blk);
+  }
+  if (region == 0) {
+    // Keys: registers j and j + 8 hold dims j0 + i and j0 + i + d/2 of one
+    // head (the column order of key tiles); rotate-half RoPE at position trow.
+#pragma unroll
+    for (int jg = 0; jg < 2; ++jg) {
+      const int vc = cb + jg * 8 + h * 4;
+      const int hd = vc / a.head_dim, e = vc - hd * a.head_dim;
+      const int j0 = (e / 32) * 16 + (e % 16);
+      float lo[4], hi[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float cs, sn;
+        rope_cs((int)trow, a.w2pi[j0 + i], cs, sn);
+        const float x = r[4 * jg + i], y = r[4 * jg + 8 + i];
+        lo[i] = x * cs - y * sn;
+        hi[i] = y * cs + x * sn;
+      }
+      uint16_t* kp = a.Kout + row * a.nkv + hd * a.head_dim + j0;
+      *reinterpret_cast<u32x2*>(kp) = u32x2{pack_bf16(lo[0], lo[1]), pack_bf16(lo[2], lo[3])};
+      *reinterpret_cast<u32x2*>(kp + a.head_dim / 2) = u32x2{pack_bf16(hi[0], hi[1]), pack_bf16(hi[2], hi[3])};
+    }
+    return;
+  }
+#pragma unroll
+  for (int jg = 0; jg < 4; ++jg) {
+    const int c = cb + jg * 8 + h * 4;
+    u32x2 o;
+    o[0] = pack_bf16(r[4 * jg + 0], r[4 * jg + 1]);
+    o[1] = pack_bf16(r[4 * jg + 2], r[4 * jg + 3]);
+    if (region == 1) {
+      *reinterpret_cast<u32x2*>(a.Vout + row * a.nkv + (c - a.nkv)) = o;
+    } else {
+      const int lc = c - 2 * a.nkv;
+      if (lc >= a.n_cols) continue;
+      const int plane = lc / a.rank, jr = lc - plane * a.rank;
+      *reinterpret_cast<u32x2*>(a.L + ((int64_t)plane * a.s_cap + row) * a.rank + jr) = o;
+    }
+  }
+}
+
 template <int TB>
 __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const PrecomputeArgs a, int n_ct, int n_tt) {
   using C = Tile<TB>;
   constexpr int KST = C::KST;
-  static_assert(2 * (C::NIX + C::NIW) * AHEAD <= 24 && (C::NIX + C::NIW) % 2 == 0 && C::NIX >= 1 && C::NIW >= 1,
+  static_assert((C::NIX + C::NIW) * AHEAD <= 24 && (C::NIX + C::NIW) % 2 == 0 && C::NIX >= 1 && C::NIW >= 1,
                 "vmcnt cases");
   static_assert(NST * 2 * TB * KST * 2 >= NCW * 4 * 16 * 64 * 4, "ring holds the split-k partials");
+  static_assert(!C::SPLITK || (KST / 16) % NCW == 0, "k steps per stage split evenly");
   // [stage][X tile, weight tile][TB x KST]
   __shared__ __attribute__((aligned(1024))) uint16_t tiles[NST][2][TB * KST];
   // Waves 0..NCW-1 compute, the others fill the LDS ring, so loading and
@@ -279,62 +335,10 @@ __global__ void __launch_bounds__((NCW + NPW) * 64) precompute_kernel(const Prec
   const int cw = C::SPLITK ? 32 * (w & 1) : 64 * (w & 1), tw = C::SPLITK ? 32 * (w >> 1) : 64 * (w >> 1);
   constexpr int NBLK = C::SPLITK ? 1 : 2;
 #pragma unroll
-  for (int bt = 0; bt < NBLK; ++bt) {
-    const int64_t t = tok0 + tw + 32 * bt + l32;
-    if (t >= a.T) continue;
-    const int64_t trow = a.tok_offset + t;  // absolute position of the token
-    // Cache row of the token: its position, or its row in the paged pools.
-    int64_t row = trow;
-    if (a.tbl != nullptr) {
-      const int q = (int)(trow / a.blk);
-      int32_t e = a.tbl[q];
-      e = e < 0 ? 0 : (e >= a.nblk ? a.nblk - 1 : e);
-      row = (int64_t)e * a.blk + (trow - (int64_t)q * a.blk);
-    }
+  for (int bt = 0; bt < NBLK; ++bt)
 #pragma unroll
-    for (int bc = 0; bc < NBLK; ++bc) {
-      const f32x16& r = acc[bc][bt];
-      const int cb = col0 + cw + 32 * bc;  // first column of this 32-column block
-      if (region == 0) {
-        // Keys: registers j and j + 8 hold dims j0 + i and j0 + i + d/2 of one
-        // head (the column order above); rotate-half RoPE at position trow.
-#pragma unroll
-        for (int jg = 0; jg < 2; ++jg) {
-          const int vc = cb + jg * 8 + h * 4;
-          const int hd = vc / a.head_dim, e = vc - hd * a.head_dim;
-          const int j0 = (e / 32) * 16 + (e % 16);
-          float lo[4], hi[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            float cs, sn;
-            rope_cs((int)trow, a.w2pi[j0 + i], cs, sn);
-            const float x = r[4 * jg + i], y = r[4 * jg + 8 + i];
-            lo[i] = x * cs - y * sn;
-            hi[i] = y * cs + x * sn;
-          }
-          uint16_t* kp = a.Kout + row * a.nkv + hd * a.head_dim + j0;
-          *reinterpret_cast<u32x2*>(kp) = u32x2{pack_bf16(lo[0], lo[1]), pack_bf16(lo[2], lo[3])};
-          *reinterpret_cast<u32x2*>(kp + a.head_dim / 2) = u32x2{pack_bf16(hi[0], hi[1]), pack_bf16(hi[2], hi[3])};
-        }
-        continue;
-      }
-#pragma unroll
-      for (int jg = 0; jg < 4; ++jg) {
-        const int c = cb + jg * 8 + h * 4;
-        u32x2 o;
-        o[0] = pack_bf16(r[4 * jg + 0], r[4 * jg + 1]);
-        o[1] = pack_bf16(r[4 * jg + 2], r[4 * jg + 3]);
-        if (region == 1) {
-          *reinterpret_cast<u32x2*>(a.Vout + row * a.nkv + (c - a.nkv)) = o;
-        } else {
-          const int lc = c - 2 * a.nkv;
-          if (lc >= a.n_cols) continue;
-          const int plane = lc / a.rank, jr = lc - plane * a.rank;
-          *reinterpret_cast<u32x2*>(a.L + ((int64_t)plane * a.s_cap + row) * a.rank + jr) = o;
-        }
-      }
-    }
-  }
+    for (int bc = 0; bc < NBLK; ++bc)
+      store_block(a, acc[bc][bt], region, col0 + cw + 32 * bc, tok0 + tw + 32 * bt + l32, h);
 }
 
 template <int TB>
@@ -350,18 +354,24 @@ hipError_t launch_tb(const PrecomputeArgs& a, hipStream_t st) {
 // A handful of rows (the K/V and LR rows of newly decoded tokens) is a
 // matrix-vector product.  One workgroup per 8 output columns (a key
 // workgroup: 8 dims of a head and their RoPE partners d/2 further on), so the
-// weights are spread over hundreds of workgroups.  Thread t takes the k rows
-// 8t .. 8t + 7 (+ 2048 per round): one 16-byte load of each of the T <= GV_T
-// rows of X, and one 16-byte load (8 columns) of each weight row.  The
-// partial sums are reduced over the lanes by shuffles and over the waves in
-// LDS.
+// weights are spread over many workgroups.  Thread t takes the k rows
+// 8t .. 8t + 7 (+ 4096 per round, so a 4096-wide hidden state is one round
+// with all of a thread's loads in flight at once): one 16-byte load of each
+// of the T <= GV_T rows of X, and one 16-byte load (8 columns) of each weight
+// row.  The partial sums are reduced over the lanes by shuffles and over the
+// waves in LDS.
 constexpr int GV_T = 4;
-constexpr int GV_W = 4;  // waves per workgroup
+constexpr int GV_W = 8;  // waves per workgroup
 
-__global__ void __launch_bounds__(64 * GV_W) project_gemv_kernel(const PrecomputeArgs a) {
+__global__ void __launch_bounds__(64 * GV_W) project_gemv_kernel(const PrecomputeArgs a, int n_units) {
   __shared__ float red[GV_W][2][GV_T][8];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int u = blockIdx.x;
+  // The 8 workgroups whose columns share 128-byte lines of the weight rows run
+  // on one XCD (workgroup L runs on XCD L % 8), so each line is fetched into
+  // one L2 only.
+  const int L = blockIdx.x, slot = L / NXCD;
+  const int u = 8 * ((slot / 8) * NXCD + L % NXCD) + slot % 8;
+  if (u >= n_units) return;
   const int half = a.head_dim / 2;
   const int n_pair = a.nkv / 16;  // key workgroups (8 pair columns each)
   const int n_val = a.nkv / 8;
@@ -434,21 +444,36 @@ __global__ void __launch_bounds__(64 * GV_W) project_gemv_kernel(const Precomput
       }
     }
   }
+  // Sum each of the 32 (token, column) partials over the wave's lanes with a
+  // transposing reduction: every step hands half of a lane's values to its
+  // partner and adds the half it keeps, so after five steps lane l holds one
+  // value, index (l >> 1) & 31, summed over the 32 lanes that share lane bit 0
+  // (32 shuffles instead of 6 per value).
+  auto reduce = [&](float (&acc)[GV_T][8]) -> float {
+    float v[32];
 #pragma unroll
-  for (int t = 0; t < GV_T; ++t)
+    for (int i = 0; i < 32; ++i) v[i] = acc[i / 8][i % 8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      float v0 = acc0[t][e], v1 = acc1[t][e];
+    for (int st = 0; st < 5; ++st) {
+      const int m = 32 >> st, half = 16 >> st;
+      const bool up = (lane & m) != 0;
 #pragma unroll
-      for (int x = 1; x < 64; x <<= 1) {
-        v0 += shfl_xor(v0, x);
-        if (region == 0) v1 += shfl_xor(v1, x);
-      }
-      if (lane == 0) {
-        red[w][0][t][e] = v0;
-        red[w][1][t][e] = v1;
+      for (int i = 0; i < half; ++i) {
+        const float send = up ? v[i] : v[i + half];
+        const float keep = up ? v[i + half] : v[i];
+        v[i] = keep + shfl_xor(send, m);
       }
     }
+    return v[0] + shfl_xor(v[0], 1);
+  };
+  static_assert(GV_T * 8 == 32, "32 partials per lane");
+  const float r0 = reduce(acc0);
+  const float r1 = region == 0 ? reduce(acc1) : 0.f;  // uniform over the workgroup
+  if ((lane & 1) == 0) {
+    const int vi = (lane >> 1) & 31;
+    red[w][0][vi / 8][vi % 8] = r0;
+    red[w][1][vi / 8][vi % 8] = r1;
+  }
   __syncthreads();
   if (tid >= T * 8) return;
   const int t = tid / 8, e = tid % 8;
@@ -479,7 +504,8 @@ __global__ void __launch_bounds__(64 * GV_W) project_gemv_kernel(const Precomput
 
 hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t st) {
   if (a.tbl == nullptr && a.T <= GV_T) {
-    hipLaunchKernelGGL(project_gemv_kernel, dim3(a.nkv / 16 + a.nkv / 8 + a.n_cols / 8), dim3(64 * GV_W), 0, st, a);
+    const int units = a.nkv / 16 + a.nkv / 8 + a.n_cols / 8;
+    hipLaunchKernelGGL(project_gemv_kernel, dim3(64 * ((units + 63) / 64)), dim3(64 * GV_W), 0, st, a, units);
     return hipGetLastError();
   }
   // 128-wide tiles halve the bytes loaded per MFMA but need enough of them to

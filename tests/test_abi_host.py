@@ -419,3 +419,12 @@ def test_noalloc_checks_size_before_the_device():
     assert L.lr_shared_attention_noalloc(ctypes.byref(bad), *args[1:]) == EUNSUP
     ok = _dims(n_tok=1)
     assert L.lr_shared_attention_noalloc(ctypes.byref(ok), *args[1:]) == 7  # no gfx950 device here
+
+
+def test_stream_read_helper_checks_arguments():
+    L = prc.lib()
+    assert L.prc_stream_read(None, 1 << 20, A16, 64, None) == EINVAL
+    assert L.prc_stream_read(A16, 100, A16, 64, None) == EINVAL
+    assert L.prc_stream_read(A16 + 8, 1 << 20, A16, 64, None) == EALIGN
+    assert L.prc_stream_read(A16, 1 << 20, A16, 0, None) == EINVAL
+    assert L.prc_stream_read(A16, 1 << 20, A16, 64, None) == 7  # no gfx950 device here
