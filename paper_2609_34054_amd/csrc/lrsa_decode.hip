@@ -184,6 +184,11 @@ lrsa_decode_kernel(const AttnArgs a) {
   const int G = a.group;
   const int q = lane >> 4, c16 = lane & 15;
   const bool has_lk = a.Lk != nullptr, has_lv = a.Lv != nullptr;
+  // The up-projection rows go out first: their latency hides behind the rest
+  // of the set-up (a split of a small batch covers only a few tiles).
+  BtStage<D, R> bts;
+  bts.issue(has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr, (int64_t)a.n_kv * D,
+            has_lk && active, lane);
 
   // Keys this request may see: t < kv_len (clamped into the buffer) and
   // t <= position of its query token.
@@ -238,8 +243,7 @@ lrsa_decode_kernel(const AttnArgs a) {
     for (int kk = 0; kk < C::NCH; ++kk) qf[kk] = as_bf16x8(ld16(qp + chunk_dim<D>(kk, q), ok));
   }
   typename Ex<R>::Frag bkf[C::NBLK][Ex<R>::NC];
-  load_bt_frags_staged<D, R>(bkf, has_lk ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr,
-                             (int64_t)a.n_kv * D, has_lk && active, lane, v_lds[w]);
+  bts.finish(bkf, v_lds[w], lane);
 
   float m_run = -INFINITY, l_part = 0.f;
   f32x4 acc[C::NBLK];   // O^T: dims blk*16 + 4q + i, head l%16
@@ -546,6 +550,10 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
   const bool has_lk = a.Lk != nullptr, has_lv = a.Lv != nullptr;
   const int64_t t_begin = (int64_t)split * a.split_tiles * TK;
   const int64_t t_cap = t_begin + (int64_t)a.split_tiles * TK;
+  // The up-projection rows go out first (see the per-request kernel).
+  BtStage<D, R> bts;
+  bts.issue(has_lk && active ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr, (int64_t)a.n_kv * D,
+            has_lk && active, lane);
 
   // Keys request r may see: t < min(kv_len, position + 1), within the split.
   auto req_end = [&](int r) -> int64_t {
@@ -661,8 +669,7 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
   }
   typename Ex<R>::Frag bkf[C::NBLK][Ex<R>::NC];
   // Staged through this wave's share of the (not yet used) V tiles.
-  load_bt_frags_staged<D, R>(bkf, has_lk && active ? a.Bk + (int64_t)b * a.b_stride + (int64_t)g * D : nullptr,
-                             (int64_t)a.n_kv * D, has_lk && active, lane, &v_lds[0][0] + w * 16 * C::V_ROW);
+  bts.finish(bkf, &v_lds[0][0] + w * 16 * C::V_ROW, lane);
 
   float m_run = -INFINITY, l_part = 0.f;
   f32x4 acc[C::NBLK];

@@ -112,64 +112,69 @@ __device__ __forceinline__ void load_bt_frags(typename Ex<R>::Frag (&f)[D / 16][
 
 // The same fragments as load_bt_frags, for kernels whose workgroups are
 // short-lived (decode splits): the head's up-projection rows are read with
-// coalesced 16-byte loads, 16 ranks at a time, into a wave-private LDS stage
-// of at least 16 x (D + 16) bf16, and come back transposed through
-// ds_read_b64_tr_b16 (lane j of each 16-lane group points at 4 consecutive
-// bf16; lane i receives element i%4 of lanes i/4, i/4+4, i/4+8, i/4+12).
-// A source lane s of group q points at rank row 4q + s/4 (within a 16-rank
-// chunk) and head dims blk_dim(blk, 4 (s%4)) .. + 3, so lane i receives ranks
-// 4q .. 4q + 3 of dim blk_dim(blk, i), the expansion's A fragment.  All loads
-// are issued before the first LDS write.
+// coalesced 16-byte loads, 16 ranks at a time, and staged through a
+// wave-private LDS area of at least 16 x (D + 16) bf16, from which they come
+// back transposed through ds_read_b64_tr_b16 (lane j of each 16-lane group
+// points at 4 consecutive bf16; lane i receives element i%4 of lanes i/4,
+// i/4+4, i/4+8, i/4+12).  A source lane s of group q points at rank row
+// 4q + s/4 (within a 16-rank chunk) and head dims blk_dim(blk, 4 (s%4)) .. + 3,
+// so lane i receives ranks 4q .. 4q + 3 of dim blk_dim(blk, i), the
+// expansion's A fragment.  Split in two so that the loads can be issued at
+// the very start of a kernel and their latency hidden behind its other set-up.
 template <int D, int R>
-__device__ __forceinline__ void load_bt_frags_staged(typename Ex<R>::Frag (&f)[D / 16][Ex<R>::NC],
-                                                     const uint16_t* bhead, int64_t ldb, bool ok, int lane,
-                                                     uint16_t* stage) {
-  using E = Ex<R>;
-  typedef short v4s __attribute__((ext_vector_type(4)));
-  typedef __attribute__((address_space(3))) v4s* lds_v4s;
-  constexpr int ROW = D + 16;                 // stage row stride (bf16)
-  constexpr int NCH = (R + 15) / 16;          // 16-rank chunks (rank 8: one, upper rows zero)
-  constexpr int PPL = 16 * (D / 8) / 64;      // 16-byte pieces per lane and chunk
-  const int q = lane >> 4, s = lane & 15;
+struct BtStage {
+  static constexpr int NCH = (R + 15) / 16;       // 16-rank chunks (rank 8: one, upper rows zero)
+  static constexpr int PPL = 16 * (D / 8) / 64;   // 16-byte pieces per lane and chunk
   u32x4 raw[NCH][PPL];
+
+  __device__ __forceinline__ void issue(const uint16_t* bhead, int64_t ldb, bool ok, int lane) {
 #pragma unroll
-  for (int rc = 0; rc < NCH; ++rc)
+    for (int rc = 0; rc < NCH; ++rc)
 #pragma unroll
-    for (int i = 0; i < PPL; ++i) {
-      const int p = lane + 64 * i, row = p / (D / 8), col = (p % (D / 8)) * 8, rank = 16 * rc + row;
-      raw[rc][i] = ld16(bhead + (int64_t)(rank < R ? rank : 0) * ldb + col, ok && rank < R);
-    }
-#pragma unroll
-  for (int rc = 0; rc < NCH; ++rc) {
-#pragma unroll
-    for (int i = 0; i < PPL; ++i) {
-      const int p = lane + 64 * i, row = p / (D / 8), col = (p % (D / 8)) * 8;
-      *reinterpret_cast<u32x4*>(stage + row * ROW + col) = raw[rc][i];
-    }
-    __builtin_amdgcn_wave_barrier();
-#pragma unroll
-    for (int blk = 0; blk < D / 16; ++blk) {
-      const int dim = blk_dim<D>(blk, 4 * (s & 3));
-      if constexpr (!E::WIDE) {
-        // Ranks 4q .. 4q + 3 of the one chunk.
-        f[blk][0] = __builtin_bit_cast(
-            u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(stage + (4 * q + (s >> 2)) * ROW + dim)));
-      } else {
-        // 32-rank chunk rc / 2 holds ranks 8q .. 8q + 7 for lane group q: rows
-        // 8 (q % 2) + 0..7 of 16-rank chunk 2 (rc / 2) + q / 2.
-        const int r0 = 8 * (q & 1) + (s >> 2);
-        const u32x2 lo =
-            __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(stage + r0 * ROW + dim)));
-        const u32x2 hi = __builtin_bit_cast(
-            u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(stage + (r0 + 4) * ROW + dim)));
-        if ((q >> 1) == (rc & 1)) f[blk][rc >> 1] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+      for (int i = 0; i < PPL; ++i) {
+        const int p = lane + 64 * i, row = p / (D / 8), col = (p % (D / 8)) * 8, rank = 16 * rc + row;
+        raw[rc][i] = ld16(bhead + (int64_t)(rank < R ? rank : 0) * ldb + col, ok && rank < R);
       }
-    }
-    // The reads of this chunk are done before the next chunk overwrites the stage.
-    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
-    __builtin_amdgcn_wave_barrier();
   }
-}
+
+  __device__ __forceinline__ void finish(typename Ex<R>::Frag (&f)[D / 16][Ex<R>::NC], uint16_t* stage,
+                                         int lane) const {
+    typedef short v4s __attribute__((ext_vector_type(4)));
+    typedef __attribute__((address_space(3))) v4s* lds_v4s;
+    constexpr int ROW = D + 16;  // stage row stride (bf16)
+    const int q = lane >> 4, s = lane & 15;
+#pragma unroll
+    for (int rc = 0; rc < NCH; ++rc) {
+#pragma unroll
+      for (int i = 0; i < PPL; ++i) {
+        const int p = lane + 64 * i, row = p / (D / 8), col = (p % (D / 8)) * 8;
+        *reinterpret_cast<u32x4*>(stage + row * ROW + col) = raw[rc][i];
+      }
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int blk = 0; blk < D / 16; ++blk) {
+        const int dim = blk_dim<D>(blk, 4 * (s & 3));
+        if constexpr (!Ex<R>::WIDE) {
+          // Ranks 4q .. 4q + 3 of the one chunk.
+          f[blk][0] = __builtin_bit_cast(
+              u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(stage + (4 * q + (s >> 2)) * ROW + dim)));
+        } else {
+          // 32-rank chunk rc / 2 holds ranks 8q .. 8q + 7 for lane group q:
+          // rows 8 (q % 2) + 0..7 of 16-rank chunk 2 (rc / 2) + q / 2.
+          const int r0 = 8 * (q & 1) + (s >> 2);
+          const u32x2 lo =
+              __builtin_bit_cast(u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(stage + r0 * ROW + dim)));
+          const u32x2 hi = __builtin_bit_cast(
+              u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s)(stage + (r0 + 4) * ROW + dim)));
+          if ((q >> 1) == (rc & 1)) f[blk][rc >> 1] = u32x4{lo[0], lo[1], hi[0], hi[1]};
+        }
+      }
+      // This chunk's reads are done before the next chunk overwrites the stage.
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+};
 
 // One LR row as the B operand of the expansion (k = rank index).
 template <int R>
