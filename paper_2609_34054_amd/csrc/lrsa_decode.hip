@@ -28,8 +28,8 @@
 //      the transposing LDS read (ds_read_b64_tr_b16), so P, already in B
 //      operand layout, needs no shuffles and the softmax rescale is a
 //      per-lane scalar.
-// The loads of the next sub-block are issued before the current one is
-// consumed.
+// The loads of the next sub-block (the next two at rank 64) are issued before
+// the current one is consumed.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
@@ -44,6 +44,10 @@ constexpr int NSB = TK / 16;  // 16-token sub-blocks per tile
 // gives each wave the whole register file (architected plus accumulation
 // registers) instead of spilling to scratch.
 constexpr int dec_waves(int rank) { return rank >= 64 ? 4 : 8; }
+// Sub-blocks whose loads are in flight ahead of the one being consumed.  With
+// one wave per SIMD (rank 64) no other wave hides a wave's load latency, and
+// the whole register file leaves room for a deeper ring of staged loads.
+constexpr int dec_prefetch(int rank) { return rank >= 64 ? 2 : 1; }
 
 template <int D, int R>
 struct Dec {
@@ -69,6 +73,9 @@ struct Dec {
   static constexpr int RPL = 64 / LPR;        // V rows per wave load
   static constexpr int NVL = 16 / RPL;        // V loads per sub-block
   static constexpr int PS = 4 + D + R;        // floats per split partial
+  static constexpr int PF = dec_prefetch(R);  // sub-blocks loaded ahead
+  static constexpr int NST = (PF + NSB) / NSB * NSB;  // staged sub-blocks: a multiple of NSB above PF
+  static constexpr int TPR = NST / NSB;       // tiles per turn of the stage ring
 };
 
 // Transposing LDS read: lane j of each 16-lane group points at 4 consecutive
@@ -261,7 +268,7 @@ lrsa_decode_kernel(const AttnArgs a) {
   const int tr_row = 4 * q + (c16 >> 2), tr_col = 4 * (c16 & 3);
 
   const StageOffsets<D, R> so = stage_offsets<D, R>(row, lane);
-  Stage<D, R> st[2];
+  Stage<D, R> st[C::NST];
   // Sub-blocks are loaded in token order, so paged caches are walked with them.
   PageWalk walk;
   if constexpr (PAGED)
@@ -272,11 +279,22 @@ lrsa_decode_kernel(const AttnArgs a) {
     if constexpr (PAGED) walk.next(16, t_end_w, kr, lr);
     stage_load<D, R>(s, so, Kb, Vb, Lk, Lv, kr, lr, row, t, t_end_w);
   };
-  load(st[0], t_begin);
+#pragma unroll
+  for (int p = 0; p < C::PF; ++p) load(st[p], t_begin + 16 * p);
 
   __syncthreads();  // base angles of the first tile, zeroed L_v tiles
 
-  for (int tile = 0; tile < n_tiles; ++tile) {
+  // The tile loop is unrolled by the tiles of one turn of the stage ring, so
+  // that every stage index is a constant.  Inside it every path issues the
+  // same loads (inactive waves and sub-blocks past the split end load zeros
+  // and compute on them), and the only early exit leaves the loop for good:
+  // the compiler's load counting then sees the same loads in flight on every
+  // path and waits for no stage before it is needed.
+  for (int tile0 = 0; tile0 < n_tiles; tile0 += C::TPR)
+#pragma unroll
+  for (int tt = 0; tt < C::TPR; ++tt) {
+    const int tile = tile0 + tt;
+    if (tile >= n_tiles) goto tiles_done;  // uniform over the workgroup
     const int64_t t0 = t_begin + (int64_t)tile * TK;
     float2* cs = cs_lds[tile & 1];
     if (has_lk) {
@@ -294,19 +312,22 @@ lrsa_decode_kernel(const AttnArgs a) {
     }
     __syncthreads();  // this tile's table is ready; double buffering keeps
                       // the previous tile's table intact for slower waves.
-    if (!active) continue;
 
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb) {
-      Stage<D, R>& cur = st[sb & 1];
-      Stage<D, R>& nxt = st[(sb + 1) & 1];
+      Stage<D, R>& cur = st[tt * NSB + sb];
+      Stage<D, R>& nxt = st[(tt * NSB + sb + C::PF) % C::NST];
+      // A sub-block past the split end (only in its last tile) holds zeros
+      // and no visible key: all its weights are exactly 0 and the running
+      // maximum does not move, so it changes nothing.
       const int64_t ts = t0 + sb * 16;
-      // A sub-block past the split end holds no visible key (and its stage
-      // buffer was never loaded).
-      if (ts >= t_end) break;
-      // Issue the next sub-block's loads before consuming this one (past the
-      // split end they read zeros and touch no memory).
-      load(nxt, ts + 16);
+      // Issue the loads of the sub-block PF ahead before consuming this one
+      // (past the split end they read zeros and touch no memory).
+      load(nxt, ts + 16 * C::PF);
+      // Keep the loads ahead of this sub-block's work: the scheduler would
+      // otherwise sink them to shorten their registers' live ranges, and the
+      // wait for this stage would then also wait for the next one.
+      __builtin_amdgcn_sched_barrier(0);
 
       // ---- V and L_v rows into the wave's LDS tile ------------------------
 #pragma unroll
@@ -394,6 +415,7 @@ lrsa_decode_kernel(const AttnArgs a) {
     }
   }
 
+tiles_done:
   if (!active) return;
   // One partial per (request, q head, split): lane l%16 is the head; lanes
   // l, l^16, l^32, l^48 share it and hold different dims of O^T.
