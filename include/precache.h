@@ -30,7 +30,8 @@
  *     must be 4-byte aligned.
  *   - Values that live in device memory (positions, kv_len) cannot be checked
  *     by the host.  Kernels clamp kv_len[b] into [0, s_cap], so no access ever
- *     leaves the caller's buffers.
+ *     leaves the caller's buffers.  The checked build of the library checks
+ *     them on the device (see prc_device_checks).
  *
  * Orientation of the weights.  Every weight matrix is passed in the
  * orientation of Eq. 1 (Sec. 2.1), Y = X (W0 + A B) with row vectors: frozen
@@ -58,7 +59,8 @@ typedef enum prc_status {
   PRC_EUNSUPPORTED = 4, /* head_dim, rank or GQA group outside the set built  */
   PRC_EWORKSPACE = 5,   /* workspace null or smaller than the size query      */
   PRC_ELAUNCH = 6,      /* a HIP launch reported an error                     */
-  PRC_EDEVICE = 7       /* no usable gfx950 device is current                 */
+  PRC_EDEVICE = 7,      /* no usable gfx950 device is current                 */
+  PRC_EDEVDATA = 8      /* checked build: kv_len or a position out of range   */
 } prc_status;
 
 /* Thread-local message describing the last non-OK status on this thread. */
@@ -67,6 +69,16 @@ const char* prc_last_error(void);
 const char* prc_status_string(prc_status s);
 /* Library version string, e.g. "0.1.0". */
 const char* prc_version(void);
+/* 1 in the checked build (libprecache_checked.so), 0 in the release build
+ * (libprecache.so).  The two export the same entry points; the checked one
+ * also verifies, on the device, before launching an attention or
+ * materialise call, that 1 <= kv_len[b] <= s_cap and 0 <= positions[b][i] <
+ * kv_len[b] (Sec. 2.2: every query sees a non-empty causal prefix of the
+ * cache).  It reads the verdict back, so each such call waits for its stream
+ * (not usable under graph capture), and on a violation it launches nothing,
+ * returns PRC_EDEVDATA and names the first offender (lowest request, then
+ * lowest token; a kv_len fault before a position fault) in prc_last_error(). */
+int prc_device_checks(void);
 
 /*
  * precompute_lr_cache -- the LR-cache precompute of Sec. 3.1 (Fig. 1 A1-A3).

@@ -19,6 +19,7 @@ from .binding import (  # noqa: F401
     project_kv_and_lr_cache,
     project_kv_and_lr_cache_paged,
     stream_read,
+    use_checked_library,
     workspace_size,
 )
 

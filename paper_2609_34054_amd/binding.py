@@ -13,18 +13,22 @@ import os
 
 import torch
 
-from .build import LIB_PATH
+from .build import CHECKED_LIB_PATH, LIB_PATH
 
-_LIB = None
+_LIBS: dict = {}
+# The checked build (device-side kv_len/position checks, a stream wait per
+# attention call) is selected with PRC_CHECKED=1 or use_checked_library().
+_CHECKED = os.environ.get("PRC_CHECKED", "0") == "1"
 
 STATUS_NAMES = {0: "PRC_OK", 1: "PRC_EINVAL", 2: "PRC_ESHAPE", 3: "PRC_EALIGN",
-                4: "PRC_EUNSUPPORTED", 5: "PRC_EWORKSPACE", 6: "PRC_ELAUNCH", 7: "PRC_EDEVICE"}
+                4: "PRC_EUNSUPPORTED", 5: "PRC_EWORKSPACE", 6: "PRC_ELAUNCH", 7: "PRC_EDEVICE",
+                8: "PRC_EDEVDATA"}
 
 EXPORTS = ("precompute_lr_cache", "project_kv_and_lr_cache", "project_kv_and_lr_cache_paged",
            "lr_shared_attention", "lr_shared_attention_workspace_size", "lr_shared_attention_paged",
            "lr_shared_attention_paged_workspace_size", "lr_shared_attention_noalloc", "materialize_agent_kv",
            "prc_stream_read", "prc_last_error",
-           "prc_status_string", "prc_version")
+           "prc_status_string", "prc_version", "prc_device_checks")
 
 
 class PrecacheError(RuntimeError):
@@ -63,14 +67,21 @@ class LrsaPaging(ctypes.Structure):
     ]
 
 
+def use_checked_library(flag: bool = True) -> None:
+    """Route every later call through libprecache_checked.so (or back)."""
+    global _CHECKED
+    _CHECKED = bool(flag)
+
+
 def lib() -> ctypes.CDLL:
-    """Load libprecache.so (built in-tree by ``build()``); raise if absent."""
-    global _LIB
-    if _LIB is None:
-        if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
+    """Load libprecache.so, or its checked twin (both built in-tree by
+    ``build()``); raise if absent."""
+    path = CHECKED_LIB_PATH if _CHECKED else LIB_PATH
+    if path not in _LIBS:
+        if not os.path.exists(path):
+            raise RuntimeError(f"{path} is not built: run __graft_entry__.build() "
                                "(python -m paper_2609_34054_amd.build)")
-        L = ctypes.CDLL(LIB_PATH)
+        L = ctypes.CDLL(path)
         vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
         L.precompute_lr_cache.argtypes = [vp, i64, i64, i64, vp, i32, i32, i32, vp, i64, i64, vp]
         L.precompute_lr_cache.restype = ctypes.c_int
@@ -101,8 +112,9 @@ def lib() -> ctypes.CDLL:
         L.prc_status_string.argtypes = [ctypes.c_int]
         L.prc_status_string.restype = ctypes.c_char_p
         L.prc_version.restype = ctypes.c_char_p
-        _LIB = L
-    return _LIB
+        L.prc_device_checks.restype = ctypes.c_int
+        _LIBS[path] = L
+    return _LIBS[path]
 
 
 def _check(func: str, status: int) -> None:

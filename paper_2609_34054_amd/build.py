@@ -2,7 +2,9 @@
 
 Usage: ``python -m paper_2609_34054_amd.build`` or ``build()`` from Python.
 Every call recompiles all sources (objects go to ``_build/``), then links
-``paper_2609_34054_amd/libprecache.so``.
+``paper_2609_34054_amd/libprecache.so`` and its checked twin
+``libprecache_checked.so`` (the same kernels; the ABI layer compiled with
+``PRC_DEVICE_CHECKS=1`` checks device-resident kv_len and positions).
 """
 from __future__ import annotations
 
@@ -18,6 +20,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "libprecache.so")
+CHECKED_LIB_PATH = os.path.join(PKG, "libprecache_checked.so")
 
 SOURCES = [
     "abi.cpp",
@@ -26,6 +29,7 @@ SOURCES = [
     "lrsa_prefill.hip",
     "materialize.hip",
     "stream_read.hip",
+    "device_checks.hip",
 ]
 
 ARCH = "gfx950"
@@ -51,9 +55,9 @@ def _hipcc() -> str:
     raise RuntimeError("hipcc not found: the ROCm toolchain is required to build libprecache.so")
 
 
-def _compile(src: str, hipcc: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [hipcc, *CFLAGS]
+def _compile(src: str, hipcc: str, verbose: bool, checked: bool = False) -> str:
+    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ("_checked" if checked else "") + ".o")
+    cmd = [hipcc, *CFLAGS, *(["-DPRC_DEVICE_CHECKS=1"] if checked else [])]
     if src.endswith(".cpp"):
         cmd += ["-x", "hip"]
     cmd += ["-c", os.path.join(CSRC, src), "-o", obj]
@@ -70,21 +74,28 @@ def _compile(src: str, hipcc: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False, jobs: int | None = None) -> str:
-    """Compile every source and link the shared library; returns its path."""
-    hipcc = _hipcc()
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    jobs = jobs or min(len(SOURCES), max(1, min(8, os.cpu_count() or 1)))
-    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
-        objs = list(ex.map(lambda s: _compile(s, hipcc, verbose), SOURCES))
-    tmp = LIB_PATH + ".tmp"
+def _link(hipcc: str, objs: list[str], path: str, verbose: bool) -> None:
+    tmp = path + ".tmp"
     cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed:\n{res.stdout}{res.stderr}")
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, path)
     if verbose:
-        print(f"built {LIB_PATH}", flush=True)
+        print(f"built {path}", flush=True)
+
+
+def build(verbose: bool = False, jobs: int | None = None) -> str:
+    """Compile every source, link both libraries; returns the release path."""
+    hipcc = _hipcc()
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    units = [(s, False) for s in SOURCES] + [("abi.cpp", True)]
+    jobs = jobs or min(len(units), max(1, min(8, os.cpu_count() or 1)))
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(lambda u: _compile(u[0], hipcc, verbose, u[1]), units))
+    release, abi_checked = objs[:len(SOURCES)], objs[-1]
+    _link(hipcc, release, LIB_PATH, verbose)
+    _link(hipcc, [abi_checked if s == "abi.cpp" else o for s, o in zip(SOURCES, release)], CHECKED_LIB_PATH, verbose)
     return LIB_PATH
 
 

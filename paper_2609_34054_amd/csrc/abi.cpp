@@ -18,6 +18,12 @@
 
 #define PRC_API extern "C" __attribute__((visibility("default")))
 
+// 1 in libprecache_checked.so: device-resident kv_len and positions are
+// checked before each attention or materialise call.
+#ifndef PRC_DEVICE_CHECKS
+#define PRC_DEVICE_CHECKS 0
+#endif
+
 namespace {
 
 thread_local std::string g_err;
@@ -93,6 +99,46 @@ prc_status launch_status(hipError_t e, const char* what) {
   if (e != hipSuccess) return fail(PRC_ELAUNCH, "%s: HIP launch failed: %s", what, hipGetErrorString(e));
   return ok();
 }
+
+#if PRC_DEVICE_CHECKS
+// Checked build: before a call's kernels run, check the device-resident
+// kv_len and positions and read the verdict back (the call then waits for the
+// stream).  A failed check launches nothing and returns PRC_EDEVDATA.
+int32_t* g_check_ptr[kMaxDevices];
+
+prc_status device_data_check(const char* who, const int32_t* positions, const int32_t* kv_len, int batch, int n_tok,
+                             int64_t s_cap, hipStream_t st) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return fail(PRC_EDEVICE, "no HIP device is current");
+  }
+  int32_t* res = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    if (g_check_ptr[dev] == nullptr) {
+      int32_t* p = nullptr;
+      const hipError_t e = prc::device_checks_result(&p);
+      if (e != hipSuccess || p == nullptr) {
+        (void)hipGetLastError();
+        return fail(PRC_EDEVICE, "%s: device check array unavailable: %s", who, hipGetErrorString(e));
+      }
+      g_check_ptr[dev] = p;
+    }
+    res = g_check_ptr[dev];
+  }
+  hipError_t e = prc::launch_device_checks(positions, kv_len, batch, n_tok, s_cap, res, st);
+  int32_t h[4] = {0, 0, 0, 0};
+  if (e == hipSuccess) e = hipMemcpyAsync(h, res, sizeof(h), hipMemcpyDeviceToHost, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail(PRC_ELAUNCH, "%s: device check failed: %s", who, hipGetErrorString(e));
+  if (h[0] == 1)
+    return fail(PRC_EDEVDATA, "%s: kv_len[%d]=%d outside [1, s_cap=%lld]", who, h[1], h[3], (long long)s_cap);
+  if (h[0] == 2)
+    return fail(PRC_EDEVDATA, "%s: positions[%d][%d]=%d outside [0, kv_len[%d])", who, h[1], h[2], h[3], h[1]);
+  return PRC_OK;
+}
+#endif
 
 // Validated view of an attention/materialise call.
 struct Checked {
@@ -228,11 +274,14 @@ PRC_API const char* prc_status_string(prc_status s) {
     case PRC_EWORKSPACE: return "PRC_EWORKSPACE";
     case PRC_ELAUNCH: return "PRC_ELAUNCH";
     case PRC_EDEVICE: return "PRC_EDEVICE";
+    case PRC_EDEVDATA: return "PRC_EDEVDATA";
   }
   return "PRC_UNKNOWN";
 }
 
 PRC_API const char* prc_version(void) { return "0.1.0"; }
+
+PRC_API int prc_device_checks(void) { return PRC_DEVICE_CHECKS; }
 
 PRC_API prc_status precompute_lr_cache(const uint16_t* X, int64_t T, int64_t d_in, int64_t ld_x,
                                        const uint16_t* A_stack, int32_t n_proj, int32_t n_agents,
@@ -433,6 +482,9 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
     if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
     int cus = 0;
     if (prc_status ds = device_ready(&cus)) return ds;
+#if PRC_DEVICE_CHECKS
+    if (prc_status dc = device_data_check(who, positions, kv_len, a.batch, a.n_tok, a.s_cap, st)) return dc;
+#endif
     prc::decode_plan(a.s_cap, a.batch, a.n_kv, a.rank,
                      pg == nullptr && prc::decode_shares_base(a.batch, a.kv_stride), cus, &a.n_splits,
                      &a.split_tiles);
@@ -452,6 +504,9 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
   }
   int cus = 0;
   if (prc_status ds = device_ready(&cus)) return ds;
+#if PRC_DEVICE_CHECKS
+  if (prc_status dc = device_data_check(who, positions, kv_len, a.batch, a.n_tok, a.s_cap, st)) return dc;
+#endif
   snprintf(what, sizeof(what), "%s (prefill)", who);
   return launch_status(prc::launch_prefill(a, st), what);
 }
@@ -576,6 +631,11 @@ PRC_API prc_status materialize_agent_kv(const lrsa_dims* dims, const uint16_t* K
     return fail(PRC_EINVAL, "K_full and V_full overlap");
   int cus = 0;
   if (prc_status ds = device_ready(&cus)) return ds;
+#if PRC_DEVICE_CHECKS
+  if (prc_status dc = device_data_check("materialize_agent_kv", nullptr, kv_len, c.a.batch, 0, c.a.s_cap,
+                                        static_cast<hipStream_t>(stream)))
+    return dc;
+#endif
   c.a.Kout = K_full;
   c.a.Vout = V_full;
   return launch_status(prc::launch_materialize(c.a, static_cast<hipStream_t>(stream)), "materialize_agent_kv");

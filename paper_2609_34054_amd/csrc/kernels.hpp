@@ -118,4 +118,12 @@ hipError_t launch_precompute(const PrecomputeArgs& a, hipStream_t stream);
 // workgroups, one XOR word per workgroup to sink.
 hipError_t launch_stream_read(const void* src, int64_t bytes, uint32_t* sink, int grid, hipStream_t stream);
 
+// Checked build: the first kv_len outside [1, s_cap] or query position
+// outside [0, kv_len[b]) (positions may be null), written to `result` as
+// {kind, request, token, value} with kind 0 for none, 1 kv_len, 2 position.
+// `result` is the per-device array whose address device_checks_result gives.
+hipError_t device_checks_result(int32_t** ptr);
+hipError_t launch_device_checks(const int32_t* positions, const int32_t* kv_len, int batch, int n_tok, int64_t s_cap,
+                                int32_t* result, hipStream_t st);
+
 }  // namespace prc

@@ -19,7 +19,7 @@ A16 = 0x10000  # fake 16-byte-aligned addresses: never dereferenced on the host
 
 def declared_functions():
     src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
-    return sorted(set(re.findall(r"^(?:prc_status|size_t|const char\*)\s+(\w+)\s*\(", src, flags=re.M)))
+    return sorted(set(re.findall(r"^(?:prc_status|size_t|const char\*|int)\s+(\w+)\s*\(", src, flags=re.M)))
 
 
 def test_header_declares_the_boundary():
@@ -33,6 +33,29 @@ def test_library_exports_every_declared_symbol():
     out = os.popen(f"nm -D --defined-only {L._name}").read()
     exported = {ln.split()[-1] for ln in out.splitlines() if " T " in ln}
     assert exported == set(declared_functions()), exported ^ set(declared_functions())
+
+
+def test_checked_build_exports_the_same_boundary():
+    """libprecache_checked.so (device-side kv_len/position checks) exports
+    exactly the release library's symbols and says which build it is."""
+    from paper_2609_34054_amd.build import CHECKED_LIB_PATH
+    C = ctypes.CDLL(CHECKED_LIB_PATH)
+    out = os.popen(f"nm -D --defined-only {CHECKED_LIB_PATH}").read()
+    exported = {ln.split()[-1] for ln in out.splitlines() if " T " in ln}
+    assert exported == set(declared_functions())
+    C.prc_status_string.restype = ctypes.c_char_p
+    assert C.prc_device_checks() == 1 and prc.lib().prc_device_checks() == 0
+    assert C.prc_status_string(8).decode() == "PRC_EDEVDATA"
+
+
+def test_checked_library_is_selectable():
+    from paper_2609_34054_amd.binding import use_checked_library
+    try:
+        use_checked_library(True)
+        assert prc.lib().prc_device_checks() == 1
+    finally:
+        use_checked_library(False)
+    assert prc.lib().prc_device_checks() == 0
 
 
 def test_version_and_status_strings():
