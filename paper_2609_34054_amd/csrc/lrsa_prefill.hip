@@ -4,12 +4,13 @@
 // cache plus the current agent's LR cache (Sec. 3.1, reuse step).
 //   keys:   each KV tile is rebuilt in LDS, K = K_base + RoPE(L_k B_k), with
 //           the rank-r expansion before RoPE (App. D.2);
-//   values: ranks 8 and 16 use associativity (App. D.2),
+//   values: rank 8 uses associativity (App. D.2),
 //           O = P V_base + (P L_v) B_v: V_base and L_v go to LDS unchanged in
 //           value, P L_v is accumulated beside P V_base and B_v is applied
-//           once in the epilogue.  Ranks 32 and 64 rebuild V = V_base + L_v B_v
+//           once in the epilogue.  Ranks 16 to 64 rebuild V = V_base + L_v B_v
 //           in the tile (bf16, like K): with 256 query rows per workgroup that
-//           is half the flops of P L_v and needs no (P L_v)^T accumulator.
+//           is half the flops of P L_v, needs no (P L_v)^T accumulator, and
+//           the expansion rides on the MFMA that transposes V anyway.
 //
 // Work split: one workgroup of 8 waves per (request, KV head, 256 query rows).
 // A query row is a (token, q head of the GQA group) pair, so the group's heads
@@ -17,9 +18,10 @@
 //   build   wave w rebuilds 16 tokens (w % 4) x half of the RoPE pair blocks
 //           (w / 4) of the next KV tile: E^T = B_k^T L_k^T on 16x16 MFMAs
 //           (lane l: token l%16, both halves of each pair in the same lane),
-//           RoPE by angle addition (exact per-tile base angle in LDS, exact
-//           per-lane offsets), + base, bf16 into LDS.  It also transposes a
-//           32-token block of V_base (and, for the first waves, of L_v) on
+//           RoPE by angle addition (exact per-tile base angle in LDS,
+//           per-lane offset angles held as fp16 pairs in registers), + base,
+//           bf16 into LDS.  It also transposes a
+//           32-token block of V_base (and, at rank 8, of L_v) on
 //           the MFMA against a shifted identity, which writes them to LDS
 //           directly in the PV A-fragment layout; from rank 32 the transpose
 //           accumulates onto L_v B_v of the same block.  Its global loads for
@@ -54,6 +56,9 @@ constexpr int NTHR = 64 * NW;
 constexpr int WROWS = 32;            // query rows per wave
 constexpr int BROWS = NW * WROWS;    // query rows per workgroup
 constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (log2 domain)
+// Value side of rank r: V = V_base + L_v B_v rebuilt in the tile, or
+// associativity with (P L_v) accumulated beside P V_base.
+constexpr bool rebuilds_v(int rank) { return rank >= 16; }
 
 template <int D, int R>
 struct Pre {
@@ -145,12 +150,12 @@ template <int D, int R, bool LK, bool LV, bool PAGED>
 __global__ void __launch_bounds__(NTHR)
 lrsa_prefill_kernel(const AttnArgs a) {
   using C = Pre<D, R>;
-  // Value side: ranks below 32 keep associativity, P V_base + (P L_v) B_v,
-  // with the softmax row sums in a spare row of (P L_v)^T.  From rank 32 on
-  // the tile's V = V_base + L_v B_v is rebuilt on chip instead: per 64-token
+  // Value side: rank 8 keeps associativity, P V_base + (P L_v) B_v, with the
+  // softmax row sums in a spare row of (P L_v)^T.  From rank 16 on the
+  // tile's V = V_base + L_v B_v is rebuilt on chip instead: per 64-token
   // tile a workgroup then spends 2 * 64 * d * r flop on the expansion rather
   // than 2 * 256 * 64 * r on P L_v, and needs no (P L_v)^T accumulator.
-  constexpr bool VREB = LV && R >= 32;
+  constexpr bool VREB = LV && rebuilds_v(R);
   constexpr bool LVA = LV && !VREB;
   constexpr int NRB = LVA ? Pre<D, R>::RB : 1;
   constexpr bool ones_sum = LVA && R < 32;
@@ -160,7 +165,6 @@ lrsa_prefill_kernel(const AttnArgs a) {
   __shared__ __attribute__((aligned(16))) float2 base_cs[2][C::HALF];
   // cos/sin of each build lane's in-tile offset at its SEG frequencies,
   // [wave][pair of frequencies][lane] (one 16-byte read per pair).
-  __shared__ __attribute__((aligned(16))) f32x4 off_cs[LK ? NW : 1][C::SEG / 2][64];
   // B_k^T fragments of this KV head for ranks > 16, [RoPE half ph][block i]
   // [lane][rank chunk]: each lane's NC 16-byte fragments are contiguous.
   __shared__ __attribute__((aligned(16))) u32x4 bk_lds[LK && !C::BK_REG ? 2 * 2 * C::NBW * 64 * C::NC : 1];
@@ -285,13 +289,18 @@ lrsa_prefill_kernel(const AttnArgs a) {
       for (int c = 0; c < C::NC; ++c) f[c] = p[c];
     }
   };
+  // cos/sin of this build lane's in-tile offset angle at each of its SEG
+  // frequencies, one fp16 pair per register (their fp16 rounding moves the
+  // rebuilt LR term by under 2^-11 of itself, far below the bf16 rounding of
+  // the rebuilt key).
+  uint32_t ocs[LK ? C::SEG : 1];
   if constexpr (LK) {
 #pragma unroll
-    for (int e = 0; e < C::SEG; e += 2) {
-      float c0, s0, c1, s1;
+    for (int e = 0; e < C::SEG; ++e) {
+      float c0, s0;
       rope_cs(delta, a.w2pi[lo_dim0 + e], c0, s0);
-      rope_cs(delta, a.w2pi[lo_dim0 + e + 1], c1, s1);
-      off_cs[w][e / 2][lane] = f32x4{c0, s0, c1, s1};
+      const _Float16 hc = (_Float16)c0, hs = (_Float16)s0;
+      ocs[e] = (uint32_t)__builtin_bit_cast(uint16_t, hc) | ((uint32_t)__builtin_bit_cast(uint16_t, hs) << 16);
     }
   }
   // Per-lane byte offsets of the staged data within a tile (constant); the
@@ -320,7 +329,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
     for (int kc = 0; kc < R / 16; ++kc) {
       offlvv[kc] = (32 * vtb + (lane & 31)) * R * 2 + (16 * kc + (lane >> 5) * 8) * 2;
-      bvf[kc] = Ex<R>::gather(bvp + (int64_t)(16 * kc + (lane >> 5) * 8) * ldb, ldb, true);
+      bvf[kc] = Ex<32>::gather(bvp + (int64_t)(16 * kc + (lane >> 5) * 8) * ldb, ldb, true);
     }
   }
   // Tiles are loaded in token order, so paged caches are walked with them.
@@ -387,8 +396,12 @@ lrsa_prefill_kernel(const AttnArgs a) {
           ehi = Ex<R>::mma(fh[c], u.lk[c], ehi);
         }
         float vlo[4], vhi[4];
-        const f32x4 od0 = off_cs[w][2 * i][lane], od1 = off_cs[w][2 * i + 1][lane];
-        const float cd[4] = {od0[0], od0[2], od1[0], od1[2]}, sd[4] = {od0[1], od0[3], od1[1], od1[3]};
+        float cd[4], sd[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          cd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] & 0xFFFFu));
+          sd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] >> 16));
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int e = 4 * i + j;
@@ -408,7 +421,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
     st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + C::HALF + lo_dim0, hi);
     {
       // Transpose the V half blocks on the MFMA and store them as fragments
-      // (2 vtb, vdb) and (2 vtb + 1, vdb); from rank 32 on the transpose
+      // (2 vtb, vdb) and (2 vtb + 1, vdb); from rank 16 on the transpose
       // accumulates onto L_v B_v of the same tokens and dims.
       f32x16 t;
 #pragma unroll
@@ -826,9 +839,9 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   // The partials are laid out for the rank this kernel was built with (a
   // call without LR runs the rank-8 build whatever dims.rank says).
   m.rank = R;
-  // From rank 32 on B_v is already inside the rebuilt V: the partials carry
+  // With V rebuilt in the tile B_v is already inside it: the partials carry
   // no (P L_v) part for the merge to expand.
-  if (LV && R >= 32) m.Lv = nullptr;
+  if (LV && rebuilds_v(R)) m.Lv = nullptr;
   return launch_split_merge(m, st);
 }
 
