@@ -28,8 +28,8 @@
 //      the transposing LDS read (ds_read_b64_tr_b16), so P, already in B
 //      operand layout, needs no shuffles and the softmax rescale is a
 //      per-lane scalar.
-// The loads of the next sub-block (the next two at rank 64) are issued before
-// the current one is consumed.
+// The loads of the next sub-block (the next two at rank 64) are in flight
+// while the current one is consumed.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
@@ -46,8 +46,10 @@ constexpr int NSB = TK / 16;  // 16-token sub-blocks per tile
 constexpr int dec_waves(int rank) { return rank >= 64 ? 4 : 8; }
 // Sub-blocks whose loads are in flight ahead of the one being consumed.  With
 // one wave per SIMD (rank 64) no other wave hides a wave's load latency, and
-// the whole register file leaves room for a deeper ring of staged loads.
+// the whole register file leaves room for one more staged sub-block; at two
+// waves per SIMD the extra stage spills and loses.
 constexpr int dec_prefetch(int rank) { return rank >= 64 ? 2 : 1; }
+constexpr int gcd_c(int a, int b) { return b == 0 ? a : gcd_c(b, a % b); }
 
 template <int D, int R>
 struct Dec {
@@ -74,8 +76,8 @@ struct Dec {
   static constexpr int NVL = 16 / RPL;        // V loads per sub-block
   static constexpr int PS = 4 + D + R;        // floats per split partial
   static constexpr int PF = dec_prefetch(R);  // sub-blocks loaded ahead
-  static constexpr int NST = (PF + NSB) / NSB * NSB;  // staged sub-blocks: a multiple of NSB above PF
-  static constexpr int TPR = NST / NSB;       // tiles per turn of the stage ring
+  static constexpr int NST = PF + 1;          // staged sub-blocks (a ring)
+  static constexpr int TPR = NST / gcd_c(NST, NSB);  // tiles per whole number of turns of the ring
 };
 
 // Transposing LDS read: lane j of each 16-lane group points at 4 consecutive
@@ -315,7 +317,7 @@ lrsa_decode_kernel(const AttnArgs a) {
 
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb) {
-      Stage<D, R>& cur = st[tt * NSB + sb];
+      Stage<D, R>& cur = st[(tt * NSB + sb) % C::NST];
       Stage<D, R>& nxt = st[(tt * NSB + sb + C::PF) % C::NST];
       // A sub-block past the split end (only in its last tile) holds zeros
       // and no visible key: all its weights are exactly 0 and the running

@@ -19,8 +19,8 @@
 //           (w / 4) of the next KV tile: E^T = B_k^T L_k^T on 16x16 MFMAs
 //           (lane l: token l%16, both halves of each pair in the same lane),
 //           RoPE by angle addition (exact per-tile base angle in LDS,
-//           per-lane offset angles held as fp16 pairs in registers), + base,
-//           bf16 into LDS.  It also transposes a
+//           per-lane offset angles in LDS, or at rank 16 as fp16 pairs in
+//           registers), + base, bf16 into LDS.  It also transposes a
 //           32-token block of V_base (and, at rank 8, of L_v) on
 //           the MFMA against a shifted identity, which writes them to LDS
 //           directly in the PV A-fragment layout; from rank 32 the transpose
@@ -84,6 +84,9 @@ struct Pre {
   static constexpr int NLP = R >= 32 ? 2 : 1;
   // B_k^T fragments of small ranks stay in registers, larger ones in LDS.
   static constexpr bool BK_REG = R <= 16;
+  // The per-lane offset angles of the rebuild stay in registers where the
+  // register budget allows it (rank 16, V rebuilt in the tile), else in LDS.
+  static constexpr bool OCS_REG = R == 16;
 };
 
 // SEG consecutive bf16 of one row.
@@ -118,6 +121,11 @@ __device__ __forceinline__ void st_seg(uint16_t* p, const Seg<SEG>& s) {
 template <int SEG>
 __device__ __forceinline__ float seg_get(const Seg<SEG>& s, int e) {
   return (e & 1) ? bf_hi(s.w[e >> 1]) : bf_lo(s.w[e >> 1]);
+}
+
+// Two floats as an fp16 pair (low half first), rounded to nearest.
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) | ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
 }
 
 // Buffer resource over `bytes` bytes from `base`: loads at offsets at or past
@@ -163,6 +171,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t v_lds[2][TKV * D];  // V^T fragments
   __shared__ __attribute__((aligned(16))) uint16_t lv_lds[LVA ? 2 : 1][LVA ? TKV * 32 * C::RB : 8];  // L_v^T fragments
   __shared__ __attribute__((aligned(16))) float2 base_cs[2][C::HALF];
+  // cos/sin of each build lane's in-tile offset at its SEG frequencies,
+  // [wave][pair of frequencies][lane] (one 16-byte read per pair), where
+  // they are not kept in registers.
+  __shared__ __attribute__((aligned(16))) f32x4 off_cs[LK && !C::OCS_REG ? NW : 1][C::SEG / 2][64];
   // cos/sin of each build lane's in-tile offset at its SEG frequencies,
   // [wave][pair of frequencies][lane] (one 16-byte read per pair).
   // B_k^T fragments of this KV head for ranks > 16, [RoPE half ph][block i]
@@ -290,17 +302,22 @@ lrsa_prefill_kernel(const AttnArgs a) {
     }
   };
   // cos/sin of this build lane's in-tile offset angle at each of its SEG
-  // frequencies, one fp16 pair per register (their fp16 rounding moves the
-  // rebuilt LR term by under 2^-11 of itself, far below the bf16 rounding of
-  // the rebuilt key).
-  uint32_t ocs[LK ? C::SEG : 1];
+  // frequencies: in registers as one fp16 pair per frequency (their fp16
+  // rounding moves the rebuilt LR term by under 2^-11 of itself, far below
+  // the bf16 rounding of the rebuilt key), or in LDS as fp32.
+  uint32_t ocs[LK && C::OCS_REG ? C::SEG : 1];
   if constexpr (LK) {
 #pragma unroll
-    for (int e = 0; e < C::SEG; ++e) {
-      float c0, s0;
+    for (int e = 0; e < C::SEG; e += 2) {
+      float c0, s0, c1, s1;
       rope_cs(delta, a.w2pi[lo_dim0 + e], c0, s0);
-      const _Float16 hc = (_Float16)c0, hs = (_Float16)s0;
-      ocs[e] = (uint32_t)__builtin_bit_cast(uint16_t, hc) | ((uint32_t)__builtin_bit_cast(uint16_t, hs) << 16);
+      rope_cs(delta, a.w2pi[lo_dim0 + e + 1], c1, s1);
+      if constexpr (C::OCS_REG) {
+        ocs[e] = pack_f16x2(c0, s0);
+        ocs[e + 1] = pack_f16x2(c1, s1);
+      } else {
+        off_cs[w][e / 2][lane] = f32x4{c0, s0, c1, s1};
+      }
     }
   }
   // Per-lane byte offsets of the staged data within a tile (constant); the
@@ -397,10 +414,16 @@ lrsa_prefill_kernel(const AttnArgs a) {
         }
         float vlo[4], vhi[4];
         float cd[4], sd[4];
+        if constexpr (C::OCS_REG) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          cd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] & 0xFFFFu));
-          sd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] >> 16));
+          for (int j = 0; j < 4; ++j) {
+            cd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] & 0xFFFFu));
+            sd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] >> 16));
+          }
+        } else {
+          const f32x4 od0 = off_cs[w][2 * i][lane], od1 = off_cs[w][2 * i + 1][lane];
+          cd[0] = od0[0], cd[1] = od0[2], cd[2] = od1[0], cd[3] = od1[2];
+          sd[0] = od0[1], sd[1] = od0[3], sd[2] = od1[1], sd[3] = od1[3];
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
