@@ -470,6 +470,7 @@ def rank_sweep(prc, w, dev, steps, warmup):
 
     runs = [("plain", 16, False, False)] + [(m, r, m == "kv", True) for m in ("qv", "kv") for r in (8, 16, 32, 64)]
     bstd = math.sqrt(0.02)
+    recs = []
     for mode, r, lk, lv in runs:
         cases = {}
         for st, nb, ntok in (("pre", 1, kv_pre), ("dec", B, S)):
@@ -489,14 +490,14 @@ def rank_sweep(prc, w, dev, steps, warmup):
         work = algorithmic_work(dict(w, r=r), lk, lv)
         pre_tf = work["prefill_flops"] / (t_pre * 1e-3) / 1e12
         dec_gbs = work["decode_bytes"] / (t_dec * 1e-3) / 1e9
-        print(json.dumps({"sweep": "rank", "mode": mode, "rank": r if (lk or lv) else 0,
+        recs.append({"sweep": "rank", "mode": mode, "rank": r if (lk or lv) else 0,
                           "prefill_ms": round(t_pre, 4), "prefill_tflops": round(pre_tf, 2),
                           "prefill_mfma_frac": round(pre_tf / MFMA_BF16_PEAK_TFLOPS, 4),
                           "decode_ms": round(t_dec, 4), "decode_gbs": round(dec_gbs, 1),
                           "decode_hbm_frac": round(dec_gbs / HBM_PEAK_GBS, 4),
-                          "decode_bytes": work["decode_bytes"], "prefill_flops": work["prefill_flops"]}),
-              flush=True)
+                          "decode_bytes": work["decode_bytes"], "prefill_flops": work["prefill_flops"]})
         del cases, O_pre, O_dec, ws
+    return recs
 
 
 def shared_base_decode(prc, w, dev, steps, warmup):
@@ -543,18 +544,19 @@ def shared_base_decode(prc, w, dev, steps, warmup):
                V_base=c["V_base"].expand(N, -1, -1, -1).contiguous())
     t_rep, O_rep = timed(rep)
     diff = (O_shared.float() - O_rep.float()).abs().max().item()
+    del rep, c
     base_bytes = S * n_kv * d * 2 * 2
     lr_bytes = N * (S * r * 2 * 2 + 2 * n_kv * d * r * 2 + 2 * n_q * d * 2)
     algo = base_bytes + lr_bytes
     gbs = algo / (t_shared * 1e-3) / 1e9
-    print(json.dumps({
+    return {
         "bench": "shared_base_decode", "agents": N, "context": S, "rank": r,
         "workload": (f"decode of {N} agents at position {S - 1} over one shared {S}-token base cache "
                      f"({n_q} q / {n_kv} KV heads, d {d}), each with its own rank-{r} k and v LR plane"),
         "ms": round(t_shared, 4), "algorithmic_bytes": algo, "gbs": round(gbs, 1),
         "hbm_frac": round(gbs / HBM_PEAK_GBS, 4),
         "per_request_copies_ms": round(t_rep, 4), "speedup_vs_per_request_copies": round(t_rep / t_shared, 3),
-        "max_abs_diff_vs_per_request": diff}), flush=True)
+        "max_abs_diff_vs_per_request": diff}
 
 
 def fused_projection(prc, w, dev, steps, warmup):
@@ -601,7 +603,7 @@ def fused_projection(prc, w, dev, steps, warmup):
     flops = 2 * T * hid * cols
     byts = (T * hid + cols * hid + T * cols) * 2
     tf = flops / (t_fused * 1e-3) / 1e12
-    print(json.dumps({
+    return {
         "bench": "fused_projection",
         "workload": (f"{T}-token segment, hidden {hid}: K_base (RoPE) and V_base for {n_kv} KV heads x {d} plus "
                      f"rank-{r} k and v LR rows of {N} agents, one GEMM of {cols} columns"),
@@ -609,7 +611,7 @@ def fused_projection(prc, w, dev, steps, warmup):
         "algorithmic_flops": flops, "algorithmic_bytes": byts,
         "base_projection_alone_ms": round(t_base, 4), "precompute_alone_ms": round(t_pre, 4),
         "separate_ms": round(t_base + t_pre, 4),
-        "lr_cost_in_fused_ms": round(t_fused - t_base, 4)}), flush=True)
+        "lr_cost_in_fused_ms": round(t_fused - t_base, 4)}
 
 
 def paged(prc, w, dev, steps, warmup):
@@ -645,6 +647,7 @@ def paged(prc, w, dev, steps, warmup):
         return e0.elapsed_time(e1) / steps
 
     work = algorithmic_work(w)
+    recs = []
     for stage in ("decode", "prefill"):
         c = x["dec" if stage == "decode" else "pre"]
         O = torch.empty_like(c["Q"])
@@ -673,7 +676,7 @@ def paged(prc, w, dev, steps, warmup):
                 rec["hbm_frac_paged"] = round(work["decode_bytes"] / (t_p * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
             else:
                 rec["mfma_frac_paged"] = round(work["prefill_flops"] / (t_p * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)
-            print(json.dumps(rec), flush=True)
+            recs.append(rec)
             del Kp, Vp, Lkp, Lvp
 
     # Segment projection (base K/V + all agents' LR rows) into paged pools.
@@ -697,9 +700,12 @@ def paged(prc, w, dev, steps, warmup):
                                                                Lp, tbl, rope_theta=theta, tok_offset=S))
         rows = torch.arange(S, s_cap, device=dev)
         same = torch.equal(Kp[tbl[rows // blk].long(), rows % blk], K[S:])
-        print(json.dumps({"bench": "paged", "stage": "projection", "block_size": blk, "tokens": T,
-                          "ms_paged": round(t_p, 4), "ms_contiguous": round(t_c, 4),
-                          "paged_over_contiguous": round(t_p / t_c, 4), "bitwise_equal": bool(same)}), flush=True)
+        recs.append({"bench": "paged", "stage": "projection", "block_size": blk, "tokens": T,
+                     "ms_paged": round(t_p, 4), "ms_contiguous": round(t_c, 4),
+                     "paged_over_contiguous": round(t_p / t_c, 4), "bitwise_equal": bool(same)})
+        del Kp, Vp, Lp
+    del x
+    return recs
 
 
 def stack_bench(prc, dev):
@@ -886,7 +892,8 @@ def stack_bench(prc, dev):
     e1.record()
     torch.cuda.synchronize()
     append_us = e0.elapsed_time(e1) / (20 * n_layers) * 1e3
-    print(json.dumps({
+    del K, V, Lp, Kf, Vf
+    return {
         "bench": "workload", "index": 5, "workload": cfg.name,
         "shape": {"layers": n_layers, "hidden": hid, "n_q_heads": n_q, "n_kv_heads": n_kv, "head_dim": d,
                   "agents": N, "rank": r, "turns": turns, "turn_tokens": turn, "prefill_tokens": n_pre,
@@ -902,7 +909,7 @@ def stack_bench(prc, dev):
         "resident_gb": {"base_cache": round(2 * n_layers * S_cap * n_kv * d * 2 / 1e9, 2),
                         "lr_planes": round(n_layers * 2 * N * S_cap * r * 2 / 1e9, 2),
                         "materialised_copy": round(2 * n_layers * S_cap * n_kv * d * 2 / 1e9, 2)},
-    }), flush=True)
+    }
 
 
 def workload_bench(prc, index, dev, steps, warmup):
@@ -1009,6 +1016,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-materialize", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="leave out the rank sweep, shared-base decode, joined projection, paged caches and the "
+                         "32-layer stack from the default line")
     ap.add_argument("--no-workloads", action="store_true",
                     help="leave out the 8k (8B-shaped) and 64k (14B-shaped, rank 64) layers that the default run "
                          "times after the step")
@@ -1046,19 +1056,21 @@ def main():
     dev = torch.device("cuda:0")
     cfg, w = workload_dims()
     if args.rank_sweep:
-        rank_sweep(prc, w, dev, max(3, args.steps // 2), args.warmup)
+        for rec in rank_sweep(prc, w, dev, max(3, args.steps // 2), args.warmup):
+            print(json.dumps(rec), flush=True)
         return
     if args.shared_base:
-        shared_base_decode(prc, w, dev, args.steps, args.warmup)
+        print(json.dumps(shared_base_decode(prc, w, dev, args.steps, args.warmup)), flush=True)
         return
     if args.fused_projection:
-        fused_projection(prc, w, dev, args.steps, args.warmup)
+        print(json.dumps(fused_projection(prc, w, dev, args.steps, args.warmup)), flush=True)
         return
     if args.paged:
-        paged(prc, w, dev, args.steps, args.warmup)
+        for rec in paged(prc, w, dev, args.steps, args.warmup):
+            print(json.dumps(rec), flush=True)
         return
     if args.workload == 5:
-        stack_bench(prc, dev)
+        print(json.dumps(stack_bench(prc, dev)), flush=True)
         return
     if args.workload is not None:
         print(json.dumps(workload_bench(prc, args.workload, dev, args.steps, args.warmup)), flush=True)
@@ -1154,6 +1166,21 @@ def main():
             res["decode"]["frac_of_measured_read_ceiling"] = round(res["decode"]["gbs"] / ceil["gbs"], 4)
             out["workloads"][key] = res
             torch.cuda.empty_cache()
+    if not args.no_extras:
+        # The other measurements of the hot path, so that one default run
+        # carries them all: the rank sweep (both wirings), the shared-base
+        # decode, the joined projection, paged caches and the 32-layer stack.
+        steps_x = max(3, args.steps // 2)
+        extras = {}
+        for key, fn in (("rank_sweep", lambda: rank_sweep(prc, w, dev, steps_x, args.warmup)),
+                        ("shared_base_decode", lambda: shared_base_decode(prc, w, dev, steps_x, args.warmup)),
+                        ("fused_projection", lambda: fused_projection(prc, w, dev, steps_x, args.warmup)),
+                        ("paged", lambda: paged(prc, w, dev, steps_x, args.warmup)),
+                        ("stack_32_layers", lambda: stack_bench(prc, dev))):
+            print(f"bench: timing {key}", file=sys.stderr, flush=True)
+            extras[key] = fn()
+            torch.cuda.empty_cache()
+        out["extras"] = extras
     if not args.no_cpu_baseline:
         print("bench: timing the fp64 oracle on a host sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_budget)
