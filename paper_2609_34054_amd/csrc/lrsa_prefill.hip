@@ -128,6 +128,15 @@ __device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) | ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
 }
 
+// acc + both bf16 halves of w, in one dot-product instruction.  The row sums
+// then add up the same bf16-rounded P that the PV product weights the values
+// with.
+__device__ __forceinline__ float sum2_bf16(uint32_t w, float acc) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), ones, acc, false);
+}
+
 // Buffer resource over `bytes` bytes from `base`: loads at offsets at or past
 // the end return zeros (raw buffer, stride 0).
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base, int32_t bytes) {
@@ -619,8 +628,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
         for (int c = 0; c < 4; ++c) {
           const float p0 = fast_exp2(__builtin_fmaf(sh[tb][hf * 8 + 2 * c], a.scale_log2, -ms));
           const float p1 = fast_exp2(__builtin_fmaf(sh[tb][hf * 8 + 2 * c + 1], a.scale_log2, -ms));
-          if constexpr (!ones_sum) ls += p0 + p1;
           pw[c] = pack_bf16(p0, p1);
+          if constexpr (!ones_sum) ls = sum2_bf16(pw[c], ls);
         }
         const bf16x8 pb = as_bf16x8(pw);
 #pragma unroll
@@ -734,11 +743,11 @@ lrsa_prefill_kernel(const AttnArgs a) {
           for (int c = 0; c < 4; ++c) {
             const float p0 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c], a.scale_log2, -ms));
             const float p1 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c + 1], a.scale_log2, -ms));
-            if constexpr (!ones_sum) {
-              ls0 += p0;
-              ls1 += p1;
-            }
             pw[hf][c] = pack_bf16(p0, p1);
+            if constexpr (!ones_sum) {
+              if (c & 1) ls1 = sum2_bf16(pw[hf][c], ls1);
+              else ls0 = sum2_bf16(pw[hf][c], ls0);
+            }
           }
         if constexpr (!ones_sum) l_run += ls0 + ls1;
         // O^T[dims x rows] += V^T[dims x 16 tok] P^T[16 tok x rows] for the two
