@@ -46,6 +46,14 @@ CFLAGS = [
     f"-I{INCLUDE}",
     f"-I{CSRC}",
 ]
+# Per-source additions.  The decode kernels keep their MFMA accumulators in
+# architected VGPRs: the softmax rescale multiplies them on the vector ALU,
+# and with accumulators in AGPRs the compiler keeps a VGPR copy of each one,
+# refreshed after every MFMA (the rank-64 kernel carried 48 such copies and
+# about 50 accumulator moves per 16-token sub-block).
+SRC_FLAGS = {
+    "lrsa_decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
 
 
 def _hipcc() -> str:
@@ -57,7 +65,7 @@ def _hipcc() -> str:
 
 def _compile(src: str, hipcc: str, verbose: bool, checked: bool = False) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ("_checked" if checked else "") + ".o")
-    cmd = [hipcc, *CFLAGS, *(["-DPRC_DEVICE_CHECKS=1"] if checked else [])]
+    cmd = [hipcc, *CFLAGS, *SRC_FLAGS.get(src, []), *(["-DPRC_DEVICE_CHECKS=1"] if checked else [])]
     if src.endswith(".cpp"):
         cmd += ["-x", "hip"]
     cmd += ["-c", os.path.join(CSRC, src), "-o", obj]

@@ -102,6 +102,13 @@ __device__ __forceinline__ float sum16(float v) {
   v += shfl_xor(v, 8);
   return v;
 }
+// Combine lane l with lane l ^ 16 through v_permlane16_swap (no LDS trip):
+// with both operands x, the two results hold rows (0,1) and (2,3) of x in
+// swapped order, so combining them pairs every lane with its l ^ 16.
+__device__ __forceinline__ float max_xor16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
 // Combine lane l with lane l ^ 32 through v_permlane32_swap (no LDS trip).
 __device__ __forceinline__ float max_xor32(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);

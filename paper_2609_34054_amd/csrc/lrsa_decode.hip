@@ -22,7 +22,7 @@
 //      comes from 16x16 MFMAs (16x16x32 over 32-rank chunks for ranks 32 and
 //      64, 16x16x16 below) whose result layout holds both halves of every
 //      RoPE pair in one lane;
-//   2. online softmax per head (lane l%16), exp2 domain;
+//   2. online softmax per head (lane l%16), exp2 domain, lazily rescaled;
 //   3. O^T += V^T P^T and (P L_v)^T += L_v^T P^T on 16x16x16 MFMAs.  V and
 //      L_v rows pass through a wave-private LDS tile and come back through
 //      the transposing LDS read (ds_read_b64_tr_b16), so P, already in B
@@ -39,6 +39,7 @@ namespace {
 
 constexpr int TK = 32;        // tokens per KV tile (one LDS table, one barrier)
 constexpr int NSB = TK / 16;  // 16-token sub-blocks per tile
+constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (log2 domain)
 // Waves per workgroup (one KV head each).  Rank 64 keeps its B_k^T
 // fragments (64 VGPRs) in registers by running one wave per SIMD, which
 // gives each wave the whole register file (architected plus accumulation
@@ -376,32 +377,36 @@ lrsa_decode_kernel(const AttnArgs a) {
       // ---- online softmax: lane l%16 is a head, 4 tokens per lane ---------
       float s2[4];
       float mx = -INFINITY;
+      const int64_t left = t_end - ts;  // visible tokens from ts on
+      const int n_vis = left < 0 ? 0 : (left < 16 ? (int)left : 16);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        s2[i] = (ts + q * 4 + i < t_end) ? sc[i] * a.scale_log2 : -INFINITY;
+        s2[i] = (q * 4 + i < n_vis) ? sc[i] * a.scale_log2 : -INFINITY;
         mx = fmaxf(mx, s2[i]);
       }
-      mx = fmaxf(mx, shfl_xor(mx, 16));
-      mx = fmaxf(mx, shfl_xor(mx, 32));
-      const float mn = fmaxf(m_run, mx);
-      const float ms = (mn == -INFINITY) ? 0.f : mn;
-      const float alpha = fast_exp2(m_run - ms);
-      m_run = mn;
-      float p[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) p[i] = fast_exp2(s2[i] - ms);
-      l_part = l_part * alpha + (p[0] + p[1]) + (p[2] + p[3]);
-      u32x2 pw;
-      pw[0] = pack_bf16(p[0], p[1]);
-      pw[1] = pack_bf16(p[2], p[3]);
-      const i16x4 pb = as_i16x4(pw);
-      // Rescale only when some head's running max moved (exact either way).
-      if (__ballot(alpha != 1.f)) {
+      mx = max_xor32(max_xor16(mx));
+      // Lazy rescale: a head's reference maximum m_run only moves when a
+      // score exceeds it by more than 2^8 (P stays below 256), so the
+      // accumulators are rescaled a few times per split, not per sub-block.
+      if (__ballot(mx > m_run + kRescaleLog2)) {
+        const float mn = fmaxf(m_run, mx);
+        const float alpha = fast_exp2(m_run - (mn == -INFINITY ? 0.f : mn));
 #pragma unroll
         for (int blk = 0; blk < C::NBLK; ++blk) acc[blk] *= alpha;
 #pragma unroll
         for (int rc = 0; rc < C::RC; ++rc) accl[rc] *= alpha;
+        l_part *= alpha;
+        m_run = mn;
       }
+      const float ms = (m_run == -INFINITY) ? 0.f : m_run;
+      float p[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) p[i] = fast_exp2(s2[i] - ms);
+      l_part += (p[0] + p[1]) + (p[2] + p[3]);
+      u32x2 pw;
+      pw[0] = pack_bf16(p[0], p[1]);
+      pw[1] = pack_bf16(p[2], p[3]);
+      const i16x4 pb = as_i16x4(pw);
       __builtin_amdgcn_wave_barrier();
 
       // ---- O^T += V^T P^T, (P L_v)^T += L_v^T P^T -----------------------
@@ -784,31 +789,33 @@ lrsa_decode_shared_kernel(const AttnArgs a) {
         // ---- online softmax: lane l%16 is a head, 4 tokens per lane ---------
         float s2[4];
         float mx = -INFINITY;
+        const int64_t left = t_end - ts;  // visible tokens from ts on
+        const int n_vis = left < 0 ? 0 : (left < 16 ? (int)left : 16);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          s2[i] = (ts + q * 4 + i < t_end) ? sc[i] * a.scale_log2 : -INFINITY;
+          s2[i] = (q * 4 + i < n_vis) ? sc[i] * a.scale_log2 : -INFINITY;
           mx = fmaxf(mx, s2[i]);
         }
-        mx = fmaxf(mx, shfl_xor(mx, 16));
-        mx = fmaxf(mx, shfl_xor(mx, 32));
-        const float mn = fmaxf(m_run, mx);
-        const float ms = (mn == -INFINITY) ? 0.f : mn;
-        const float alpha = fast_exp2(m_run - ms);
-        m_run = mn;
-        float p[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) p[i] = fast_exp2(s2[i] - ms);
-        l_part = l_part * alpha + (p[0] + p[1]) + (p[2] + p[3]);
-        u32x2 pw;
-        pw[0] = pack_bf16(p[0], p[1]);
-        pw[1] = pack_bf16(p[2], p[3]);
-        const i16x4 pb = as_i16x4(pw);
-        if (__ballot(alpha != 1.f)) {
+        mx = max_xor32(max_xor16(mx));
+        if (__ballot(mx > m_run + kRescaleLog2)) {  // lazy rescale, as above
+          const float mn = fmaxf(m_run, mx);
+          const float alpha = fast_exp2(m_run - (mn == -INFINITY ? 0.f : mn));
 #pragma unroll
           for (int blk = 0; blk < C::NBLK; ++blk) acc[blk] *= alpha;
 #pragma unroll
           for (int rc = 0; rc < C::RC; ++rc) accl[rc] *= alpha;
+          l_part *= alpha;
+          m_run = mn;
         }
+        const float ms = (m_run == -INFINITY) ? 0.f : m_run;
+        float p[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) p[i] = fast_exp2(s2[i] - ms);
+        l_part += (p[0] + p[1]) + (p[2] + p[3]);
+        u32x2 pw;
+        pw[0] = pack_bf16(p[0], p[1]);
+        pw[1] = pack_bf16(p[2], p[3]);
+        const i16x4 pb = as_i16x4(pw);
         __builtin_amdgcn_wave_barrier();
         // ---- O^T += V^T P^T, (P L_v)^T += L_v^T P^T -----------------------
 #pragma unroll
