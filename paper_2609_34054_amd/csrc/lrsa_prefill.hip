@@ -567,13 +567,23 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // maximum and one (rare) rescale per tile, then a single straight-line
   // block that holds the exponentials and PV of both halves and the build of
   // the next tile, so that the compiler can interleave the build's vector
-  // work and transposes with the PV MFMAs.
+  // work and transposes with the PV MFMAs.  A wave raises its issue
+  // priority while it attends, so that when the two waves of a SIMD are in
+  // different parts of the tile the one with the MFMA-heavy work issues
+  // first.  With LR keys (a heavier build) the two waves also take the
+  // build and the attention in opposite order, as in the per-half loop.
   int tile = t_lo;
   const int main_end = n_full < t_hi ? n_full : t_hi;
   if constexpr (kMainLoop)
   for (; tile < main_end; ++tile) {
     const int buf = tile & 1;
     const int64_t t0 = (int64_t)tile * TKV;
+    const bool build_now = LK && build_first;
+    if (build_now) {
+      rebuild(u, buf ^ 1);
+      load_unit(u, t0 + 2 * TKV);
+    }
+    __builtin_amdgcn_s_setprio(1);
     bf16x8 kf[C::NKQ];
     auto k_frag = [&](int tb, int kk) {
       return as_bf16x8(*reinterpret_cast<const u32x4*>(k_lds[buf] + (tb * 32 + l32) * C::K_ROW + h32 * 8 + kk * 16));
@@ -641,10 +651,13 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
     }
     if constexpr (!ones_sum) l_run += ls;
+    __builtin_amdgcn_s_setprio(0);
     // Build tile + 1 and start the loads of tile + 2 (past the last tile this
     // writes a buffer no wave reads again and loads nothing).
-    rebuild(u, buf ^ 1);
-    load_unit(u, t0 + 2 * TKV);
+    if (!build_now) {
+      rebuild(u, buf ^ 1);
+      load_unit(u, t0 + 2 * TKV);
+    }
     base_angles(t0 + 2 * TKV, buf);
     __syncthreads();  // tile + 1 in LDS; tile consumed by every wave
   }
