@@ -124,11 +124,7 @@ __device__ __forceinline__ float readlane_f(float v, int lane) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// ---------------------------------------------------------------- RoPE ----
-// cos/sin of the angle pos * omega_j, where w2pi = omega_j / (2 pi) in fp64.
-// The angle is formed in fp64 revolutions, reduced to [0, 1) in fp64, and only
-// then rounded to fp32 for the hardware sin/cos (which take revolutions).  The
-// fp32 error stays near 1e-7 at every position below 2^31.
+// ----------------------------------------------------------- paged walk ----
 // Walks one request's rows of the block tables of paged caches in token
 // order, one tile of `step` tokens at a time (step divides the block size,
 // so no tile straddles two blocks).  A block's table entries are fetched
@@ -176,6 +172,11 @@ struct PageWalk {
   }
 };
 
+// ---------------------------------------------------------------- RoPE ----
+// cos/sin of the angle pos * omega_j, where w2pi = omega_j / (2 pi) in fp64.
+// The angle is formed in fp64 revolutions, reduced to [0, 1) in fp64, and only
+// then rounded to fp32 for the hardware sin/cos (which take revolutions).  The
+// fp32 error stays near 1e-7 at every position below 2^31.
 __device__ __forceinline__ void rope_cs(int pos, double w2pi, float& c, float& s) {
   double rev = (double)pos * w2pi;
   rev -= __builtin_floor(rev);
