@@ -571,14 +571,15 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // priority while it attends, so that when the two waves of a SIMD are in
   // different parts of the tile the one with the MFMA-heavy work issues
   // first.  With LR keys (a heavier build) the two waves also take the
-  // build and the attention in opposite order, as in the per-half loop.
+  // build and the attention in opposite order, as in the per-half loop
+  // (not over paged caches, where it measured slower).
   int tile = t_lo;
   const int main_end = n_full < t_hi ? n_full : t_hi;
   if constexpr (kMainLoop)
   for (; tile < main_end; ++tile) {
     const int buf = tile & 1;
     const int64_t t0 = (int64_t)tile * TKV;
-    const bool build_now = LK && build_first;
+    const bool build_now = LK && !PAGED && build_first;
     if (build_now) {
       rebuild(u, buf ^ 1);
       load_unit(u, t0 + 2 * TKV);
