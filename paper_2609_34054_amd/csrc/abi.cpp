@@ -435,17 +435,23 @@ PRC_API prc_status project_kv_and_lr_cache_paged(const uint16_t* X, int64_t T, i
 
 namespace {
 
-size_t workspace_size(const lrsa_dims* dims, bool paged) {
+size_t workspace_size(const lrsa_dims* dims, bool paged, bool tile_cache = true) {
   if (dims == nullptr || dims->n_tok < 1 || dims->batch < 1 || dims->n_kv_heads < 1 || dims->s_cap < 1 ||
       dims->n_q_heads < dims->n_kv_heads)
     return 0;
   const int r = rank_ok(dims->rank) ? dims->rank : 8;
   if (dims->n_tok > 1) {
     // Prefill: partials of a split over the KV tiles, when the call is too
-    // small to fill the GPU otherwise.
+    // small to fill the GPU otherwise; else, for calls with enough row tiles
+    // per KV head at rank 16, the tile cache (room is asked for whenever the
+    // rank is 16, since dims do not say whether the call brings L_k).
     int splits = 1, split_tiles = 0;
-    prc::prefill_plan(dims->n_tok, dims->n_q_heads / dims->n_kv_heads, dims->n_kv_heads, dims->batch, dims->s_cap,
-                      plan_cus(), &splits, &split_tiles);
+    const int group = dims->n_q_heads / dims->n_kv_heads;
+    prc::prefill_plan(dims->n_tok, group, dims->n_kv_heads, dims->batch, dims->s_cap, plan_cus(), &splits,
+                      &split_tiles);
+    if (tile_cache && !paged && rank_ok(dims->rank) &&
+        prc::prefill_uses_tile_cache(dims->n_tok, group, dims->head_dim, dims->rank, true, paged, splits))
+      return prc::prefill_tile_cache_bytes(dims->batch, dims->n_kv_heads, dims->s_cap);
     return prc::prefill_workspace_bytes(dims->batch, dims->n_tok, dims->n_q_heads, splits, dims->head_dim, r);
   }
   int n_splits = 0, split_tiles = 0;
@@ -501,6 +507,17 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
                   need);
     if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
     a.ws = static_cast<float*>(workspace);
+  } else if (prc::prefill_uses_tile_cache(a.n_tok, a.group, a.head_dim, a.rank, L_k != nullptr, pg != nullptr,
+                                          a.pf_splits)) {
+    // The tile cache is taken when the workspace has room for it (a smaller
+    // or absent workspace only means every workgroup rebuilds every tile).
+    const size_t need = prc::prefill_tile_cache_bytes(a.batch, a.n_kv, a.s_cap);
+    if (need > 0 && workspace != nullptr && workspace_bytes >= need && aligned(workspace, 256)) {
+      const size_t fb = prc::prefill_tile_cache_flag_bytes(a.batch, a.n_kv, a.s_cap);
+      a.tc_flags = static_cast<uint32_t*>(workspace);
+      a.tc_data = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + fb);
+      a.tc_tiles = (int32_t)((a.s_cap + 63) / 64);
+    }
   }
   int cus = 0;
   if (prc_status ds = device_ready(&cus)) return ds;
@@ -556,7 +573,8 @@ PRC_API prc_status lr_shared_attention_noalloc(const lrsa_dims* dims, const uint
   Checked c;
   prc_status s = check_attention(dims, Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len, true, nullptr, &c);
   if (s != PRC_OK || c.empty) return s;
-  const size_t need = workspace_size(dims, false);
+  // The split partials must fit; the tile cache is used when it fits too.
+  const size_t need = workspace_size(dims, false, false);
   if (need > kStaticWsBytes)
     return fail(PRC_EWORKSPACE, "the call needs %zu bytes of split partials, above the %zu-byte static workspace",
                 need, kStaticWsBytes);

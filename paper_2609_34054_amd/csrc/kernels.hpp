@@ -53,6 +53,13 @@ struct AttnArgs {
   int32_t split_tiles;  // decode: KV tiles per split
   int32_t pf_splits;    // prefill: KV splits per row tile (1: none)
   int32_t pf_split_tiles;  // prefill: 64-token KV tiles per split
+  // Prefill tile cache in the workspace (tc_data == nullptr: off).  The
+  // rebuilt K rows and V^T fragments of a full 64-token tile, in the LDS
+  // layout, in eight 4 KB parts (one per wave), [request][KV head][tile][part],
+  // beside one flag per part that turns nonzero once the part is published.
+  uint32_t* tc_flags;
+  uint32_t* tc_data;
+  int32_t tc_tiles;     // tiles per (request, KV head) slot
   float scale_log2;     // softmax scale * log2(e)
   double w2pi[kMaxHalfDim];  // RoPE omega_j / (2 pi), fp64
 };
@@ -78,6 +85,15 @@ hipError_t launch_split_merge(const AttnArgs& a, hipStream_t stream);
 void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int cus, int* splits,
                   int* split_tiles);
 size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int head_dim, int rank);
+// Whether a prefill call shares rebuilt tiles through the workspace tile
+// cache: unsplit, contiguous caches, d = 128, rank 16 with LR on the keys,
+// and enough row-tile workgroups per KV head (at least 16) for the reuse to
+// pay for the cache's writes (measured: a gain at rank 16 with k LR, a loss
+// at rank 64 and with LR on v only).  tile_cache_bytes: its size (flags,
+// then data).
+bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged, int splits);
+size_t prefill_tile_cache_bytes(int batch, int n_kv, int64_t s_cap);
+size_t prefill_tile_cache_flag_bytes(int batch, int n_kv, int64_t s_cap);
 hipError_t launch_prefill(const AttnArgs& a, hipStream_t stream);
 
 // Reference point: write the full per-agent K/V.

@@ -148,6 +148,11 @@ __device__ __forceinline__ u32x4 buf_ld16(__amdgpu_buffer_rsrc_t r, int32_t off)
 __device__ __forceinline__ u32x2 buf_ld8(__amdgpu_buffer_rsrc_t r, int32_t off) {
   return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
+// 16-byte store at device scope (sc1): written through to the memory side,
+// where workgroups on other XCDs read it.
+__device__ __forceinline__ void buf_st16_dev(u32x4 v, __amdgpu_buffer_rsrc_t r, int32_t off) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, off, 0, 16);
+}
 
 // Global data one wave stages for one KV tile.
 template <int D, int R>
@@ -163,7 +168,9 @@ struct Unit {
 
 // PAGED: the caches are pools reached through block tables (a separate
 // instantiation, so the contiguous kernel carries none of the walk's state).
-template <int D, int R, bool LK, bool LV, bool PAGED>
+// TCON: the instantiation that shares rebuilt tiles through the workspace
+// tile cache (launched only when the call has one).
+template <int D, int R, bool LK, bool LV, bool PAGED, bool TCON = false>
 __global__ void __launch_bounds__(NTHR)
 lrsa_prefill_kernel(const AttnArgs a) {
   using C = Pre<D, R>;
@@ -256,6 +263,32 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const uint16_t* Vb = a.Vb + (int64_t)b * a.kv_stride + (int64_t)g * D;
   const uint16_t* Lk = LK ? a.Lk + (int64_t)b * a.l_stride : nullptr;
   const uint16_t* Lv = LV ? a.Lv + (int64_t)b * a.l_stride : nullptr;
+
+  // ---- tile cache -------------------------------------------------------------
+  // Every full tile (all 64 rows below kv_hi) that a wave rebuilds is also
+  // stored, as the wave's 4 KB part of the tile in LDS layout, to this
+  // (request, KV head)'s slot of the workspace, and its flag is set once the
+  // stores have completed.  A wave that finds the flag of its part set loads
+  // the part instead of the raw rows and writes it to LDS unchanged: the
+  // bytes are those the rebuild would produce.  No wave ever waits for a
+  // flag, so there is no ordering between workgroups to deadlock on.  The
+  // workgroups of a KV head walk their unmasked tiles from staggered
+  // starting points, so each tile is mostly rebuilt once.  Flags are read
+  // and data written at device scope (other XCDs' L2s are not coherent);
+  // the data is read through L2, which holds no line of a part before its
+  // flag was seen set (the flags are cleared by a kernel before this one).
+  constexpr bool TC = TCON && LK && R == 16 && D == 128 && !PAGED;
+  constexpr bool tc_on = TC;
+  const int64_t tc_slot = ((int64_t)b * a.n_kv + g) * a.tc_tiles;  // first tile of the slot
+  // Buffer resources over the slot's flags and data; empty (loads read 0,
+  // stores are dropped) when the cache is off, so that every path issues
+  // the same memory instructions and the compiler's load counting stays
+  // exact.  Offset INT32_MIN is out of range: no access.
+  const __amdgpu_buffer_rsrc_t tc_frsrc = __builtin_amdgcn_make_buffer_rsrc(
+      tc_on ? a.tc_flags + tc_slot * NW : nullptr, (short)0, tc_on ? a.tc_tiles * NW * 4 : 0, 0x00020000);
+  const __amdgpu_buffer_rsrc_t tc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      tc_on ? a.tc_data + tc_slot * NW * 1024 : nullptr, (short)0, tc_on ? a.tc_tiles * NW * 4096 : 0, 0x00020000);
+  auto tc_off = [&](int T, int c) { return (T * NW + w) * 4096 + (c * 64 + lane) * 16; };
 
   // ---- build role: 16 tokens x SEG pair dims, 8 V rows, 8 L_v rows --------
   const int q = lane >> 4, c16 = lane & 15;
@@ -359,18 +392,21 @@ lrsa_prefill_kernel(const AttnArgs a) {
     }
   }
   // Tiles are loaded in token order, so paged caches are walked with them.
-  auto load_unit = [&](Unit<D, R>& u, int64_t t0) {
+  // `cached`: the tile's part comes from the tile cache instead (its K and V
+  // loads are pointed there, the L_k / L_v loads at empty resources).
+  auto load_unit = [&](Unit<D, R>& u, int64_t t0, bool cached, int T) {
     // Valid rows of this tile; a tile at or past kv_hi gets empty resources
     // (its loads return zeros).
     const int64_t left = kv_hi - t0;
-    const int rows = (int)(left < TKV ? (left > 0 ? left : 0) : TKV);
+    const int rows = cached ? 0 : (int)(left < TKV ? (left > 0 ? left : 0) : TKV);
     const int32_t kv_bytes = rows > 0 ? (rows - 1) * (int32_t)(row_el * 2) + D * 2 : 0;
     int64_t kr = t0, lr = t0;  // cache rows of the tile's first token
     if constexpr (PAGED) walk.next(TKV, kv_hi, kr, lr);
-    const auto rk = make_rsrc(Kb + kr * row_el, kv_bytes);
-    const auto rv = make_rsrc(Vb + kr * row_el, kv_bytes);
+    const auto rk = cached ? tc_rsrc : make_rsrc(Kb + kr * row_el, kv_bytes);
+    const auto rv = cached ? tc_rsrc : make_rsrc(Vb + kr * row_el, kv_bytes);
     if constexpr (C::SEG == 8) {
-      const u32x4 lo = buf_ld16(rk, offk), hi = buf_ld16(rk, offk + C::HALF * 2);
+      const u32x4 lo = buf_ld16(rk, cached ? tc_off(T, 0) : offk);
+      const u32x4 hi = buf_ld16(rk, cached ? tc_off(T, 1) : offk + C::HALF * 2);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         u.klo.w[i] = lo[i];
@@ -395,7 +431,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
     }
 #pragma unroll
-    for (int hb = 0; hb < C::NHB; ++hb) u.v[hb] = buf_ld16(rv, offv[hb]);
+    for (int hb = 0; hb < C::NHB; ++hb) u.v[hb] = buf_ld16(rv, cached ? tc_off(T, 2 + hb) : offv[hb]);
     if constexpr (LVA) {
       const auto rl = make_rsrc(Lv + lr * R, rows * R * 2);
 #pragma unroll
@@ -407,54 +443,70 @@ lrsa_prefill_kernel(const AttnArgs a) {
       for (int kc = 0; kc < R / 16; ++kc) u.lvv[kc] = buf_ld16(rl, offlvv[kc]);
     }
   };
+  // Tile-cache state of this wave: whether u holds a cached part (and of
+  // which tile), and the tile whose part was stored but not yet flagged.
+  bool u_cached = false;
+  int u_tile = 0, pub_tile = -1;
+  uint32_t fl_next = 0;  // flag of the tile fetched next (read a fetch ahead)
+  auto publish = [&]() {
+    // vmcnt(0): the part's stores have completed (issued a tile ago; the
+    // loads this build consumes are waited for here anyway).  Then the flag,
+    // at device scope, from every lane (same address, same value).
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __builtin_amdgcn_raw_buffer_store_b32(1u, tc_frsrc, pub_tile >= 0 ? (pub_tile * NW + w) * 4 : INT32_MIN, 0, 16);
+    pub_tile = -1;
+  };
   auto rebuild = [&](const Unit<D, R>& u, int buf) {
+    if constexpr (TC) publish();  // the previous part: its stores were issued a tile ago
     Seg<C::SEG> lo = u.klo, hi = u.khi;
-    if constexpr (LK) {
+    // With the cache, a cached part skips the rebuild: u holds the K rows of
+    // this lane's token and its two V^T fragments as the rebuild makes them.
+    const bool compute = !(TC && u_cached);
+    u32x4 fv[2] = {u.v[0], u.v[C::NHB - 1]};
+    if (compute) {
+      if constexpr (LK) {
 #pragma unroll
-      for (int i = 0; i < C::NBW; ++i) {
-        f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
-        Frag fl[C::NC], fh[C::NC];
-        bk_set(i, fl);
-        bk_set(C::NBW + i, fh);
+        for (int i = 0; i < C::NBW; ++i) {
+          f32x4 elo = {0.f, 0.f, 0.f, 0.f}, ehi = {0.f, 0.f, 0.f, 0.f};
+          Frag fl[C::NC], fh[C::NC];
+          bk_set(i, fl);
+          bk_set(C::NBW + i, fh);
 #pragma unroll
-        for (int c = 0; c < C::NC; ++c) {
-          elo = Ex<R>::mma(fl[c], u.lk[c], elo);
-          ehi = Ex<R>::mma(fh[c], u.lk[c], ehi);
-        }
-        float vlo[4], vhi[4];
-        float cd[4], sd[4];
-        if constexpr (C::OCS_REG) {
+          for (int c = 0; c < C::NC; ++c) {
+            elo = Ex<R>::mma(fl[c], u.lk[c], elo);
+            ehi = Ex<R>::mma(fh[c], u.lk[c], ehi);
+          }
+          float vlo[4], vhi[4];
+          float cd[4], sd[4];
+          if constexpr (C::OCS_REG) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              cd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] & 0xFFFFu));
+              sd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] >> 16));
+            }
+          } else {
+            const f32x4 od0 = off_cs[w][2 * i][lane], od1 = off_cs[w][2 * i + 1][lane];
+            cd[0] = od0[0], cd[1] = od0[2], cd[2] = od1[0], cd[3] = od1[2];
+            sd[0] = od0[1], sd[1] = od0[3], sd[2] = od1[1], sd[3] = od1[3];
+          }
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
-            cd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] & 0xFFFFu));
-            sd[j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(ocs[4 * i + j] >> 16));
+            const int e = 4 * i + j;
+            const float2 bc = base_cs[buf][lo_dim0 + e];
+            const float c = bc.x * cd[j] - bc.y * sd[j];
+            const float s = bc.y * cd[j] + bc.x * sd[j];
+            vlo[j] = seg_get(u.klo, e) + elo[j] * c - ehi[j] * s;
+            vhi[j] = seg_get(u.khi, e) + ehi[j] * c + elo[j] * s;
           }
-        } else {
-          const f32x4 od0 = off_cs[w][2 * i][lane], od1 = off_cs[w][2 * i + 1][lane];
-          cd[0] = od0[0], cd[1] = od0[2], cd[2] = od1[0], cd[3] = od1[2];
-          sd[0] = od0[1], sd[1] = od0[3], sd[2] = od1[1], sd[3] = od1[3];
+          lo.w[2 * i] = pack_bf16(vlo[0], vlo[1]);
+          lo.w[2 * i + 1] = pack_bf16(vlo[2], vlo[3]);
+          hi.w[2 * i] = pack_bf16(vhi[0], vhi[1]);
+          hi.w[2 * i + 1] = pack_bf16(vhi[2], vhi[3]);
         }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int e = 4 * i + j;
-          const float2 bc = base_cs[buf][lo_dim0 + e];
-          const float c = bc.x * cd[j] - bc.y * sd[j];
-          const float s = bc.y * cd[j] + bc.x * sd[j];
-          vlo[j] = seg_get(u.klo, e) + elo[j] * c - ehi[j] * s;
-          vhi[j] = seg_get(u.khi, e) + ehi[j] * c + elo[j] * s;
-        }
-        lo.w[2 * i] = pack_bf16(vlo[0], vlo[1]);
-        lo.w[2 * i + 1] = pack_bf16(vlo[2], vlo[3]);
-        hi.w[2 * i] = pack_bf16(vhi[0], vhi[1]);
-        hi.w[2 * i + 1] = pack_bf16(vhi[2], vhi[3]);
       }
-    }
-    st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + lo_dim0, lo);
-    st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + C::HALF + lo_dim0, hi);
-    {
-      // Transpose the V half blocks on the MFMA and store them as fragments
-      // (2 vtb, vdb) and (2 vtb + 1, vdb); from rank 16 on the transpose
-      // accumulates onto L_v B_v of the same tokens and dims.
+      // Transpose the V half blocks on the MFMA into fragments (2 vtb, vdb)
+      // and (2 vtb + 1, vdb); from rank 16 on the transpose accumulates onto
+      // L_v B_v of the same tokens and dims.
       f32x16 t;
 #pragma unroll
       for (int j = 0; j < 16; ++j) t[j] = 0.f;
@@ -464,17 +516,29 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
 #pragma unroll
       for (int hb = 0; hb < C::NHB; ++hb) t = mfma32x32x16(as_bf16x8(u.v[hb]), as_bf16x8(vid[vp0 + hb]), t);
-      // With one half block per wave (d = 64) the wave owns only its 16 dims
-      // of each fragment; the other half's lanes are written by another wave.
-      if (C::NHB == 2 || (lane & 31) / 16 == vp0) {
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          u32x4 f;
+      for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-          for (int c = 0; c < 4; ++c) f[c] = pack_bf16(t[8 * hf + 2 * c], t[8 * hf + 2 * c + 1]);
-          *reinterpret_cast<u32x4*>(v_lds[buf] + (((2 * vtb + hf) * C::NDB + vdb) * 64 + lane) * 8) = f;
-        }
-      }
+        for (int c = 0; c < 4; ++c) fv[hf][c] = pack_bf16(t[8 * hf + 2 * c], t[8 * hf + 2 * c + 1]);
+    }
+    st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + lo_dim0, lo);
+    st_seg<C::SEG>(k_lds[buf] + delta * C::K_ROW + C::HALF + lo_dim0, hi);
+    // With one half block per wave (d = 64) the wave owns only its 16 dims
+    // of each fragment; the other half's lanes are written by another wave.
+    if (C::NHB == 2 || (lane & 31) / 16 == vp0) {
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf)
+        *reinterpret_cast<u32x4*>(v_lds[buf] + (((2 * vtb + hf) * C::NDB + vdb) * 64 + lane) * 8) = fv[hf];
+    }
+    if constexpr (TC) {
+      // A full tile rebuilt here goes to the cache too (flagged at the next
+      // build); the stores are issued on every path, out of range when not.
+      const bool store_part = compute && tc_on && (u_tile + 1) * TKV <= kv_hi;
+      buf_st16_dev(u32x4{lo.w[0], lo.w[1], lo.w[2], lo.w[3]}, tc_rsrc, store_part ? tc_off(u_tile, 0) : INT32_MIN);
+      buf_st16_dev(u32x4{hi.w[0], hi.w[1], hi.w[2], hi.w[3]}, tc_rsrc, store_part ? tc_off(u_tile, 1) : INT32_MIN);
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) buf_st16_dev(fv[hf], tc_rsrc, store_part ? tc_off(u_tile, 2 + hf) : INT32_MIN);
+      if (store_part) pub_tile = u_tile;
     }
     if (LVA && lv_wave) {
       // L_v^T fragments (2 ltb + hf, lrb).  With rank < 32, rank row `rank`
@@ -548,18 +612,45 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // workgroup is laid out) take the two jobs in opposite order.
   const bool build_first = ((w >> 2) ^ w) & 1;
 
+  // Tiles are walked as a sequence k = t_lo .. t_hi - 1, LDS buffer k & 1.
+  // With the tile cache the unmasked tiles [0, n_rot) are walked from a
+  // starting point staggered over the row tiles of the KV head (the online
+  // softmax does not depend on the order), the rest in order.
+  const int n_rot = tc_on ? (n_full_raw < t_hi ? n_full_raw : t_hi) : 0;
+  const int rot = n_rot > 0 ? (int)(((int64_t)rtile * n_rot) / gridDim.x) : 0;
+  auto tile_at = [&](int k) {
+    if (k >= n_rot) return k;
+    const int t = k + rot;
+    return t >= n_rot ? t - n_rot : t;
+  };
+  // Loads of sequence step k into u: its cached part if the flag read one
+  // fetch earlier says it is published, else the raw rows.  The flag of the
+  // next step's tile is read here for the next fetch.
+  Unit<D, R> u;
+  auto fetch = [&](int k) {
+    const int T = tile_at(k);
+    bool cached = false;
+    if constexpr (TC) {
+      cached = tc_on && __builtin_amdgcn_readfirstlane(fl_next) != 0;
+      u_cached = cached;
+      u_tile = T;
+      const int Tn = tile_at(k + 1);
+      fl_next = __builtin_amdgcn_raw_buffer_load_b32(tc_frsrc, Tn < n_tiles ? (Tn * NW + w) * 4 : INT32_MIN, 0, 16);
+    }
+    load_unit(u, (int64_t)T * TKV, cached, T);
+  };
+
   // Prologue: the first tile into its LDS buffer (tile parity), the next in
   // flight.
-  Unit<D, R> u;
   if (t_lo < t_hi) {
-    load_unit(u, (int64_t)t_lo * TKV);
-    base_angles((int64_t)t_lo * TKV, t_lo & 1);
+    fetch(t_lo);
+    base_angles((int64_t)tile_at(t_lo) * TKV, t_lo & 1);
   }
   __syncthreads();
   if (t_lo < t_hi) rebuild(u, t_lo & 1);
   if (t_lo + 1 < t_hi) {
-    load_unit(u, (int64_t)(t_lo + 1) * TKV);
-    base_angles((int64_t)(t_lo + 1) * TKV, (t_lo + 1) & 1);
+    fetch(t_lo + 1);
+    base_angles((int64_t)tile_at(t_lo + 1) * TKV, (t_lo + 1) & 1);
   }
   __syncthreads();
 
@@ -573,16 +664,15 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // first.  With LR keys (a heavier build) the two waves also take the
   // build and the attention in opposite order, as in the per-half loop
   // (not over paged caches, where it measured slower).
-  int tile = t_lo;
+  int tile = t_lo;  // sequence step (the tile itself is tile_at(tile))
   const int main_end = n_full < t_hi ? n_full : t_hi;
   if constexpr (kMainLoop)
   for (; tile < main_end; ++tile) {
     const int buf = tile & 1;
-    const int64_t t0 = (int64_t)tile * TKV;
     const bool build_now = LK && !PAGED && build_first;
     if (build_now) {
       rebuild(u, buf ^ 1);
-      load_unit(u, t0 + 2 * TKV);
+      fetch(tile + 2);
     }
     __builtin_amdgcn_s_setprio(1);
     bf16x8 kf[C::NKQ];
@@ -657,21 +747,21 @@ lrsa_prefill_kernel(const AttnArgs a) {
     // writes a buffer no wave reads again and loads nothing).
     if (!build_now) {
       rebuild(u, buf ^ 1);
-      load_unit(u, t0 + 2 * TKV);
+      fetch(tile + 2);
     }
-    base_angles(t0 + 2 * TKV, buf);
+    base_angles((int64_t)tile_at(tile + 2) * TKV, buf);
     __syncthreads();  // tile + 1 in LDS; tile consumed by every wave
   }
 
   // Tiles that cross some row's causal limit.
   for (; tile < t_hi; ++tile) {
     const int buf = tile & 1;
-    const int64_t t0 = (int64_t)tile * TKV;
-    // Build tile + 1 (its data arrived during the previous tile) and start
-    // the loads of tile + 2.
+    const int64_t t0 = (int64_t)tile_at(tile) * TKV;
+    // Build step + 1 (its data arrived during the previous step) and start
+    // the loads of step + 2.
     auto build = [&]() {
       if (tile + 1 < t_hi) rebuild(u, buf ^ 1);
-      if (tile + 2 < t_hi) load_unit(u, t0 + 2 * TKV);
+      if (tile + 2 < t_hi) fetch(tile + 2);
     };
     if (build_first) build();
     if (t0 <= (int64_t)wave_last) {
@@ -779,9 +869,11 @@ lrsa_prefill_kernel(const AttnArgs a) {
       }
     }
     if (!build_first) build();
-    if (tile + 2 < t_hi) base_angles(t0 + 2 * TKV, buf);
+    if (tile + 2 < t_hi) base_angles((int64_t)tile_at(tile + 2) * TKV, buf);
     __syncthreads();  // tile + 1 in LDS; tile consumed by every wave
   }
+
+  if constexpr (TC) publish();  // the last part this wave stored
 
   // Row sum: from the ones row of (P L_v)^T (row R: register 4 (R/8) + R%4 of
   // block 0 in lanes (R%8)/4*32 .. +31), else from the per-lane partial sums.
@@ -876,8 +968,14 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const dim3 grid(tiles, a.n_kv * nsp, a.batch);
   if (a.kv_tbl != nullptr)
     hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, true>), grid, dim3(NTHR), 0, st, a);
-  else
+  else if constexpr (LK && R == 16 && D == 128) {
+    if (a.tc_data != nullptr)
+      hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, false, true>), grid, dim3(NTHR), 0, st, a);
+    else
+      hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, false>), grid, dim3(NTHR), 0, st, a);
+  } else {
     hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, false>), grid, dim3(NTHR), 0, st, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || nsp == 1) return e;
   AttnArgs m = a;
@@ -949,7 +1047,43 @@ size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int he
   return (size_t)batch * n_tok * n_q * splits * (4 + head_dim + rank) * sizeof(float);
 }
 
+bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged, int splits) {
+  const int64_t row_tiles = ((int64_t)n_tok * group + BROWS - 1) / BROWS;
+  return has_lk && !paged && splits <= 1 && head_dim == 128 && rank == 16 && row_tiles >= 16;
+}
+
+namespace {
+int64_t tc_slot_tiles(int64_t s_cap) { return (s_cap + TKV - 1) / TKV; }
+}  // namespace
+
+size_t prefill_tile_cache_flag_bytes(int batch, int n_kv, int64_t s_cap) {
+  const size_t flags = (size_t)batch * n_kv * tc_slot_tiles(s_cap) * NW * sizeof(uint32_t);
+  return (flags + 255) / 256 * 256;
+}
+
+size_t prefill_tile_cache_bytes(int batch, int n_kv, int64_t s_cap) {
+  // Flags, then 32 KB of rebuilt K and V^T per tile.  A slot is addressed
+  // with 32-bit offsets, so it must stay under 2 GB (s_cap < 4M tokens).
+  if (tc_slot_tiles(s_cap) * NW * 4096 >= ((int64_t)1 << 31)) return 0;
+  return prefill_tile_cache_flag_bytes(batch, n_kv, s_cap) +
+         (size_t)batch * n_kv * tc_slot_tiles(s_cap) * NW * 4096;
+}
+
+namespace {
+// Clears the tile cache's flags (a kernel, not a memset, so that the call can
+// be captured into a graph).
+__global__ void __launch_bounds__(256) tc_clear_kernel(uint32_t* flags, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (int64_t)gridDim.x * 256) flags[i] = 0u;
+}
+}  // namespace
+
 hipError_t launch_prefill(const AttnArgs& a, hipStream_t st) {
+  if (a.tc_data != nullptr) {
+    const int64_t n = (int64_t)a.batch * a.n_kv * a.tc_tiles * NW;
+    const int64_t blocks = (n + 255) / 256;
+    hipLaunchKernelGGL(tc_clear_kernel, dim3((unsigned)(blocks < 1024 ? blocks : 1024)), dim3(256), 0, st, a.tc_flags, n);
+    if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
+  }
   if (a.head_dim == 64) return launch_r<64>(a, st);
   if (a.head_dim == 128) return launch_r<128>(a, st);
   return hipErrorInvalidValue;

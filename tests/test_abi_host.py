@@ -277,10 +277,18 @@ def test_decode_workspace_query_and_check():
     d = _dims(n_tok=1)
     need = L.lr_shared_attention_workspace_size(ctypes.byref(d))
     assert need > 0
-    # Prefill needs no workspace when one pass per KV head already fills the
-    # chip (4096 queries, 8 KV heads) or the context is a handful of tiles.
-    assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=4096, batch=1, s_cap=36864))) == 0
+    # Prefill needs no split partials when one pass per KV head already fills
+    # the chip (4096 queries, 8 KV heads) or the context is a handful of
+    # tiles.  With an LR rank and 64 row tiles per KV head the query asks for
+    # the optional tile cache instead: one flag per wave and tile, then 32 KB
+    # of rebuilt K and V^T per tile (576 tiles x 8 KV heads).
+    tiles = 36864 // 64
+    cache = -(-(8 * tiles * 8 * 4) // 256) * 256 + 8 * tiles * 32768
+    assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=4096, batch=1, s_cap=36864))) == cache
+    # No LR rank (plain attention), few row tiles, or paged caches: no cache.
+    assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=4096, batch=1, s_cap=36864, rank=0))) == 0
     assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=8, s_cap=256))) == 0
+    assert L.lr_shared_attention_paged_workspace_size(ctypes.byref(_dims(n_tok=4096, batch=1, s_cap=36864))) == 0
     assert _attn(d, ws=None) == EWS
     assert _attn(d, ws=A16, ws_bytes=need - 1) == EWS
     assert _attn(d, ws=A16 + 4, ws_bytes=need) == EALIGN
@@ -409,10 +417,11 @@ def test_prefill_split_count(n_tok, n_q, s_cap, splits):
     """The prefill split count minimises ceil(units * ns / 256) / ns over
     ns in 1..8 (splits at least 8 tiles), smallest on ties, and splits only
     when that gains at least 10% over one pass; the workspace query reports
-    one fp32 partial per row and split."""
+    one fp32 partial per row and split.  (The paged query: the same plan,
+    without the optional tile cache that unsplit contiguous calls ask for.)"""
     d = _dims(batch=1, n_tok=n_tok, n_q_heads=n_q, n_kv_heads=8, s_cap=s_cap, kv_req_stride=0, l_req_stride=0,
               b_req_stride=0)
-    need = prc.lib().lr_shared_attention_workspace_size(ctypes.byref(d))
+    need = prc.lib().lr_shared_attention_paged_workspace_size(ctypes.byref(d))
     assert need == (0 if splits == 1 else n_tok * n_q * splits * (4 + 128 + 16) * 4)
 
 

@@ -1,0 +1,75 @@
+"""The prefill tile cache: rebuilt K/V tiles published in the workspace and
+reused by the other row-tile workgroups of a KV head.  Large unsplit rank-16
+prefills with LR on the keys take it when the workspace has room; the cached
+bytes are the ones a rebuild produces, so a call must give the same result
+whether a tile was rebuilt or loaded, whatever the workspace held before,
+and must match the fp64 oracle (Sec. 3.1: K = K_base + RoPE(L_k B_k),
+V = V_base + L_v B_v).  Wirings that do not take the cache run the same
+checks (the workspace is then unused)."""
+import ctypes
+
+import pytest
+import torch
+
+from gpu_cases import ATOL_MAX, ATOL_MEAN, LSE_ATOL, attn_errors, lse_error, oracle_attention, to_dev
+from paper_2609_34054_amd.binding import lib, make_dims
+from workload import Config, attention_case
+
+pytestmark = pytest.mark.gpu
+
+
+def _p(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _call(dims, g, ws):
+    O = torch.full_like(g["Q"], float("nan"))
+    lse = torch.full(g["Q"].shape[:3], float("nan"), dtype=torch.float32, device="cuda")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    st = lib().lr_shared_attention(ctypes.byref(dims), _p(g["Q"]), _p(g["K_base"]), _p(g["V_base"]), _p(g["L_k"]),
+                                   _p(g["L_v"]), _p(g["B_k"]), _p(g["B_v"]), _p(g["positions"]),
+                                   _p(g["kv_len"]), _p(O), _p(lse), _p(ws),
+                                   0 if ws is None else ws.numel(), stream)
+    assert st == 0, lib().prc_last_error()
+    torch.cuda.synchronize()
+    return O, lse
+
+
+# (id, rank, LR on k, LR on v): 1024 queries x 4 heads = 16 row tiles per KV
+# head, two requests with ragged lengths (partial last tiles, separate slots).
+# The first two take the cache.
+CASES = [("kv_r16", 16, True, True), ("k_r16", 16, True, False), ("qv_r16", 16, False, True),
+         ("kv_r64", 64, True, True)]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_tile_cache_matches_rebuild_and_oracle(case):
+    cid, r, lk, lv = case
+    print(f"tile cache {cid}", flush=True)
+    cfg = Config(95, "tile cache", hidden=256, n_q=32, n_kv=8, head_dim=128, theta=5e5, n_agents=1, rank=r,
+                 context=0, prefill_tokens=0, decode_batch=0, precompute_rows=0)
+    n_tok, kv_lens, s_cap = 1024, [5000, 4100], 5120
+    pos = [list(range(k - n_tok, k)) for k in kv_lens]
+    c = attention_case(cfg, batch=2, n_tok=n_tok, kv_len=kv_lens, positions=pos, s_cap=s_cap, lr_k=lk, lr_v=lv,
+                       seed_base=7 * r + lk)
+    g = to_dev(c)
+    dims = make_dims(g["Q"], g["K_base"], g["L_k"], g["L_v"], g["B_k"], g["B_v"], cfg.theta)
+    need = lib().lr_shared_attention_workspace_size(ctypes.byref(dims))
+    if r == 16:
+        assert need >= 2 * 8 * (s_cap // 64) * 32768  # the cache is asked for
+    need = max(need, 16)
+    # A workspace full of garbage (every flag nonzero) must not be trusted,
+    # and a second call over the first call's cache must give the same bytes.
+    ws = torch.full((need,), 0xFF, dtype=torch.uint8, device="cuda")
+    O1, l1 = _call(dims, g, ws)
+    O2, l2 = _call(dims, g, ws)
+    assert torch.equal(O1, O2) and torch.equal(l1, l2)
+    # Without a workspace every workgroup rebuilds every tile (in order).
+    O0, l0 = _call(dims, g, None)
+    assert (O1.float() - O0.float()).abs().max().item() <= ATOL_MAX
+    toks = [0, 1, 255, 256, 511, 700, 1023]
+    Oref, lref = oracle_attention(c, cfg.theta, toks=toks)
+    for O, lse in ((O1, l1), (O0, l0)):
+        mx, mean = attn_errors(O[:, toks], Oref)
+        assert mx <= ATOL_MAX and mean <= ATOL_MEAN, (cid, mx, mean)
+        assert lse_error(lse[:, toks], lref) <= LSE_ATOL
