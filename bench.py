@@ -137,6 +137,11 @@ def run_fused(prc, x, w, steps, warmup):
     dims = prc.make_dims(x["dec"]["Q"], x["dec"]["K_base"], x["dec"]["L_k"], x["dec"]["L_v"], x["dec"]["B_k"],
                          x["dec"]["B_v"], theta)
     ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=O_dec.device)
+    # The prefill's workspace (its tile cache), allocated once outside the
+    # timed region like the decode's.
+    dims_pre = prc.make_dims(x["pre"]["Q"], x["pre"]["K_base"], x["pre"]["L_k"], x["pre"]["L_v"], x["pre"]["B_k"],
+                             x["pre"]["B_v"], theta)
+    ws_pre = torch.empty(max(1, prc.workspace_size(dims_pre)), dtype=torch.uint8, device=O_dec.device)
 
     def step(i, ev=None):
         if ev is not None:
@@ -144,7 +149,7 @@ def run_fused(prc, x, w, steps, warmup):
         prc.precompute_lr_cache(x["X"][i % 4], x["A_stack"], 2, w["N"], w["r"], x["L_planes"], tok_offset=w["S"])
         if ev is not None:
             ev[1].record()
-        attn(prc, x["pre"], theta, O_pre, None)
+        attn(prc, x["pre"], theta, O_pre, ws_pre)
         if ev is not None:
             ev[2].record()
         attn(prc, x["dec"], theta, O_dec, ws)
@@ -485,7 +490,10 @@ def rank_sweep(prc, w, dev, steps, warmup):
         cd = cases["dec"]
         dims = prc.make_dims(cd["Q"], cd["K_base"], cd["L_k"], cd["L_v"], cd["B_k"], cd["B_v"], w["theta"])
         ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
-        t_pre = timed(lambda: attn(prc, cases["pre"], w["theta"], O_pre, None))
+        cp = cases["pre"]
+        dims_p = prc.make_dims(cp["Q"], cp["K_base"], cp["L_k"], cp["L_v"], cp["B_k"], cp["B_v"], w["theta"])
+        ws_p = torch.empty(max(1, prc.workspace_size(dims_p)), dtype=torch.uint8, device=dev)
+        t_pre = timed(lambda: attn(prc, cases["pre"], w["theta"], O_pre, ws_p))
         t_dec = timed(lambda: attn(prc, cases["dec"], w["theta"], O_dec, ws))
         work = algorithmic_work(dict(w, r=r), lk, lv)
         pre_tf = work["prefill_flops"] / (t_pre * 1e-3) / 1e12
