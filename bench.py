@@ -123,10 +123,10 @@ def make_inputs(w, dev, seed=3000):
 
 
 # ------------------------------------------------------------ GPU timing loop
-def attn(prc, c, theta, O, ws):
+def attn(prc, c, theta, O, ws, tile_cache=True):
     return prc.lr_shared_attention(c["Q"], c["K_base"], c["V_base"], c["L_k"], c["L_v"], c["B_k"],
                                    c["B_v"], c["positions"], c["kv_len"], rope_theta=theta, O=O,
-                                   workspace=ws)
+                                   workspace=ws, tile_cache=tile_cache)
 
 
 def run_fused(prc, x, w, steps, warmup):
@@ -662,7 +662,12 @@ def paged(prc, w, dev, steps, warmup):
         O2 = torch.empty_like(c["Q"])
         dims = prc.make_dims(c["Q"], c["K_base"], c["L_k"], c["L_v"], c["B_k"], c["B_v"], theta)
         ws = torch.empty(max(1, prc.workspace_size(dims)), dtype=torch.uint8, device=dev)
-        t_c = timeit(lambda: attn(prc, c, theta, O, ws))
+        # Paged calls take no tile cache: the contiguous reference runs without
+        # it too (same tile order, so the results must be bitwise equal), and
+        # with it for the record.
+        t_c = timeit(lambda: attn(prc, c, theta, O, ws, tile_cache=False))
+        t_ctc = timeit(lambda: attn(prc, c, theta, O2, ws))
+        attn(prc, c, theta, O, ws, tile_cache=False)
         S = c["K_base"].shape[1]
         for blk in (64, 256):
             if S % blk:
@@ -679,7 +684,8 @@ def paged(prc, w, dev, steps, warmup):
             t_p = timeit(run)
             rec = {"bench": "paged", "stage": stage, "block_size": blk, "requests": B, "context": S,
                    "ms_paged": round(t_p, 4), "ms_contiguous": round(t_c, 4),
-                   "paged_over_contiguous": round(t_p / t_c, 4), "bitwise_equal": bool(torch.equal(O, O2))}
+                   "paged_over_contiguous": round(t_p / t_c, 4), "bitwise_equal": bool(torch.equal(O, O2)),
+                   "ms_contiguous_tile_cache": round(t_ctc, 4)}
             if stage == "decode":
                 rec["hbm_frac_paged"] = round(work["decode_bytes"] / (t_p * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)
             else:

@@ -14,6 +14,7 @@ from .binding import (  # noqa: F401
     lr_shared_attention_noalloc,
     lr_shared_attention_paged,
     make_dims,
+    paged_workspace_size,
     materialize_agent_kv,
     precompute_lr_cache,
     project_kv_and_lr_cache,

@@ -277,14 +277,21 @@ def workspace_size(dims: LrsaDims) -> int:
     return int(lib().lr_shared_attention_workspace_size(ctypes.byref(dims)))
 
 
+def paged_workspace_size(dims: LrsaDims) -> int:
+    return int(lib().lr_shared_attention_paged_workspace_size(ctypes.byref(dims)))
+
+
 def lr_shared_attention(Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len, *, rope_theta: float,
                         softmax_scale: float = 0.0, O=None, lse=None, want_lse: bool = False,
-                        workspace=None, stream=None):
+                        workspace=None, tile_cache: bool = True, stream=None):
     """Attention over the shared base cache plus one agent's LR cache (Sec. 3.1).
 
     Shapes: ``Q [B, n_tok, n_q, d]``; ``K_base, V_base [B|1, s_cap, n_kv, d]``;
     ``L_k, L_v [B|1, s_cap, r]`` or None; ``B_k, B_v [B|1, r, n_kv*d]`` or None
     (Eq. 1 orientation); ``positions [B, n_tok]`` and ``kv_len [B]`` int32.
+    A workspace is allocated when none (or too small a one) is given; with
+    ``tile_cache=False`` it is sized without the optional prefill tile cache
+    (the size the paged query reports), so the call rebuilds every tile.
     Returns ``(O, lse)`` (``lse`` None unless requested).
     """
     for name, t, nd in (("Q", Q, 4), ("K_base", K_base, 4), ("V_base", V_base, 4), ("L_k", L_k, 3),
@@ -310,10 +317,14 @@ def lr_shared_attention(Q, K_base, V_base, L_k, L_v, B_k, B_v, positions, kv_len
         O = torch.empty_like(Q)
     if lse is None and want_lse:
         lse = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device)
-    need = workspace_size(dims)
+    need = workspace_size(dims) if tile_cache else paged_workspace_size(dims)
     if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=Q.device)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    if not tile_cache:
+        ws_bytes = min(ws_bytes, need)
+        if ws_bytes == 0:
+            workspace = None
     st = lib().lr_shared_attention(ctypes.byref(dims), _ptr(Q), _ptr(K_base), _ptr(V_base), _ptr(L_k),
                                    _ptr(L_v), _ptr(B_k), _ptr(B_v), _ptr(positions), _ptr(kv_len), _ptr(O),
                                    _ptr(lse), _ptr(workspace), ws_bytes, _stream(stream))
