@@ -443,8 +443,9 @@ size_t workspace_size(const lrsa_dims* dims, bool paged, bool tile_cache = true)
   if (dims->n_tok > 1) {
     // Prefill: partials of a split over the KV tiles, when the call is too
     // small to fill the GPU otherwise; else, for calls with enough row tiles
-    // per KV head at rank 16, the tile cache (room is asked for whenever the
-    // rank is 16, since dims do not say whether the call brings L_k).
+    // per KV head at rank 16 or 32, the tile cache (room is asked for
+    // whenever the rank is one of those, since dims do not say whether the
+    // call brings L_k).
     int splits = 1, split_tiles = 0;
     const int group = dims->n_q_heads / dims->n_kv_heads;
     prc::prefill_plan(dims->n_tok, group, dims->n_kv_heads, dims->batch, dims->s_cap, plan_cus(), &splits,

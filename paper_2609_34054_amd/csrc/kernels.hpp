@@ -86,11 +86,11 @@ void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int 
                   int* split_tiles);
 size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int head_dim, int rank);
 // Whether a prefill call shares rebuilt tiles through the workspace tile
-// cache: unsplit, contiguous caches, d = 128, rank 16 with LR on the keys,
-// and enough row-tile workgroups per KV head (at least 16) for the reuse to
-// pay for the cache's writes (measured: a gain at rank 16 with k LR, a loss
-// at rank 64 and with LR on v only).  tile_cache_bytes: its size (flags,
-// then data).
+// cache: unsplit, contiguous caches, d = 128, rank 16 or 32 with LR on the
+// keys, and enough row-tile workgroups per KV head (at least 16) for the
+// reuse to pay for the cache's writes (measured: gains at ranks 16 and 32
+// with k LR, none at rank 64, a loss with LR on v only).  tile_cache_bytes:
+// its size (flags, then data).
 bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged, int splits);
 size_t prefill_tile_cache_bytes(int batch, int n_kv, int64_t s_cap);
 size_t prefill_tile_cache_flag_bytes(int batch, int n_kv, int64_t s_cap);

@@ -277,7 +277,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // and data written at device scope (other XCDs' L2s are not coherent);
   // the data is read through L2, which holds no line of a part before its
   // flag was seen set (the flags are cleared by a kernel before this one).
-  constexpr bool TC = TCON && LK && R == 16 && D == 128 && !PAGED;
+  constexpr bool TC = TCON && LK && (R == 16 || R == 32) && D == 128 && !PAGED;
   constexpr bool tc_on = TC;
   const int64_t tc_slot = ((int64_t)b * a.n_kv + g) * a.tc_tiles;  // first tile of the slot
   // Buffer resources over the slot's flags and data; empty (loads read 0,
@@ -968,7 +968,7 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const dim3 grid(tiles, a.n_kv * nsp, a.batch);
   if (a.kv_tbl != nullptr)
     hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, true>), grid, dim3(NTHR), 0, st, a);
-  else if constexpr (LK && R == 16 && D == 128) {
+  else if constexpr (LK && (R == 16 || R == 32) && D == 128) {
     if (a.tc_data != nullptr)
       hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, false, true>), grid, dim3(NTHR), 0, st, a);
     else
@@ -1049,7 +1049,7 @@ size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int he
 
 bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged, int splits) {
   const int64_t row_tiles = ((int64_t)n_tok * group + BROWS - 1) / BROWS;
-  return has_lk && !paged && splits <= 1 && head_dim == 128 && rank == 16 && row_tiles >= 16;
+  return has_lk && !paged && splits <= 1 && head_dim == 128 && (rank == 16 || rank == 32) && row_tiles >= 16;
 }
 
 namespace {

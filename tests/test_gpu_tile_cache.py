@@ -1,6 +1,6 @@
 """The prefill tile cache: rebuilt K/V tiles published in the workspace and
 reused by the other row-tile workgroups of a KV head.  Large unsplit rank-16
-prefills with LR on the keys take it when the workspace has room; the cached
+and rank-32 prefills with LR on the keys take it when the workspace has room; the cached
 bytes are the ones a rebuild produces, so a call must give the same result
 whether a tile was rebuilt or loaded, whatever the workspace held before,
 and must match the fp64 oracle (Sec. 3.1: K = K_base + RoPE(L_k B_k),
@@ -37,9 +37,9 @@ def _call(dims, g, ws):
 
 # (id, rank, LR on k, LR on v): 1024 queries x 4 heads = 16 row tiles per KV
 # head, two requests with ragged lengths (partial last tiles, separate slots).
-# The first two take the cache.
-CASES = [("kv_r16", 16, True, True), ("k_r16", 16, True, False), ("qv_r16", 16, False, True),
-         ("kv_r64", 64, True, True)]
+# The first three take the cache.
+CASES = [("kv_r16", 16, True, True), ("k_r16", 16, True, False), ("kv_r32", 32, True, True),
+         ("qv_r16", 16, False, True), ("kv_r64", 64, True, True)]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
@@ -55,7 +55,7 @@ def test_tile_cache_matches_rebuild_and_oracle(case):
     g = to_dev(c)
     dims = make_dims(g["Q"], g["K_base"], g["L_k"], g["L_v"], g["B_k"], g["B_v"], cfg.theta)
     need = lib().lr_shared_attention_workspace_size(ctypes.byref(dims))
-    if r == 16:
+    if r in (16, 32):
         assert need >= 2 * 8 * (s_cap // 64) * 32768  # the cache is asked for
     need = max(need, 16)
     # A workspace full of garbage (every flag nonzero) must not be trusted,
