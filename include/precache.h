@@ -229,10 +229,10 @@ typedef struct lrsa_dims {
  *              query rows x KV head x request) fill the device's CUs so
  *              unevenly that splitting the KV tiles 2-8 ways shortens the
  *              modelled time (rounds of one unit per CU) by at least 10%.
- *              For an unsplit rank-16 or rank-32 prefill with at least 16
- *              row tiles (256 query rows each) per KV head, d = 128 and
- *              contiguous caches, the size instead covers an optional tile
- *              cache: with
+ *              For a prefill of rank 16, 32 or 64 with at least 16 row
+ *              tiles (256 query rows each) per KV head, d = 128 and
+ *              contiguous caches, the size also covers an optional tile
+ *              cache (after the partials, 256-byte aligned): with
  *              L_k given and a 256-byte aligned workspace of at least that
  *              size, each rebuilt 64-token K/V tile is shared between the
  *              row tiles of its KV head through it; otherwise every row tile

@@ -442,18 +442,22 @@ size_t workspace_size(const lrsa_dims* dims, bool paged, bool tile_cache = true)
   const int r = rank_ok(dims->rank) ? dims->rank : 8;
   if (dims->n_tok > 1) {
     // Prefill: partials of a split over the KV tiles, when the call is too
-    // small to fill the GPU otherwise; else, for calls with enough row tiles
-    // per KV head at rank 16 or 32, the tile cache (room is asked for
-    // whenever the rank is one of those, since dims do not say whether the
-    // call brings L_k).
+    // small to fill the GPU otherwise; then, for calls with enough row tiles
+    // per KV head at rank >= 16, the tile cache (room is asked for whenever
+    // the rank is one of those, since dims do not say whether the call
+    // brings L_k).
     int splits = 1, split_tiles = 0;
     const int group = dims->n_q_heads / dims->n_kv_heads;
     prc::prefill_plan(dims->n_tok, group, dims->n_kv_heads, dims->batch, dims->s_cap, plan_cus(), &splits,
                       &split_tiles);
+    const size_t parts =
+        prc::prefill_workspace_bytes(dims->batch, dims->n_tok, dims->n_q_heads, splits, dims->head_dim, r);
     if (tile_cache && !paged && rank_ok(dims->rank) &&
-        prc::prefill_uses_tile_cache(dims->n_tok, group, dims->head_dim, dims->rank, true, paged, splits))
-      return prc::prefill_tile_cache_bytes(dims->batch, dims->n_kv_heads, dims->s_cap);
-    return prc::prefill_workspace_bytes(dims->batch, dims->n_tok, dims->n_q_heads, splits, dims->head_dim, r);
+        prc::prefill_uses_tile_cache(dims->n_tok, group, dims->head_dim, dims->rank, true, paged)) {
+      const size_t cache = prc::prefill_tile_cache_bytes(dims->batch, dims->n_kv_heads, dims->s_cap);
+      if (cache > 0) return (parts + 255) / 256 * 256 + cache;
+    }
+    return parts;
   }
   int n_splits = 0, split_tiles = 0;
   // Paged caches always take the per-request decode kernel.
@@ -501,22 +505,25 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
   }
   const int plan_cu = plan_cus();
   prc::prefill_plan(a.n_tok, a.group, a.n_kv, a.batch, a.s_cap, plan_cu, &a.pf_splits, &a.pf_split_tiles);
+  // Split partials first (required when the plan splits), then the tile
+  // cache, taken when the workspace has room for it (a smaller or absent
+  // workspace only means every workgroup rebuilds every tile).
+  const size_t parts = prc::prefill_workspace_bytes(a.batch, a.n_tok, a.n_q, a.pf_splits, a.head_dim, a.rank);
   if (a.pf_splits > 1) {
-    const size_t need = prc::prefill_workspace_bytes(a.batch, a.n_tok, a.n_q, a.pf_splits, a.head_dim, a.rank);
-    if (workspace == nullptr || workspace_bytes < need)
+    if (workspace == nullptr || workspace_bytes < parts)
       return fail(PRC_EWORKSPACE, "workspace of %zu bytes given, %zu needed", workspace == nullptr ? 0 : workspace_bytes,
-                  need);
+                  parts);
     if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
     a.ws = static_cast<float*>(workspace);
-  } else if (prc::prefill_uses_tile_cache(a.n_tok, a.group, a.head_dim, a.rank, L_k != nullptr, pg != nullptr,
-                                          a.pf_splits)) {
-    // The tile cache is taken when the workspace has room for it (a smaller
-    // or absent workspace only means every workgroup rebuilds every tile).
+  }
+  if (prc::prefill_uses_tile_cache(a.n_tok, a.group, a.head_dim, a.rank, L_k != nullptr, pg != nullptr)) {
+    const size_t off = (parts + 255) / 256 * 256;
     const size_t need = prc::prefill_tile_cache_bytes(a.batch, a.n_kv, a.s_cap);
-    if (need > 0 && workspace != nullptr && workspace_bytes >= need && aligned(workspace, 256)) {
+    if (need > 0 && workspace != nullptr && workspace_bytes >= off + need && aligned(workspace, 256)) {
       const size_t fb = prc::prefill_tile_cache_flag_bytes(a.batch, a.n_kv, a.s_cap);
-      a.tc_flags = static_cast<uint32_t*>(workspace);
-      a.tc_data = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace) + fb);
+      char* base = static_cast<char*>(workspace) + off;
+      a.tc_flags = reinterpret_cast<uint32_t*>(base);
+      a.tc_data = reinterpret_cast<uint32_t*>(base + fb);
       a.tc_tiles = (int32_t)((a.s_cap + 63) / 64);
     }
   }

@@ -86,12 +86,13 @@ void prefill_plan(int n_tok, int group, int n_kv, int batch, int64_t s_cap, int 
                   int* split_tiles);
 size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int head_dim, int rank);
 // Whether a prefill call shares rebuilt tiles through the workspace tile
-// cache: unsplit, contiguous caches, d = 128, rank 16 or 32 with LR on the
-// keys, and enough row-tile workgroups per KV head (at least 16) for the
-// reuse to pay for the cache's writes (measured: gains at ranks 16 and 32
-// with k LR, none at rank 64, a loss with LR on v only).  tile_cache_bytes:
-// its size (flags, then data).
-bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged, int splits);
+// cache: contiguous caches, d = 128, rank >= 16 with LR on the keys, and
+// enough row-tile workgroups per KV head (at least 16) for the reuse to pay
+// for the cache's writes (measured: gains at ranks 16, 32 and 64 with k LR,
+// a loss with LR on v only).  A split call keeps its partials first in the
+// workspace, the cache after them (256-byte aligned).  tile_cache_bytes: its
+// size (flags, then data).
+bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged);
 size_t prefill_tile_cache_bytes(int batch, int n_kv, int64_t s_cap);
 size_t prefill_tile_cache_flag_bytes(int batch, int n_kv, int64_t s_cap);
 hipError_t launch_prefill(const AttnArgs& a, hipStream_t stream);

@@ -277,7 +277,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // and data written at device scope (other XCDs' L2s are not coherent);
   // the data is read through L2, which holds no line of a part before its
   // flag was seen set (the flags are cleared by a kernel before this one).
-  constexpr bool TC = TCON && LK && (R == 16 || R == 32) && D == 128 && !PAGED;
+  constexpr bool TC = TCON && LK && R >= 16 && D == 128 && !PAGED;
   constexpr bool tc_on = TC;
   const int64_t tc_slot = ((int64_t)b * a.n_kv + g) * a.tc_tiles;  // first tile of the slot
   // Buffer resources over the slot's flags and data; empty (loads read 0,
@@ -613,15 +613,17 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const bool build_first = ((w >> 2) ^ w) & 1;
 
   // Tiles are walked as a sequence k = t_lo .. t_hi - 1, LDS buffer k & 1.
-  // With the tile cache the unmasked tiles [0, n_rot) are walked from a
-  // starting point staggered over the row tiles of the KV head (the online
-  // softmax does not depend on the order), the rest in order.
-  const int n_rot = tc_on ? (n_full_raw < t_hi ? n_full_raw : t_hi) : 0;
+  // With the tile cache the unmasked tiles of this workgroup's range are
+  // walked from a starting point staggered over the row tiles of the KV
+  // head (the online softmax does not depend on the order), the rest in
+  // order.
+  const int r_end = tc_on ? (n_full_raw < t_hi ? n_full_raw : t_hi) : t_lo;  // rotated steps [t_lo, r_end)
+  const int n_rot = r_end > t_lo ? r_end - t_lo : 0;
   const int rot = n_rot > 0 ? (int)(((int64_t)rtile * n_rot) / gridDim.x) : 0;
   auto tile_at = [&](int k) {
-    if (k >= n_rot) return k;
+    if (k >= t_lo + n_rot) return k;
     const int t = k + rot;
-    return t >= n_rot ? t - n_rot : t;
+    return t >= t_lo + n_rot ? t - n_rot : t;
   };
   // Loads of sequence step k into u: its cached part if the flag read one
   // fetch earlier says it is published, else the raw rows.  The flag of the
@@ -968,7 +970,7 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const dim3 grid(tiles, a.n_kv * nsp, a.batch);
   if (a.kv_tbl != nullptr)
     hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, true>), grid, dim3(NTHR), 0, st, a);
-  else if constexpr (LK && (R == 16 || R == 32) && D == 128) {
+  else if constexpr (LK && R >= 16 && D == 128) {
     if (a.tc_data != nullptr)
       hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, false, true>), grid, dim3(NTHR), 0, st, a);
     else
@@ -1047,9 +1049,9 @@ size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int he
   return (size_t)batch * n_tok * n_q * splits * (4 + head_dim + rank) * sizeof(float);
 }
 
-bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged, int splits) {
+bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged) {
   const int64_t row_tiles = ((int64_t)n_tok * group + BROWS - 1) / BROWS;
-  return has_lk && !paged && splits <= 1 && head_dim == 128 && (rank == 16 || rank == 32) && row_tiles >= 16;
+  return has_lk && !paged && head_dim == 128 && rank >= 16 && row_tiles >= 16;
 }
 
 namespace {

@@ -1,6 +1,6 @@
 """The prefill tile cache: rebuilt K/V tiles published in the workspace and
-reused by the other row-tile workgroups of a KV head.  Large unsplit rank-16
-and rank-32 prefills with LR on the keys take it when the workspace has room; the cached
+reused by the other row-tile workgroups of a KV head.  Large unsplit prefills
+of rank 16 to 64 with LR on the keys take it when the workspace has room; the cached
 bytes are the ones a rebuild produces, so a call must give the same result
 whether a tile was rebuilt or loaded, whatever the workspace held before,
 and must match the fp64 oracle (Sec. 3.1: K = K_base + RoPE(L_k B_k),
@@ -37,26 +37,31 @@ def _call(dims, g, ws):
 
 # (id, rank, LR on k, LR on v): 1024 queries x 4 heads = 16 row tiles per KV
 # head, two requests with ragged lengths (partial last tiles, separate slots).
-# The first three take the cache.
-CASES = [("kv_r16", 16, True, True), ("k_r16", 16, True, False), ("kv_r32", 32, True, True),
-         ("qv_r16", 16, False, True), ("kv_r64", 64, True, True)]
+# All but the value-only one take the cache.
+CASES = [("kv_r16", 16, True, True, 2), ("k_r16", 16, True, False, 2), ("kv_r32", 32, True, True, 2),
+         ("qv_r16", 16, False, True, 2), ("kv_r64", 64, True, True, 2),
+         # one request: 128 units of work for 256 CUs, so the KV tiles are also
+         # split (partials first in the workspace, the cache after them)
+         ("kv_r64_split", 64, True, True, 1)]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
 def test_tile_cache_matches_rebuild_and_oracle(case):
-    cid, r, lk, lv = case
+    cid, r, lk, lv, batch = case
     print(f"tile cache {cid}", flush=True)
     cfg = Config(95, "tile cache", hidden=256, n_q=32, n_kv=8, head_dim=128, theta=5e5, n_agents=1, rank=r,
                  context=0, prefill_tokens=0, decode_batch=0, precompute_rows=0)
-    n_tok, kv_lens, s_cap = 1024, [5000, 4100], 5120
+    n_tok, kv_lens, s_cap = 1024, [5000, 4100][:batch], 5120
     pos = [list(range(k - n_tok, k)) for k in kv_lens]
-    c = attention_case(cfg, batch=2, n_tok=n_tok, kv_len=kv_lens, positions=pos, s_cap=s_cap, lr_k=lk, lr_v=lv,
+    c = attention_case(cfg, batch=batch, n_tok=n_tok, kv_len=kv_lens, positions=pos, s_cap=s_cap, lr_k=lk, lr_v=lv,
                        seed_base=7 * r + lk)
     g = to_dev(c)
     dims = make_dims(g["Q"], g["K_base"], g["L_k"], g["L_v"], g["B_k"], g["B_v"], cfg.theta)
     need = lib().lr_shared_attention_workspace_size(ctypes.byref(dims))
-    if r in (16, 32):
-        assert need >= 2 * 8 * (s_cap // 64) * 32768  # the cache is asked for
+    if r >= 16:
+        assert need >= batch * 8 * (s_cap // 64) * 32768  # the cache is asked for
+    if batch == 1:
+        assert need > 8 * (s_cap // 64) * 32768 + n_tok * 32 * (4 + 128 + r) * 4  # partials as well
     need = max(need, 16)
     # A workspace full of garbage (every flag nonzero) must not be trusted,
     # and a second call over the first call's cache must give the same bytes.
@@ -64,8 +69,10 @@ def test_tile_cache_matches_rebuild_and_oracle(case):
     O1, l1 = _call(dims, g, ws)
     O2, l2 = _call(dims, g, ws)
     assert torch.equal(O1, O2) and torch.equal(l1, l2)
-    # Without a workspace every workgroup rebuilds every tile (in order).
-    O0, l0 = _call(dims, g, None)
+    # With room only for the split partials (none, unless split) every
+    # workgroup rebuilds every tile, in order.
+    parts = lib().lr_shared_attention_paged_workspace_size(ctypes.byref(dims))
+    O0, l0 = _call(dims, g, torch.empty(parts, dtype=torch.uint8, device="cuda") if parts else None)
     assert (O1.float() - O0.float()).abs().max().item() <= ATOL_MAX
     toks = [0, 1, 255, 256, 511, 700, 1023]
     Oref, lref = oracle_attention(c, cfg.theta, toks=toks)
