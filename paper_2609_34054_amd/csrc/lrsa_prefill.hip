@@ -1051,7 +1051,7 @@ size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int he
 
 bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged) {
   const int64_t row_tiles = ((int64_t)n_tok * group + BROWS - 1) / BROWS;
-  return has_lk && !paged && head_dim == 128 && rank >= 16 && row_tiles >= 16;
+  return has_lk && !paged && head_dim == 128 && rank >= 16 && row_tiles >= 8;
 }
 
 namespace {
