@@ -280,10 +280,11 @@ lrsa_prefill_kernel(const AttnArgs a) {
   constexpr bool TC = TCON && LK && R >= 16 && D == 128 && !PAGED;
   constexpr bool tc_on = TC;
   const int64_t tc_slot = ((int64_t)b * a.n_kv + g) * a.tc_tiles;  // first tile of the slot
-  // Buffer resources over the slot's flags and data; empty (loads read 0,
-  // stores are dropped) when the cache is off, so that every path issues
-  // the same memory instructions and the compiler's load counting stays
-  // exact.  Offset INT32_MIN is out of range: no access.
+  // Buffer resources over the slot's flags and data; empty (loads read 0)
+  // when the cache is off, so that every path issues the same loads and the
+  // compiler's load counting stays exact.  Offset INT32_MIN is out of range:
+  // no access.  The stores of a built part and its flag are issued only
+  // after a build, under a wave-uniform branch.
   const __amdgpu_buffer_rsrc_t tc_frsrc = __builtin_amdgcn_make_buffer_rsrc(
       tc_on ? a.tc_flags + tc_slot * NW : nullptr, (short)0, tc_on ? a.tc_tiles * NW * 4 : 0, 0x00020000);
   const __amdgpu_buffer_rsrc_t tc_rsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -449,12 +450,15 @@ lrsa_prefill_kernel(const AttnArgs a) {
   int u_tile = 0, pub_tile = -1;
   uint32_t fl_next = 0;  // flag of the tile fetched next (read a fetch ahead)
   auto publish = [&]() {
-    // vmcnt(0): the part's stores have completed (issued a tile ago; the
-    // loads this build consumes are waited for here anyway).  Then the flag,
-    // at device scope, from every lane (same address, same value).
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    __builtin_amdgcn_raw_buffer_store_b32(1u, tc_frsrc, pub_tile >= 0 ? (pub_tile * NW + w) * 4 : INT32_MIN, 0, 16);
-    pub_tile = -1;
+    // Only after a build (a few tiles per wave): vmcnt(0), so the part's
+    // stores, issued a tile ago, have completed; then the flag, at device
+    // scope, from every lane (same address, same value).  An unconditional
+    // wait here drained the loads in flight on every tile and cost 2-4%.
+    if (pub_tile >= 0) {
+      __builtin_amdgcn_s_waitcnt(0x0F70);
+      __builtin_amdgcn_raw_buffer_store_b32(1u, tc_frsrc, (pub_tile * NW + w) * 4, 0, 16);
+      pub_tile = -1;
+    }
   };
   auto rebuild = [&](const Unit<D, R>& u, int buf) {
     if constexpr (TC) publish();  // the previous part: its stores were issued a tile ago
@@ -532,13 +536,16 @@ lrsa_prefill_kernel(const AttnArgs a) {
     }
     if constexpr (TC) {
       // A full tile rebuilt here goes to the cache too (flagged at the next
-      // build); the stores are issued on every path, out of range when not.
+      // build).  The branch is wave-uniform; every wait on these stores is
+      // the one in publish().
       const bool store_part = compute && tc_on && (u_tile + 1) * TKV <= kv_hi;
-      buf_st16_dev(u32x4{lo.w[0], lo.w[1], lo.w[2], lo.w[3]}, tc_rsrc, store_part ? tc_off(u_tile, 0) : INT32_MIN);
-      buf_st16_dev(u32x4{hi.w[0], hi.w[1], hi.w[2], hi.w[3]}, tc_rsrc, store_part ? tc_off(u_tile, 1) : INT32_MIN);
+      if (store_part) {
+        buf_st16_dev(u32x4{lo.w[0], lo.w[1], lo.w[2], lo.w[3]}, tc_rsrc, tc_off(u_tile, 0));
+        buf_st16_dev(u32x4{hi.w[0], hi.w[1], hi.w[2], hi.w[3]}, tc_rsrc, tc_off(u_tile, 1));
 #pragma unroll
-      for (int hf = 0; hf < 2; ++hf) buf_st16_dev(fv[hf], tc_rsrc, store_part ? tc_off(u_tile, 2 + hf) : INT32_MIN);
-      if (store_part) pub_tile = u_tile;
+        for (int hf = 0; hf < 2; ++hf) buf_st16_dev(fv[hf], tc_rsrc, tc_off(u_tile, 2 + hf));
+        pub_tile = u_tile;
+      }
     }
     if (LVA && lv_wave) {
       // L_v^T fragments (2 ltb + hf, lrb).  With rank < 32, rank row `rank`
