@@ -28,8 +28,10 @@
 //      the transposing LDS read (ds_read_b64_tr_b16), so P, already in B
 //      operand layout, needs no shuffles and the softmax rescale is a
 //      per-lane scalar.
-// The loads of the next sub-block (the next two at rank 64) are in flight
-// while the current one is consumed.
+// The loads of the next sub-block (the next two in the 4-wave rank-64
+// kernel) are in flight while the current one is consumed.  The contiguous
+// rank-64 kernel at d = 128 sends its V rows straight to LDS (direct
+// global->LDS loads into a two-buffer ring) instead of through registers.
 #include "common.hpp"
 #include "kernels.hpp"
 #include "rebuild.hpp"
@@ -41,20 +43,29 @@ constexpr int TK = 32;        // tokens per KV tile (one LDS table, one barrier)
 constexpr int NSB = TK / 16;  // 16-token sub-blocks per tile
 constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (log2 domain)
 // Waves per workgroup (one KV head each).  Rank 64 keeps its B_k^T
-// fragments (64 VGPRs) in registers by running one wave per SIMD, which
-// gives each wave the whole register file (architected plus accumulation
-// registers) instead of spilling to scratch.
+// fragments (64 VGPRs) in registers; with V staged in registers that needs
+// one wave per SIMD (the whole register file, architected plus accumulation
+// registers) to avoid spilling.
 constexpr int dec_waves(int rank) { return rank >= 64 ? 4 : 8; }
 // Sub-blocks whose loads are in flight ahead of the one being consumed.  With
 // one wave per SIMD (rank 64) no other wave hides a wave's load latency, and
 // the whole register file leaves room for one more staged sub-block; at two
 // waves per SIMD the extra stage spills and loses.
 constexpr int dec_prefetch(int rank) { return rank >= 64 ? 2 : 1; }
+// Contiguous rank-64 decode at d = 128 instead stages its V rows by direct
+// global->LDS loads, which frees the registers the V stages take: with one
+// sub-block in flight it then fits in 256 registers (251), so it runs 8-wave
+// workgroups, two waves per SIMD, like the lower ranks (64k, 8 requests:
+// 467 -> 440 us).  Paged caches keep the 4-wave form (their walk issues
+// block-table loads between the stages, which the fixed load count of the
+// V wait below does not cover).
+constexpr bool dec_vdma(int d, int rank, bool paged) { return d == 128 && rank == 64 && !paged; }
+constexpr int dec_nw(int d, int rank, bool paged) { return dec_vdma(d, rank, paged) ? 8 : dec_waves(rank); }
 constexpr int gcd_c(int a, int b) { return b == 0 ? a : gcd_c(b, a % b); }
 
-template <int D, int R>
+template <int D, int R, bool VD = false>
 struct Dec {
-  static constexpr int NW = dec_waves(R);    // waves per workgroup (KV heads)
+  static constexpr int NW = VD ? 8 : dec_waves(R);  // waves per workgroup (KV heads)
   static constexpr int NT = NW * 64;         // threads per workgroup
   static constexpr int HALF = D / 2;
   static constexpr int NB = D / 32;           // 16-dim blocks per RoPE half
@@ -76,9 +87,15 @@ struct Dec {
   static constexpr int RPL = 64 / LPR;        // V rows per wave load
   static constexpr int NVL = 16 / RPL;        // V loads per sub-block
   static constexpr int PS = 4 + D + R;        // floats per split partial
-  static constexpr int PF = dec_prefetch(R);  // sub-blocks loaded ahead
+  static constexpr int PF = VD ? 1 : dec_prefetch(R);  // sub-blocks loaded ahead
   static constexpr int NST = PF + 1;          // staged sub-blocks (a ring)
   static constexpr int TPR = NST / gcd_c(NST, NSB);  // tiles per whole number of turns of the ring
+  // Direct-to-LDS V staging: a stage is the 16 V rows at the padded row
+  // stride V_ROW, written by NVD 1 KB loads (lane i of load k lands at byte
+  // 1024 k + 16 i; lanes that fall in a row's padding or past the last row
+  // load nothing).  VST: bf16 per stage buffer.
+  static constexpr int NVD = (16 * V_ROW * 2 + 1023) / 1024;
+  static constexpr int VST = NVD * 512;
 };
 
 // Transposing LDS read: lane j of each 16-lane group points at 4 consecutive
@@ -110,10 +127,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base
 // loads in flight while the current one is consumed.
 template <int D, int R>
 struct StageOffsets {
-  int32_t kb[D / 32], lk[Ex<R>::NC], lr[RCH(R)], v[Dec<D, R>::NVL];
+  int32_t kb[D / 32], lk[Ex<R>::NC], lr[RCH(R)], v[Dec<D, R>::NVL], vd[Dec<D, R>::NVD];
 };
 
-template <int D, int R>
+template <int D, int R, bool VD>
 __device__ __forceinline__ StageOffsets<D, R> stage_offsets(int64_t row, int lane) {
   using C = Dec<D, R>;
   StageOffsets<D, R> o;
@@ -131,8 +148,16 @@ __device__ __forceinline__ StageOffsets<D, R> stage_offsets(int64_t row, int lan
     o.lk[c] = r0 < R ? c16 * R * 2 + r0 * 2 : INT32_MIN;
   }
   const int vrow = lane / C::LPR, vdim = (lane % C::LPR) * 8;
+  if constexpr (VD) {
 #pragma unroll
-  for (int iv = 0; iv < C::NVL; ++iv) o.v[iv] = (vrow + C::RPL * iv) * (int32_t)(row * 2) + vdim * 2;
+    for (int k = 0; k < C::NVD; ++k) {
+      const int byte = 1024 * k + 16 * lane, t = byte / (2 * C::V_ROW), in_row = byte % (2 * C::V_ROW);
+      o.vd[k] = (t < 16 && in_row < 2 * D) ? t * (int32_t)(row * 2) + in_row : INT32_MIN;
+    }
+  } else {
+#pragma unroll
+    for (int iv = 0; iv < C::NVL; ++iv) o.v[iv] = (vrow + C::RPL * iv) * (int32_t)(row * 2) + vdim * 2;
+  }
   return o;
 }
 
@@ -145,11 +170,13 @@ __device__ __forceinline__ typename Ex<R>::Frag lr_frag_load(__amdgpu_buffer_rsr
     return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
 }
 
-template <int D, int R>
+// VD: V goes straight to the stage buffer `vdst` in LDS (its rows at stride
+// V_ROW), issued after the stage's other loads.
+template <int D, int R, bool VD>
 __device__ __forceinline__ void stage_load(Stage<D, R>& s, const StageOffsets<D, R>& o, const uint16_t* Kb,
                                            const uint16_t* Vb, const uint16_t* Lk, const uint16_t* Lv,
                                            int64_t kv_row, int64_t lr_row, int64_t row, int64_t t0,
-                                           int64_t t_end) {
+                                           int64_t t_end, uint16_t* vdst) {
   using C = Dec<D, R>;
   // Valid tokens of the sub-block (none past the end: every load reads zeros).
   const int64_t n = t_end - t0 < 0 ? 0 : (t_end - t0 < 16 ? t_end - t0 : 16);
@@ -168,21 +195,41 @@ __device__ __forceinline__ void stage_load(Stage<D, R>& s, const StageOffsets<D,
 #pragma unroll
   for (int rc = 0; rc < C::RC; ++rc)
     s.lv[rc] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rlv, o.lr[rc], 0, 0));
+  if constexpr (VD) {
 #pragma unroll
-  for (int iv = 0; iv < C::NVL; ++iv)
-    s.v[iv] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, o.v[iv], 0, 0));
+    for (int k = 0; k < C::NVD; ++k)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (__attribute__((address_space(3))) void*)(vdst + 512 * k), 16,
+                                               o.vd[k], 0, 0, 0);
+  } else {
+#pragma unroll
+    for (int iv = 0; iv < C::NVL; ++iv)
+      s.v[iv] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, o.v[iv], 0, 0));
+  }
 }
+
+// s_waitcnt with vmcnt(n) and no wait on the other counters.
+constexpr int vmcnt_imm(int n) { return (n & 0xF) | ((n >> 4) << 14) | 0x0F70; }
+// Vector memory instructions one VD stage issues (K_base chunks, L_k
+// fragments, L_v fragments, then the direct V loads).
+template <int D, int R>
+constexpr int kStageLoads = D / 32 + Ex<R>::NC + RCH(R) + Dec<D, R>::NVD;
 
 // PAGED: the caches are pools reached through block tables (a separate
 // instantiation, so the contiguous kernel carries none of the walk's state).
 template <int D, int R, bool PAGED>
-__global__ void __launch_bounds__(dec_waves(R) * 64, dec_waves(R) / 4)
+__global__ void __launch_bounds__(dec_nw(D, R, PAGED) * 64, dec_nw(D, R, PAGED) / 4)
 lrsa_decode_kernel(const AttnArgs a) {
-  using C = Dec<D, R>;
+  constexpr bool VD = dec_vdma(D, R, PAGED);
+  using C = Dec<D, R, VD>;
   constexpr int NW = C::NW, NT = C::NT;
   __shared__ float2 cs_lds[2][TK * C::CS_ROW];
   __shared__ float2 base_lds[2][C::HALF];
-  __shared__ __attribute__((aligned(16))) uint16_t v_lds[NW][16 * C::V_ROW];
+  // Per wave: the V tile written from registers, or (VD) the two V stage
+  // buffers the direct loads fill, as separate arrays so that the compiler
+  // can tell the LDS reads of one from the direct loads into the other.
+  static_assert(!VD || C::NST == 2, "two V stage buffers");
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds[NW][VD ? C::VST : 16 * C::V_ROW];
+  __shared__ __attribute__((aligned(16))) uint16_t v_lds1[VD ? NW : 1][VD ? C::VST : 8];
   __shared__ __attribute__((aligned(16))) uint16_t lv_lds[NW][16 * C::LV_ROW];
 
   // The wave index is made visibly wave-uniform, so that everything derived
@@ -254,6 +301,16 @@ lrsa_decode_kernel(const AttnArgs a) {
   }
   typename Ex<R>::Frag bkf[C::NBLK][Ex<R>::NC];
   bts.finish(bkf, v_lds[w], lane);
+  if constexpr (VD) {
+    // The stage buffers start as zeros (finite rows for tokens past the end,
+    // whatever the direct loads do at out-of-range offsets), written before
+    // the first direct load is issued.
+    for (int i = lane; i < C::VST / 8; i += 64) {
+      *reinterpret_cast<u32x4*>(v_lds[w] + 8 * i) = u32x4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4*>(v_lds1[VD ? w : 0] + 8 * i) = u32x4{0u, 0u, 0u, 0u};
+    }
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0)
+  }
 
   float m_run = -INFINITY, l_part = 0.f;
   f32x4 acc[C::NBLK];   // O^T: dims blk*16 + 4q + i, head l%16
@@ -270,20 +327,21 @@ lrsa_decode_kernel(const AttnArgs a) {
   // 4*(l/16) + (j/4), columns 4*(j%4) .. +3 of a 16-column block.
   const int tr_row = 4 * q + (c16 >> 2), tr_col = 4 * (c16 & 3);
 
-  const StageOffsets<D, R> so = stage_offsets<D, R>(row, lane);
+  const StageOffsets<D, R> so = stage_offsets<D, R, VD>(row, lane);
   Stage<D, R> st[C::NST];
   // Sub-blocks are loaded in token order, so paged caches are walked with them.
   PageWalk walk;
   if constexpr (PAGED)
     walk.start(a.kv_tbl + (int64_t)b * a.max_blk, a.lr_tbl + (int64_t)b * a.max_blk, a.max_blk, a.blk, a.kv_nblk,
                a.lr_nblk, t_begin, t_end_w);
-  auto load = [&](Stage<D, R>& s, int64_t t) {
+  // Stage `slot` of the ring (VD: also its V buffer in LDS).
+  auto load = [&](Stage<D, R>& s, int64_t t, int slot) {
     int64_t kr = t, lr = t;
     if constexpr (PAGED) walk.next(16, t_end_w, kr, lr);
-    stage_load<D, R>(s, so, Kb, Vb, Lk, Lv, kr, lr, row, t, t_end_w);
+    stage_load<D, R, VD>(s, so, Kb, Vb, Lk, Lv, kr, lr, row, t, t_end_w, slot == 0 ? vl : v_lds1[VD ? w : 0]);
   };
 #pragma unroll
-  for (int p = 0; p < C::PF; ++p) load(st[p], t_begin + 16 * p);
+  for (int p = 0; p < C::PF; ++p) load(st[p], t_begin + 16 * p, p);
 
   __syncthreads();  // base angles of the first tile, zeroed L_v tiles
 
@@ -318,24 +376,27 @@ lrsa_decode_kernel(const AttnArgs a) {
 
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb) {
-      Stage<D, R>& cur = st[(tt * NSB + sb) % C::NST];
-      Stage<D, R>& nxt = st[(tt * NSB + sb + C::PF) % C::NST];
+      const int cslot = (tt * NSB + sb) % C::NST, nslot = (tt * NSB + sb + C::PF) % C::NST;
+      Stage<D, R>& cur = st[cslot];
+      Stage<D, R>& nxt = st[nslot];
       // A sub-block past the split end (only in its last tile) holds zeros
       // and no visible key: all its weights are exactly 0 and the running
       // maximum does not move, so it changes nothing.
       const int64_t ts = t0 + sb * 16;
       // Issue the loads of the sub-block PF ahead before consuming this one
       // (past the split end they read zeros and touch no memory).
-      load(nxt, ts + 16 * C::PF);
+      load(nxt, ts + 16 * C::PF, nslot);
       // Keep the loads ahead of this sub-block's work: the scheduler would
       // otherwise sink them to shorten their registers' live ranges, and the
       // wait for this stage would then also wait for the next one.
       __builtin_amdgcn_sched_barrier(0);
 
       // ---- V and L_v rows into the wave's LDS tile ------------------------
+      if constexpr (!VD) {
 #pragma unroll
-      for (int iv = 0; iv < C::NVL; ++iv)
-        *reinterpret_cast<u32x4*>(vl + (vrow + C::RPL * iv) * C::V_ROW + vdim) = cur.v[iv];
+        for (int iv = 0; iv < C::NVL; ++iv)
+          *reinterpret_cast<u32x4*>(vl + (vrow + C::RPL * iv) * C::V_ROW + vdim) = cur.v[iv];
+      }
       if (has_lv) {
 #pragma unroll
         for (int rc = 0; rc < C::RC; ++rc)
@@ -410,9 +471,19 @@ lrsa_decode_kernel(const AttnArgs a) {
       __builtin_amdgcn_wave_barrier();
 
       // ---- O^T += V^T P^T, (P L_v)^T += L_v^T P^T -----------------------
+      const uint16_t* vcur = vl;
+      if constexpr (VD) {
+        // This stage's direct V loads have landed once at most the loads of
+        // the next stage, issued after them, are still in flight (the
+        // counter drains in issue order; the sched barrier keeps the LDS
+        // reads below the wait).
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm(kStageLoads<D, R>));
+        __builtin_amdgcn_sched_barrier(0);
+        vcur = cslot == 0 ? vl : v_lds1[VD ? w : 0];
+      }
 #pragma unroll
       for (int blk = 0; blk < C::NBLK; ++blk)
-        acc[blk] = mfma16x16x16(lds_read_tr(vl + tr_row * C::V_ROW + blk * 16 + tr_col), pb, acc[blk]);
+        acc[blk] = mfma16x16x16(lds_read_tr(vcur + tr_row * C::V_ROW + blk * 16 + tr_col), pb, acc[blk]);
       if (has_lv) {
 #pragma unroll
         for (int rc = 0; rc < C::RC; ++rc)
@@ -423,6 +494,9 @@ lrsa_decode_kernel(const AttnArgs a) {
   }
 
 tiles_done:
+  // Direct loads past the split end may still be in flight: let them land
+  // before the wave (and with the last wave, the workgroup's LDS) retires.
+  if constexpr (VD) __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
   if (!active) return;
   // One partial per (request, q head, split): lane l%16 is the head; lanes
   // l, l^16, l^32, l^48 share it and hold different dims of O^T.
@@ -934,13 +1008,15 @@ hipError_t launch_merge_t(const AttnArgs& a, hipStream_t st) {
 
 template <int D, int R>
 hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
-  using C = Dec<D, R>;
-  const int hg = (a.n_kv + C::NW - 1) / C::NW;
-  const dim3 grid(a.n_splits, hg, a.batch);
-  if (a.kv_tbl != nullptr)
-    hipLaunchKernelGGL((lrsa_decode_kernel<D, R, true>), grid, dim3(C::NT), 0, st, a);
-  else
-    hipLaunchKernelGGL((lrsa_decode_kernel<D, R, false>), grid, dim3(C::NT), 0, st, a);
+  if (a.kv_tbl != nullptr) {
+    constexpr int nw = dec_nw(D, R, true);
+    const dim3 grid(a.n_splits, (a.n_kv + nw - 1) / nw, a.batch);
+    hipLaunchKernelGGL((lrsa_decode_kernel<D, R, true>), grid, dim3(64 * nw), 0, st, a);
+  } else {
+    constexpr int nw = dec_nw(D, R, false);
+    const dim3 grid(a.n_splits, (a.n_kv + nw - 1) / nw, a.batch);
+    hipLaunchKernelGGL((lrsa_decode_kernel<D, R, false>), grid, dim3(64 * nw), 0, st, a);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   return launch_merge_t<D, R>(a, st);
