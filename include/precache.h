@@ -233,7 +233,8 @@ typedef struct lrsa_dims {
  *              tiles (256 query rows each) per KV head, d = 128 and
  *              contiguous caches, the size also covers an optional tile
  *              cache (after the partials, 256-byte aligned): with
- *              L_k given and a 256-byte aligned workspace of at least that
+ *              L_k given (or L_v alone at rank 32 or 64) and a 256-byte
+ *              aligned workspace of at least that
  *              size, each rebuilt 64-token K/V tile is shared between the
  *              row tiles of its KV head through it; otherwise every row tile
  *              rebuilds every tile (the result then differs only by the

@@ -453,7 +453,7 @@ size_t workspace_size(const lrsa_dims* dims, bool paged, bool tile_cache = true)
     const size_t parts =
         prc::prefill_workspace_bytes(dims->batch, dims->n_tok, dims->n_q_heads, splits, dims->head_dim, r);
     if (tile_cache && !paged && rank_ok(dims->rank) &&
-        prc::prefill_uses_tile_cache(dims->n_tok, group, dims->head_dim, dims->rank, true, paged)) {
+        prc::prefill_uses_tile_cache(dims->n_tok, group, dims->head_dim, dims->rank, true, true, paged)) {
       const size_t cache = prc::prefill_tile_cache_bytes(dims->batch, dims->n_kv_heads, dims->s_cap);
       if (cache > 0) return (parts + 255) / 256 * 256 + cache;
     }
@@ -516,7 +516,8 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
     if (!aligned(workspace, 16)) return fail(PRC_EALIGN, "workspace is not 16-byte aligned");
     a.ws = static_cast<float*>(workspace);
   }
-  if (prc::prefill_uses_tile_cache(a.n_tok, a.group, a.head_dim, a.rank, L_k != nullptr, pg != nullptr)) {
+  if (prc::prefill_uses_tile_cache(a.n_tok, a.group, a.head_dim, a.rank, L_k != nullptr, L_v != nullptr,
+                                   pg != nullptr)) {
     const size_t off = (parts + 255) / 256 * 256;
     const size_t need = prc::prefill_tile_cache_bytes(a.batch, a.n_kv, a.s_cap);
     if (need > 0 && workspace != nullptr && workspace_bytes >= off + need && aligned(workspace, 256)) {

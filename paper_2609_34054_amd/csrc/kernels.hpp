@@ -92,7 +92,7 @@ size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int he
 // a loss with LR on v only).  A split call keeps its partials first in the
 // workspace, the cache after them (256-byte aligned).  tile_cache_bytes: its
 // size (flags, then data).
-bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged);
+bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool has_lv, bool paged);
 size_t prefill_tile_cache_bytes(int batch, int n_kv, int64_t s_cap);
 size_t prefill_tile_cache_flag_bytes(int batch, int n_kv, int64_t s_cap);
 hipError_t launch_prefill(const AttnArgs& a, hipStream_t stream);

@@ -243,9 +243,12 @@ lrsa_prefill_kernel(const AttnArgs a) {
   const int n_tiles = (int)((kv_hi + TKV - 1) / TKV);
   // Tiles [0, n_full) lie wholly at or below every row's last visible key:
   // no row needs a mask there and every wave attends them.  Rank 64 with key
-  // LR keeps the per-half loop for all tiles: with it the straight-line main
-  // loop needs more registers than there are (16 spilled against 4).
-  constexpr bool kMainLoop = R < 64 || (VREB && !LK);
+  // LR keeps the per-half loop for all tiles when it rebuilds every tile:
+  // with it the straight-line main loop needs more registers than there are
+  // (16 spilled against 4).  With the tile cache the rebuild (and its
+  // spills) runs for a few tiles per wave only, and the main loop wins
+  // (32k: 2.91 -> 2.56 ms; 64k, 2048 queries: 3.56 -> 3.24 ms).
+  constexpr bool kMainLoop = R < 64 || (VREB && !LK) || (TCON && LK && D == 128 && !PAGED);
   const int n_full_raw = s_minpos < 0 ? 0 : (int)(((int64_t)s_minpos + 1) / TKV);
   const int n_full = !kMainLoop ? 0 : (n_full_raw < n_tiles ? n_full_raw : n_tiles);
   // This workgroup's tiles: all of them, or its split's share.
@@ -277,7 +280,10 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // and data written at device scope (other XCDs' L2s are not coherent);
   // the data is read through L2, which holds no line of a part before its
   // flag was seen set (the flags are cleared by a kernel before this one).
-  constexpr bool TC = TCON && LK && R >= 16 && D == 128 && !PAGED;
+  // Taken with LR on the keys, and with LR on the values only from rank 32
+  // (at rank 64 the value rebuild alone costs 28% over plain attention; at
+  // rank 16 there is too little to save).
+  constexpr bool TC = TCON && (LK || (LV && R >= 32)) && R >= 16 && D == 128 && !PAGED;
   constexpr bool tc_on = TC;
   const int64_t tc_slot = ((int64_t)b * a.n_kv + g) * a.tc_tiles;  // first tile of the slot
   // Buffer resources over the slot's flags and data; empty (loads read 0)
@@ -977,7 +983,7 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const dim3 grid(tiles, a.n_kv * nsp, a.batch);
   if (a.kv_tbl != nullptr)
     hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, true>), grid, dim3(NTHR), 0, st, a);
-  else if constexpr (LK && R >= 16 && D == 128) {
+  else if constexpr ((LK || (LV && R >= 32)) && R >= 16 && D == 128) {
     if (a.tc_data != nullptr)
       hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, false, true>), grid, dim3(NTHR), 0, st, a);
     else
@@ -1056,9 +1062,9 @@ size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int he
   return (size_t)batch * n_tok * n_q * splits * (4 + head_dim + rank) * sizeof(float);
 }
 
-bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool paged) {
+bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool has_lv, bool paged) {
   const int64_t row_tiles = ((int64_t)n_tok * group + BROWS - 1) / BROWS;
-  return has_lk && !paged && head_dim == 128 && rank >= 16 && row_tiles >= 8;
+  return (has_lk || (has_lv && rank >= 32)) && !paged && head_dim == 128 && rank >= 16 && row_tiles >= 8;
 }
 
 namespace {

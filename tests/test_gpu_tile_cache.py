@@ -1,6 +1,7 @@
 """The prefill tile cache: rebuilt K/V tiles published in the workspace and
-reused by the other row-tile workgroups of a KV head.  Large unsplit prefills
-of rank 16 to 64 with LR on the keys take it when the workspace has room; the cached
+reused by the other row-tile workgroups of a KV head.  Large prefills of
+rank 16 to 64 with LR on the keys, or on the values only at rank 32 and 64,
+take it when the workspace has room; the cached
 bytes are the ones a rebuild produces, so a call must give the same result
 whether a tile was rebuilt or loaded, whatever the workspace held before,
 and must match the fp64 oracle (Sec. 3.1: K = K_base + RoPE(L_k B_k),
@@ -37,9 +38,10 @@ def _call(dims, g, ws):
 
 # (id, rank, LR on k, LR on v): 1024 queries x 4 heads = 16 row tiles per KV
 # head, two requests with ragged lengths (partial last tiles, separate slots).
-# All but the value-only one take the cache.
+# All but the rank-16 value-only one take the cache.
 CASES = [("kv_r16", 16, True, True, 2), ("k_r16", 16, True, False, 2), ("kv_r32", 32, True, True, 2),
-         ("qv_r16", 16, False, True, 2), ("kv_r64", 64, True, True, 2),
+         ("qv_r16", 16, False, True, 2), ("qv_r32", 32, False, True, 2), ("qv_r64", 64, False, True, 2),
+         ("kv_r64", 64, True, True, 2),
          # one request: 128 units of work for 256 CUs, so the KV tiles are also
          # split (partials first in the workspace, the cache after them)
          ("kv_r64_split", 64, True, True, 1)]
