@@ -196,6 +196,11 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // B_k^T fragments of this KV head for ranks > 16, [RoPE half ph][block i]
   // [lane][rank chunk]: each lane's NC 16-byte fragments are contiguous.
   __shared__ __attribute__((aligned(16))) u32x4 bk_lds[LK && !C::BK_REG ? 2 * 2 * C::NBW * 64 * C::NC : 1];
+  // Rank-64 k+v with the tile cache: the B_v fragments of the value rebuild
+  // wait in LDS (one copy per 32-dim block), since the rebuild runs for a
+  // few tiles per wave only and their 16 VGPRs made the main loop spill.
+  constexpr bool BV_LDS = TCON && LK && LV && R == 64 && D == 128 && !PAGED;
+  __shared__ __attribute__((aligned(16))) u32x4 bv_lds[BV_LDS ? C::NDB * (R / 16) * 64 : 1];
   __shared__ int s_maxpos, s_minpos;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -389,13 +394,18 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // dim column l%32, same ranks), so that the expansion lands in the layout
   // of the V transpose.
   int32_t offlvv[VREB ? R / 16 : 1];
-  u32x4 bvf[VREB ? R / 16 : 1];
+  u32x4 bvf[VREB && !BV_LDS ? R / 16 : 1];
   if constexpr (VREB) {
     const uint16_t* bvp = a.Bv + (int64_t)b * a.b_stride + (int64_t)g * D + 32 * vdb + (lane & 31);
 #pragma unroll
     for (int kc = 0; kc < R / 16; ++kc) {
       offlvv[kc] = (32 * vtb + (lane & 31)) * R * 2 + (16 * kc + (lane >> 5) * 8) * 2;
-      bvf[kc] = Ex<32>::gather(bvp + (int64_t)(16 * kc + (lane >> 5) * 8) * ldb, ldb, true);
+      const u32x4 f = Ex<32>::gather(bvp + (int64_t)(16 * kc + (lane >> 5) * 8) * ldb, ldb, true);
+      if constexpr (BV_LDS) {
+        if ((w & 1) == 0) bv_lds[(vdb * (R / 16) + kc) * 64 + lane] = f;  // visible after the prologue's barrier
+      } else {
+        bvf[kc] = f;
+      }
     }
   }
   // Tiles are loaded in token order, so paged caches are walked with them.
@@ -522,7 +532,14 @@ lrsa_prefill_kernel(const AttnArgs a) {
       for (int j = 0; j < 16; ++j) t[j] = 0.f;
       if constexpr (VREB) {
 #pragma unroll
-        for (int kc = 0; kc < R / 16; ++kc) t = mfma32x32x16(as_bf16x8(u.lvv[kc]), as_bf16x8(bvf[kc]), t);
+        for (int kc = 0; kc < R / 16; ++kc) {
+          u32x4 bv;
+          if constexpr (BV_LDS)
+            bv = bv_lds[(vdb * (R / 16) + kc) * 64 + lane];
+          else
+            bv = bvf[kc];
+          t = mfma32x32x16(as_bf16x8(u.lvv[kc]), as_bf16x8(bv), t);
+        }
       }
 #pragma unroll
       for (int hb = 0; hb < C::NHB; ++hb) t = mfma32x32x16(as_bf16x8(u.v[hb]), as_bf16x8(vid[vp0 + hb]), t);
