@@ -229,7 +229,7 @@ typedef struct lrsa_dims {
  *              query rows x KV head x request) fill the device's CUs so
  *              unevenly that splitting the KV tiles 2-8 ways shortens the
  *              modelled time (rounds of one unit per CU) by at least 10%.
- *              For a prefill of rank 16, 32 or 64 with at least 8 row
+ *              For a prefill of rank 8, 16, 32 or 64 with at least 8 row
  *              tiles (256 query rows each) per KV head, d = 128 and
  *              contiguous caches, the size also covers an optional tile
  *              cache (after the partials, 256-byte aligned): with

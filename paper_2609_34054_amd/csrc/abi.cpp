@@ -443,7 +443,7 @@ size_t workspace_size(const lrsa_dims* dims, bool paged, bool tile_cache = true)
   if (dims->n_tok > 1) {
     // Prefill: partials of a split over the KV tiles, when the call is too
     // small to fill the GPU otherwise; then, for calls with enough row tiles
-    // per KV head at rank >= 16, the tile cache (room is asked for whenever
+    // per KV head with an LR rank, the tile cache (room is asked for whenever
     // the rank is one of those, since dims do not say whether the call
     // brings L_k).
     int splits = 1, split_tiles = 0;

@@ -285,10 +285,12 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // and data written at device scope (other XCDs' L2s are not coherent);
   // the data is read through L2, which holds no line of a part before its
   // flag was seen set (the flags are cleared by a kernel before this one).
-  // Taken with LR on the keys, and with LR on the values only from rank 32
+  // Taken with LR on the keys (at rank 8 the L_v^T fragments, kept in
+  // associativity form, are not part of a cached tile), and with LR on the
+  // values only from rank 32
   // (at rank 64 the value rebuild alone costs 28% over plain attention; at
   // rank 16 there is too little to save).
-  constexpr bool TC = TCON && (LK || (LV && R >= 32)) && R >= 16 && D == 128 && !PAGED;
+  constexpr bool TC = TCON && (LK || (LV && R >= 32)) && D == 128 && !PAGED;
   constexpr bool tc_on = TC;
   const int64_t tc_slot = ((int64_t)b * a.n_kv + g) * a.tc_tiles;  // first tile of the slot
   // Buffer resources over the slot's flags and data; empty (loads read 0)
@@ -415,7 +417,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
     // Valid rows of this tile; a tile at or past kv_hi gets empty resources
     // (its loads return zeros).
     const int64_t left = kv_hi - t0;
-    const int rows = cached ? 0 : (int)(left < TKV ? (left > 0 ? left : 0) : TKV);
+    const int rows_all = (int)(left < TKV ? (left > 0 ? left : 0) : TKV);
+    const int rows = cached ? 0 : rows_all;
     const int32_t kv_bytes = rows > 0 ? (rows - 1) * (int32_t)(row_el * 2) + D * 2 : 0;
     int64_t kr = t0, lr = t0;  // cache rows of the tile's first token
     if constexpr (PAGED) walk.next(TKV, kv_hi, kr, lr);
@@ -450,7 +453,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
     for (int hb = 0; hb < C::NHB; ++hb) u.v[hb] = buf_ld16(rv, cached ? tc_off(T, 2 + hb) : offv[hb]);
     if constexpr (LVA) {
-      const auto rl = make_rsrc(Lv + lr * R, rows * R * 2);
+      // L_v^T fragments are not cached: their rows are loaded either way.
+      const auto rl = make_rsrc(Lv + lr * R, rows_all * R * 2);
 #pragma unroll
       for (int p = 0; p < C::NLP; ++p) u.lv[p] = lv_wave ? buf_ld16(rl, offlv[p]) : u32x4{0u, 0u, 0u, 0u};
     }
@@ -1000,7 +1004,7 @@ hipError_t launch_t(const AttnArgs& a, hipStream_t st) {
   const dim3 grid(tiles, a.n_kv * nsp, a.batch);
   if (a.kv_tbl != nullptr)
     hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, true>), grid, dim3(NTHR), 0, st, a);
-  else if constexpr ((LK || (LV && R >= 32)) && R >= 16 && D == 128) {
+  else if constexpr ((LK || (LV && R >= 32)) && D == 128) {
     if (a.tc_data != nullptr)
       hipLaunchKernelGGL((lrsa_prefill_kernel<D, R, LK, LV, false, true>), grid, dim3(NTHR), 0, st, a);
     else
@@ -1081,7 +1085,7 @@ size_t prefill_workspace_bytes(int batch, int n_tok, int n_q, int splits, int he
 
 bool prefill_uses_tile_cache(int n_tok, int group, int head_dim, int rank, bool has_lk, bool has_lv, bool paged) {
   const int64_t row_tiles = ((int64_t)n_tok * group + BROWS - 1) / BROWS;
-  return (has_lk || (has_lv && rank >= 32)) && !paged && head_dim == 128 && rank >= 16 && row_tiles >= 8;
+  return (has_lk || (has_lv && rank >= 32)) && !paged && head_dim == 128 && rank >= 8 && row_tiles >= 8;
 }
 
 namespace {
