@@ -982,24 +982,39 @@ def workload_bench(prc, index, dev, steps, warmup):
         attn(prc, plain(c, K, V), w["theta"], O, wsp)
 
     def timed(fn, n_sets):
-        for i in range(warmup):
+        # Eager warm-up (kernels loaded, workspaces settled), then one HIP
+        # graph holding a call per input set, replayed back to back: the GPU
+        # time per call without the host's launch overhead between calls
+        # (short calls, such as a batch-1 decode, take less GPU time than
+        # their launches take on the host).
+        for i in range(max(warmup, n_sets)):
             fn(i % n_sets)
         torch.cuda.synchronize()
-        ts = []
-        for i in range(steps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            fn(i % n_sets)
-            e1.record()
-            ts.append((e0, e1))
+        gr = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(gr):
+            for i in range(n_sets):
+                fn(i)
+        gr.replay()
         torch.cuda.synchronize()
-        v = sorted(a.elapsed_time(b) for a, b in ts)
-        return v[len(v) // 2]
+        reps = max(2, -(-steps // n_sets))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            gr.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        del gr
+        return e0.elapsed_time(e1) / (reps * n_sets)
 
+    # The prefill's workspace (split partials and its tile cache), also used
+    # by the plain prefill of the reference.
+    dims_pre = prc.make_dims(pre[0]["Q"], pre[0]["K_base"], pre[0]["L_k"], pre[0]["L_v"], pre[0]["B_k"],
+                             pre[0]["B_v"], w["theta"])
+    ws_pre = torch.empty(max(1, prc.workspace_size(dims_pre)), dtype=torch.uint8, device=dev)
     t_pc = timed(lambda i: prc.precompute_lr_cache(X[i % 4], A_stack, 2, N, r, L), 4)
-    t_pre = timed(lambda i: attn(prc, pre[i], w["theta"], O_pre, None), n_pre)
+    t_pre = timed(lambda i: attn(prc, pre[i], w["theta"], O_pre, ws_pre), n_pre)
     t_dec = timed(lambda i: attn(prc, dec[i], w["theta"], O_dec, ws), n_dec)
-    t_pre_m = timed(lambda i: materialised(pre[i], Kp, Vp, O_pre, None), n_pre)
+    t_pre_m = timed(lambda i: materialised(pre[i], Kp, Vp, O_pre, ws_pre), n_pre)
     t_dec_m = timed(lambda i: materialised(dec[i], Kd, Vd, O_dec, ws), n_dec)
     pre_tf = work["prefill_flops"] / (t_pre * 1e-3) / 1e12
     dec_gbs = work["decode_bytes"] / (t_dec * 1e-3) / 1e9
