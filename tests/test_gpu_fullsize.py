@@ -13,17 +13,17 @@ from workload import CONFIGS, attention_case
 pytestmark = pytest.mark.gpu
 
 
-def request_case(cfg, b, n_tok, kv_len, pos, s_cap, tag):
+def request_case(cfg, b, n_tok, kv_len, pos, s_cap, tag, lr_k=True, lr_v=True, rank=None):
     """Inputs of request b alone (batch 1), seeded per request."""
     return attention_case(cfg, batch=1, n_tok=n_tok, kv_len=[kv_len], positions=[pos], s_cap=s_cap,
-                          seed_base=10_000 * tag + 37 * b, poison_tail=False)
+                          seed_base=10_000 * tag + 37 * b, poison_tail=False, lr_k=lr_k, lr_v=lr_v, rank=rank)
 
 
-def build_batch(cfg, B, n_tok, kv_len, pos_of, s_cap, tag):
+def build_batch(cfg, B, n_tok, kv_len, pos_of, s_cap, tag, **wiring):
     """Device tensors for the whole batch, filled request by request."""
     g = None
     for b in range(B):
-        c = request_case(cfg, b, n_tok, kv_len, pos_of(b), s_cap, tag)
+        c = request_case(cfg, b, n_tok, kv_len, pos_of(b), s_cap, tag, **wiring)
         if g is None:
             g = {k: (torch.empty((B,) + tuple(v.shape[1:]), dtype=v.dtype, device="cuda") if v is not None else None)
                  for k, v in c.items()}
@@ -33,9 +33,9 @@ def build_batch(cfg, B, n_tok, kv_len, pos_of, s_cap, tag):
     return g
 
 
-def check_sampled(cfg, g, O, lse, n_tok, kv_len, pos_of, s_cap, tag, reqs, toks):
+def check_sampled(cfg, g, O, lse, n_tok, kv_len, pos_of, s_cap, tag, reqs, toks, **wiring):
     for b in reqs:
-        c = request_case(cfg, b, n_tok, kv_len, pos_of(b), s_cap, tag)
+        c = request_case(cfg, b, n_tok, kv_len, pos_of(b), s_cap, tag, **wiring)
         Q = f64(c["Q"])[:, toks]
         pos = c["positions"].numpy()[:, toks]
         Oref, lref = oracle.lr_shared_attention(Q, f64(c["K_base"]), f64(c["V_base"]), f64(c["L_k"]),
@@ -96,3 +96,17 @@ def test_c4_prefill_2048_at_64k():
     g = build_batch(cfg, 1, n, S + n, lambda b: pos, S + n, 7)
     O, lse = gpu_attention(g, cfg.theta)
     check_sampled(cfg, g, O, lse, n, S + n, lambda b: pos, S + n, 7, [0], [0, 25, 26, 1024, 2047])
+
+
+@pytest.mark.parametrize("wiring", [dict(lr_k=False, lr_v=True, rank=64), dict(lr_k=False, lr_v=True, rank=32),
+                                    dict(lr_k=True, lr_v=True, rank=8), dict(lr_k=True, lr_v=True, rank=64)],
+                         ids=["qv_r64", "qv_r32", "kv_r8", "kv_r64"])
+def test_c3_prefill_rank_sweep_wirings(wiring):
+    # The rank sweep's prefill shapes (4096 queries at 32k, the tile-cache
+    # instantiations: values-only LR from rank 32, k and v at ranks 8 and 64).
+    cfg = CONFIGS[3]
+    S, n = cfg.context, cfg.prefill_tokens
+    pos = list(range(S, S + n))
+    g = build_batch(cfg, 1, n, S + n, lambda b: pos, S + n, 8, **wiring)
+    O, lse = gpu_attention(g, cfg.theta)
+    check_sampled(cfg, g, O, lse, n, S + n, lambda b: pos, S + n, 8, [0], [0, 63, 64, 2047, 4031, 4095], **wiring)
