@@ -345,6 +345,27 @@ lrsa_decode_kernel(const AttnArgs a) {
 
   __syncthreads();  // base angles of the first tile, zeroed L_v tiles
 
+  // RoPE table of tile k (from its base angles in base_lds[k & 1]) into
+  // cs_lds[k & 1], and the base angles of tile k + 1 into base_lds[(k + 1) & 1].
+  // Tile 0's here; each later one while the tile before it runs, beside that
+  // tile's first loads, so that the barrier at the head of a tile has no
+  // table work in front of it.
+  auto build_table = [&](int k) {
+    float2* csk = cs_lds[k & 1];
+    const float2* base = base_lds[k & 1];
+#pragma unroll
+    for (int e = 0; e < C::EPT; ++e) {
+      const float2 bc = base[ej[e]];
+      csk[eidx[e]] = make_float2(bc.x * cdl[e] - bc.y * sdl[e], bc.y * cdl[e] + bc.x * sdl[e]);
+    }
+    if (tid < C::HALF && k + 1 < n_tiles) {
+      float c, sn;
+      rope_cs((int)(t_begin + (int64_t)(k + 1) * TK), w2pi_t, c, sn);
+      base_lds[(k + 1) & 1][tid] = make_float2(c, sn);
+    }
+  };
+  if (has_lk && n_tiles > 0) build_table(0);
+
   // The tile loop is unrolled by the tiles of one turn of the stage ring, so
   // that every stage index is a constant.  Inside it every path issues the
   // same loads (inactive waves and sub-blocks past the split end load zeros
@@ -358,21 +379,9 @@ lrsa_decode_kernel(const AttnArgs a) {
     if (tile >= n_tiles) goto tiles_done;  // uniform over the workgroup
     const int64_t t0 = t_begin + (int64_t)tile * TK;
     float2* cs = cs_lds[tile & 1];
-    if (has_lk) {
-      const float2* base = base_lds[tile & 1];
-#pragma unroll
-      for (int k = 0; k < C::EPT; ++k) {
-        const float2 bc = base[ej[k]];
-        cs[eidx[k]] = make_float2(bc.x * cdl[k] - bc.y * sdl[k], bc.y * cdl[k] + bc.x * sdl[k]);
-      }
-      if (tid < C::HALF && tile + 1 < n_tiles) {
-        float c, s;
-        rope_cs((int)(t0 + TK), w2pi_t, c, s);
-        base_lds[(tile + 1) & 1][tid] = make_float2(c, s);
-      }
-    }
-    __syncthreads();  // this tile's table is ready; double buffering keeps
-                      // the previous tile's table intact for slower waves.
+    __syncthreads();  // this tile's table and the next tile's base angles are
+                      // ready, and every wave is done with the previous tile
+                      // (whose table buffer the next table goes into).
 
 #pragma unroll
     for (int sb = 0; sb < NSB; ++sb) {
@@ -390,6 +399,8 @@ lrsa_decode_kernel(const AttnArgs a) {
       // otherwise sink them to shorten their registers' live ranges, and the
       // wait for this stage would then also wait for the next one.
       __builtin_amdgcn_sched_barrier(0);
+      // The next tile's table, while this sub-block's data is still landing.
+      if (sb == 0 && has_lk && tile + 1 < n_tiles) build_table(tile + 1);
 
       // ---- V and L_v rows into the wave's LDS tile ------------------------
       if constexpr (!VD) {
