@@ -285,6 +285,8 @@ def test_decode_workspace_query_and_check():
     tiles = 36864 // 64
     cache = -(-(8 * tiles * 8 * 4) // 256) * 256 + 8 * tiles * 32768
     assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=4096, batch=1, s_cap=36864))) == cache
+    # Rank 8 takes it too (its L_v^T fragments stay outside the cached tile).
+    assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=4096, batch=1, s_cap=36864, rank=8))) == cache
     # No LR rank (plain attention), few row tiles, or paged caches: no cache.
     assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=4096, batch=1, s_cap=36864, rank=0))) == 0
     assert L.lr_shared_attention_workspace_size(ctypes.byref(_dims(n_tok=8, s_cap=256))) == 0
