@@ -60,7 +60,7 @@ constexpr float kRescaleLog2 = 8.f;  // lazy-rescale threshold (log2 domain)
 // associativity with (P L_v) accumulated beside P V_base.
 constexpr bool rebuilds_v(int rank) { return rank >= 16; }
 
-template <int D, int R>
+template <int D, int R, bool TCN = false>
 struct Pre {
   static_assert(D == 64 || D == 128, "head dims 64 and 128");
   static constexpr int HALF = D / 2;
@@ -82,11 +82,13 @@ struct Pre {
   // L_v^T likewise, fragment (m, rb) for ranks 32 rb + l%32: waves
   // 0 .. 2 RB - 1 each transpose 32 tokens x 32 ranks, in NLP 16-rank halves.
   static constexpr int NLP = R >= 32 ? 2 : 1;
-  // B_k^T fragments of small ranks stay in registers, larger ones in LDS.
-  static constexpr bool BK_REG = R <= 16;
+  // B_k^T fragments of small ranks stay in registers, larger ones in LDS;
+  // the tile-cache instantiation (TCN) rebuilds a few tiles per wave only and
+  // keeps them in LDS at every rank, freeing registers for the main loop.
+  static constexpr bool BK_REG = R <= 16 && !TCN;
   // The per-lane offset angles of the rebuild stay in registers where the
   // register budget allows it (rank 16, V rebuilt in the tile), else in LDS.
-  static constexpr bool OCS_REG = R == 16;
+  static constexpr bool OCS_REG = R == 16 && !TCN;
 };
 
 // SEG consecutive bf16 of one row.
@@ -173,7 +175,7 @@ struct Unit {
 template <int D, int R, bool LK, bool LV, bool PAGED, bool TCON = false>
 __global__ void __launch_bounds__(NTHR)
 lrsa_prefill_kernel(const AttnArgs a) {
-  using C = Pre<D, R>;
+  using C = Pre<D, R, TCON && LK && D == 128 && !PAGED>;
   // Value side: rank 8 keeps associativity, P V_base + (P L_v) B_v, with the
   // softmax row sums in a spare row of (P L_v)^T.  From rank 16 on the
   // tile's V = V_base + L_v B_v is rebuilt on chip instead: per 64-token
@@ -195,7 +197,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // [wave][pair of frequencies][lane] (one 16-byte read per pair).
   // B_k^T fragments of this KV head for ranks > 16, [RoPE half ph][block i]
   // [lane][rank chunk]: each lane's NC 16-byte fragments are contiguous.
-  __shared__ __attribute__((aligned(16))) u32x4 bk_lds[LK && !C::BK_REG ? 2 * 2 * C::NBW * 64 * C::NC : 1];
+  __shared__ __attribute__((aligned(16))) typename Ex<R>::Frag bk_lds[LK && !C::BK_REG ? 2 * 2 * C::NBW * 64 * C::NC : 1];
   // Rank-64 k+v with the tile cache: the B_v fragments of the value rebuild
   // wait in LDS (one copy per 32-dim block), since the rebuild runs for a
   // few tiles per wave only and their 16 VGPRs made the main loop spill.
@@ -292,6 +294,12 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // rank 16 there is too little to save).
   constexpr bool TC = TCON && (LK || (LV && R >= 32)) && D == 128 && !PAGED;
   constexpr bool tc_on = TC;
+  // With the tile cache, Q is scaled by log2(e)/sqrt(d) once (rounded to
+  // bf16) and the main loop's score MFMAs start from a register block that
+  // holds minus the reference maximum, so the exponentials read the scores
+  // directly.
+  constexpr bool MSC = TC && R <= 32;
+  const float qscale = MSC ? 1.f : a.scale_log2;
   const int64_t tc_slot = ((int64_t)b * a.n_kv + g) * a.tc_tiles;  // first tile of the slot
   // Buffer resources over the slot's flags and data; empty (loads read 0)
   // when the cache is off, so that every path issues the same loads and the
@@ -352,7 +360,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
       for (int c = 0; c < C::NC; ++c) f[c] = bkr[i][c];
     } else {
-      const u32x4* p = bk_lds + ((ph * 2 * C::NBW + i) * 64 + lane) * C::NC;
+      const typename Ex<R>::Frag* p = bk_lds + ((ph * 2 * C::NBW + i) * 64 + lane) * C::NC;
 #pragma unroll
       for (int c = 0; c < C::NC; ++c) f[c] = p[c];
     }
@@ -624,6 +632,18 @@ lrsa_prefill_kernel(const AttnArgs a) {
     const uint16_t* qp = a.Q + (((int64_t)b * a.n_tok + qi) * a.n_q + (int64_t)g * G + hh) * D;
 #pragma unroll
     for (int kk = 0; kk < C::NKQ; ++kk) qf[kk] = as_bf16x8(ld16(qp + kk * 16 + h32 * 8, row_ok));
+    if constexpr (MSC) {
+#pragma unroll
+      for (int kk = 0; kk < C::NKQ; ++kk) {
+        u32x4 w = __builtin_bit_cast(u32x4, qf[kk]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float lo = __uint_as_float(w[i] << 16) * a.scale_log2, hi = __uint_as_float(w[i] & 0xFFFF0000u) * a.scale_log2;
+          w[i] = pack_bf16(lo, hi);
+        }
+        qf[kk] = as_bf16x8(w);
+      }
+    }
   }
   // Let these one-time loads (Q, B_k) land before the tile loop: across the
   // loop's back edge the compiler could not tell them from the tile loads in
@@ -640,6 +660,9 @@ lrsa_prefill_kernel(const AttnArgs a) {
 #pragma unroll
     for (int j = 0; j < 16; ++j) accl[rb][j] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
+  f32x16 negm;  // MSC: minus the reference maximum (0 while there is none)
+#pragma unroll
+  for (int j = 0; j < 16; ++j) negm[j] = 0.f;
 
 
   // The two waves of a SIMD (w and w + 4, or w and w ^ 1, depending on how the
@@ -718,21 +741,28 @@ lrsa_prefill_kernel(const AttnArgs a) {
     f32x16 sh[2];
 #pragma unroll
     for (int kk = 0; kk < C::NKQ; ++kk) kf[kk] = k_frag(0, kk);
+    f32x16 zinit;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) sh[0][j] = sh[1][j] = 0.f;
+    for (int j = 0; j < 16; ++j) zinit[j] = 0.f;
+    sh[0] = mfma32x32x16(kf[0], qf[0], MSC ? negm : zinit);
+    kf[0] = k_frag(1, 0);
 #pragma unroll
-    for (int kk = 0; kk < C::NKQ; ++kk) {
+    for (int kk = 1; kk < C::NKQ; ++kk) {
       sh[0] = mfma32x32x16(kf[kk], qf[kk], sh[0]);
       kf[kk] = k_frag(1, kk);
     }
+    sh[1] = mfma32x32x16(kf[0], qf[0], MSC ? negm : zinit);
 #pragma unroll
-    for (int kk = 0; kk < C::NKQ; ++kk) sh[1] = mfma32x32x16(kf[kk], qf[kk], sh[1]);
+    for (int kk = 1; kk < C::NKQ; ++kk) sh[1] = mfma32x32x16(kf[kk], qf[kk], sh[1]);
     float mx = fmaxf(sh[0][0], sh[0][1]);
 #pragma unroll
     for (int j = 2; j < 16; ++j) mx = fmaxf(mx, sh[0][j]);
 #pragma unroll
     for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sh[1][j]);
-    mx = max_xor32(mx) * a.scale_log2;
+    // MSC: the scores are relative to the reference ms0 (0 before the first
+    // maximum is known).
+    const float ms0 = (m_run == -INFINITY) ? 0.f : m_run;
+    mx = MSC ? max_xor32(mx) + ms0 : max_xor32(mx) * a.scale_log2;
     if (__ballot(mx > m_run + kRescaleLog2)) {
       const float mn = fmaxf(m_run, mx);
       const float alpha = fast_exp2(m_run - (mn == -INFINITY ? 0.f : mn));
@@ -742,6 +772,15 @@ lrsa_prefill_kernel(const AttnArgs a) {
       for (int rb = 0; rb < NRB; ++rb) accl[rb] *= alpha;
       l_run *= alpha;
       m_run = mn;
+      if constexpr (MSC) {
+        const float shift = (mn == -INFINITY ? 0.f : mn) - ms0;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          sh[0][j] -= shift;
+          sh[1][j] -= shift;
+          negm[j] = -(mn == -INFINITY ? 0.f : mn);
+        }
+      }
     }
     const float ms = (m_run == -INFINITY) ? 0.f : m_run;
     float ls = 0.f;
@@ -763,8 +802,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
         u32x4 pw;  // bf16 P of this 16-token chunk
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
-          const float p0 = fast_exp2(__builtin_fmaf(sh[tb][hf * 8 + 2 * c], a.scale_log2, -ms));
-          const float p1 = fast_exp2(__builtin_fmaf(sh[tb][hf * 8 + 2 * c + 1], a.scale_log2, -ms));
+          const float p0 = MSC ? fast_exp2(sh[tb][hf * 8 + 2 * c]) : fast_exp2(__builtin_fmaf(sh[tb][hf * 8 + 2 * c], a.scale_log2, -ms));
+          const float p1 = MSC ? fast_exp2(sh[tb][hf * 8 + 2 * c + 1]) : fast_exp2(__builtin_fmaf(sh[tb][hf * 8 + 2 * c + 1], a.scale_log2, -ms));
           pw[c] = pack_bf16(p0, p1);
           if constexpr (!ones_sum) ls = sum2_bf16(pw[c], ls);
         }
@@ -839,7 +878,7 @@ lrsa_prefill_kernel(const AttnArgs a) {
         float mx = s[0];
 #pragma unroll
         for (int j = 1; j < 16; ++j) mx = fmaxf(mx, s[j]);
-        mx = max_xor32(mx) * a.scale_log2;
+        mx = max_xor32(mx) * qscale;
         // Lazy rescale: the reference maximum m_run only moves when some row's
         // maximum exceeds it by more than 2^8, so P stays below 256 and the
         // accumulators are rescaled a handful of times per row.
@@ -881,8 +920,8 @@ lrsa_prefill_kernel(const AttnArgs a) {
         for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
           for (int c = 0; c < 4; ++c) {
-            const float p0 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c], a.scale_log2, -ms));
-            const float p1 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c + 1], a.scale_log2, -ms));
+            const float p0 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c], qscale, -ms));
+            const float p1 = fast_exp2(__builtin_fmaf(s[hf * 8 + 2 * c + 1], qscale, -ms));
             pw[hf][c] = pack_bf16(p0, p1);
             if constexpr (!ones_sum) {
               if (c & 1) ls1 = sum2_bf16(pw[hf][c], ls1);
