@@ -294,11 +294,13 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // rank 16 there is too little to save).
   constexpr bool TC = TCON && (LK || (LV && R >= 32)) && D == 128 && !PAGED;
   constexpr bool tc_on = TC;
-  // With the tile cache, Q is scaled by log2(e)/sqrt(d) once (rounded to
-  // bf16) and the main loop's score MFMAs start from a register block that
-  // holds minus the reference maximum, so the exponentials read the scores
-  // directly.
-  constexpr bool MSC = TC && R <= 32;
+  // Q is scaled by log2(e)/sqrt(d) once (rounded to bf16) and the main
+  // loop's score MFMAs start from a register block that holds minus the
+  // reference maximum, so the exponentials read the scores directly.  It
+  // needs 16 more VGPRs: taken by the tile-cache kernels up to rank 32 (their
+  // build state lives in LDS) and by the kernels without key LR, not by the
+  // others (they would spill).
+  constexpr bool MSC = D == 128 && ((TC && R <= 32) || (!TCON && !LK));
   const float qscale = MSC ? 1.f : a.scale_log2;
   const int64_t tc_slot = ((int64_t)b * a.n_kv + g) * a.tc_tiles;  // first tile of the slot
   // Buffer resources over the slot's flags and data; empty (loads read 0)
