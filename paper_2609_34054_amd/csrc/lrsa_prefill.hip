@@ -30,14 +30,20 @@
 //           halves of 32 tokens:
 //     scores  S^T = K Q^T on 32x32x16 MFMAs, so softmax statistics are per
 //             lane; causal mask only on halves that cross it;
-//     softmax online, exp2 domain, lazily rescaled;
+//     softmax online, exp2 domain, lazily rescaled; where the registers
+//             allow it (plain and values-only kernels, tile-cache kernels
+//             up to rank 32) Q is pre-scaled once and the main loop's score
+//             MFMAs start from a block holding minus the reference maximum;
 //     PV      O^T += V^T P^T (and, below rank 32, (P L_v)^T += L_v^T P^T) on
 //             32x32x16 MFMAs,
 //             one conflict-free 16-byte LDS read per A fragment; P is
 //             already in the B operand layout.
 // LDS instructions, not bytes, bound the tile rate here (each costs the CU
 // about 4 cycles whatever its width), hence the fragment layouts above and
-// the register-resident identities and small-rank B_k fragments.  Tiles
+// the register-resident identities and small-rank B_k fragments (in LDS in
+// the tile-cache kernels, which rebuild a few tiles per wave).  Large
+// contiguous calls share rebuilt tiles between the row-tile workgroups of a
+// KV head through a tile cache in the workspace (see below).  Tiles
 // below every row's causal limit run a straight-line main loop (scores, then
 // one block of exponentials, PV and the next tile's build); tiles that cross
 // a limit run a per-half loop in which the two waves sharing a SIMD take
