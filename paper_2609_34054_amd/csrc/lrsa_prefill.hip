@@ -682,17 +682,19 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // walked from a starting point staggered over the row tiles of the KV
   // head (the online softmax does not depend on the order), the rest in
   // order.
-  // The starting points are shared by groups of four row tiles that run on
-  // one XCD (row tiles r, r + 8, r + 16, r + 24 of a block of 32; workgroup i
-  // runs on XCD i % 8): a group walks in step, so one memory-side read of a
-  // cached part serves its four workgroups through L2, at the price of up to
-  // four rebuilds of the group's first tiles (32k rank 16: 2.318 -> 2.263 ms;
-  // 64k rank 64: 3.304 -> 3.125 ms; groups of eight measured slower).
+  // The starting points are shared by groups of row tiles that run on one
+  // XCD (workgroup i runs on XCD i % 8, so row tiles r, r + 8, r + 16, ...):
+  // a group walks in step, so one memory-side read of a cached part serves
+  // its workgroups through L2, at the price of rebuilding the group's first
+  // tiles once per member.  Groups of four from 32 row tiles on, of two from
+  // 16 (32k rank 16: 2.318 -> 2.263 ms; 64k rank 64: 3.304 -> 3.125 ms;
+  // groups of eight measured slower, and with 8 row tiles, one per XCD,
+  // grouping only adds rebuilds).
   const int r_end = tc_on ? (n_full_raw < t_hi ? n_full_raw : t_hi) : t_lo;  // rotated steps [t_lo, r_end)
   const int n_rot = r_end > t_lo ? r_end - t_lo : 0;
-  const int ngrp = (int)gridDim.x / 4 > 0 ? (int)gridDim.x / 4 : 1;
-  const int gidx = (rtile / 32) * 8 + rtile % 8;
-  const int grp = gidx < ngrp ? gidx : rtile % ngrp;
+  const int gsz = gridDim.x >= 32 ? 4 : (gridDim.x >= 16 ? 2 : 1);
+  const int ngrp = (int)((gridDim.x + 8 * gsz - 1) / (8 * gsz)) * 8;  // > every group index
+  const int grp = (rtile / (8 * gsz)) * 8 + rtile % 8;
   const int rot = n_rot > 0 ? (int)(((int64_t)grp * n_rot) / ngrp) % n_rot : 0;
   auto tile_at = [&](int k) {
     if (k >= t_lo + n_rot) return k;
