@@ -462,7 +462,8 @@ size_t workspace_size(const lrsa_dims* dims, bool paged, bool tile_cache = true)
   int n_splits = 0, split_tiles = 0;
   // Paged caches always take the per-request decode kernel.
   const bool shared = !paged && prc::decode_shares_base(dims->batch, dims->kv_req_stride);
-  prc::decode_plan(dims->s_cap, dims->batch, dims->n_kv_heads, r, shared, plan_cus(), &n_splits, &split_tiles);
+  prc::decode_plan(dims->s_cap, dims->batch, dims->n_kv_heads, dims->head_dim, r, shared, paged, plan_cus(), &n_splits,
+                   &split_tiles);
   return prc::decode_workspace_bytes(dims->batch, dims->n_q_heads, n_splits, dims->head_dim, r);
 }
 
@@ -496,8 +497,8 @@ prc_status attention_impl(const char* who, const lrsa_dims* dims, const lrsa_pag
 #if PRC_DEVICE_CHECKS
     if (prc_status dc = device_data_check(who, positions, kv_len, a.batch, a.n_tok, a.s_cap, st)) return dc;
 #endif
-    prc::decode_plan(a.s_cap, a.batch, a.n_kv, a.rank,
-                     pg == nullptr && prc::decode_shares_base(a.batch, a.kv_stride), cus, &a.n_splits,
+    prc::decode_plan(a.s_cap, a.batch, a.n_kv, a.head_dim, a.rank,
+                     pg == nullptr && prc::decode_shares_base(a.batch, a.kv_stride), pg != nullptr, cus, &a.n_splits,
                      &a.split_tiles);
     a.ws = static_cast<float*>(workspace);
     snprintf(what, sizeof(what), "%s (decode)", who);

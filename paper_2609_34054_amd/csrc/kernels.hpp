@@ -69,9 +69,10 @@ int decode_tile_tokens();
 // A decode batch whose requests all read one base cache (request stride 0)
 // runs the shared-base kernel: each base tile is read once for all of them.
 bool decode_shares_base(int batch, int64_t kv_req_stride);
-// `cus`: compute units of the device the call runs on.
-void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base, int cus, int* n_splits,
-                 int* split_tiles);
+// `cus`: compute units of the device the call runs on; `paged`: the caches
+// are block pools (the plan follows the kernel form the call takes).
+void decode_plan(int64_t s_cap, int batch, int n_kv, int head_dim, int rank, bool shared_base, bool paged, int cus,
+                 int* n_splits, int* split_tiles);
 size_t decode_workspace_bytes(int batch, int n_q, int n_splits, int head_dim, int rank);
 hipError_t launch_decode(const AttnArgs& a, hipStream_t stream);
 

@@ -1071,8 +1071,8 @@ int decode_tile_tokens() { return TK; }
 
 bool decode_shares_base(int batch, int64_t kv_req_stride) { return batch > 1 && kv_req_stride == 0; }
 
-void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base, int cus, int* n_splits,
-                 int* split_tiles) {
+void decode_plan(int64_t s_cap, int batch, int n_kv, int head_dim, int rank, bool shared_base, bool paged, int cus,
+                 int* n_splits, int* split_tiles) {
   const int64_t tiles = (s_cap + TK - 1) / TK;
   const int nw = dec_waves(rank);
   const int64_t nb = batch > 0 ? batch : 1;
@@ -1095,9 +1095,13 @@ void decode_plan(int64_t s_cap, int batch, int n_kv, int rank, bool shared_base,
   // batches) while splits stay at least 8 tiles long; otherwise one round:
   // small batches then get longer splits, each CU at most one workgroup,
   // and half the partials to merge (batch 1 at 36k: 46 -> 38 us per call).
+  // The rank-64 kernel that stages V by direct global->LDS loads holds its
+  // workgroup's whole register file per CU and keeps one sub-block in flight
+  // per wave: one round of longer splits measured faster there (64k, 8
+  // requests: 426 -> 419 us; two, three and four rounds 426, 442, 446 us).
   int64_t ns, st;
   plan(2, &ns, &st);
-  if (st < 8) plan(1, &ns, &st);
+  if (st < 8 || (!shared_base && dec_vdma(head_dim, rank, paged))) plan(1, &ns, &st);
   *n_splits = (int)ns;
   *split_tiles = (int)st;
 }
