@@ -684,18 +684,26 @@ lrsa_prefill_kernel(const AttnArgs a) {
   // order.
   // The starting points are shared by groups of row tiles that run on one
   // XCD (workgroup i runs on XCD i % 8, so row tiles r, r + 8, r + 16, ...):
-  // a group walks in step, so one memory-side read of a cached part serves
-  // its workgroups through L2, at the price of rebuilding the group's first
-  // tiles once per member.  Groups of four from 32 row tiles on, of two from
-  // 16 (32k rank 16: 2.318 -> 2.263 ms; 64k rank 64: 3.304 -> 3.125 ms;
-  // groups of eight measured slower, and with 8 row tiles, one per XCD,
-  // grouping only adds rebuilds).
+  // a group walks nearly in step, so one memory-side read of a cached part
+  // serves its workgroups through L2.  Groups of four from 32 row tiles on,
+  // of two from 16 (32k rank 16: 2.318 -> 2.263 ms; 64k rank 64: 3.304 ->
+  // 3.125 ms; groups of eight measured slower, and with 8 row tiles, one per
+  // XCD, grouping only adds rebuilds).  Member m of a group starts kMemberLag
+  // tiles after member m - 1 rather than at the same tile: members that
+  // start together all rebuild every tile of the group's own stretch, while
+  // a few tiles of lag let the later members find most of them published
+  // and still keep the group's reads close enough to share L2 (32k rank 16:
+  // no lag 2.239 ms, lags 1, 2, 3: 2.207, 2.197, 2.194 ms on one box; lags 3,
+  // 5, 8: 2.150, 2.182, 2.268 ms on another; rank 64 2.429 -> 2.353 ms).
+  constexpr int kMemberLag = 3;
   const int r_end = tc_on ? (n_full_raw < t_hi ? n_full_raw : t_hi) : t_lo;  // rotated steps [t_lo, r_end)
   const int n_rot = r_end > t_lo ? r_end - t_lo : 0;
   const int gsz = gridDim.x >= 32 ? 4 : (gridDim.x >= 16 ? 2 : 1);
   const int ngrp = (int)((gridDim.x + 8 * gsz - 1) / (8 * gsz)) * 8;  // > every group index
   const int grp = (rtile / (8 * gsz)) * 8 + rtile % 8;
-  const int rot = n_rot > 0 ? (int)(((int64_t)grp * n_rot) / ngrp) % n_rot : 0;
+  const int member = (rtile / 8) % gsz;
+  const int rot =
+      n_rot > 0 ? (int)((((int64_t)grp * n_rot) / ngrp + (int64_t)member * kMemberLag) % n_rot) : 0;
   auto tile_at = [&](int k) {
     if (k >= t_lo + n_rot) return k;
     const int t = k + rot;
